@@ -1,0 +1,206 @@
+"""Pins for any implementation of the clipped row softmax.
+
+Each ``pin_*`` function takes ``impl(x: float32 [R, C]) -> float64 [R, C]``
+and raises AssertionError when ``impl`` violates a fact fixed by the paper or
+by mathematics, not by the oracle's own code:
+
+  * closed forms of the definition (Sec. 1.1 Eq. (1); Sec. 1.2 Fig. 1 with
+    the -64 clip of the shifted logits, Sec. 2.1);
+  * the two-class special case, which is the logistic function (Sec. 1.1
+    calls softmax the multi-class extension of logistic regression), checked
+    against ``scipy.special.expit``;
+  * a 50-digit ``decimal`` brute force stored in ``tests/golden``;
+  * ``torch.softmax`` in float64 where the clip is inactive;
+  * invariants: uniform rows, exact shift invariance on dyadic grids, row
+    sums, permutation equivariance, monotonicity and the clip's lower bound;
+  * the non-finite-input reading.
+
+``tests/test_oracle_pins.py`` runs them on the oracle and
+``tests/test_oracle_mutants.py`` shows that planted mistakes fail them.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+from decimal import Decimal
+
+import numpy as np
+
+from workloads import random_logits
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+E64 = math.exp(-64.0)
+
+
+def _f32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+
+
+def _rel(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.max(np.abs(a - b) / np.abs(b)))
+
+
+def pin_uniform_rows(impl):
+    """Equal logits give exactly 1/N (Eq. (1) with all terms equal)."""
+    for n in (1, 2, 3, 7, 50, 1000, 4097):
+        for v in (0.0, -5.25, 17.0, -1.0e4):
+            y = impl(_f32(np.full((3, n), v)))
+            assert y.shape == (3, n)
+            assert np.all(y == 1.0 / n), (n, v)
+
+
+def pin_single_class(impl):
+    """C = 1 gives exactly 1 for any finite logit."""
+    y = impl(_f32([[3.0], [-1.0e4], [0.0], [65.5]]))
+    assert np.all(y == 1.0)
+
+
+def pin_two_class_logistic(impl):
+    """C = 2 reduces to the logistic function sigma(a - b) (Sec. 1.1)."""
+    from scipy.special import expit
+    rng = np.random.default_rng(5)
+    a = rng.uniform(-30.0, 30.0, 200)
+    b = rng.uniform(-30.0, 30.0, 200)
+    x = _f32(np.stack([a, b], axis=1))
+    y = impl(x)
+    diff = x[:, 0].astype(np.float64) - x[:, 1].astype(np.float64)
+    assert _rel(y[:, 0], expit(diff)) < 1e-14
+    assert _rel(y[:, 1], expit(-diff)) < 1e-14
+    # Beyond the clip: the smaller class is held at e^-64 / (1 + e^-64).
+    x = _f32([[0.0, -100.0], [-100.0, 0.0], [5.0, -70.0]])
+    y = impl(x)
+    lo, hi = E64 / (1.0 + E64), 1.0 / (1.0 + E64)
+    assert _rel([y[0, 1], y[1, 0], y[2, 1]], [lo, lo, lo]) < 1e-14
+    assert _rel([y[0, 0], y[1, 1], y[2, 0]], [hi, hi, hi]) < 1e-15
+
+
+def pin_clip_closed_form(impl):
+    """The clip of Fig. 1 on the shifted logits, in closed form.
+
+    Row [0, -100, -64, -63.5, -1e4]: clipped shifts [0, -64, -64, -63.5, -64]
+    and S = 1 + 3 e^-64 + e^-63.5.  The same row with a common offset and in
+    every rotation must give the same (rotated) values."""
+    base = np.array([0.0, -100.0, -64.0, -63.5, -1.0e4])
+    s = 1.0 + 3.0 * E64 + math.exp(-63.5)
+    want = np.array([1.0, E64, E64, math.exp(-63.5), E64]) / s
+    for off in (0.0, 37.25, -20.5):
+        for r in range(5):
+            x = _f32(np.roll(base + off, r)[None, :])
+            y = impl(x)[0]
+            assert _rel(y, np.roll(want, r)) < 1e-14, (off, r)
+
+
+def pin_brute_force_decimal(impl):
+    """Tiny rows against a 50-digit decimal evaluation (tests/golden)."""
+    with open(os.path.join(GOLDEN, "brute_force_rows.json")) as f:
+        doc = json.load(f)
+    for rec in doc["rows"]:
+        x = _f32([[float.fromhex(h) for h in rec["x_hex"]]])
+        y = impl(x)[0]
+        want = np.array([float(Decimal(v)) for v in rec["y"]])
+        assert _rel(y, want) < 1e-14, rec["x_hex"]
+        if "y_eq1" in rec:
+            want1 = np.array([float(Decimal(v)) for v in rec["y_eq1"]])
+            assert _rel(y, want1) < 1e-14
+
+
+def pin_library_unclipped(impl):
+    """Where no shifted logit is below -64, torch.softmax (float64) agrees."""
+    import torch
+    for (r, c, seed) in ((4, 1000, 1), (33, 50, 2), (2, 5000, 3)):
+        x = random_logits(r, c, seed, "normal", 4.0)
+        want = torch.softmax(torch.from_numpy(x).double(), dim=-1).numpy()
+        assert _rel(impl(x), want) < 1e-13
+
+
+def pin_shift_invariance(impl):
+    """Adding k to a dyadic row leaves every shifted logit bit-identical, so
+    the output must be bit-identical too."""
+    x = random_logits(6, 257, 7, "dyadic")
+    y0 = impl(x)
+    for k in (0.5, 2.0, 64.0, 1024.0, -256.0):
+        xk = _f32(x.astype(np.float64) + k)
+        assert np.array_equal(xk.astype(np.float64) - k, x.astype(np.float64))
+        assert np.array_equal(impl(xk), y0), k
+
+
+def pin_row_sums(impl):
+    """Every row sums to 1 (up to float64 rounding)."""
+    for (r, c, kind, seed) in ((8, 1000, "normal", 11), (3, 262144, "offset", 12),
+                              (16, 50, "clip_heavy", 13), (5, 4099, "uniform", 14)):
+        y = impl(random_logits(r, c, seed, kind))
+        for row in y:
+            assert abs(math.fsum(row) - 1.0) < 1e-13
+
+
+def pin_permutation_equivariance(impl):
+    """Permuting classes permutes the outputs."""
+    x = random_logits(4, 301, 21, "clip_heavy")
+    perm = np.random.default_rng(22).permutation(301)
+    assert _rel(impl(x[:, perm]), impl(x)[:, perm]) < 1e-14
+
+
+def pin_axis_is_rows(impl):
+    """Normalisation runs along each row of a non-square [R, C] matrix."""
+    x = random_logits(7, 3, 23, "normal")
+    y = impl(x)
+    assert y.shape == (7, 3)
+    assert np.allclose(y.sum(axis=1), 1.0, rtol=0, atol=1e-14)
+    assert not np.allclose(y.sum(axis=0), 1.0, atol=1e-3)
+
+
+def pin_monotonicity(impl):
+    """Raising one logit never lowers its own output nor raises another's;
+    it raises its own output strictly once the raised logit is unclipped."""
+    x = random_logits(1, 40, 31, "clip_heavy")
+    y0 = impl(x)[0]
+    for j in (0, 5, 17, 39):
+        x1 = x.copy()
+        x1[0, j] += np.float32(3.0)
+        y1 = impl(x1)[0]
+        others = np.arange(40) != j
+        assert y1[j] >= y0[j]
+        assert np.all(y1[others] <= y0[others] * (1 + 1e-15))
+        if x1[0, j] - x.max() > -64.0:
+            assert y1[j] > y0[j]
+
+
+def pin_lower_bound(impl):
+    """The clip keeps every output at or above e^-64 / C (Sec. 2.1: no
+    zeros), with equality for clipped entries of a row whose other entries
+    are all at the max."""
+    x = random_logits(32, 64, 41, "clip_heavy")
+    y = impl(x)
+    assert np.all(y >= E64 / 64 * (1 - 1e-14))
+    x = _f32([[0.0] * 3 + [-500.0]])
+    y = impl(x)[0]
+    assert _rel(y[3], E64 / (3.0 + E64)) < 1e-14
+
+
+def pin_nonfinite(impl):
+    """Reading of non-finite inputs: NaN or +inf poisons the row; -inf clips
+    to e^-64; an all -inf row is NaN."""
+    x = _f32([[1.0, np.nan, 0.0],
+              [1.0, np.inf, 0.0],
+              [-np.inf, -np.inf, -np.inf],
+              [0.0, -np.inf, 0.0],
+              [0.0, 1.0, 2.0]])
+    y = impl(x)
+    assert np.all(np.isnan(y[0])) and np.all(np.isnan(y[1]))
+    assert np.all(np.isnan(y[2]))
+    s = 2.0 + E64
+    assert _rel(y[3], [1 / s, E64 / s, 1 / s]) < 1e-14
+    assert np.all(np.isfinite(y[4]))
+
+
+def pin_empty(impl):
+    """Empty inputs give empty outputs of the same shape."""
+    for shape in ((0, 5), (5, 0), (0, 0)):
+        y = impl(np.zeros(shape, dtype=np.float32))
+        assert y.shape == shape
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

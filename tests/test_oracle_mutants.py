@@ -1,0 +1,105 @@
+"""Planted mistakes in copies of the oracle must each fail at least one pin.
+
+Every mutant below is a plausible slip when writing the clipped softmax
+(a dropped term, a sign, the wrong axis, the clip in the wrong place, a wrong
+constant, a float32 shortcut, ...).  The mistake is planted in a local copy
+of the float64 oracle on the CPU; nothing here touches the GPU path.
+"""
+import numpy as np
+import pytest
+
+from tests import pins
+
+L = -64.0
+
+
+def _base(x, shift="max", clip_on="d", clip_lo=L, axis=1, base_e=False,
+          drop_last=False, denom="sum", dtype=np.float64,
+          clip_kind="lower"):
+    x64 = np.asarray(x, dtype=dtype)
+    if x64.size == 0:
+        return np.zeros(x64.shape, dtype=np.float64)
+    with np.errstate(all="ignore"):
+        if shift == "max":
+            m = np.max(x64, axis=axis, keepdims=True)
+        elif shift == "first":
+            m = np.take(x64, [0], axis=axis)
+        else:
+            m = np.zeros_like(np.take(x64, [0], axis=axis))
+        if clip_on == "d":
+            d = x64 - m
+            src = d
+        else:  # clip applied to the raw logits, then shifted
+            src = x64
+        if clip_kind == "lower":
+            c = np.where(src < clip_lo, clip_lo, src)
+        elif clip_kind == "fmax":
+            c = np.fmax(src, clip_lo)
+        elif clip_kind == "upper":
+            c = np.where(src > clip_lo, clip_lo, src)
+        else:
+            c = src
+        if clip_on == "x":
+            c = c - m
+        e = np.power(2.0, c) if base_e else np.exp(c)
+        if drop_last:
+            s = np.sum(np.take(e, np.arange(e.shape[axis] - 1), axis=axis),
+                       axis=axis, keepdims=True)
+        elif denom == "sum":
+            s = np.sum(e, axis=axis, keepdims=True)
+        elif denom == "mean":
+            s = np.mean(e, axis=axis, keepdims=True)
+        elif denom == "sum_plus_one":
+            s = np.sum(e, axis=axis, keepdims=True) + 1.0
+        y = e / s
+        return np.asarray(y, dtype=np.float64)
+
+
+MUTANTS = {
+    "reference_copy_is_clean": None,
+    "dropped_sum_term": dict(drop_last=True),
+    "wrong_sign_shift": "neg",
+    "transposed_axis": dict(axis=0),
+    "no_clip": dict(clip_kind="none"),
+    "clip_as_upper_bound": dict(clip_kind="upper"),
+    "clip_constant_-63": dict(clip_lo=-63.0),
+    "clip_constant_-65": dict(clip_lo=-65.0),
+    "clip_on_raw_logits": dict(clip_on="x"),
+    "shift_by_first_element": dict(shift="first"),
+    "no_shift": dict(shift="none"),
+    "base_2_instead_of_e": dict(base_e=True),
+    "mean_instead_of_sum": dict(denom="mean"),
+    "off_by_one_denominator": dict(denom="sum_plus_one"),
+    # An IEEE max-style clip turns NaN into the bound instead of keeping it.
+    # (A NaN-ignoring row max is not listed: the NaN element still poisons
+    # the row through its own exp and the sum, so it is an equivalent form.)
+    "fmax_clip_drops_nan": dict(clip_kind="fmax"),
+    "float32_arithmetic": dict(dtype=np.float32),
+}
+
+
+def _impl(spec):
+    if spec is None:
+        return lambda x: _base(x)
+    if spec == "neg":
+        return lambda x: _base(-np.asarray(x, dtype=np.float64))
+    return lambda x: _base(x, **spec)
+
+
+def _failures(impl):
+    failed = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(impl)
+        except (AssertionError, ValueError, FloatingPointError, IndexError):
+            failed.append(pin.__name__)
+    return failed
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name):
+    failed = _failures(_impl(MUTANTS[name]))
+    if MUTANTS[name] is None:
+        assert failed == [], failed
+    else:
+        assert failed, f"mutant {name} passed every pin"

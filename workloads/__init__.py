@@ -1,0 +1,154 @@
+"""Seeded synthetic inputs for the row-softmax workloads.
+
+This module only draws random numbers and shapes them into logits matrices.
+It performs none of the softmax arithmetic, so both the float64 oracle and the
+GPU path can take their inputs from here without sharing any of the method.
+
+The paper measures softmax inside inference of the Deep Attention Matching
+(DAM) model (Sec. 1 and Sec. 3); its model, data and figure values are not
+available, so every workload below is synthetic.  Each one is shaped like a
+use the paper names: DAM attention rows, classifier rows, NLP vocabulary rows,
+plus a long-row case.  Draw order is fixed and uses numpy's PCG64
+(``default_rng(seed)``); values are drawn in float64 and cast once to float32
+(round to nearest even).
+
+The DAM-style scores are formed as Q.K^T / sqrt(200) from 200-dim standard
+normal vectors that are first rounded to multiples of 2^-10.  With that
+rounding every product and every partial sum of the 200-term dot product is
+exact in float64, so the result does not depend on the summation order that
+a BLAS or einsum kernel happens to use on a given host CPU.
+"""
+from __future__ import annotations
+
+import hashlib
+from dataclasses import dataclass
+
+import numpy as np
+
+__all__ = ["Workload", "WORKLOADS", "generate", "sha256_f32", "random_logits"]
+
+
+@dataclass(frozen=True)
+class Workload:
+    key: str
+    rows: int
+    cols: int
+    seed: int
+    description: str
+
+    @property
+    def elements(self) -> int:
+        return self.rows * self.cols
+
+    @property
+    def algorithmic_bytes(self) -> int:
+        """One fp32 read of x and one fp32 write of y per element."""
+        return 8 * self.rows * self.cols
+
+
+WORKLOADS: dict[str, Workload] = {
+    w.key: w
+    for w in (
+        Workload("plumbing_64x1000", 64, 1000, 0,
+                 "uniform(-10, 10) logits, 64 rows x 1000 classes"),
+        Workload("dam_attention_115200x50", 115200, 50, 1,
+                 "DAM-style attention scores: 256 batch x 9 turns x 50 queries "
+                 "rows over 50 keys; score = q.k / sqrt(200)"),
+        Workload("classifier_4096x1000", 4096, 1000, 2,
+                 "N(0, 3^2) classifier logits with one true class boosted by +8"),
+        Workload("vocab_512x32768", 512, 32768, 3,
+                 "N(0, 2^2) vocabulary logits; 5% of entries set to -1e4, "
+                 "5 rows with a single +80 outlier"),
+        Workload("longrow_64x262144", 64, 262144, 4,
+                 "N(0,1) + per-row offset uniform(-50, 50), 64 rows x 262144"),
+    )
+}
+
+# Short aliases by position (1-based, in the order above).
+_BY_INDEX = {i + 1: k for i, k in enumerate(WORKLOADS)}
+
+
+def _resolve(key) -> Workload:
+    if isinstance(key, int):
+        key = _BY_INDEX[key]
+    return WORKLOADS[key]
+
+
+def _dam_scores(rng: np.random.Generator) -> np.ndarray:
+    batch_turns, q, k, dim = 2304, 50, 50, 200
+    qv = rng.standard_normal((batch_turns, q, dim))
+    kv = rng.standard_normal((batch_turns, k, dim))
+    qv = np.round(qv * 1024.0) / 1024.0
+    kv = np.round(kv * 1024.0) / 1024.0
+    s = np.matmul(qv, kv.transpose(0, 2, 1))
+    s = s / np.sqrt(200.0)
+    return s.reshape(batch_turns * q, k)
+
+
+def generate(key) -> np.ndarray:
+    """Return the float32 [rows, cols] logits matrix for a workload.
+
+    ``key`` is a workload name from ``WORKLOADS`` or its 1-based position.
+    """
+    w = _resolve(key)
+    rng = np.random.default_rng(w.seed)
+    if w.key == "plumbing_64x1000":
+        x = rng.uniform(-10.0, 10.0, (w.rows, w.cols))
+    elif w.key == "dam_attention_115200x50":
+        x = _dam_scores(rng)
+    elif w.key == "classifier_4096x1000":
+        x = 3.0 * rng.standard_normal((w.rows, w.cols))
+        t = rng.integers(0, w.cols, w.rows)
+        x[np.arange(w.rows), t] += 8.0
+    elif w.key == "vocab_512x32768":
+        x = 2.0 * rng.standard_normal((w.rows, w.cols))
+        base = x.copy()
+        mask = rng.random(x.shape) < 0.05
+        x[mask] = -1.0e4
+        rows = rng.choice(w.rows, 5, replace=False)
+        cols = rng.integers(0, w.cols, 5)
+        x[rows, cols] = base[rows, cols] + 80.0
+    elif w.key == "longrow_64x262144":
+        off = rng.uniform(-50.0, 50.0, (w.rows, 1))
+        x = rng.standard_normal((w.rows, w.cols)) + off
+    else:  # pragma: no cover
+        raise KeyError(w.key)
+    out = np.ascontiguousarray(x.astype(np.float32))
+    assert out.shape == (w.rows, w.cols)
+    return out
+
+
+def sha256_f32(x: np.ndarray) -> str:
+    """SHA-256 of the little-endian float32 bytes of a C-contiguous array."""
+    a = np.ascontiguousarray(x, dtype="<f4")
+    return hashlib.sha256(a.tobytes()).hexdigest()
+
+
+def random_logits(rows: int, cols: int, seed: int, kind: str = "normal",
+                  scale: float = 4.0) -> np.ndarray:
+    """Seeded float32 logits for edge-shape tests.
+
+    kinds: ``normal`` (N(0, scale^2)), ``uniform`` (U(-scale, scale)),
+    ``clip_heavy`` (a few large values over a wide negative spread, so that
+    many shifted logits fall below -64), ``offset`` (N(0,1) plus a per-row
+    offset in U(-50, 50)), ``dyadic`` (multiples of 1/64 in [-8, 8]).
+    """
+    rng = np.random.default_rng(seed)
+    shape = (rows, cols)
+    if kind == "normal":
+        x = scale * rng.standard_normal(shape)
+    elif kind == "uniform":
+        x = rng.uniform(-scale, scale, shape)
+    elif kind == "clip_heavy":
+        x = rng.uniform(-150.0, 0.0, shape)
+        if rows and cols:
+            hot = rng.integers(0, cols, rows)
+            x[np.arange(rows), hot] = 20.0
+    elif kind == "offset":
+        off = rng.uniform(-50.0, 50.0, (rows, 1))
+        x = rng.standard_normal(shape) + off
+    elif kind == "dyadic":
+        x = rng.integers(-512, 513, shape) / 64.0
+    else:
+        raise ValueError(kind)
+    return np.ascontiguousarray(x.astype(np.float32))
