@@ -1,0 +1,140 @@
+/*
+ * softmax_mi355x.h -- C ABI of the MI355X (gfx950) row-softmax library.
+ *
+ * The operation (Sec. 1.1, Eq. (1) of "Softmax Optimizations for Intel Xeon
+ * Processor-based Platforms", with the reference functor's clip of the
+ * shifted logits, Sec. 1.2 Fig. 1, and the row-major [batch_size,
+ * num_classes] layout of the optimised functor, Sec. 2.3 Fig. 4):
+ *
+ *   for every row i of x (rows x cols, fp32, row-major, leading dim = cols):
+ *     M_i  = max_j x[i,j]
+ *     c_ij = max(x[i,j] - M_i, SOFTMAX_CLIP_LO)      (compare-select)
+ *     y[i,j] = exp(c_ij) / sum_k exp(c_ik)
+ *
+ * Accuracy: every output is within 4e-6 relative of the exact value of the
+ * formula above (derivation: the exp argument is carried in extended
+ * precision, v_exp_f32 is within 1 ulp, the row sum is a fixed-depth tree).
+ * Outputs are bitwise deterministic for a given input, shape and alignment.
+ *
+ * Non-finite inputs: a NaN or +inf anywhere in a row, or a row of all -inf,
+ * gives a row of NaN; a -inf entry among finite ones clips to e^-64 / S.
+ *
+ * All functions are thread-safe.  Only the entry points below are exported.
+ */
+#ifndef SOFTMAX_MI355X_H
+#define SOFTMAX_MI355X_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SOFTMAX_API __attribute__((visibility("default")))
+
+/* Lower bound applied to the shifted logit x - rowmax before exp.  The
+ * paper's reference functor clips here (Sec. 1.2 Fig. 1; purpose in
+ * Sec. 2.1) without printing the constant; this library fixes it at -64,
+ * so no output is 0 and none is denormal for any row length below 2^33. */
+#define SOFTMAX_CLIP_LO (-64.0f)
+
+/* Return codes. */
+#define SOFTMAX_OK 0
+#define SOFTMAX_ERR_INVALID_ARG 1 /* bad size, null or overlapping pointer */
+#define SOFTMAX_ERR_HIP 2         /* a HIP call or launch failed */
+#define SOFTMAX_ERR_NOT_DEVICE 3  /* pointer is not memory the current
+                                     device can use, or the byte range runs
+                                     past its allocation */
+
+/* Kernel families reported by softmax_plan(). */
+#define SOFTMAX_KERNEL_NONE 0      /* rows*cols == 0: nothing is launched */
+#define SOFTMAX_KERNEL_PACKED 1    /* cols <= 64: several rows per wavefront */
+#define SOFTMAX_KERNEL_WAVE_ROW 2  /* cols <= 4096: one wavefront per row */
+#define SOFTMAX_KERNEL_BLOCK_ROW 3 /* cols <= 32768: one workgroup per row */
+#define SOFTMAX_KERNEL_SPLIT_ROW 4 /* longer rows: several workgroups per row,
+                                      two launches */
+
+/*
+ * softmax_fwd -- row-wise clipped softmax, fp32 in and out.
+ *
+ *   x      device pointer to rows*cols fp32 values, row-major (element (i,j)
+ *          at x[i*cols + j]).  Read only.
+ *   y      device pointer to rows*cols fp32 values, same layout; written.
+ *          y == x (in place) is allowed; any other overlap of the two byte
+ *          ranges is rejected.
+ *   rows   number of rows (the paper's batch_size), >= 0.
+ *   cols   number of classes per row (num_classes), >= 0.
+ *   stream HIP stream to enqueue on (0 = the null stream).
+ *
+ * Ownership: x and y are allocated and owned by the caller and must be memory
+ * the current HIP device can access (hipMalloc, torch CUDA tensors, managed
+ * or pinned host memory); the call checks this and the byte ranges against
+ * the allocations before launching.  No alignment is required: 128-bit
+ * accesses are used when x and y are 16-byte aligned (and, above 64
+ * columns, cols % 4 == 0); otherwise 32-bit accesses.
+ *
+ * Asynchrony: work is enqueued on `stream` and the call returns without
+ * waiting; y is valid once the stream has reached that point.
+ *
+ * Workspace: rows longer than 32768 columns use a device workspace of 1 MiB
+ * that the library allocates on first use per device and keeps until the
+ * process ends.  Such calls on different streams of one device are ordered
+ * by the library with an event, so they never race on it.
+ *
+ * Returns SOFTMAX_OK, or SOFTMAX_ERR_INVALID_ARG (rows or cols < 0,
+ * rows*cols*4 overflows int64, x or y null while rows*cols > 0, partial
+ * overlap), SOFTMAX_ERR_NOT_DEVICE, or SOFTMAX_ERR_HIP (the HIP error is
+ * kept for softmax_last_hip_error()).  On any error nothing is launched
+ * except for SOFTMAX_ERR_HIP from a failed launch.  rows*cols == 0 returns
+ * SOFTMAX_OK without touching the GPU.
+ */
+SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols,
+                            hipStream_t stream);
+
+/* Static description of a return code.  Never NULL. */
+SOFTMAX_API const char* softmax_strerror(int code);
+
+/* hipError_t of the last SOFTMAX_ERR_HIP returned on this thread (0 if none). */
+SOFTMAX_API int softmax_last_hip_error(void);
+
+/* What softmax_fwd would launch for these arguments.  Host only: no HIP call,
+ * no launch; x and y are only inspected for alignment and overlap. */
+typedef struct softmax_plan_t {
+  int32_t kernel;          /* SOFTMAX_KERNEL_* */
+  int32_t vec_width;       /* 4: 128-bit loads and stores; 1: 32-bit */
+  int32_t lanes_per_row;   /* lanes that share one row (or one chunk) */
+  int32_t elems_per_lane;  /* elements each lane holds per row or chunk */
+  int32_t block_threads;   /* threads per workgroup */
+  int32_t launches;        /* kernel launches per call */
+  int64_t chunks_per_row;  /* workgroups per row (split rows), else 1 */
+  int64_t grid;            /* workgroups in each launch */
+  int64_t workspace_bytes; /* library workspace the call touches */
+} softmax_plan_t;
+
+SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64_t cols,
+                             softmax_plan_t* plan);
+
+/*
+ * softmax_exp_probe -- diagnostic: e[i] = exp(max(x[i] - m[i], -64)) for
+ * 0 <= i < n, through the same device routine the softmax kernels use for
+ * the clipped exp (Sec. 1.2 Fig. 1, the ValueClip then exp).  x, m, e are
+ * device fp32 arrays of n elements owned by the caller (e must not overlap
+ * x or m).  Same error rules as softmax_fwd.
+ */
+SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int64_t n,
+                                  hipStream_t stream);
+
+/*
+ * softmax_copy_probe -- diagnostic: y[i] = x[i] for 0 <= i < n with 128-bit
+ * accesses when both are 16-byte aligned.  The memory-bound ceiling for the
+ * same bytes softmax moves (the paper's memcpy comparison, Sec. 2.6).
+ * x and y are caller-owned device arrays that must not overlap.
+ */
+SOFTMAX_API int softmax_copy_probe(const float* x, float* y, int64_t n, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOFTMAX_MI355X_H */

@@ -1,0 +1,198 @@
+"""Python binding for the MI355X row-softmax C ABI (include/softmax_mi355x.h).
+
+Argument marshalling only: every step of the softmax runs in the HIP kernels
+of ``lib/libsoftmax_mi355x.so``.  torch supplies device memory and the
+current stream.  There is no fallback: if the library is not built, or the
+tensors are not on the GPU, these functions raise.
+
+Functions keep the C names:
+
+    softmax_fwd(x, out=None, stream=None) -> torch.Tensor
+    softmax_fwd_ptr(x_ptr, y_ptr, rows, cols, stream_handle) -> int
+    softmax_plan(rows, cols, x_ptr=1 << 44, y_ptr=1 << 45) -> dict
+    softmax_exp_probe(x, m, out=None, stream=None) -> torch.Tensor
+    softmax_copy_probe(x, out=None, stream=None) -> torch.Tensor
+    softmax_strerror(code) -> str
+    softmax_last_hip_error() -> int
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "LIB_PATH", "HEADER_PATH", "SoftmaxError", "load_library", "softmax_fwd",
+    "softmax_fwd_ptr", "softmax_plan", "softmax_exp_probe", "softmax_copy_probe",
+    "softmax_strerror", "softmax_last_hip_error", "CLIP_LO", "KERNEL_NAMES",
+]
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "lib", "libsoftmax_mi355x.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "softmax_mi355x.h")
+
+CLIP_LO = -64.0
+OK, ERR_INVALID_ARG, ERR_HIP, ERR_NOT_DEVICE = 0, 1, 2, 3
+KERNEL_NAMES = {0: "none", 1: "packed", 2: "wave_row", 3: "block_row", 4: "split_row"}
+
+
+class SoftmaxError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        self.code = code
+        msg = f"{what}: {softmax_strerror(code)} (code {code})"
+        if code == ERR_HIP:
+            msg += f", hipError_t {softmax_last_hip_error()}"
+        super().__init__(msg)
+
+
+class _Plan(ctypes.Structure):
+    _fields_ = [
+        ("kernel", ctypes.c_int32),
+        ("vec_width", ctypes.c_int32),
+        ("lanes_per_row", ctypes.c_int32),
+        ("elems_per_lane", ctypes.c_int32),
+        ("block_threads", ctypes.c_int32),
+        ("launches", ctypes.c_int32),
+        ("chunks_per_row", ctypes.c_int64),
+        ("grid", ctypes.c_int64),
+        ("workspace_bytes", ctypes.c_int64),
+    ]
+
+
+_lib = None
+
+
+def load_library() -> ctypes.CDLL:
+    """Load the built library (no HIP call happens at load time)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run `python -m paper_1904_12380_amd.build` "
+            "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64 = ctypes.c_void_p, ctypes.c_int64
+    lib.softmax_fwd.argtypes = [vp, vp, i64, i64, vp]
+    lib.softmax_fwd.restype = ctypes.c_int
+    lib.softmax_strerror.argtypes = [ctypes.c_int]
+    lib.softmax_strerror.restype = ctypes.c_char_p
+    lib.softmax_last_hip_error.argtypes = []
+    lib.softmax_last_hip_error.restype = ctypes.c_int
+    lib.softmax_plan.argtypes = [vp, vp, i64, i64, ctypes.POINTER(_Plan)]
+    lib.softmax_plan.restype = ctypes.c_int
+    lib.softmax_exp_probe.argtypes = [vp, vp, vp, i64, vp]
+    lib.softmax_exp_probe.restype = ctypes.c_int
+    lib.softmax_copy_probe.argtypes = [vp, vp, i64, vp]
+    lib.softmax_copy_probe.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def softmax_strerror(code: int) -> str:
+    return load_library().softmax_strerror(int(code)).decode()
+
+
+def softmax_last_hip_error() -> int:
+    return int(load_library().softmax_last_hip_error())
+
+
+def softmax_plan(rows: int, cols: int, x_ptr: int = 1 << 44,
+                 y_ptr: int = 1 << 45) -> dict:
+    """Host-only description of what softmax_fwd would launch.  The default
+    pointers are 16-byte aligned placeholders; they are never dereferenced."""
+    p = _Plan()
+    rc = load_library().softmax_plan(x_ptr, y_ptr, rows, cols, ctypes.byref(p))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_plan")
+    d = {name: int(getattr(p, name)) for name, _ in _Plan._fields_}
+    d["kernel_name"] = KERNEL_NAMES[d["kernel"]]
+    return d
+
+
+def softmax_fwd_ptr(x_ptr: int, y_ptr: int, rows: int, cols: int,
+                    stream_handle: int = 0) -> int:
+    """Raw C call; returns the C return code."""
+    return int(load_library().softmax_fwd(x_ptr, y_ptr, rows, cols, stream_handle))
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(stream) -> int:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _check_f32_cuda(t, name: str):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (no CPU path exists)")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous (row-major, leading dim = cols)")
+
+
+def softmax_fwd(x, out=None, stream=None):
+    """Row-wise clipped softmax of a 2-D float32 GPU tensor [rows, cols].
+
+    ``out`` may be ``x`` itself (in place).  Runs on ``stream`` (default: the
+    current torch stream) and returns without synchronising."""
+    torch = _torch()
+    _check_f32_cuda(x, "x")
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [rows, cols]")
+    if out is None:
+        out = torch.empty_like(x)
+    else:
+        _check_f32_cuda(out, "out")
+        if out.shape != x.shape or out.device != x.device:
+            raise ValueError("out must match x in shape and device")
+    rows, cols = x.shape
+    with torch.cuda.device(x.device):
+        rc = softmax_fwd_ptr(x.data_ptr(), out.data_ptr(), rows, cols,
+                             _stream_handle(stream))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_fwd")
+    return out
+
+
+def softmax_exp_probe(x, m, out=None, stream=None):
+    """e = exp(max(x - m, -64)) elementwise through the kernels' exp routine."""
+    torch = _torch()
+    _check_f32_cuda(x, "x")
+    _check_f32_cuda(m, "m")
+    if m.shape != x.shape:
+        raise ValueError("m must match x")
+    if out is None:
+        out = torch.empty_like(x)
+    _check_f32_cuda(out, "out")
+    with torch.cuda.device(x.device):
+        rc = int(load_library().softmax_exp_probe(
+            x.data_ptr(), m.data_ptr(), out.data_ptr(), x.numel(), _stream_handle(stream)))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_exp_probe")
+    return out
+
+
+def softmax_copy_probe(x, out=None, stream=None):
+    """out = x through the library's 128-bit copy kernel (bandwidth ceiling)."""
+    torch = _torch()
+    _check_f32_cuda(x, "x")
+    if out is None:
+        out = torch.empty_like(x)
+    _check_f32_cuda(out, "out")
+    if out.numel() != x.numel():
+        raise ValueError("out must have as many elements as x")
+    with torch.cuda.device(x.device):
+        rc = int(load_library().softmax_copy_probe(
+            x.data_ptr(), out.data_ptr(), x.numel(), _stream_handle(stream)))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_copy_probe")
+    return out

@@ -1,0 +1,404 @@
+// C ABI of the row-softmax library: argument checks, the dispatch on cols,
+// and the launches.  Declarations and the contract are in
+// include/softmax_mi355x.h.
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+
+#include "../../include/softmax_mi355x.h"
+#include "sm_kernels.hpp"
+
+namespace {
+
+using namespace smx;
+
+// Largest grid any launch uses; the kernels loop over the rest.
+constexpr int64_t kMaxGrid = int64_t(1) << 20;
+
+// Bucket limits on cols.
+constexpr int64_t kPackedMaxCols = 64;
+constexpr int64_t kWaveRowMaxCols = 4096;
+constexpr int64_t kBlockRowMaxCols = 32768;
+
+// Split rows: 512-thread workgroups holding 8 float4 per lane, i.e. chunks
+// of 16384 columns (64 KiB of x) per workgroup.
+constexpr int kSplitThreads = 512;
+constexpr int kSplitV = 8;
+constexpr int64_t kSplitChunk = int64_t(4) * kSplitV * kSplitThreads;
+
+// Library-owned workspace for split-row partials, per device.
+constexpr int64_t kWorkspaceBytes = int64_t(1) << 20;
+constexpr int64_t kWorkspacePairs = kWorkspaceBytes / int64_t(sizeof(float2));
+constexpr int kMaxDevices = 64;
+
+thread_local int tl_last_hip_error = 0;
+
+struct DeviceState {
+  float2* ws = nullptr;
+  hipEvent_t last = nullptr;
+  hipStream_t last_stream = nullptr;
+  bool has_last = false;
+};
+std::mutex g_mu;
+DeviceState g_dev[kMaxDevices];
+
+inline bool aligned16(const void* p) {
+  return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+}
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+inline int64_t pow2_at_least(int64_t v) {
+  int64_t p = 1;
+  while (p < v) p <<= 1;
+  return p;
+}
+
+int fail_hip(hipError_t e) {
+  tl_last_hip_error = static_cast<int>(e);
+  return SOFTMAX_ERR_HIP;
+}
+
+// rows*cols*4 must fit in int64 and both counts must be non-negative.
+int check_sizes(int64_t rows, int64_t cols) {
+  if (rows < 0 || cols < 0) return SOFTMAX_ERR_INVALID_ARG;
+  if (rows == 0 || cols == 0) return SOFTMAX_OK;
+  if (rows > INT64_MAX / 4 / cols) return SOFTMAX_ERR_INVALID_ARG;
+  return SOFTMAX_OK;
+}
+
+// Byte ranges [a, a+n) and [b, b+n) overlap without being identical.
+bool partial_overlap(const void* a, const void* b, int64_t n) {
+  const uintptr_t pa = reinterpret_cast<uintptr_t>(a);
+  const uintptr_t pb = reinterpret_cast<uintptr_t>(b);
+  if (pa == pb) return false;
+  return pa < pb + static_cast<uintptr_t>(n) && pb < pa + static_cast<uintptr_t>(n);
+}
+
+bool any_overlap(const void* a, const void* b, int64_t n) {
+  const uintptr_t pa = reinterpret_cast<uintptr_t>(a);
+  const uintptr_t pb = reinterpret_cast<uintptr_t>(b);
+  return pa < pb + static_cast<uintptr_t>(n) && pb < pa + static_cast<uintptr_t>(n);
+}
+
+// The device can use [p, p+bytes): memory registered with HIP, on the
+// current device when it is device memory, and inside one allocation.
+int check_device_range(const void* p, int64_t bytes, int dev) {
+  hipPointerAttribute_t a;
+  hipError_t e = hipPointerGetAttributes(&a, p);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return SOFTMAX_ERR_NOT_DEVICE;
+  }
+  if (a.type == hipMemoryTypeDevice) {
+    if (a.device != dev) return SOFTMAX_ERR_NOT_DEVICE;
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    e = hipMemGetAddressRange(&base, &size, const_cast<void*>(p));
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return SOFTMAX_ERR_NOT_DEVICE;
+    }
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(base);
+    const uintptr_t pp = reinterpret_cast<uintptr_t>(p);
+    if (pp < lo || pp + static_cast<uintptr_t>(bytes) > lo + size)
+      return SOFTMAX_ERR_NOT_DEVICE;
+    return SOFTMAX_OK;
+  }
+  // Pinned (registered) host memory and managed memory are usable by the
+  // device; unregistered pageable memory is not.
+  if (a.type == hipMemoryTypeHost || a.type == hipMemoryTypeManaged) return SOFTMAX_OK;
+  return SOFTMAX_ERR_NOT_DEVICE;
+}
+
+softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t cols) {
+  softmax_plan_t p{};
+  p.chunks_per_row = 1;
+  if (rows == 0 || cols == 0) {
+    p.kernel = SOFTMAX_KERNEL_NONE;
+    return p;
+  }
+  const bool a16 = aligned16(x) && aligned16(y);
+  const bool vec_rows = a16 && (cols % 4 == 0);
+  if (cols <= kPackedMaxCols) {
+    const int64_t g = cols <= 4 ? 1 : cols <= 8 ? 2 : cols <= 16 ? 4 : cols <= 32 ? 8 : 16;
+    p.kernel = SOFTMAX_KERNEL_PACKED;
+    p.vec_width = a16 ? 4 : 1;
+    p.lanes_per_row = static_cast<int32_t>(g);
+    p.elems_per_lane = 4;
+    p.block_threads = 256;
+    const int64_t tile = 4 * (256 / g);
+    p.grid = std::min(ceil_div(rows, tile), kMaxGrid);
+    p.launches = 1;
+  } else if (cols <= kWaveRowMaxCols) {
+    const int64_t v = pow2_at_least(ceil_div(cols, 256));
+    p.kernel = SOFTMAX_KERNEL_WAVE_ROW;
+    p.vec_width = vec_rows ? 4 : 1;
+    p.lanes_per_row = 64;
+    p.elems_per_lane = static_cast<int32_t>(4 * v);
+    p.block_threads = 256;
+    p.grid = std::min(ceil_div(rows, 4), kMaxGrid);
+    p.launches = 1;
+  } else if (cols <= kBlockRowMaxCols) {
+    const int64_t v = std::max<int64_t>(2, pow2_at_least(ceil_div(cols, 4096)));
+    p.kernel = SOFTMAX_KERNEL_BLOCK_ROW;
+    p.vec_width = vec_rows ? 4 : 1;
+    p.lanes_per_row = 1024;
+    p.elems_per_lane = static_cast<int32_t>(4 * v);
+    p.block_threads = 1024;
+    p.grid = std::min(rows, kMaxGrid);
+    p.launches = 1;
+  } else {
+    const int64_t g = ceil_div(cols, kSplitChunk);
+    p.kernel = SOFTMAX_KERNEL_SPLIT_ROW;
+    p.vec_width = vec_rows ? 4 : 1;
+    p.lanes_per_row = kSplitThreads;
+    p.elems_per_lane = 4 * kSplitV;
+    p.block_threads = kSplitThreads;
+    p.chunks_per_row = g;
+    const int64_t rows_per_batch = std::max<int64_t>(1, kWorkspacePairs / g);
+    const int64_t batch_rows = std::min(rows, rows_per_batch);
+    p.grid = std::min(batch_rows * g, kMaxGrid);
+    p.launches = static_cast<int32_t>(2 * ceil_div(rows, rows_per_batch));
+    p.workspace_bytes = kWorkspaceBytes;
+  }
+  return p;
+}
+
+hipError_t launch(const void* fn, int64_t grid, int block, void** args, hipStream_t s) {
+  return hipLaunchKernel(fn, dim3(static_cast<uint32_t>(grid)), dim3(block), args, 0, s);
+}
+
+template <int G, bool VEC4>
+hipError_t run_packed(const float* x, float* y, int64_t rows, int64_t cols, int64_t grid,
+                      hipStream_t s) {
+  void* args[] = {&x, &y, &rows, &cols};
+  return launch(reinterpret_cast<const void*>(&k_packed<G, 4, VEC4>), grid, 256, args, s);
+}
+
+template <bool VEC4>
+hipError_t dispatch_packed(const softmax_plan_t& p, const float* x, float* y,
+                           int64_t rows, int64_t cols, hipStream_t s) {
+  switch (p.lanes_per_row) {
+    case 1: return run_packed<1, VEC4>(x, y, rows, cols, p.grid, s);
+    case 2: return run_packed<2, VEC4>(x, y, rows, cols, p.grid, s);
+    case 4: return run_packed<4, VEC4>(x, y, rows, cols, p.grid, s);
+    case 8: return run_packed<8, VEC4>(x, y, rows, cols, p.grid, s);
+    default: return run_packed<16, VEC4>(x, y, rows, cols, p.grid, s);
+  }
+}
+
+template <int V, bool VEC4>
+hipError_t run_wave(const float* x, float* y, int64_t rows, int64_t cols, int64_t grid,
+                    hipStream_t s) {
+  void* args[] = {&x, &y, &rows, &cols};
+  return launch(reinterpret_cast<const void*>(&k_wave_row<V, VEC4>), grid, 256, args, s);
+}
+
+template <bool VEC4>
+hipError_t dispatch_wave(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
+                         int64_t cols, hipStream_t s) {
+  switch (p.elems_per_lane / 4) {
+    case 1: return run_wave<1, VEC4>(x, y, rows, cols, p.grid, s);
+    case 2: return run_wave<2, VEC4>(x, y, rows, cols, p.grid, s);
+    case 4: return run_wave<4, VEC4>(x, y, rows, cols, p.grid, s);
+    case 8: return run_wave<8, VEC4>(x, y, rows, cols, p.grid, s);
+    default: return run_wave<16, VEC4>(x, y, rows, cols, p.grid, s);
+  }
+}
+
+template <int V, bool VEC4>
+hipError_t run_block(const float* x, float* y, int64_t rows, int64_t cols, int64_t grid,
+                     hipStream_t s) {
+  void* args[] = {&x, &y, &rows, &cols};
+  return launch(reinterpret_cast<const void*>(&k_block_row<1024, V, VEC4>), grid, 1024,
+                args, s);
+}
+
+template <bool VEC4>
+hipError_t dispatch_block(const softmax_plan_t& p, const float* x, float* y,
+                          int64_t rows, int64_t cols, hipStream_t s) {
+  switch (p.elems_per_lane / 4) {
+    case 2: return run_block<2, VEC4>(x, y, rows, cols, p.grid, s);
+    case 4: return run_block<4, VEC4>(x, y, rows, cols, p.grid, s);
+    default: return run_block<8, VEC4>(x, y, rows, cols, p.grid, s);
+  }
+}
+
+template <bool VEC4>
+hipError_t run_split(const float* x, float* y, float2* ws, int64_t rows, int64_t cols,
+                     int64_t chunks, hipStream_t s) {
+  const int64_t rows_per_batch = std::max<int64_t>(1, kWorkspacePairs / chunks);
+  for (int64_t r0 = 0; r0 < rows; r0 += rows_per_batch) {
+    int64_t nb = std::min(rows_per_batch, rows - r0);
+    const float* xb = x + r0 * cols;
+    float* yb = y + r0 * cols;
+    const int64_t grid = std::min(nb * chunks, kMaxGrid);
+    void* a1[] = {&xb, &ws, &nb, &cols, &chunks};
+    hipError_t e = launch(
+        reinterpret_cast<const void*>(&k_split_stats<kSplitThreads, kSplitV, VEC4>), grid,
+        kSplitThreads, a1, s);
+    if (e != hipSuccess) return e;
+    const float2* wsc = ws;
+    void* a2[] = {&xb, &yb, &wsc, &nb, &cols, &chunks};
+    e = launch(reinterpret_cast<const void*>(&k_split_apply<kSplitThreads, kSplitV, VEC4>),
+               grid, kSplitThreads, a2, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// Split rows: the workspace is per device; calls on different streams are
+// chained with an event so they never use it at the same time.
+int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
+               int64_t cols, int dev, hipStream_t s) {
+  if (dev < 0 || dev >= kMaxDevices) return SOFTMAX_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceState& st = g_dev[dev];
+  hipError_t e;
+  if (st.ws == nullptr) {
+    void* mem = nullptr;
+    e = hipMalloc(&mem, kWorkspaceBytes);
+    if (e != hipSuccess) return fail_hip(e);
+    st.ws = static_cast<float2*>(mem);
+    e = hipEventCreateWithFlags(&st.last, hipEventDisableTiming);
+    if (e != hipSuccess) return fail_hip(e);
+  }
+  if (st.has_last && st.last_stream != s) {
+    e = hipStreamWaitEvent(s, st.last, 0);
+    if (e != hipSuccess) return fail_hip(e);
+  }
+  e = p.vec_width == 4 ? run_split<true>(x, y, st.ws, rows, cols, p.chunks_per_row, s)
+                       : run_split<false>(x, y, st.ws, rows, cols, p.chunks_per_row, s);
+  if (e != hipSuccess) return fail_hip(e);
+  e = hipEventRecord(st.last, s);
+  if (e != hipSuccess) return fail_hip(e);
+  st.last_stream = s;
+  st.has_last = true;
+  return SOFTMAX_OK;
+}
+
+int check_pointers(const float* x, const float* y, int64_t n_elems, int* dev) {
+  const int64_t bytes = n_elems * 4;
+  if (x == nullptr || y == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+  if (partial_overlap(x, y, bytes)) return SOFTMAX_ERR_INVALID_ARG;
+  hipError_t e = hipGetDevice(dev);
+  if (e != hipSuccess) return fail_hip(e);
+  int rc = check_device_range(x, bytes, *dev);
+  if (rc != SOFTMAX_OK) return rc;
+  if (y != x) rc = check_device_range(y, bytes, *dev);
+  return rc;
+}
+
+}  // namespace
+
+extern "C" {
+
+SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64_t cols,
+                             softmax_plan_t* plan) {
+  if (plan == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+  const int rc = check_sizes(rows, cols);
+  if (rc != SOFTMAX_OK) return rc;
+  if (rows > 0 && cols > 0) {
+    if (x == nullptr || y == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+    if (partial_overlap(x, y, rows * cols * 4)) return SOFTMAX_ERR_INVALID_ARG;
+  }
+  *plan = make_plan(x, y, rows, cols);
+  return SOFTMAX_OK;
+}
+
+SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols,
+                            hipStream_t stream) {
+  int rc = check_sizes(rows, cols);
+  if (rc != SOFTMAX_OK) return rc;
+  if (rows == 0 || cols == 0) return SOFTMAX_OK;
+  int dev = 0;
+  rc = check_pointers(x, y, rows * cols, &dev);
+  if (rc != SOFTMAX_OK) return rc;
+
+  const softmax_plan_t p = make_plan(x, y, rows, cols);
+  hipError_t e = hipSuccess;
+  switch (p.kernel) {
+    case SOFTMAX_KERNEL_PACKED:
+      e = p.vec_width == 4 ? dispatch_packed<true>(p, x, y, rows, cols, stream)
+                           : dispatch_packed<false>(p, x, y, rows, cols, stream);
+      break;
+    case SOFTMAX_KERNEL_WAVE_ROW:
+      e = p.vec_width == 4 ? dispatch_wave<true>(p, x, y, rows, cols, stream)
+                           : dispatch_wave<false>(p, x, y, rows, cols, stream);
+      break;
+    case SOFTMAX_KERNEL_BLOCK_ROW:
+      e = p.vec_width == 4 ? dispatch_block<true>(p, x, y, rows, cols, stream)
+                           : dispatch_block<false>(p, x, y, rows, cols, stream);
+      break;
+    case SOFTMAX_KERNEL_SPLIT_ROW:
+      return split_call(p, x, y, rows, cols, dev, stream);
+    default:
+      return SOFTMAX_OK;
+  }
+  if (e != hipSuccess) return fail_hip(e);
+  return SOFTMAX_OK;
+}
+
+SOFTMAX_API const char* softmax_strerror(int code) {
+  switch (code) {
+    case SOFTMAX_OK: return "success";
+    case SOFTMAX_ERR_INVALID_ARG:
+      return "invalid argument (negative or overflowing size, null pointer, "
+             "or partially overlapping x and y)";
+    case SOFTMAX_ERR_HIP: return "HIP call or kernel launch failed";
+    case SOFTMAX_ERR_NOT_DEVICE:
+      return "pointer is not memory the current device can use, or the range "
+             "runs past its allocation";
+    default: return "unknown softmax error code";
+  }
+}
+
+SOFTMAX_API int softmax_last_hip_error(void) { return tl_last_hip_error; }
+
+SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int64_t n,
+                                  hipStream_t stream) {
+  if (n < 0 || n > INT64_MAX / 4) return SOFTMAX_ERR_INVALID_ARG;
+  if (n == 0) return SOFTMAX_OK;
+  if (x == nullptr || m == nullptr || e == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+  if (any_overlap(e, x, n * 4) || any_overlap(e, m, n * 4)) return SOFTMAX_ERR_INVALID_ARG;
+  int dev = 0;
+  hipError_t he = hipGetDevice(&dev);
+  if (he != hipSuccess) return fail_hip(he);
+  int rc = check_device_range(x, n * 4, dev);
+  if (rc == SOFTMAX_OK) rc = check_device_range(m, n * 4, dev);
+  if (rc == SOFTMAX_OK) rc = check_device_range(e, n * 4, dev);
+  if (rc != SOFTMAX_OK) return rc;
+  const int64_t grid = std::min(ceil_div(n, 256), kMaxGrid);
+  void* args[] = {&x, &m, &e, &n};
+  he = launch(reinterpret_cast<const void*>(&k_exp_probe), grid, 256, args, stream);
+  return he == hipSuccess ? SOFTMAX_OK : fail_hip(he);
+}
+
+SOFTMAX_API int softmax_copy_probe(const float* x, float* y, int64_t n, hipStream_t stream) {
+  if (n < 0 || n > INT64_MAX / 4) return SOFTMAX_ERR_INVALID_ARG;
+  if (n == 0) return SOFTMAX_OK;
+  if (x == nullptr || y == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+  if (any_overlap(x, y, n * 4)) return SOFTMAX_ERR_INVALID_ARG;
+  int dev = 0;
+  hipError_t he = hipGetDevice(&dev);
+  if (he != hipSuccess) return fail_hip(he);
+  int rc = check_device_range(x, n * 4, dev);
+  if (rc == SOFTMAX_OK) rc = check_device_range(y, n * 4, dev);
+  if (rc != SOFTMAX_OK) return rc;
+  if (aligned16(x) && aligned16(y) && n % 4 == 0) {
+    const float4* x4 = reinterpret_cast<const float4*>(x);
+    float4* y4 = reinterpret_cast<float4*>(y);
+    int64_t n4 = n / 4;
+    const int64_t grid = std::min(ceil_div(n4, 256 * kCopyUnroll), kMaxGrid);
+    void* args[] = {&x4, &y4, &n4};
+    he = launch(reinterpret_cast<const void*>(&k_copy4), grid, 256, args, stream);
+  } else {
+    const int64_t grid = std::min(ceil_div(n, 256), kMaxGrid);
+    void* args[] = {&x, &y, &n};
+    he = launch(reinterpret_cast<const void*>(&k_copy1), grid, 256, args, stream);
+  }
+  return he == hipSuccess ? SOFTMAX_OK : fail_hip(he);
+}
+
+}  // extern "C"

@@ -1,0 +1,141 @@
+"""C ABI checks that need no GPU: the library loads, exports every entry
+point the header declares, reports its dispatch plan, and rejects bad
+arguments before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1904_12380_amd as sm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADERS = [os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))
+           if f.endswith(".h")]
+
+
+def declared_functions():
+    names = []
+    for h in HEADERS:
+        text = open(h).read()
+        names += re.findall(r"SOFTMAX_API\s+[\w\s\*]+?\b(\w+)\s*\(", text)
+    return names
+
+
+def test_header_declares_entry_points():
+    names = declared_functions()
+    for n in ("softmax_fwd", "softmax_strerror", "softmax_last_hip_error", "softmax_plan",
+              "softmax_exp_probe", "softmax_copy_probe"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = sm.load_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_only_declared_symbols_are_exported():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", sm.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines()
+                if line.split()[1:2] == ["T"]}
+    assert exported == set(declared_functions())
+
+
+def test_strerror_codes():
+    for code in range(4):
+        assert sm.softmax_strerror(code)
+    assert "unknown" in sm.softmax_strerror(99)
+    assert sm.softmax_last_hip_error() == 0
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    monkeypatch.setattr(sm, "_lib", None)
+    monkeypatch.setattr(sm, "LIB_PATH", os.path.join(ROOT, "no_such_lib.so"))
+    with pytest.raises(ImportError):
+        sm.load_library()
+
+
+def test_cpu_tensor_is_rejected():
+    torch = pytest.importorskip("torch")
+    with pytest.raises(ValueError):
+        sm.softmax_fwd(torch.zeros(4, 5))
+
+
+@pytest.mark.parametrize("rows,cols,kernel,vec,extra", [
+    (64, 1000, "wave_row", 4, dict(elems_per_lane=16)),
+    (115200, 50, "packed", 4, dict(lanes_per_row=16, grid=1800)),
+    (4096, 1000, "wave_row", 4, dict(grid=1024)),
+    (512, 32768, "block_row", 4, dict(elems_per_lane=32, grid=512)),
+    (64, 262144, "split_row", 4, dict(chunks_per_row=16, launches=2, grid=1024)),
+    (3, 1, "packed", 4, dict(lanes_per_row=1)),
+    (3, 65, "wave_row", 1, dict(elems_per_lane=4)),
+    (3, 4096, "wave_row", 4, dict(elems_per_lane=64)),
+    (3, 4097, "block_row", 1, dict(elems_per_lane=8)),
+    (3, 32769, "split_row", 1, dict(chunks_per_row=3)),
+    (0, 5, "none", 0, {}),
+    (5, 0, "none", 0, {}),
+])
+def test_plan_buckets(rows, cols, kernel, vec, extra):
+    p = sm.softmax_plan(rows, cols)
+    assert p["kernel_name"] == kernel
+    assert p["vec_width"] == vec
+    for k, v in extra.items():
+        assert p[k] == v, (k, p)
+
+
+def test_plan_vector_width_follows_alignment():
+    a, b = 1 << 40, 1 << 41
+    assert sm.softmax_plan(10, 1000, a, b)["vec_width"] == 4
+    assert sm.softmax_plan(10, 1000, a + 4, b)["vec_width"] == 1
+    assert sm.softmax_plan(10, 50, a, b + 8)["vec_width"] == 1
+    assert sm.softmax_plan(10, 50, a, b)["vec_width"] == 4
+    assert sm.softmax_plan(10, 1002, a, b)["vec_width"] == 1
+    assert sm.softmax_plan(10, 1000, a, a)["vec_width"] == 4     # in place
+
+
+def test_plan_split_batches_rows_to_fit_workspace():
+    p = sm.softmax_plan(10000, 262144)
+    pairs = p["workspace_bytes"] // 8
+    per_batch = pairs // p["chunks_per_row"]
+    assert p["launches"] == 2 * -(-10000 // per_batch)
+    assert p["grid"] == per_batch * p["chunks_per_row"]
+
+
+def _raw_fwd(x, y, rows, cols):
+    return sm.softmax_fwd_ptr(x, y, rows, cols, 0)
+
+
+def test_invalid_arguments_rejected_before_any_hip_call():
+    # Every call below returns from the size/pointer checks, which run before
+    # the library makes any HIP call, so no GPU is needed.
+    assert _raw_fwd(0x1000, 0x2000000, -1, 5) == sm.ERR_INVALID_ARG
+    assert _raw_fwd(0x1000, 0x2000000, 5, -1) == sm.ERR_INVALID_ARG
+    assert _raw_fwd(0x1000, 0x2000000, 2**40, 2**30) == sm.ERR_INVALID_ARG
+    assert _raw_fwd(0, 0x2000000, 5, 5) == sm.ERR_INVALID_ARG
+    assert _raw_fwd(0x1000, 0, 5, 5) == sm.ERR_INVALID_ARG
+    # partial overlap (4 bytes apart, 100 bytes long)
+    assert _raw_fwd(0x1000, 0x1004, 5, 5) == sm.ERR_INVALID_ARG
+    # empty inputs succeed without touching the GPU, even with null pointers
+    assert _raw_fwd(0, 0, 0, 5) == sm.OK
+    assert _raw_fwd(0, 0, 7, 0) == sm.OK
+
+
+def test_plan_rejects_bad_arguments():
+    with pytest.raises(sm.SoftmaxError):
+        sm.softmax_plan(-1, 3)
+    with pytest.raises(sm.SoftmaxError):
+        sm.softmax_plan(3, 3, 0x1000, 0x1008)
+    lib = sm.load_library()
+    assert lib.softmax_plan(None, None, 2, 2, None) == sm.ERR_INVALID_ARG
+
+
+def test_probes_reject_bad_arguments():
+    lib = sm.load_library()
+    assert lib.softmax_copy_probe(0x1000, 0x1000, 16, None) == sm.ERR_INVALID_ARG
+    assert lib.softmax_copy_probe(0x1000, 0x2000, -1, None) == sm.ERR_INVALID_ARG
+    assert lib.softmax_copy_probe(None, 0x2000, 4, None) == sm.ERR_INVALID_ARG
+    assert lib.softmax_exp_probe(0x1000, 0x8000, 0x1004, 16, None) == sm.ERR_INVALID_ARG
+    assert lib.softmax_exp_probe(0x1000, 0x8000, 0x10000, 0, None) == sm.OK

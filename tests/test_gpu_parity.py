@@ -1,0 +1,295 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Bar (per element, per row): max |y - y_ref| / y_ref <= 4e-6 and
+|sum_j y_ij - 1| <= 1e-5, with y_ref from ``oracle.softmax_clipped`` on the
+same seeded fp32 input.  Special rows (uniform, NaN, inf) are checked
+exactly against the oracle's reading.
+"""
+import ctypes
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_1904_12380_amd as sm
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+REL_TOL = 4e-6
+SUM_TOL = 1e-5
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dev():
+    return _torch().device("cuda:0")
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_gpu(x: np.ndarray) -> np.ndarray:
+    torch = _torch()
+    xt = torch.from_numpy(np.ascontiguousarray(x)).to(_dev())
+    yt = sm.softmax_fwd(xt)
+    torch.cuda.synchronize()
+    return yt.cpu().numpy()
+
+
+def check_parity(x: np.ndarray, y: np.ndarray, what: str):
+    want = oracle.softmax_clipped(x)
+    y64 = y.astype(np.float64)
+    finite = np.isfinite(want)
+    assert np.array_equal(np.isnan(y64), np.isnan(want)), what
+    rel = np.abs(y64[finite] - want[finite]) / want[finite]
+    worst = float(rel.max()) if rel.size else 0.0
+    if worst > REL_TOL:
+        idx = np.unravel_index(np.argmax(np.where(finite, np.abs(y64 - want) / np.where(finite, want, 1), 0)), y.shape)
+        pytest.fail(f"{what}: max rel err {worst:.3e} at {idx}: got {y64[idx]!r}, "
+                    f"want {want[idx]!r}, x={x[idx]!r}, rowmax={x[idx[0]].max()!r}")
+    rows_ok = np.all(finite, axis=1)
+    if rows_ok.any():
+        sums = np.abs(y64[rows_ok].sum(axis=1) - 1.0)
+        assert float(sums.max()) <= SUM_TOL, (what, float(sums.max()))
+    return worst
+
+
+@pytest.mark.parametrize("key", list(workloads.WORKLOADS))
+def test_workload_parity(key):
+    log(f"[parity] workload {key}")
+    x = workloads.generate(key)
+    y = run_gpu(x)
+    worst = check_parity(x, y, key)
+    log(f"[parity] {key}: max rel err {worst:.3e}")
+
+
+EDGE_COLS = [1, 2, 3, 4, 5, 7, 8, 15, 16, 17, 31, 32, 33, 49, 50, 51, 63, 64, 65, 100, 127,
+             128, 129, 255, 256, 257, 1000, 1001, 1023, 1024, 1025, 2048, 4095, 4096, 4097,
+             8191, 8192, 16384, 32767, 32768, 32769, 65536, 65537, 100003]
+EDGE_ROWS = [1, 2, 3, 5, 63, 64, 65, 1000]
+
+
+@pytest.mark.parametrize("cols", EDGE_COLS)
+def test_edge_shapes(cols):
+    log(f"[parity] edge cols={cols}")
+    for rows in EDGE_ROWS:
+        if rows * cols > 4_000_000:
+            continue
+        for kind in ("normal", "clip_heavy"):
+            x = workloads.random_logits(rows, cols, seed=rows * 7919 + cols, kind=kind)
+            check_parity(x, run_gpu(x), f"{rows}x{cols} {kind}")
+
+
+@pytest.mark.parametrize("rows,cols", [(257, 50), (64, 1000), (33, 1001), (5, 8192), (3, 100003),
+                                       (131, 7)])
+def test_misaligned_views(rows, cols):
+    """x and y start 4 bytes past a 16-byte boundary: the 32-bit paths."""
+    torch = _torch()
+    log(f"[parity] misaligned {rows}x{cols}")
+    x = workloads.random_logits(rows, cols, seed=cols, kind="offset")
+    n = rows * cols
+    xb = torch.empty(n + 4, dtype=torch.float32, device=_dev())
+    yb = torch.empty(n + 4, dtype=torch.float32, device=_dev())
+    xb[1:n + 1] = torch.from_numpy(x.reshape(-1)).to(_dev())
+    xv = xb[1:n + 1].view(rows, cols)
+    yv = yb[1:n + 1].view(rows, cols)
+    assert xv.data_ptr() % 16 == 4
+    p = sm.softmax_plan(rows, cols, xv.data_ptr(), yv.data_ptr())
+    assert p["vec_width"] == 1
+    sm.softmax_fwd(xv, out=yv)
+    torch.cuda.synchronize()
+    check_parity(x, yv.cpu().numpy(), f"misaligned {rows}x{cols}")
+
+
+@pytest.mark.parametrize("rows,cols", [(115200, 50), (64, 1000), (512, 32768), (64, 262144),
+                                       (7, 3)])
+def test_in_place(rows, cols):
+    torch = _torch()
+    log(f"[parity] in-place {rows}x{cols}")
+    x = workloads.random_logits(rows, cols, seed=3, kind="normal")
+    xt = torch.from_numpy(x).to(_dev())
+    out = sm.softmax_fwd(xt, out=xt)
+    assert out.data_ptr() == xt.data_ptr()
+    torch.cuda.synchronize()
+    check_parity(x, xt.cpu().numpy(), f"in-place {rows}x{cols}")
+
+
+def test_non_default_stream_and_determinism():
+    torch = _torch()
+    log("[parity] side stream + determinism")
+    for key in ("dam_attention_115200x50", "vocab_512x32768", "longrow_64x262144"):
+        x = workloads.generate(key)
+        xt = torch.from_numpy(x).to(_dev())
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            y1 = sm.softmax_fwd(xt)
+            y2 = sm.softmax_fwd(xt)
+        s.synchronize()
+        y3 = sm.softmax_fwd(xt)
+        torch.cuda.synchronize()
+        a, b, c = y1.cpu().numpy(), y2.cpu().numpy(), y3.cpu().numpy()
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), key
+        assert np.array_equal(a.view(np.uint32), c.view(np.uint32)), key
+        check_parity(x, a, key)
+
+
+@pytest.mark.parametrize("cols", [1, 3, 50, 64, 1000, 4096, 32768, 262144])
+def test_uniform_rows_are_exactly_one_over_n(cols):
+    """Equal logits: exp gives exactly 1, the sum exactly N, and the output
+    must be the fp32 division 1/N (bitwise)."""
+    log(f"[parity] uniform cols={cols}")
+    rows = max(1, min(64, 2_000_000 // cols))
+    x = np.full((rows, cols), -3.75, dtype=np.float32)
+    x[::2] = 12.5
+    y = run_gpu(x)
+    want = np.float32(1.0) / np.float32(cols)
+    assert np.all(y == want), (cols, np.unique(y)[:5], want)
+
+
+def test_clip_rows():
+    """Rows where the clip is active, including values straddling -64."""
+    log("[parity] clip rows")
+    base = [
+        [0.0, -100.0, -64.0, -63.5, -1.0e4],
+        [10.0, -54.0, -53.999996185302734, -54.000003814697266, 9.0],
+        [-3.0, -70.0, -2.0, -66.5, -67.0, -65.99999237060547],
+    ]
+    for row in base:
+        for cols in (len(row), 50, 1000, 40000):
+            x = np.full((4, cols), -500.0, dtype=np.float32)
+            x[:, :len(row)] = np.asarray(row, dtype=np.float32)
+            check_parity(x, run_gpu(x), f"clip row {row[:2]} cols={cols}")
+            e64 = np.exp(-64.0)
+            assert np.all(run_gpu(x) >= np.float32(e64 / cols * (1 - 1e-5)))
+
+
+@pytest.mark.parametrize("cols", [5, 50, 1000, 8192, 70000])
+def test_nonfinite_rows(cols):
+    log(f"[parity] non-finite cols={cols}")
+    x = workloads.random_logits(6, cols, seed=cols, kind="normal")
+    x[0, cols // 2] = np.nan
+    x[1, cols - 1] = np.inf
+    x[2, :] = -np.inf
+    x[3, 0] = -np.inf
+    x[4, :] = -np.inf
+    x[4, cols // 3] = 1.0
+    y = run_gpu(x)
+    want = oracle.softmax_clipped(x)
+    assert np.all(np.isnan(y[0])) and np.all(np.isnan(y[1])) and np.all(np.isnan(y[2]))
+    check_parity(x[3:], y[3:], f"non-finite finite rows cols={cols}")
+    assert np.allclose(y[4].astype(np.float64), want[4], rtol=REL_TOL, atol=0)
+
+
+@pytest.mark.parametrize("rows,cols", [(257, 50), (65, 1000), (3, 8192), (2, 262144)])
+def test_guard_bands_untouched(rows, cols):
+    """Sentinels before and after y survive the call."""
+    torch = _torch()
+    log(f"[parity] guard bands {rows}x{cols}")
+    pad = 1024
+    n = rows * cols
+    x = workloads.random_logits(rows, cols, seed=11, kind="normal")
+    xt = torch.from_numpy(x).to(_dev())
+    yb = torch.full((n + 2 * pad,), 12345.0, dtype=torch.float32, device=_dev())
+    yv = yb[pad:pad + n].view(rows, cols)
+    sm.softmax_fwd(xt, out=yv)
+    torch.cuda.synchronize()
+    yb_h = yb.cpu().numpy()
+    assert np.all(yb_h[:pad] == 12345.0) and np.all(yb_h[pad + n:] == 12345.0)
+    check_parity(x, yv.cpu().numpy(), f"guard {rows}x{cols}")
+
+
+def test_empty_inputs_launch_nothing():
+    torch = _torch()
+    for shape in ((0, 50), (5, 0)):
+        xt = torch.empty(shape, dtype=torch.float32, device=_dev())
+        assert sm.softmax_fwd(xt).shape == shape
+
+
+def test_exp_probe_error_bound():
+    """The kernels' clipped exp against float64 exp over the whole clipped
+    domain, with x and m drawn so that x - m is not exact in fp32."""
+    torch = _torch()
+    log("[parity] exp probe")
+    rng = np.random.default_rng(99)
+    n = 1 << 22
+    m = rng.uniform(-60.0, 60.0, n).astype(np.float32)
+    d = np.concatenate([rng.uniform(-70.0, 0.0, n - 4096),
+                        rng.uniform(-64.001, -63.999, 4096)])
+    x = (m.astype(np.float64) + d).astype(np.float32)
+    e = sm.softmax_exp_probe(torch.from_numpy(x).to(_dev()),
+                             torch.from_numpy(m).to(_dev())).cpu().numpy()
+    want = oracle.exp_clipped(x.astype(np.float64) - m.astype(np.float64))
+    rel = np.abs(e.astype(np.float64) - want) / want
+    worst = float(rel.max())
+    log(f"[parity] exp probe max rel err {worst:.3e} ({worst / 2**-24:.2f} half-ulps)")
+    assert worst <= 4.0 * 2.0**-24   # 2 ulp
+
+
+def test_copy_probe():
+    torch = _torch()
+    x = torch.randn(1 << 20, device=_dev())
+    assert torch.equal(sm.softmax_copy_probe(x), x)
+    xo = x[1:]
+    assert torch.equal(sm.softmax_copy_probe(xo), xo)
+
+
+def _hip():
+    lib = ctypes.CDLL("libamdhip64.so")
+    lib.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
+    lib.hipFree.argtypes = [ctypes.c_void_p]
+    lib.hipMemGetAddressRange.argtypes = [ctypes.POINTER(ctypes.c_void_p),
+                                          ctypes.POINTER(ctypes.c_size_t), ctypes.c_void_p]
+    return lib
+
+
+def test_range_past_allocation_is_rejected():
+    """A byte range that ends 16 bytes past a hipMalloc allocation is refused
+    before launch.  The overrun is inside the allocation's page, so the check
+    is exercised without any access outside mapped memory."""
+    torch = _torch()
+    torch.cuda.init()
+    hip = _hip()
+    nbytes = 1 << 20
+    p = ctypes.c_void_p()
+    assert hip.hipMalloc(ctypes.byref(p), nbytes) == 0
+    try:
+        base, size = ctypes.c_void_p(), ctypes.c_size_t()
+        assert hip.hipMemGetAddressRange(ctypes.byref(base), ctypes.byref(size), p) == 0
+        if size.value != nbytes:
+            pytest.skip(f"allocation reported as {size.value} bytes")
+        xp = p.value + 16
+        # rows*cols*4 == nbytes: ends 16 bytes past the allocation
+        rc = sm.softmax_fwd_ptr(xp, xp, 1, nbytes // 4, 0)
+        assert rc == sm.ERR_NOT_DEVICE
+        assert sm.softmax_fwd_ptr(p.value, p.value, 1, nbytes // 4, 0) == sm.OK
+        torch.cuda.synchronize()
+    finally:
+        hip.hipFree(p)
+
+
+def test_host_pointer_is_rejected():
+    """Unregistered host memory is refused before launch.  The test first
+    confirms through HIP itself that the pointer is unregistered."""
+    torch = _torch()
+    torch.cuda.init()
+    hip = ctypes.CDLL("libamdhip64.so")
+    buf = np.zeros(4096, dtype=np.float32)
+
+    class Attr(ctypes.Structure):
+        _fields_ = [("type", ctypes.c_int), ("device", ctypes.c_int),
+                    ("devicePointer", ctypes.c_void_p), ("hostPointer", ctypes.c_void_p),
+                    ("isManaged", ctypes.c_int), ("allocationFlags", ctypes.c_uint)]
+    a = Attr()
+    hip.hipPointerGetAttributes.argtypes = [ctypes.POINTER(Attr), ctypes.c_void_p]
+    rc = hip.hipPointerGetAttributes(ctypes.byref(a), buf.ctypes.data)
+    hip.hipGetLastError()
+    if rc == 0 and a.type != 0:
+        pytest.skip(f"HIP reports host memory type {a.type}")
+    assert sm.softmax_fwd_ptr(buf.ctypes.data, buf.ctypes.data, 64, 64, 0) == sm.ERR_NOT_DEVICE
