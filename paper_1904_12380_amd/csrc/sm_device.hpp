@@ -1,10 +1,11 @@
 // Device primitives for the clipped row softmax on CDNA4 (gfx950, wave64).
 //
-//   * exp_shift_clip(): e = exp(max(x - M, -64)) with the shift carried as an
-//     exact double-float and the exp argument in extended precision, so the
-//     result is within about 1.5 ulp of the true value over the whole clipped
-//     range (the clip is the ValueClip of the paper's reference functor,
-//     Sec. 1.2 Fig. 1; the bound -64 is this library's documented choice).
+//   * exp_shift_clip(): e = exp(max(x - M, -64)) with the shift and the exp
+//     argument in binary64 (full rate on gfx950) and v_exp_f32 on the fp32
+//     part, so the result is within 1.5 ulp of the exact value over the
+//     whole clipped range (the clip is the ValueClip of the paper's
+//     reference functor, Sec. 1.2 Fig. 1; the bound -64 is this library's
+//     documented choice).
 //   * seg_max / seg_sum: reductions over aligned groups of W lanes using DPP
 //     (quad_perm, row_half_mirror, row_mirror) inside a 16-lane row and the
 //     gfx950 permlane16/permlane32 swaps across rows.  These play the part of
@@ -12,8 +13,8 @@
 //     on a 64-lane wavefront.  Every lane of a group ends with the same bits.
 //
 // Floating-point contraction is off for this whole library (-ffp-contract=off
-// on the command line and the pragma below): the two-sum below is only exact
-// if the compiler keeps every rounding step as written.
+// on the command line and the pragma below), so every rounding step of the
+// exp argument happens exactly as written.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -25,43 +26,72 @@ namespace smx {
 
 // Lower bound applied to the shifted logit x - max before exp.
 constexpr float kClipLo = -64.0f;
+// RN(e^-64): the value of every clipped exponential.
+constexpr float kExpClipLo = 0x1.969d48p-93f;  // 1.6038109e-28
 
-// log2(e) split into fp32 parts: hi = RN(log2 e), lo = RN(log2 e - hi).
-constexpr float kLog2eHi = 0x1.715476p+0f;   // 1.44269502162933349609375
-constexpr float kLog2eLo = 0x1.4ae0c0p-26f;  // 1.925963033500011e-08
-// RN(ln 2): only scales the tiny low-order part of the exponent.
-constexpr float kLn2 = 0x1.62e430p-1f;
+// RN(log2 e) and RN(ln 2) in binary64.
+constexpr double kLog2e = 0x1.71547652b82fep+0;
+constexpr double kLn2 = 0x1.62e42fefa39efp-1;
 
-__device__ __forceinline__ float fma_(float a, float b, float c) {
-  return __builtin_fmaf(a, b, c);
+// Native 4 x fp32 vector: loads and stores of it are single 128-bit
+// accesses (global_load_dwordx4 / global_store_dwordx4).
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Streaming 128-bit load and store: x is read once and y written once, so
+// both use the nontemporal cache policy.
+__device__ __forceinline__ f32x4 ld_stream(const float* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+}
+__device__ __forceinline__ void st_stream(float* p, f32x4 v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(p));
 }
 
-// exp(max(x + neg_m, kClipLo)) where neg_m = -(row max).
+// Per-row constants of the shifted, clipped exponential.
+//   neg_m: -M in binary64.
+//   tc:    the smallest fp32 value >= M - 64 (computed exactly), so that for
+//          every fp32 x:  x < tc  <=>  x - M < -64.  The clip test is then one
+//          fp32 compare per element.  M = NaN gives tc = NaN (no element is
+//          clipped and NaN propagates); M = -inf gives tc = -inf.
+struct RowShift {
+  double neg_m;
+  float tc;
+};
+
+__device__ __forceinline__ RowShift row_shift(float m) {
+  RowShift r;
+  r.neg_m = -static_cast<double>(m);
+  // M - 64 is exact in binary64 unless |M| < 2^-23, where the rounding is
+  // below 2^-47 and only moves the boundary by that much.
+  const double s = static_cast<double>(m) - 64.0;
+  float f = static_cast<float>(s);
+  if (static_cast<double>(f) < s) {
+    // next fp32 towards +inf (f < s <= M - 64 <= f + ulp, f finite)
+    const unsigned u = __builtin_bit_cast(unsigned, f);
+    f = __builtin_bit_cast(float, f < 0.0f ? u - 1u : (f == 0.0f ? 1u : u + 1u));
+  }
+  r.tc = f;
+  return r;
+}
+
+// exp(max(x - M, -64)) for fp32 x, within 1.5 ulp of the exact value.
 //
-// 1. Knuth's two-sum gives d = x + neg_m exactly as dh + dl (|dl| <= ulp/2).
-// 2. The clip is decided on the exact d: d < L  <=>  dh < L or (dh == L and
-//    dl < 0), because L = -64 is an fp32 value and rounding is monotonic.
-//    A compare-select (not an IEEE max) keeps NaN as NaN; d = -inf clips.
-// 3. t = c * log2(e) as th + tl: th = RN(ch * hi); tl gathers the product's
-//    rounding error (one fma, exact), ch * lo and cl * hi.
-// 4. e = 2^th * 2^tl ~= v_exp_f32(th) * (1 + tl * ln2); |tl| <= 4e-6, so the
-//    dropped quadratic term is below 1e-11 relative.
-// Domain after the clip: th in [-92.33, 0], so 2^th is a normal fp32 and
-// v_exp_f32 needs no denormal scaling.
-__device__ __forceinline__ float exp_shift_clip(float x, float neg_m) {
-  const float dh = x + neg_m;
-  const float xv = dh - neg_m;
-  const float mv = dh - xv;
-  const float dl = (x - xv) + (neg_m - mv);
-  const bool clip = (dh < kClipLo) || ((dh == kClipLo) && (dl < 0.0f));
-  const float ch = clip ? kClipLo : dh;
-  const float cl = clip ? 0.0f : dl;
-  const float th = ch * kLog2eHi;
-  float tl = fma_(ch, kLog2eHi, -th);
-  tl = fma_(ch, kLog2eLo, tl);
-  tl = fma_(cl, kLog2eHi, tl);
+// 1. d = x - M in binary64: exact whenever the exponents of x and M differ by
+//    at most 29; otherwise its relative error is below 2^-53.
+// 2. t = d * log2(e) in binary64, th = RN32(t), and the remainder
+//    r = d - th * ln2 from one binary64 fma (|r| <= 2^-18 * ln2 = 2.6e-6).
+// 3. e = 2^th * e^r = v_exp_f32(th) * (1 + r), rounded once by an fp32 fma;
+//    the dropped r^2/2 is below 4e-12.  For unclipped x, th is in
+//    [-92.34, 0], where 2^th is a normal fp32.
+// 4. Clipped elements (x < tc) return RN(e^-64) exactly; this also covers
+//    x = -inf.  NaN inputs, and rows whose max is +inf or -inf, give NaN.
+__device__ __forceinline__ float exp_shift_clip(float x, RowShift rs) {
+  const double d = static_cast<double>(x) + rs.neg_m;
+  const double t = d * kLog2e;
+  const float th = static_cast<float>(t);
+  const double r = __builtin_fma(static_cast<double>(th), -kLn2, d);
   const float e0 = __builtin_amdgcn_exp2f(th);
-  return fma_(e0, tl * kLn2, e0);
+  const float e = __builtin_fmaf(e0, static_cast<float>(r), e0);
+  return x < rs.tc ? kExpClipLo : e;
 }
 
 // ---------------------------------------------------------------------------

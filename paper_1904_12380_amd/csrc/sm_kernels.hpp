@@ -61,7 +61,9 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 // Loads N = 4*V elements of one row (or chunk) into registers: element i of
 // this lane sits at column base + lane_off + stride*i (scalar) or, for
 // 128-bit loads, at base + 4*(lane_off + stride*j) + k with i = 4j + k.
-// Columns at or past `limit` read as -inf.
+// Columns at or past `limit` read as -inf: they take part in the max as a
+// neutral value and their clipped exponential (e^-64) changes a row sum of at
+// least 1 by under 1e-24 relative, so no per-element mask is needed later.
 template <int V, bool VEC4>
 __device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* row,
                                            int64_t base, int64_t lane_off,
@@ -70,45 +72,38 @@ __device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* row,
 #pragma unroll
     for (int j = 0; j < V; ++j) {
       const int64_t c = base + 4 * (lane_off + stride * j);
-      if (c < limit) {
-        const float4 q = *reinterpret_cast<const float4*>(row + c);
-        v[4 * j + 0] = q.x;
-        v[4 * j + 1] = q.y;
-        v[4 * j + 2] = q.z;
-        v[4 * j + 3] = q.w;
+      f32x4 q;
+      // Strip j covers columns [base + 4*stride*j, base + 4*stride*(j+1)):
+      // when all of it is inside the row (a uniform test) no lane needs a mask.
+      if (base + 4 * stride * (j + 1) <= limit) {
+        q = ld_stream(row + c);
       } else {
-        v[4 * j + 0] = v[4 * j + 1] = v[4 * j + 2] = v[4 * j + 3] = kNegInf;
+        q = f32x4{kNegInf, kNegInf, kNegInf, kNegInf};
+        if (c < limit) q = ld_stream(row + c);
       }
+      v[4 * j + 0] = q.x;
+      v[4 * j + 1] = q.y;
+      v[4 * j + 2] = q.z;
+      v[4 * j + 3] = q.w;
     }
   } else {
 #pragma unroll
     for (int i = 0; i < 4 * V; ++i) {
       const int64_t c = base + lane_off + stride * i;
-      v[i] = (c < limit) ? row[c] : kNegInf;
+      if (base + stride * (i + 1) <= limit)
+        v[i] = __builtin_nontemporal_load(row + c);
+      else
+        v[i] = (c < limit) ? __builtin_nontemporal_load(row + c) : kNegInf;
     }
   }
 }
 
-template <int V, bool VEC4>
-__device__ __forceinline__ bool strip_valid(int i, int64_t base, int64_t lane_off,
-                                            int64_t stride, int64_t limit) {
-  if constexpr (VEC4)
-    return base + 4 * (lane_off + stride * (i >> 2)) < limit;
-  else
-    return base + lane_off + stride * i < limit;
-}
-
-// Replaces v by the clipped exponentials (0 for columns past `limit`) and
-// returns this lane's pairwise partial sum.
-template <int V, bool VEC4>
-__device__ __forceinline__ float exp_strip(float (&v)[4 * V], float neg_m, int64_t base,
-                                           int64_t lane_off, int64_t stride,
-                                           int64_t limit) {
+// Replaces v by the clipped exponentials and returns this lane's pairwise
+// partial sum.
+template <int N>
+__device__ __forceinline__ float exp_strip(float (&v)[N], RowShift rs) {
 #pragma unroll
-  for (int i = 0; i < 4 * V; ++i)
-    v[i] = strip_valid<V, VEC4>(i, base, lane_off, stride, limit)
-               ? exp_shift_clip(v[i], neg_m)
-               : 0.0f;
+  for (int i = 0; i < N; ++i) v[i] = exp_shift_clip(v[i], rs);
   return tree_sum(v);
 }
 
@@ -120,84 +115,106 @@ __device__ __forceinline__ void store_strip(const float (&v)[4 * V], float scale
 #pragma unroll
     for (int j = 0; j < V; ++j) {
       const int64_t c = base + 4 * (lane_off + stride * j);
-      if (c < limit) {
-        float4 q;
-        q.x = v[4 * j + 0] * scale;
-        q.y = v[4 * j + 1] * scale;
-        q.z = v[4 * j + 2] * scale;
-        q.w = v[4 * j + 3] * scale;
-        *reinterpret_cast<float4*>(row + c) = q;
-      }
+      f32x4 q;
+      q.x = v[4 * j + 0] * scale;
+      q.y = v[4 * j + 1] * scale;
+      q.z = v[4 * j + 2] * scale;
+      q.w = v[4 * j + 3] * scale;
+      if (base + 4 * stride * (j + 1) <= limit || c < limit) st_stream(row + c, q);
     }
   } else {
 #pragma unroll
     for (int i = 0; i < 4 * V; ++i) {
       const int64_t c = base + lane_off + stride * i;
-      if (c < limit) row[c] = v[i] * scale;
+      if (base + stride * (i + 1) <= limit || c < limit)
+        __builtin_nontemporal_store(v[i] * scale, row + c);
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// (a) Packed rows, cols <= G*EPL with G lanes per row.
+// (a) Packed rows, cols <= 16*G, with G lanes per row (G = 1, 2, 4, ...).
 //
-// A 256-thread workgroup owns tiles of TILE = 4 * (256/G) consecutive rows.
-// TILE is a multiple of 4, so a tile starts on a 16-byte boundary whenever
-// x and y do, whatever cols is (cols = 50 gives 200-byte rows).
-template <int G, int EPL, bool VEC4>
+// A 256-thread workgroup owns tiles of kRows = 256/G consecutive rows: one
+// row per group of G lanes, so a tile is done in one pass.  kRows is a
+// multiple of 4, so a tile starts on a 16-byte boundary whenever x and y
+// do, whatever cols is (cols = 50 gives 200-byte rows).  The tile moves
+// HBM -> LDS -> HBM with 128-bit accesses; lane j of a row group handles
+// columns j, j+G, ..., j+(epl-1)G with epl = ceil(cols/G) <= 16.
+template <int G, bool VEC4>
 __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_t rows,
-                                                int64_t cols) {
-  constexpr int kRowsPerPass = 256 / G;
-  constexpr int kPasses = 4;
-  constexpr int kTile = kRowsPerPass * kPasses;
-  __shared__ float tile[kTile * G * EPL];
+                                                int64_t cols, int epl) {
+  constexpr int kRows = 256 / G;
+  constexpr int kMaxEpl = 16;
+  constexpr int kTileFloats = kRows * G * kMaxEpl;  // = 4096
+  __shared__ float tile[kTileFloats];
 
   const int tid = threadIdx.x;
   const int ccols = static_cast<int>(cols);
-  const int64_t ntiles = (rows + kTile - 1) / kTile;
+  const int64_t ntiles = (rows + kRows - 1) / kRows;
+  const int r = tid / G;
   const int j = tid % G;
 
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    const int64_t row0 = t * kTile;
-    const int nr = static_cast<int>(rows - row0 < kTile ? rows - row0 : kTile);
+    const int64_t row0 = t * kRows;
+    const int nr = static_cast<int>(rows - row0 < kRows ? rows - row0 : kRows);
     const int n = nr * ccols;
     const float* xs = x + row0 * cols;
     float* ys = y + row0 * cols;
 
+    // Every load of the tile is issued before the first LDS write.
     if constexpr (VEC4) {
+      constexpr int kVecPerThread = kTileFloats / 4 / 256;
       const int n4 = n >> 2;
-      for (int i = tid; i < n4; i += 256)
-        reinterpret_cast<float4*>(tile)[i] = reinterpret_cast<const float4*>(xs)[i];
+      f32x4 q[kVecPerThread];
+#pragma unroll
+      for (int u = 0; u < kVecPerThread; ++u) {
+        const int i = tid + 256 * u;
+        q[u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (i < n4) q[u] = ld_stream(xs + 4 * i);
+      }
+#pragma unroll
+      for (int u = 0; u < kVecPerThread; ++u) {
+        const int i = tid + 256 * u;
+        if (i < n4) *reinterpret_cast<f32x4*>(tile + 4 * i) = q[u];
+      }
       for (int i = (n4 << 2) + tid; i < n; i += 256) tile[i] = xs[i];
     } else {
-      for (int i = tid; i < n; i += 256) tile[i] = xs[i];
+      constexpr int kPerThread = kTileFloats / 256;
+      float q[kPerThread];
+#pragma unroll
+      for (int u = 0; u < kPerThread; ++u) {
+        const int i = tid + 256 * u;
+        q[u] = 0.0f;
+        if (i < n) q[u] = __builtin_nontemporal_load(xs + i);
+      }
+#pragma unroll
+      for (int u = 0; u < kPerThread; ++u) {
+        const int i = tid + 256 * u;
+        if (i < n) tile[i] = q[u];
+      }
     }
     __syncthreads();
 
-#pragma unroll
-    for (int p = 0; p < kPasses; ++p) {
-      const int r = p * kRowsPerPass + tid / G;
+    {
       const bool active = r < nr;
       float* tr = tile + r * ccols;
-      float v[EPL];
+      float v[kMaxEpl];
 #pragma unroll
-      for (int k = 0; k < EPL; ++k) {
+      for (int k = 0; k < kMaxEpl; ++k) {
         const int c = j + G * k;
-        v[k] = (active && c < ccols) ? tr[c] : kNegInf;
+        v[k] = (k < epl && active && c < ccols) ? tr[c] : kNegInf;
       }
       const float m = seg_max<G>(array_max(v));
-      const float neg_m = -m;
+      const RowShift rs = row_shift(m);
 #pragma unroll
-      for (int k = 0; k < EPL; ++k) {
-        const int c = j + G * k;
-        v[k] = (active && c < ccols) ? exp_shift_clip(v[k], neg_m) : 0.0f;
-      }
+      for (int k = 0; k < kMaxEpl; ++k) v[k] = (k < epl) ? exp_shift_clip(v[k], rs) : 0.0f;
       const float s = seg_sum<G>(tree_sum(v));
       const float rcp = 1.0f / s;
 #pragma unroll
-      for (int k = 0; k < EPL; ++k) {
+      for (int k = 0; k < kMaxEpl; ++k) {
         const int c = j + G * k;
-        if (active && c < ccols) tr[c] = v[k] * rcp;
+        if (k < epl && active && c < ccols) tr[c] = v[k] * rcp;
       }
     }
     __syncthreads();
@@ -205,17 +222,17 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
     if constexpr (VEC4) {
       const int n4 = n >> 2;
       for (int i = tid; i < n4; i += 256)
-        reinterpret_cast<float4*>(ys)[i] = reinterpret_cast<const float4*>(tile)[i];
+        st_stream(ys + 4 * i, *reinterpret_cast<const f32x4*>(tile + 4 * i));
       for (int i = (n4 << 2) + tid; i < n; i += 256) ys[i] = tile[i];
     } else {
-      for (int i = tid; i < n; i += 256) ys[i] = tile[i];
+      for (int i = tid; i < n; i += 256) __builtin_nontemporal_store(tile[i], ys + i);
     }
     __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
-// (b) One wavefront per row, cols <= 256*V (VEC4) or 256*V scalar elements.
+// (b) One wavefront per row, cols <= 256*V (4*V elements per lane).
 // Four wavefronts per workgroup work on four rows independently.
 template <int V, bool VEC4>
 __global__ __launch_bounds__(256) void k_wave_row(const float* x, float* y, int64_t rows,
@@ -228,9 +245,8 @@ __global__ __launch_bounds__(256) void k_wave_row(const float* x, float* y, int6
     float* yr = y + row * cols;
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, 0, lane, 64, cols);
-    const float m = seg_max<64>(array_max(v));
-    const float neg_m = -m;
-    const float s = seg_sum<64>(exp_strip<V, VEC4>(v, neg_m, 0, lane, 64, cols));
+    const RowShift rs = row_shift(seg_max<64>(array_max(v)));
+    const float s = seg_sum<64>(exp_strip(v, rs));
     const float rcp = 1.0f / s;
     store_strip<V, VEC4>(v, rcp, yr, 0, lane, 64, cols);
   }
@@ -250,9 +266,8 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int6
     float* yr = y + row * cols;
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, 0, tid, NT, cols);
-    const float m = block_max<NW>(array_max(v), red_max);
-    const float neg_m = -m;
-    const float s = block_sum<NW>(exp_strip<V, VEC4>(v, neg_m, 0, tid, NT, cols), red_sum);
+    const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max));
+    const float s = block_sum<NW>(exp_strip(v, rs), red_sum);
     const float rcp = 1.0f / s;
     store_strip<V, VEC4>(v, rcp, yr, 0, tid, NT, cols);
   }
@@ -292,8 +307,8 @@ __global__ __launch_bounds__(NT) void k_split_stats(const float* x, float2* part
     load_strip<V, VEC4>(v, xr, c0, tid, NT, cols);
     const float m = block_max<NW>(array_max(v), red_max);
     const bool empty_max = (m == kNegInf);
-    const float neg_m = empty_max ? 0.0f : -m;
-    float s = block_sum<NW>(exp_strip<V, VEC4>(v, neg_m, c0, tid, NT, cols), red_sum);
+    const RowShift rs = row_shift(empty_max ? 0.0f : m);
+    float s = block_sum<NW>(exp_strip(v, rs), red_sum);
     if (empty_max) {
       const int64_t left = cols - c0;
       s = static_cast<float>(left < CH ? left : CH);
@@ -322,17 +337,16 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
     const float2* pr = part + row * chunks;
     float mm = kNegInf;
     for (int64_t l = lane; l < chunks; l += 64) mm = fmaxf(mm, pr[l].x);
-    const float neg_big_m = -seg_max<64>(mm);
+    const RowShift rs = row_shift(seg_max<64>(mm));
     float ss = 0.0f;
     for (int64_t l = lane; l < chunks; l += 64) {
       const float2 p = pr[l];
-      ss = ss + p.y * exp_shift_clip(p.x, neg_big_m);
+      ss = ss + p.y * exp_shift_clip(p.x, rs);
     }
     const float rcp = 1.0f / seg_sum<64>(ss);
 
 #pragma unroll
-    for (int i = 0; i < 4 * V; ++i)
-      v[i] = exp_shift_clip(v[i], neg_big_m);
+    for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip(v[i], rs);
     store_strip<V, VEC4>(v, rcp, yr, c0, tid, NT, cols);
   }
 }
@@ -346,27 +360,27 @@ __global__ __launch_bounds__(256) void k_exp_probe(const float* x, const float* 
                                                    float* e, int64_t n) {
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
        i += static_cast<int64_t>(gridDim.x) * 256)
-    e[i] = exp_shift_clip(x[i], -m[i]);
+    e[i] = exp_shift_clip(x[i], row_shift(m[i]));
 }
 
-// Plain copy with 128-bit accesses: the memory-bound ceiling that the paper
-// compares softmax against (Sec. 2.6), for the same bytes moved.
+// Plain copy with 128-bit streaming accesses: the memory-bound ceiling that
+// the paper compares softmax against (Sec. 2.6), for the same bytes moved.
 constexpr int kCopyUnroll = 4;
-__global__ __launch_bounds__(256) void k_copy4(const float4* x, float4* y, int64_t n4) {
+__global__ __launch_bounds__(256) void k_copy4(const float* x, float* y, int64_t n4) {
   const int64_t step = static_cast<int64_t>(gridDim.x) * 256 * kCopyUnroll;
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 * kCopyUnroll + threadIdx.x;
-       i < n4; i += step) {
-    float4 t[kCopyUnroll];
+  int64_t i = static_cast<int64_t>(blockIdx.x) * 256 * kCopyUnroll + threadIdx.x;
+  // Full groups: all loads in flight before the stores, no per-element guard.
+  for (; i + (kCopyUnroll - 1) * 256 < n4; i += step) {
+    f32x4 t[kCopyUnroll];
 #pragma unroll
-    for (int u = 0; u < kCopyUnroll; ++u) {
-      const int64_t k = i + u * 256;
-      if (k < n4) t[u] = x[k];
-    }
+    for (int u = 0; u < kCopyUnroll; ++u) t[u] = ld_stream(x + 4 * (i + u * 256));
 #pragma unroll
-    for (int u = 0; u < kCopyUnroll; ++u) {
-      const int64_t k = i + u * 256;
-      if (k < n4) y[k] = t[u];
-    }
+    for (int u = 0; u < kCopyUnroll; ++u) st_stream(y + 4 * (i + u * 256), t[u]);
+  }
+  // The last, partial group of this thread.
+  for (int u = 0; u < kCopyUnroll; ++u) {
+    const int64_t k = i + u * 256;
+    if (k < n4) st_stream(y + 4 * k, ld_stream(x + 4 * k));
   }
 }
 

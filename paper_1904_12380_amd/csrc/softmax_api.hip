@@ -121,13 +121,14 @@ softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t c
   const bool a16 = aligned16(x) && aligned16(y);
   const bool vec_rows = a16 && (cols % 4 == 0);
   if (cols <= kPackedMaxCols) {
-    const int64_t g = cols <= 4 ? 1 : cols <= 8 ? 2 : cols <= 16 ? 4 : cols <= 32 ? 8 : 16;
+    // G lanes per row with at most 16 columns per lane.
+    const int64_t g = cols <= 16 ? 1 : cols <= 32 ? 2 : 4;
     p.kernel = SOFTMAX_KERNEL_PACKED;
     p.vec_width = a16 ? 4 : 1;
     p.lanes_per_row = static_cast<int32_t>(g);
-    p.elems_per_lane = 4;
+    p.elems_per_lane = static_cast<int32_t>(ceil_div(cols, g));
     p.block_threads = 256;
-    const int64_t tile = 4 * (256 / g);
+    const int64_t tile = 256 / g;
     p.grid = std::min(ceil_div(rows, tile), kMaxGrid);
     p.launches = 1;
   } else if (cols <= kWaveRowMaxCols) {
@@ -170,21 +171,20 @@ hipError_t launch(const void* fn, int64_t grid, int block, void** args, hipStrea
 }
 
 template <int G, bool VEC4>
-hipError_t run_packed(const float* x, float* y, int64_t rows, int64_t cols, int64_t grid,
-                      hipStream_t s) {
-  void* args[] = {&x, &y, &rows, &cols};
-  return launch(reinterpret_cast<const void*>(&k_packed<G, 4, VEC4>), grid, 256, args, s);
+hipError_t run_packed(const float* x, float* y, int64_t rows, int64_t cols, int epl,
+                      int64_t grid, hipStream_t s) {
+  void* args[] = {&x, &y, &rows, &cols, &epl};
+  return launch(reinterpret_cast<const void*>(&k_packed<G, VEC4>), grid, 256, args, s);
 }
 
 template <bool VEC4>
 hipError_t dispatch_packed(const softmax_plan_t& p, const float* x, float* y,
                            int64_t rows, int64_t cols, hipStream_t s) {
+  const int epl = p.elems_per_lane;
   switch (p.lanes_per_row) {
-    case 1: return run_packed<1, VEC4>(x, y, rows, cols, p.grid, s);
-    case 2: return run_packed<2, VEC4>(x, y, rows, cols, p.grid, s);
-    case 4: return run_packed<4, VEC4>(x, y, rows, cols, p.grid, s);
-    case 8: return run_packed<8, VEC4>(x, y, rows, cols, p.grid, s);
-    default: return run_packed<16, VEC4>(x, y, rows, cols, p.grid, s);
+    case 1: return run_packed<1, VEC4>(x, y, rows, cols, epl, p.grid, s);
+    case 2: return run_packed<2, VEC4>(x, y, rows, cols, epl, p.grid, s);
+    default: return run_packed<4, VEC4>(x, y, rows, cols, epl, p.grid, s);
   }
 }
 
@@ -256,7 +256,13 @@ int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
   std::lock_guard<std::mutex> lock(g_mu);
   DeviceState& st = g_dev[dev];
   hipError_t e;
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  e = hipStreamIsCapturing(s, &cap);
+  if (e != hipSuccess) return fail_hip(e);
+  const bool capturing = (cap != hipStreamCaptureStatusNone);
   if (st.ws == nullptr) {
+    // First use on this device must not be inside a stream capture.
+    if (capturing) return SOFTMAX_ERR_INVALID_ARG;
     void* mem = nullptr;
     e = hipMalloc(&mem, kWorkspaceBytes);
     if (e != hipSuccess) return fail_hip(e);
@@ -264,17 +270,22 @@ int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
     e = hipEventCreateWithFlags(&st.last, hipEventDisableTiming);
     if (e != hipSuccess) return fail_hip(e);
   }
-  if (st.has_last && st.last_stream != s) {
+  // Under stream capture the graph's own order applies: the captured kernels
+  // run in sequence on the capturing stream, and graphs that use split rows
+  // must not be replayed concurrently on one device.
+  if (!capturing && st.has_last && st.last_stream != s) {
     e = hipStreamWaitEvent(s, st.last, 0);
     if (e != hipSuccess) return fail_hip(e);
   }
   e = p.vec_width == 4 ? run_split<true>(x, y, st.ws, rows, cols, p.chunks_per_row, s)
                        : run_split<false>(x, y, st.ws, rows, cols, p.chunks_per_row, s);
   if (e != hipSuccess) return fail_hip(e);
-  e = hipEventRecord(st.last, s);
-  if (e != hipSuccess) return fail_hip(e);
-  st.last_stream = s;
-  st.has_last = true;
+  if (!capturing) {
+    e = hipEventRecord(st.last, s);
+    if (e != hipSuccess) return fail_hip(e);
+    st.last_stream = s;
+    st.has_last = true;
+  }
   return SOFTMAX_OK;
 }
 
@@ -387,11 +398,9 @@ SOFTMAX_API int softmax_copy_probe(const float* x, float* y, int64_t n, hipStrea
   if (rc == SOFTMAX_OK) rc = check_device_range(y, n * 4, dev);
   if (rc != SOFTMAX_OK) return rc;
   if (aligned16(x) && aligned16(y) && n % 4 == 0) {
-    const float4* x4 = reinterpret_cast<const float4*>(x);
-    float4* y4 = reinterpret_cast<float4*>(y);
     int64_t n4 = n / 4;
     const int64_t grid = std::min(ceil_div(n4, 256 * kCopyUnroll), kMaxGrid);
-    void* args[] = {&x4, &y4, &n4};
+    void* args[] = {&x, &y, &n4};
     he = launch(reinterpret_cast<const void*>(&k_copy4), grid, 256, args, stream);
   } else {
     const int64_t grid = std::min(ceil_div(n, 256), kMaxGrid);

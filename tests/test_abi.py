@@ -66,11 +66,14 @@ def test_cpu_tensor_is_rejected():
 
 @pytest.mark.parametrize("rows,cols,kernel,vec,extra", [
     (64, 1000, "wave_row", 4, dict(elems_per_lane=16)),
-    (115200, 50, "packed", 4, dict(lanes_per_row=16, grid=1800)),
+    (115200, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13, grid=1800)),
     (4096, 1000, "wave_row", 4, dict(grid=1024)),
     (512, 32768, "block_row", 4, dict(elems_per_lane=32, grid=512)),
     (64, 262144, "split_row", 4, dict(chunks_per_row=16, launches=2, grid=1024)),
-    (3, 1, "packed", 4, dict(lanes_per_row=1)),
+    (3, 1, "packed", 4, dict(lanes_per_row=1, elems_per_lane=1)),
+    (300, 16, "packed", 4, dict(lanes_per_row=1, elems_per_lane=16, grid=2)),
+    (300, 17, "packed", 4, dict(lanes_per_row=2, elems_per_lane=9, grid=3)),
+    (300, 64, "packed", 4, dict(lanes_per_row=4, elems_per_lane=16, grid=5)),
     (3, 65, "wave_row", 1, dict(elems_per_lane=4)),
     (3, 4096, "wave_row", 4, dict(elems_per_lane=64)),
     (3, 4097, "block_row", 1, dict(elems_per_lane=8)),
