@@ -7,20 +7,36 @@ A step is one softmax_fwd call (every stage of the path: load, row max,
 shift, clip, exp, row sum, reciprocal scale, store) over the whole workload
 matrix.  Inputs sit in HBM before the timed region starts.  Each step uses a
 different (x, y) pair out of a rotation set of at least 1 GiB, so no step
-finds its input in the 256 MB last-level (MALL) cache left warm by the
-previous steps; every x_k holds the same seeded matrix.
+finds its input in the 256 MB last-level (MALL) cache left warm by earlier
+steps; every x_k holds the same seeded matrix.
 
-Timing: W untimed steps, then exactly K steps between two synchronisations,
-measured with HIP events recorded on the stream the kernels run on.  The
-roofline object uses the algorithmic traffic of one call (8 bytes per
-element: one fp32 read of x, one fp32 write of y) divided by the average
-step time.  ``cpu_baseline`` times the float64 oracle on the host, and
+Timing: the K steps are captured once into a HIP graph (torch.cuda.CUDAGraph)
+and the graph is replayed: W untimed steps, then exactly K steps between two
+synchronisations, timed with HIP events recorded on the stream the kernels
+run on.  The graph removes host launch overhead (about 3 us per call through
+the C ABI); the same steps launched one by one from Python are reported as
+``eager``.  The roofline object uses the algorithmic traffic of one call
+(8 bytes per element: one fp32 read of x, one fp32 write of y) divided by the
+average step time.  ``cpu_baseline`` times the float64 oracle on the host,
 ``cpu_fp32_baseline`` a plain single-thread fp32 C loop.
+
+Counter passes (FETCH_SIZE, WRITE_SIZE) use two extra modes:
+
+    rocprofv3 --pmc FETCH_SIZE -d DIR/fetch -o run -- python3 bench.py --pmc-run --workload KEY
+    rocprofv3 --pmc WRITE_SIZE -d DIR/write -o run -- python3 bench.py --pmc-run --workload KEY
+    python3 bench.py --summarize-pmc DIR --workload KEY
+
+The summary (profiles/pmc_KEY.json and .md) scales each counter by what it
+reads for the library's copy kernel on the same number of bytes; ``traffic``
+in the JSON line comes from it only while the kernel sources are unchanged.
 """
 from __future__ import annotations
 
 import argparse
+import csv
 import ctypes
+import glob
+import hashlib
 import json
 import math
 import os
@@ -40,6 +56,8 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, 8 TB/s
 ROTATE_BYTES = 1 << 30          # >= 4x the 256 MB MALL
 METRIC = "softmax rows/s and achieved HBM GB/s (% of MI355X peak), fp32, 1 GPU"
 DEFAULT_WORKLOAD = "dam_attention_115200x50"
+CSRC = os.path.join(ROOT, "paper_1904_12380_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def log(msg: str) -> None:
@@ -57,76 +75,116 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, warmup: int,
-             check: bool = True) -> dict:
-    dev = torch.device("cuda:0")
-    pair_bytes = 8 * w.elements
-    nbuf = max(2, math.ceil(ROTATE_BYTES / pair_bytes))
-    xs, ys = [], []
-    x0 = torch.from_numpy(x_host).to(dev)
-    for _ in range(nbuf):
-        xs.append(x0.clone())
-        ys.append(torch.empty_like(x0))
-    del x0
-    stream = torch.cuda.current_stream()
-    plan = sm.softmax_plan(w.rows, w.cols, xs[0].data_ptr(), ys[0].data_ptr())
+def kernel_source_sha256() -> str:
+    """Hash of the HIP sources: counter summaries are tied to it."""
+    h = hashlib.sha256()
+    for path in sorted(glob.glob(os.path.join(CSRC, "*"))):
+        if path.endswith((".hip", ".hpp", ".h")):
+            h.update(os.path.basename(path).encode())
+            with open(path, "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
 
+
+class Rotation:
+    """K (x, y) pairs of the workload resident in HBM, at least 1 GiB."""
+
+    def __init__(self, torch, x_host: np.ndarray):
+        dev = torch.device("cuda:0")
+        pair_bytes = 8 * x_host.size
+        self.n = max(2, math.ceil(ROTATE_BYTES / pair_bytes))
+        x0 = torch.from_numpy(x_host).to(dev)
+        self.xs = [x0.clone() for _ in range(self.n)]
+        self.ys = [torch.empty_like(x0) for _ in range(self.n)]
+
+    def pair(self, i):
+        return self.xs[i % self.n], self.ys[i % self.n]
+
+
+def time_steps(torch, launch, steps: int, warmup: int) -> tuple[float, float]:
+    """Capture `steps` calls of launch(i, stream) into one graph; replay it
+    once untimed (after `warmup` eager calls), then time one replay.
+    Returns (graph ms per step, eager ms per step)."""
+    stream = torch.cuda.current_stream()
     for i in range(warmup):
-        sm.softmax_fwd(xs[i % nbuf], out=ys[i % nbuf], stream=stream)
+        launch(i, stream)
     torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
+    # eager: one call per step from Python
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
     start.record(stream)
     for i in range(steps):
-        sm.softmax_fwd(xs[i % nbuf], out=ys[i % nbuf], stream=stream)
+        launch(i, stream)
     stop.record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gpu_ms = start.elapsed_time(stop)
+    eager_ms = start.elapsed_time(stop) / steps
+    # graph: the same steps captured once
+    g = torch.cuda.CUDAGraph()
+    cs = torch.cuda.Stream()
+    cs.wait_stream(stream)
+    with torch.cuda.graph(g, stream=cs):
+        for i in range(steps):
+            launch(i, cs)
+    torch.cuda.synchronize()
+    g.replay()                      # warm replay
+    torch.cuda.synchronize()
+    start.record(stream)
+    g.replay()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    graph_ms = start.elapsed_time(stop) / steps
+    del g
+    return graph_ms, eager_ms
 
-    # Copy ceiling over the same bytes and the same rotation (Sec. 2.6's
-    # memcpy comparison, on the GPU).
-    for i in range(min(warmup, nbuf)):
-        sm.softmax_copy_probe(xs[i % nbuf], out=ys[i % nbuf], stream=stream)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(steps):
-        sm.softmax_copy_probe(xs[i % nbuf], out=ys[i % nbuf], stream=stream)
-    stop.record(stream)
-    torch.cuda.synchronize()
-    copy_ms = start.elapsed_time(stop)
+
+def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, warmup: int,
+             check: bool = True) -> dict:
+    rot = Rotation(torch, x_host)
+    plan = sm.softmax_plan(w.rows, w.cols, rot.xs[0].data_ptr(), rot.ys[0].data_ptr())
+
+    def fwd(i, s):
+        x, y = rot.pair(i)
+        sm.softmax_fwd(x, out=y, stream=s)
+
+    def cpy(i, s):
+        x, y = rot.pair(i)
+        sm.softmax_copy_probe(x, out=y, stream=s)
+
+    ms, eager_ms = time_steps(torch, fwd, steps, warmup)
+    copy_ms, _ = time_steps(torch, cpy, steps, warmup)
 
     max_rel = None
     if check:
         # Re-run once on pair 0 and check sampled rows against the oracle.
         import oracle
-        sm.softmax_fwd(xs[0], out=ys[0], stream=stream)
+        x0, y0 = rot.pair(0)
+        sm.softmax_fwd(x0, out=y0)
         torch.cuda.synchronize()
         rng = np.random.default_rng(0)
         rows = np.unique(rng.integers(0, w.rows, size=min(w.rows, 64)))
-        y = ys[0][torch.from_numpy(rows).to(dev)].cpu().numpy().astype(np.float64)
+        dev = y0.device
+        y = y0[torch.from_numpy(rows).to(dev)].cpu().numpy().astype(np.float64)
         want = oracle.softmax_clipped(x_host[rows])
         max_rel = float(np.max(np.abs(y - want) / want))
         if max_rel > 4e-6:
             raise SystemExit(f"bench output failed parity on {w.key}: {max_rel:.3e}")
-    del xs, ys
+    nbuf = rot.n
+    del rot
     torch.cuda.empty_cache()
 
-    ms = gpu_ms / steps
     gbps = w.algorithmic_bytes / (ms * 1e-3) / 1e9
-    copy_step_ms = copy_ms / steps
     return {
         "ms_per_step": ms,
         "rows_per_s": w.rows / (ms * 1e-3),
         "elements_per_s": w.elements / (ms * 1e-3),
         "hbm_gbps": gbps,
         "frac_of_peak": gbps / HBM_PEAK_GBPS,
-        "copy_ms_per_step": copy_step_ms,
-        "copy_gbps": w.algorithmic_bytes / (copy_step_ms * 1e-3) / 1e9,
-        "softmax_over_copy_time": ms / copy_step_ms,
-        "host_wall_ms_per_step": wall * 1e3 / steps,
+        "eager_ms_per_step": eager_ms,
+        "eager_hbm_gbps": w.algorithmic_bytes / (eager_ms * 1e-3) / 1e9,
+        "copy_ms_per_step": copy_ms,
+        "copy_gbps": w.algorithmic_bytes / (copy_ms * 1e-3) / 1e9,
+        "softmax_over_copy_time": ms / copy_ms,
         "rotation_buffers": nbuf,
         "plan": plan,
         "sampled_max_rel_err": max_rel,
@@ -135,7 +193,7 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
 
 def time_cpu_oracle(x: np.ndarray, budget_s: float) -> dict:
     """float64 oracle (numpy, one thread) on whole passes over the matrix,
-    repeated until `budget_s` of CPU time is spent."""
+    repeated until `budget_s` of wall time is spent."""
     import oracle
     passes, t0 = 0, time.perf_counter()
     while True:
@@ -173,6 +231,162 @@ def time_cpu_fp32(x: np.ndarray, budget_s: float) -> dict | None:
             "gbps": 8 * x.size / per / 1e9}
 
 
+def pmc_summary_path(key: str, ext: str) -> str:
+    return os.path.join(PROFILES, f"pmc_{key}.{ext}")
+
+
+def load_traffic(key: str) -> tuple[float | None, str | None]:
+    """HBM bytes per launch from the committed counter summary, or None when
+    there is none or the kernel sources changed since it was taken."""
+    path = pmc_summary_path(key, "json")
+    if not os.path.exists(path):
+        return None, None
+    with open(path) as f:
+        doc = json.load(f)
+    if doc.get("source_sha256") != kernel_source_sha256():
+        return None, "kernel changed since the counters were taken"
+    return doc["traffic_bytes_per_launch"], None
+
+
+def pmc_run(sm, torch, w: workloads.Workload, launches: int) -> None:
+    """Launches for a counter pass: `launches` softmax calls on the rotation,
+    then as many copy-kernel calls over the same bytes."""
+    rot = Rotation(torch, workloads.generate(w.key))
+    for i in range(launches):
+        x, y = rot.pair(i)
+        sm.softmax_fwd(x, out=y)
+    torch.cuda.synchronize()
+    for i in range(launches):
+        x, y = rot.pair(i)
+        sm.softmax_copy_probe(x, out=y)
+    torch.cuda.synchronize()
+    print(json.dumps({"pmc_run": w.key, "launches": launches}), flush=True)
+
+
+def _counter_rows(directory: str):
+    """(kernel name, counter name, value per dispatch) from a rocprofv3 pass:
+    counter_collection.csv (--output-format csv) or the rocpd database."""
+    files = glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)
+    for path in files:
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                yield r["Kernel_Name"], r["Counter_Name"], float(r["Counter_Value"])
+    if files:
+        return
+    dbs = glob.glob(os.path.join(directory, "**", "*.db"), recursive=True)
+    if not dbs:
+        raise SystemExit(f"no counter output under {directory}")
+    import sqlite3
+    for path in dbs:
+        con = sqlite3.connect(path)
+        try:
+            for name, cname, val in con.execute(
+                    "select kernel_name, counter_name, value from counters_collection"):
+                yield name, cname, float(val)
+        finally:
+            con.close()
+
+
+def summarize_pmc(directory: str, w: workloads.Workload, command: str) -> dict:
+    """Average FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the softmax
+    kernel and of the copy kernel, scaled by the copy kernel's reading for
+    its known byte count (4 * elements read, 4 * elements written)."""
+    per = {}
+    for sub in ("fetch", "write"):
+        for name, cname, val in _counter_rows(os.path.join(directory, sub)):
+            key = "copy" if "k_copy" in name else ("softmax" if "smx::k_" in name else None)
+            if key is None:
+                continue
+            per.setdefault((key, cname, name), []).append(val)
+    agg = {}
+    for (key, cname, name), vals in per.items():
+        agg.setdefault(key, {})[cname] = float(np.median(vals))
+        agg[key].setdefault("kernels", set()).add(name.split("(")[0])
+    bytes_each_way = 4.0 * w.elements
+    scale_fetch = bytes_each_way / (agg["copy"]["FETCH_SIZE"] * 1024.0)
+    scale_write = bytes_each_way / (agg["copy"]["WRITE_SIZE"] * 1024.0)
+    fetch_b = agg["softmax"]["FETCH_SIZE"] * 1024.0 * scale_fetch
+    write_b = agg["softmax"]["WRITE_SIZE"] * 1024.0 * scale_write
+    doc = {
+        "workload": w.key,
+        "softmax_kernels": sorted(agg["softmax"]["kernels"]),
+        "source_sha256": kernel_source_sha256(),
+        "softmax_fetch_kib_per_dispatch": agg["softmax"]["FETCH_SIZE"],
+        "softmax_write_kib_per_dispatch": agg["softmax"]["WRITE_SIZE"],
+        "copy_fetch_kib_per_dispatch": agg["copy"]["FETCH_SIZE"],
+        "copy_write_kib_per_dispatch": agg["copy"]["WRITE_SIZE"],
+        "copy_bytes_each_way": bytes_each_way,
+        "scale_fetch": scale_fetch,
+        "scale_write": scale_write,
+        "traffic_fetch_bytes_per_launch": fetch_b,
+        "traffic_write_bytes_per_launch": write_b,
+        "traffic_bytes_per_launch": fetch_b + write_b,
+        "algorithmic_bytes_per_launch": float(w.algorithmic_bytes),
+        "traffic_over_algorithmic": (fetch_b + write_b) / w.algorithmic_bytes,
+        "command": command,
+    }
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(pmc_summary_path(w.key, "json"), "w") as f:
+        json.dump(doc, f, indent=1)
+        f.write("\n")
+    with open(pmc_summary_path(w.key, "md"), "w") as f:
+        f.write(f"# HBM traffic counters: {', '.join(doc['softmax_kernels'])} on {w.key}\n\n")
+        f.write("Commands (from the repository root on the GPU machine):\n\n```\n"
+                f"{command}\n```\n\n")
+        f.write("| quantity | softmax kernel | copy kernel (same bytes) |\n|---|---|---|\n")
+        f.write(f"| FETCH_SIZE KiB/dispatch (median) | {doc['softmax_fetch_kib_per_dispatch']:.1f} | "
+                f"{doc['copy_fetch_kib_per_dispatch']:.1f} |\n")
+        f.write(f"| WRITE_SIZE KiB/dispatch (median) | {doc['softmax_write_kib_per_dispatch']:.1f} | "
+                f"{doc['copy_write_kib_per_dispatch']:.1f} |\n\n")
+        f.write(f"Copy kernel moves {bytes_each_way:.0f} bytes each way; scale factors "
+                f"fetch {scale_fetch:.4f}, write {scale_write:.4f}.\n\n")
+        f.write(f"Scaled traffic per launch: fetch {fetch_b:.0f} B + write {write_b:.0f} B = "
+                f"{fetch_b + write_b:.0f} B; algorithmic {w.algorithmic_bytes} B; ratio "
+                f"{doc['traffic_over_algorithmic']:.4f}.\n\n"
+                f"Kernel sources sha256: {doc['source_sha256']}\n")
+    return doc
+
+
+def summarize_trace(directory: str, w: workloads.Workload, command: str,
+                    bench_json: str | None) -> str:
+    """profiles/<kernel>_<workload>_trace.md from a rocprofv3 --kernel-trace
+    --stats run of this script: per-kernel call counts and durations, next
+    to the step times the same run printed."""
+    files = glob.glob(os.path.join(directory, "**", "*kernel_stats.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_stats.csv under {directory}")
+    with open(files[0]) as f:
+        rows = list(csv.DictReader(f))
+    ours = [r for r in rows if "smx::" in r["Name"]]
+    main_k = None
+    bench = None
+    if bench_json:
+        with open(bench_json) as f:
+            bench = json.loads(f.read().strip().splitlines()[-1])
+        kname = {"packed": "k_packed", "wave_row": "k_wave_row", "block_row": "k_block_row",
+                 "split_row": "k_split"}[bench["config"]["kernel"]]
+        main_k = kname
+    name = f"{main_k or 'kernels'}_{w.key}_trace.md"
+    path = os.path.join(PROFILES, name)
+    with open(path, "w") as f:
+        f.write(f"# Kernel trace: bench.py on {w.key} (and the other workloads it times)\n\n")
+        f.write(f"Command (repository root, GPU machine):\n\n```\n{command}\n```\n\n")
+        f.write("| kernel | calls | average us | min us | max us |\n|---|---|---|---|---|\n")
+        for r in ours + [r for r in rows if r not in ours]:
+            f.write(f"| `{r['Name'].split('(')[0]}` | {r['Calls']} | "
+                    f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                    f"{float(r['MaxNs']) / 1e3:.2f} |\n")
+        if bench:
+            f.write(f"\nThe same run's JSON line: {bench['config']['workload']} "
+                    f"{bench['ms_per_step'] * 1e3:.2f} us per step by HIP events "
+                    f"(graph replay); other workloads: ")
+            f.write(", ".join(f"{k} {v['ms_per_step'] * 1e3:.2f} us"
+                              for k, v in bench["other_workloads"].items()))
+            f.write(".  Kernel averages include the eager and the graph-replayed "
+                    "launches and the profiler's own per-dispatch overhead.\n")
+    return path
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -182,7 +396,25 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra-workloads", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--pmc-run", action="store_true",
+                    help="only launch the kernels for a rocprofv3 counter pass")
+    ap.add_argument("--pmc-launches", type=int, default=20)
+    ap.add_argument("--summarize-pmc", metavar="DIR",
+                    help="write profiles/pmc_<workload>.{json,md} from DIR/fetch and DIR/write")
+    ap.add_argument("--pmc-command", default="", help="commands recorded in the summary")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="write profiles/<kernel>_<workload>_trace.md from a kernel-trace run")
+    ap.add_argument("--trace-json", help="JSON line printed by the traced run")
     args = ap.parse_args()
+
+    w = workloads.WORKLOADS[args.workload]
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, w, args.pmc_command, args.trace_json))
+        return 0
+    if args.summarize_pmc:
+        doc = summarize_pmc(args.summarize_pmc, w, args.pmc_command)
+        print(json.dumps(doc), flush=True)
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the softmax rows are independent, so a "
@@ -198,10 +430,13 @@ def main() -> int:
         return 2
     sm.load_library()
 
-    w = workloads.WORKLOADS[args.workload]
+    if args.pmc_run:
+        pmc_run(sm, torch, w, args.pmc_launches)
+        return 0
+
     log(f"[bench] generating {w.key}")
     x = workloads.generate(w.key)
-    log(f"[bench] timing {w.key}: {args.warmup} warmup + {args.steps} steps")
+    log(f"[bench] timing {w.key}: {args.warmup} warmup + {args.steps} steps (graph replay)")
     main_res = time_gpu(sm, torch, w, x, args.steps, args.warmup)
     log(f"[bench] {w.key}: {main_res['ms_per_step'] * 1e3:.2f} us/step, "
         f"{main_res['hbm_gbps']:.0f} GB/s")
@@ -216,6 +451,7 @@ def main() -> int:
             extra[key] = {k: (round(v, 6) if isinstance(v, float) else v)
                           for k, v in r.items() if k != "plan"}
             extra[key]["kernel"] = r["plan"]["kernel_name"]
+            extra[key]["launches_per_step"] = r["plan"]["launches"]
             log(f"[bench] {key}: {r['ms_per_step'] * 1e3:.2f} us/step, {r['hbm_gbps']:.0f} GB/s")
 
     cpu = None
@@ -226,7 +462,9 @@ def main() -> int:
         log("[bench] CPU fp32 baseline")
         cpu32 = time_cpu_fp32(x, min(args.cpu_budget, 5.0))
 
+    traffic, traffic_note = load_traffic(w.key)
     ms = main_res["ms_per_step"]
+    plan = main_res["plan"]
     out = {
         "metric": METRIC,
         "value": main_res["rows_per_s"],
@@ -242,8 +480,9 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": w.key, "rows": w.rows, "cols": w.cols, "seed": w.seed,
                    "input_sha256": workloads.sha256_f32(x),
-                   "kernel": main_res["plan"]["kernel_name"],
-                   "rotation_buffers": main_res["rotation_buffers"]},
+                   "kernel": plan["kernel_name"], "launches_per_step": plan["launches"],
+                   "rotation_buffers": main_res["rotation_buffers"],
+                   "timing": "HIP graph of the timed steps, HIP events on its stream"},
         "elements_per_s": main_res["elements_per_s"],
         "hbm_gbps": main_res["hbm_gbps"],
         "roofline": {
@@ -252,11 +491,14 @@ def main() -> int:
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": main_res["frac_of_peak"],
-            "traffic": None,
+            "traffic": traffic,
+            "traffic_note": traffic_note,
             "algorithmic_bytes_per_launch": w.algorithmic_bytes,
-            "timing": "HIP events over the timed steps on the launch stream",
         },
+        "eager": {"ms_per_step": main_res["eager_ms_per_step"],
+                  "hbm_gbps": main_res["eager_hbm_gbps"]},
         "copy_ceiling": {"gbps": main_res["copy_gbps"],
+                         "ms_per_step": main_res["copy_ms_per_step"],
                          "softmax_over_copy_time": main_res["softmax_over_copy_time"]},
         "cpu_baseline": cpu,
         "cpu_fp32_baseline": cpu32,

@@ -52,8 +52,7 @@ extern "C" {
 #define SOFTMAX_KERNEL_PACKED 1    /* cols <= 64: several rows per wavefront */
 #define SOFTMAX_KERNEL_WAVE_ROW 2  /* cols <= 4096: one wavefront per row */
 #define SOFTMAX_KERNEL_BLOCK_ROW 3 /* cols <= 32768: one workgroup per row */
-#define SOFTMAX_KERNEL_SPLIT_ROW 4 /* longer rows: several workgroups per row,
-                                      two launches */
+#define SOFTMAX_KERNEL_SPLIT_ROW 4 /* longer rows: several workgroups per row */
 
 /*
  * softmax_fwd -- row-wise clipped softmax, fp32 in and out.
@@ -77,10 +76,22 @@ extern "C" {
  * Asynchrony: work is enqueued on `stream` and the call returns without
  * waiting; y is valid once the stream has reached that point.
  *
- * Workspace: rows longer than 32768 columns use a device workspace of 1 MiB
- * that the library allocates on first use per device and keeps until the
- * process ends.  Such calls on different streams of one device are ordered
- * by the library with an event, so they never race on it.
+ * Workspace: rows longer than 32768 columns use a 256 KiB device workspace
+ * that the library allocates (hipMalloc, zeroed) on the first such call on
+ * each (device, stream) and keeps until the process ends, so calls on
+ * different streams never share one.  Up to 64 streams per device get their
+ * own; past that the least recently used one is reassigned after a
+ * hipDeviceSynchronize().  Under stream capture no allocation is made: the
+ * capture uses one workspace per device, created by an earlier uncaptured
+ * long-row call on that device (otherwise SOFTMAX_ERR_INVALID_ARG), and
+ * replays of such graphs must not overlap other long-row work on the device.
+ *
+ * Long rows are done in one pass when a row spans at most 64 workgroups
+ * (cols <= 2097152): the workgroups of a row exchange partial (max, sum)
+ * pairs in the middle of the kernel and wait for each other.  Workgroups are
+ * dispatched in ID order, so this always progresses while 64 workgroups of
+ * the launch can be resident; the wait is bounded, and a workgroup that
+ * times out writes NaN instead of stalling.  Longer rows use two passes.
  *
  * Returns SOFTMAX_OK, or SOFTMAX_ERR_INVALID_ARG (rows or cols < 0,
  * rows*cols*4 overflows int64, x or y null while rows*cols > 0, partial

@@ -58,28 +58,29 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return tree_sum(t);
 }
 
-// Loads N = 4*V elements of one row (or chunk) into registers: element i of
-// this lane sits at column base + lane_off + stride*i (scalar) or, for
-// 128-bit loads, at base + 4*(lane_off + stride*j) + k with i = 4j + k.
-// Columns at or past `limit` read as -inf: they take part in the max as a
-// neutral value and their clipped exponential (e^-64) changes a row sum of at
-// least 1 by under 1e-24 relative, so no per-element mask is needed later.
+// Loads N = 4*V elements of a row segment p[0, lim) into registers: element
+// i of this lane sits at p[lane_off + stride*i] (scalar) or, for 128-bit
+// loads, at p[4*(lane_off + stride*j) + k] with i = 4j + k.  Offsets are
+// 32-bit (a segment is at most 2^20 columns), so the address is one base
+// register plus a 32-bit lane offset.  Columns at or past `lim` read as
+// -inf: they take part in the max as a neutral value and their clipped
+// exponential (e^-64) changes a row sum of at least 1 by under 1e-24
+// relative, so no per-element mask is needed later.  Strip j covers
+// [4*stride*j, 4*stride*(j+1)); when all of it is inside the segment (a
+// uniform test) no lane is masked.
 template <int V, bool VEC4>
-__device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* row,
-                                           int64_t base, int64_t lane_off,
-                                           int64_t stride, int64_t limit) {
+__device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* p, int lane_off,
+                                           int stride, int lim) {
   if constexpr (VEC4) {
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-      const int64_t c = base + 4 * (lane_off + stride * j);
+      const int c = 4 * (lane_off + stride * j);
       f32x4 q;
-      // Strip j covers columns [base + 4*stride*j, base + 4*stride*(j+1)):
-      // when all of it is inside the row (a uniform test) no lane needs a mask.
-      if (base + 4 * stride * (j + 1) <= limit) {
-        q = ld_stream(row + c);
+      if (4 * stride * (j + 1) <= lim) {
+        q = ld_stream(p + c);
       } else {
         q = f32x4{kNegInf, kNegInf, kNegInf, kNegInf};
-        if (c < limit) q = ld_stream(row + c);
+        if (c < lim) q = ld_stream(p + c);
       }
       v[4 * j + 0] = q.x;
       v[4 * j + 1] = q.y;
@@ -89,11 +90,11 @@ __device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* row,
   } else {
 #pragma unroll
     for (int i = 0; i < 4 * V; ++i) {
-      const int64_t c = base + lane_off + stride * i;
-      if (base + stride * (i + 1) <= limit)
-        v[i] = __builtin_nontemporal_load(row + c);
+      const int c = lane_off + stride * i;
+      if (stride * (i + 1) <= lim)
+        v[i] = __builtin_nontemporal_load(p + c);
       else
-        v[i] = (c < limit) ? __builtin_nontemporal_load(row + c) : kNegInf;
+        v[i] = (c < lim) ? __builtin_nontemporal_load(p + c) : kNegInf;
     }
   }
 }
@@ -108,28 +109,32 @@ __device__ __forceinline__ float exp_strip(float (&v)[N], RowShift rs) {
 }
 
 template <int V, bool VEC4>
-__device__ __forceinline__ void store_strip(const float (&v)[4 * V], float scale,
-                                            float* row, int64_t base, int64_t lane_off,
-                                            int64_t stride, int64_t limit) {
+__device__ __forceinline__ void store_strip(const float (&v)[4 * V], float scale, float* p,
+                                            int lane_off, int stride, int lim) {
   if constexpr (VEC4) {
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-      const int64_t c = base + 4 * (lane_off + stride * j);
+      const int c = 4 * (lane_off + stride * j);
       f32x4 q;
       q.x = v[4 * j + 0] * scale;
       q.y = v[4 * j + 1] * scale;
       q.z = v[4 * j + 2] * scale;
       q.w = v[4 * j + 3] * scale;
-      if (base + 4 * stride * (j + 1) <= limit || c < limit) st_stream(row + c, q);
+      if (4 * stride * (j + 1) <= lim || c < lim) st_stream(p + c, q);
     }
   } else {
 #pragma unroll
     for (int i = 0; i < 4 * V; ++i) {
-      const int64_t c = base + lane_off + stride * i;
-      if (base + stride * (i + 1) <= limit || c < limit)
-        __builtin_nontemporal_store(v[i] * scale, row + c);
+      const int c = lane_off + stride * i;
+      if (stride * (i + 1) <= lim || c < lim) __builtin_nontemporal_store(v[i] * scale, p + c);
     }
   }
+}
+
+// Columns of a row segment that starts at column c0: min(cols - c0, cap).
+__device__ __forceinline__ int seg_len(int64_t cols, int64_t c0, int64_t cap) {
+  const int64_t left = cols - c0;
+  return static_cast<int>(left < cap ? left : cap);
 }
 
 // ---------------------------------------------------------------------------
@@ -235,7 +240,7 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
 // (b) One wavefront per row, cols <= 256*V (4*V elements per lane).
 // Four wavefronts per workgroup work on four rows independently.
 template <int V, bool VEC4>
-__global__ __launch_bounds__(256) void k_wave_row(const float* x, float* y, int64_t rows,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_wave_row(const float* x, float* y, int64_t rows,
                                                   int64_t cols) {
   const int lane = __lane_id();
   const int wave = threadIdx.x >> 6;
@@ -243,12 +248,13 @@ __global__ __launch_bounds__(256) void k_wave_row(const float* x, float* y, int6
        row += static_cast<int64_t>(gridDim.x) * 4) {
     const float* xr = x + row * cols;
     float* yr = y + row * cols;
+    const int lim = static_cast<int>(cols);
     float v[4 * V];
-    load_strip<V, VEC4>(v, xr, 0, lane, 64, cols);
+    load_strip<V, VEC4>(v, xr, lane, 64, lim);
     const RowShift rs = row_shift(seg_max<64>(array_max(v)));
     const float s = seg_sum<64>(exp_strip(v, rs));
     const float rcp = 1.0f / s;
-    store_strip<V, VEC4>(v, rcp, yr, 0, lane, 64, cols);
+    store_strip<V, VEC4>(v, rcp, yr, lane, 64, lim);
   }
 }
 
@@ -264,12 +270,13 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int6
   for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
     const float* xr = x + row * cols;
     float* yr = y + row * cols;
+    const int lim = static_cast<int>(cols);
     float v[4 * V];
-    load_strip<V, VEC4>(v, xr, 0, tid, NT, cols);
+    load_strip<V, VEC4>(v, xr, tid, NT, lim);
     const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max));
     const float s = block_sum<NW>(exp_strip(v, rs), red_sum);
     const float rcp = 1.0f / s;
-    store_strip<V, VEC4>(v, rcp, yr, 0, tid, NT, cols);
+    store_strip<V, VEC4>(v, rcp, yr, tid, NT, lim);
   }
 }
 
@@ -302,17 +309,15 @@ __global__ __launch_bounds__(NT) void k_split_stats(const float* x, float2* part
     const int64_t row = b / chunks;
     const int64_t g = b - row * chunks;
     const int64_t c0 = g * CH;
-    const float* xr = x + row * cols;
+    const float* xr = x + row * cols + c0;
+    const int lim = seg_len(cols, c0, CH);
     float v[4 * V];
-    load_strip<V, VEC4>(v, xr, c0, tid, NT, cols);
+    load_strip<V, VEC4>(v, xr, tid, NT, lim);
     const float m = block_max<NW>(array_max(v), red_max);
     const bool empty_max = (m == kNegInf);
     const RowShift rs = row_shift(empty_max ? 0.0f : m);
     float s = block_sum<NW>(exp_strip(v, rs), red_sum);
-    if (empty_max) {
-      const int64_t left = cols - c0;
-      s = static_cast<float>(left < CH ? left : CH);
-    }
+    if (empty_max) s = static_cast<float>(lim);
     if (tid == 0) part[b] = make_float2(m, s);
   }
 }
@@ -329,10 +334,11 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
     const int64_t row = b / chunks;
     const int64_t g = b - row * chunks;
     const int64_t c0 = g * CH;
-    const float* xr = x + row * cols;
-    float* yr = y + row * cols;
+    const float* xr = x + row * cols + c0;
+    float* yr = y + row * cols + c0;
+    const int lim = seg_len(cols, c0, CH);
     float v[4 * V];
-    load_strip<V, VEC4>(v, xr, c0, tid, NT, cols);
+    load_strip<V, VEC4>(v, xr, tid, NT, lim);
 
     const float2* pr = part + row * chunks;
     float mm = kNegInf;
@@ -347,8 +353,135 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
 
 #pragma unroll
     for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip(v[i], rs);
-    store_strip<V, VEC4>(v, rcp, yr, c0, tid, NT, cols);
+    store_strip<V, VEC4>(v, rcp, yr, tid, NT, lim);
   }
+}
+
+// ---------------------------------------------------------------------------
+// (c, split, one pass) All rows*G workgroups of a launch exchange partials
+// in the middle, so x is read from HBM exactly once.
+//
+// Workgroup (row, g) keeps e = exp(max(x - m_g, -64)) of its chunk in
+// registers, publishes (m_g, s_g) and adds its share to the row's arrival
+// counter; once every chunk of the row has arrived it merges the partials
+// into M and S and writes
+//     y = max(e * exp(m_g - M), e^-64) / S.
+// For an element with x - M >= -64 the rescaled e equals exp(x - M) >= e^-64;
+// for x - M < -64 it is below e^-64, so the max is exactly the clip of the
+// definition.  A NaN element makes s_g, hence S and the whole row, NaN.
+//
+// Progress: a row's G workgroups have consecutive IDs and workgroups are
+// dispatched in ID order, so the lowest unfinished row always has all of
+// its chunks dispatched once G workgroup slots are free; every wait ends as
+// long as G workgroups of the launch fit on the device at once (G <= 64).
+// The wait is also bounded: a workgroup that gives up writes NaN for its
+// chunk instead of stalling the device.
+//
+// Arrival counters are never reset: every launch adds exactly kArriveQuantum
+// to each counter it uses (chunk 0 adds kArriveQuantum - G + 1, the others 1),
+// so a launch's base is the counter value rounded down to a multiple of
+// kArriveQuantum and it waits for base + kArriveQuantum.  Launches that share
+// the counters must not overlap in time (the host gives each stream its own).
+constexpr unsigned kArriveQuantum = 1024;
+constexpr unsigned kSpinLimit = 1u << 20;
+
+__device__ __forceinline__ unsigned long long pack_pair(float a, float b) {
+  return static_cast<unsigned long long>(__builtin_bit_cast(unsigned, a)) |
+         (static_cast<unsigned long long>(__builtin_bit_cast(unsigned, b)) << 32);
+}
+
+template <int NT, int V, bool VEC4>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_split_onepass(const float* x, float* y,
+                                                   unsigned long long* part,
+                                                   unsigned* arrive, int64_t cols,
+                                                   int chunks) {
+  constexpr int NW = NT / 64;
+  constexpr int64_t CH = int64_t(4) * V * NT;
+  __shared__ float red_max[NW];
+  __shared__ float red_sum[NW];
+  __shared__ float bcast[3];
+  const int tid = threadIdx.x;
+  const int64_t b = blockIdx.x;
+  const int64_t row = b / chunks;
+  const int g = static_cast<int>(b - row * chunks);
+  const int64_t c0 = g * CH;
+  const float* xr = x + row * cols + c0;
+  float* yr = y + row * cols + c0;
+  const int lim = seg_len(cols, c0, CH);
+
+  float v[4 * V];
+  load_strip<V, VEC4>(v, xr, tid, NT, lim);
+  const float m = block_max<NW>(array_max(v), red_max);
+  const bool empty_max = (m == kNegInf);
+  float s = block_sum<NW>(exp_strip(v, row_shift(empty_max ? 0.0f : m)), red_sum);
+  if (empty_max) s = static_cast<float>(lim);
+
+  // Exchange.  Every access below is a device-scope atomic, performed at the
+  // device's coherence point rather than in a per-XCD L2, so no cache
+  // writeback or invalidate is needed (a release/acquire pair here costs
+  // two whole-L2 operations per workgroup, about 10 us per launch):
+  //  * the partial is published with an atomic exchange, and the arrival
+  //    add is not issued until the exchange has returned (the empty asm
+  //    makes the add's operand depend on the returned value), so the
+  //    partial is in place before the count can include it;
+  //  * a reader issues its partial loads only after a poll has returned the
+  //    full count (the loop exit depends on the loaded value, and a
+  //    wavefront does not issue memory operations speculatively).
+  if (tid == 0) {
+    const unsigned long long prev = __hip_atomic_exchange(
+        &part[b], pack_pair(m, s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    unsigned add = (g == 0) ? kArriveQuantum - static_cast<unsigned>(chunks) + 1u : 1u;
+    asm volatile("" : "+v"(add) : "v"(prev));
+    const unsigned old = __hip_atomic_fetch_add(&arrive[row], add, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned target = (old & ~(kArriveQuantum - 1u)) + kArriveQuantum;
+    unsigned spins = 0;
+    bool ok = true;
+    while (static_cast<int>(__hip_atomic_load(&arrive[row], __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT) -
+                            target) < 0) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++spins > kSpinLimit) {
+        ok = false;
+        break;
+      }
+    }
+    bcast[2] = ok ? 1.0f : 0.0f;
+  }
+  __syncthreads();
+
+  // Wave 0 merges the row's partials and broadcasts the two output factors.
+  if (tid < 64) {
+    const unsigned long long* pr = part + row * chunks;
+    float mm = kNegInf;
+    for (int l = tid; l < chunks; l += 64) {
+      const unsigned long long q =
+          __hip_atomic_load(&pr[l], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      mm = fmaxf(mm, __builtin_bit_cast(float, static_cast<unsigned>(q)));
+    }
+    const RowShift rs = row_shift(seg_max<64>(mm));
+    float ss = 0.0f;
+    for (int l = tid; l < chunks; l += 64) {
+      const unsigned long long q =
+          __hip_atomic_load(&pr[l], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const float pm = __builtin_bit_cast(float, static_cast<unsigned>(q));
+      const float ps = __builtin_bit_cast(float, static_cast<unsigned>(q >> 32));
+      ss = ss + ps * exp_shift_clip(pm, rs);
+    }
+    const float rcp = 1.0f / seg_sum<64>(ss);
+    if (tid == 0) {
+      const float scale = exp_shift_clip(m, rs) * rcp;  // e^(m_g - M) / S
+      const bool ok = bcast[2] != 0.0f;
+      bcast[0] = ok ? scale : __builtin_nanf("");
+      bcast[1] = ok ? kExpClipLo * rcp : __builtin_nanf("");  // e^-64 / S
+    }
+  }
+  __syncthreads();
+  const float scale = bcast[0];
+  const float floor_y = bcast[1];
+#pragma unroll
+  for (int i = 0; i < 4 * V; ++i) v[i] = fmaxf(v[i] * scale, floor_y);
+  store_strip<V, VEC4>(v, 1.0f, yr, tid, NT, lim);
 }
 
 // ---------------------------------------------------------------------------

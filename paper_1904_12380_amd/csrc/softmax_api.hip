@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <mutex>
+#include <vector>
 
 #include "../../include/softmax_mi355x.h"
 #include "sm_kernels.hpp"
@@ -20,24 +21,50 @@ constexpr int64_t kPackedMaxCols = 64;
 constexpr int64_t kWaveRowMaxCols = 4096;
 constexpr int64_t kBlockRowMaxCols = 32768;
 
-// Split rows: 512-thread workgroups holding 8 float4 per lane, i.e. chunks
-// of 16384 columns (64 KiB of x) per workgroup.
+// Split rows, one-pass kernel: workgroups of kOnePassThreads threads holding
+// 4*kOnePassV columns per lane (chunks of 32768 columns).
+constexpr int kOnePassThreads = 512;
+constexpr int kOnePassV = 16;
+constexpr int64_t kOnePassChunk = int64_t(4) * kOnePassV * kOnePassThreads;
+// Rows per launch are chosen so that a launch has at most kOnePassMaxBlocks
+// workgroups: two per CU on MI355X's 256 CUs (the kernel's registers allow
+// two 512-thread workgroups per CU), so all of them are resident together.
+constexpr int64_t kOnePassMaxBlocks = 512;
+// A row may span at most this many workgroups on the one-pass path.
+constexpr int64_t kOnePassMaxChunks = 64;
+static_assert(kOnePassMaxChunks <= kArriveQuantum, "arrival quantum covers a row");
+
+// Split rows, two-pass fallback for rows longer than kOnePassMaxChunks
+// chunks: 512-thread workgroups holding 32 columns per lane (chunks of
+// 16384 columns).
 constexpr int kSplitThreads = 512;
 constexpr int kSplitV = 8;
 constexpr int64_t kSplitChunk = int64_t(4) * kSplitV * kSplitThreads;
 
-// Library-owned workspace for split-row partials, per device.
-constexpr int64_t kWorkspaceBytes = int64_t(1) << 20;
-constexpr int64_t kWorkspacePairs = kWorkspaceBytes / int64_t(sizeof(float2));
+// Library-owned workspace for split rows: partials in the first half,
+// arrival counters (one-pass) in the second.  One per (device, stream) for
+// eager calls, so launches that may overlap in time never share one, and
+// one per device shared by captured graphs.
+constexpr int64_t kWorkspaceBytes = int64_t(256) << 10;
+constexpr int64_t kWorkspacePairs = kWorkspaceBytes / 2 / int64_t(sizeof(float2));
+constexpr int64_t kArriveOffset = kWorkspaceBytes / 2;
+constexpr int64_t kArriveCount = kWorkspaceBytes / 2 / int64_t(sizeof(unsigned));
+static_assert(kOnePassMaxBlocks <= kWorkspacePairs, "one-pass partials fit");
+static_assert(kOnePassMaxBlocks <= kArriveCount, "one arrival counter per row");
 constexpr int kMaxDevices = 64;
+constexpr int kMaxStreamWorkspaces = 64;  // per device
 
 thread_local int tl_last_hip_error = 0;
 
+struct StreamWorkspace {
+  hipStream_t stream;
+  char* mem;
+  uint64_t last_use;
+};
 struct DeviceState {
-  float2* ws = nullptr;
-  hipEvent_t last = nullptr;
-  hipStream_t last_stream = nullptr;
-  bool has_last = false;
+  std::vector<StreamWorkspace> per_stream;
+  char* capture_ws = nullptr;
+  uint64_t clock = 0;
 };
 std::mutex g_mu;
 DeviceState g_dev[kMaxDevices];
@@ -150,18 +177,30 @@ softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t c
     p.grid = std::min(rows, kMaxGrid);
     p.launches = 1;
   } else {
-    const int64_t g = ceil_div(cols, kSplitChunk);
     p.kernel = SOFTMAX_KERNEL_SPLIT_ROW;
     p.vec_width = vec_rows ? 4 : 1;
-    p.lanes_per_row = kSplitThreads;
-    p.elems_per_lane = 4 * kSplitV;
-    p.block_threads = kSplitThreads;
-    p.chunks_per_row = g;
-    const int64_t rows_per_batch = std::max<int64_t>(1, kWorkspacePairs / g);
-    const int64_t batch_rows = std::min(rows, rows_per_batch);
-    p.grid = std::min(batch_rows * g, kMaxGrid);
-    p.launches = static_cast<int32_t>(2 * ceil_div(rows, rows_per_batch));
     p.workspace_bytes = kWorkspaceBytes;
+    const int64_t g1 = ceil_div(cols, kOnePassChunk);
+    if (g1 <= kOnePassMaxChunks) {
+      // One pass: whole rows per launch, at most kOnePassMaxBlocks workgroups.
+      const int64_t rows_per_launch = kOnePassMaxBlocks / g1;
+      p.lanes_per_row = kOnePassThreads;
+      p.elems_per_lane = 4 * kOnePassV;
+      p.block_threads = kOnePassThreads;
+      p.chunks_per_row = g1;
+      p.grid = std::min(rows, rows_per_launch) * g1;
+      p.launches = static_cast<int32_t>(ceil_div(rows, rows_per_launch));
+    } else {
+      // Two passes: partials, then merge and write, in batches of rows.
+      const int64_t g2 = ceil_div(cols, kSplitChunk);
+      const int64_t rows_per_batch = std::max<int64_t>(1, kWorkspacePairs / g2);
+      p.lanes_per_row = kSplitThreads;
+      p.elems_per_lane = 4 * kSplitV;
+      p.block_threads = kSplitThreads;
+      p.chunks_per_row = g2;
+      p.grid = std::min(std::min(rows, rows_per_batch) * g2, kMaxGrid);
+      p.launches = static_cast<int32_t>(2 * ceil_div(rows, rows_per_batch));
+    }
   }
   return p;
 }
@@ -248,45 +287,106 @@ hipError_t run_split(const float* x, float* y, float2* ws, int64_t rows, int64_t
   return hipSuccess;
 }
 
-// Split rows: the workspace is per device; calls on different streams are
-// chained with an event so they never use it at the same time.
+template <bool VEC4>
+hipError_t run_onepass(const float* x, float* y, char* ws, int64_t rows, int64_t cols,
+                       int64_t chunks, hipStream_t s) {
+  unsigned long long* part = reinterpret_cast<unsigned long long*>(ws);
+  unsigned* arrive = reinterpret_cast<unsigned*>(ws + kArriveOffset);
+  const int64_t rows_per_launch = kOnePassMaxBlocks / chunks;
+  int ichunks = static_cast<int>(chunks);
+  for (int64_t r0 = 0; r0 < rows; r0 += rows_per_launch) {
+    const int64_t nb = std::min(rows_per_launch, rows - r0);
+    const float* xb = x + r0 * cols;
+    float* yb = y + r0 * cols;
+    void* args[] = {&xb, &yb, &part, &arrive, &cols, &ichunks};
+    hipError_t e = launch(
+        reinterpret_cast<const void*>(&k_split_onepass<kOnePassThreads, kOnePassV, VEC4>),
+        nb * chunks, kOnePassThreads, args, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// A zeroed workspace allocation (counters must start at zero once).
+hipError_t new_workspace(char** out) {
+  void* mem = nullptr;
+  hipError_t e = hipMalloc(&mem, kWorkspaceBytes);
+  if (e != hipSuccess) return e;
+  e = hipMemset(mem, 0, kWorkspaceBytes);
+  if (e != hipSuccess) {
+    (void)hipFree(mem);
+    return e;
+  }
+  *out = static_cast<char*>(mem);
+  return hipSuccess;
+}
+
+// Workspace for a split-row call on (dev, s).  Eager calls get one per
+// stream (allocated on first use); under stream capture the device's shared
+// capture workspace is used, which an earlier eager split-row call on the
+// device must have created.
+int workspace_for(int dev, hipStream_t s, bool capturing, char** out) {
+  DeviceState& st = g_dev[dev];
+  hipError_t e;
+  if (capturing) {
+    if (st.capture_ws == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+    *out = st.capture_ws;
+    return SOFTMAX_OK;
+  }
+  ++st.clock;
+  for (StreamWorkspace& w : st.per_stream) {
+    if (w.stream == s) {
+      w.last_use = st.clock;
+      *out = w.mem;
+      return SOFTMAX_OK;
+    }
+  }
+  if (st.capture_ws == nullptr) {
+    e = new_workspace(&st.capture_ws);
+    if (e != hipSuccess) return fail_hip(e);
+  }
+  if (static_cast<int>(st.per_stream.size()) >= kMaxStreamWorkspaces) {
+    // Recycle the least recently used stream's workspace once the device
+    // is idle, so none of that stream's work can still be using it.
+    e = hipDeviceSynchronize();
+    if (e != hipSuccess) return fail_hip(e);
+    StreamWorkspace* lru = &st.per_stream[0];
+    for (StreamWorkspace& w : st.per_stream)
+      if (w.last_use < lru->last_use) lru = &w;
+    lru->stream = s;
+    lru->last_use = st.clock;
+    *out = lru->mem;
+    return SOFTMAX_OK;
+  }
+  char* mem = nullptr;
+  e = new_workspace(&mem);
+  if (e != hipSuccess) return fail_hip(e);
+  st.per_stream.push_back(StreamWorkspace{s, mem, st.clock});
+  *out = mem;
+  return SOFTMAX_OK;
+}
+
 int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
                int64_t cols, int dev, hipStream_t s) {
   if (dev < 0 || dev >= kMaxDevices) return SOFTMAX_ERR_INVALID_ARG;
-  std::lock_guard<std::mutex> lock(g_mu);
-  DeviceState& st = g_dev[dev];
-  hipError_t e;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-  e = hipStreamIsCapturing(s, &cap);
+  hipError_t e = hipStreamIsCapturing(s, &cap);
   if (e != hipSuccess) return fail_hip(e);
-  const bool capturing = (cap != hipStreamCaptureStatusNone);
-  if (st.ws == nullptr) {
-    // First use on this device must not be inside a stream capture.
-    if (capturing) return SOFTMAX_ERR_INVALID_ARG;
-    void* mem = nullptr;
-    e = hipMalloc(&mem, kWorkspaceBytes);
-    if (e != hipSuccess) return fail_hip(e);
-    st.ws = static_cast<float2*>(mem);
-    e = hipEventCreateWithFlags(&st.last, hipEventDisableTiming);
-    if (e != hipSuccess) return fail_hip(e);
+  char* ws = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_mu);
+    const int rc = workspace_for(dev, s, cap != hipStreamCaptureStatusNone, &ws);
+    if (rc != SOFTMAX_OK) return rc;
   }
-  // Under stream capture the graph's own order applies: the captured kernels
-  // run in sequence on the capturing stream, and graphs that use split rows
-  // must not be replayed concurrently on one device.
-  if (!capturing && st.has_last && st.last_stream != s) {
-    e = hipStreamWaitEvent(s, st.last, 0);
-    if (e != hipSuccess) return fail_hip(e);
+  if (p.lanes_per_row == kOnePassThreads && p.elems_per_lane == 4 * kOnePassV) {
+    e = p.vec_width == 4 ? run_onepass<true>(x, y, ws, rows, cols, p.chunks_per_row, s)
+                         : run_onepass<false>(x, y, ws, rows, cols, p.chunks_per_row, s);
+  } else {
+    float2* part = reinterpret_cast<float2*>(ws);
+    e = p.vec_width == 4 ? run_split<true>(x, y, part, rows, cols, p.chunks_per_row, s)
+                         : run_split<false>(x, y, part, rows, cols, p.chunks_per_row, s);
   }
-  e = p.vec_width == 4 ? run_split<true>(x, y, st.ws, rows, cols, p.chunks_per_row, s)
-                       : run_split<false>(x, y, st.ws, rows, cols, p.chunks_per_row, s);
-  if (e != hipSuccess) return fail_hip(e);
-  if (!capturing) {
-    e = hipEventRecord(st.last, s);
-    if (e != hipSuccess) return fail_hip(e);
-    st.last_stream = s;
-    st.has_last = true;
-  }
-  return SOFTMAX_OK;
+  return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
 }
 
 int check_pointers(const float* x, const float* y, int64_t n_elems, int* dev) {

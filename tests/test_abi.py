@@ -69,7 +69,7 @@ def test_cpu_tensor_is_rejected():
     (115200, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13, grid=1800)),
     (4096, 1000, "wave_row", 4, dict(grid=1024)),
     (512, 32768, "block_row", 4, dict(elems_per_lane=32, grid=512)),
-    (64, 262144, "split_row", 4, dict(chunks_per_row=16, launches=2, grid=1024)),
+    (64, 262144, "split_row", 4, dict(chunks_per_row=8, launches=1, grid=512)),
     (3, 1, "packed", 4, dict(lanes_per_row=1, elems_per_lane=1)),
     (300, 16, "packed", 4, dict(lanes_per_row=1, elems_per_lane=16, grid=2)),
     (300, 17, "packed", 4, dict(lanes_per_row=2, elems_per_lane=9, grid=3)),
@@ -77,7 +77,8 @@ def test_cpu_tensor_is_rejected():
     (3, 65, "wave_row", 1, dict(elems_per_lane=4)),
     (3, 4096, "wave_row", 4, dict(elems_per_lane=64)),
     (3, 4097, "block_row", 1, dict(elems_per_lane=8)),
-    (3, 32769, "split_row", 1, dict(chunks_per_row=3)),
+    (3, 32769, "split_row", 1, dict(chunks_per_row=2, launches=1)),
+    (300, 262144, "split_row", 4, dict(chunks_per_row=8, launches=5, grid=512)),
     (0, 5, "none", 0, {}),
     (5, 0, "none", 0, {}),
 ])
@@ -99,12 +100,22 @@ def test_plan_vector_width_follows_alignment():
     assert sm.softmax_plan(10, 1000, a, a)["vec_width"] == 4     # in place
 
 
-def test_plan_split_batches_rows_to_fit_workspace():
+def test_plan_split_batches_rows_per_one_pass_launch():
     p = sm.softmax_plan(10000, 262144)
-    pairs = p["workspace_bytes"] // 8
-    per_batch = pairs // p["chunks_per_row"]
-    assert p["launches"] == 2 * -(-10000 // per_batch)
-    assert p["grid"] == per_batch * p["chunks_per_row"]
+    per_launch = p["grid"] // p["chunks_per_row"]
+    assert p["grid"] <= 512 and per_launch * p["chunks_per_row"] == p["grid"]
+    assert p["launches"] == -(-10000 // per_launch)
+
+
+def test_plan_very_long_rows_use_two_passes():
+    # more than 64 one-pass chunks per row
+    p = sm.softmax_plan(2, 1 << 30)
+    assert p["kernel_name"] == "split_row" and p["launches"] % 2 == 0
+    assert p["chunks_per_row"] == (1 << 30) // 16384
+    p = sm.softmax_plan(1, 64 * 32768 + 1)
+    assert p["launches"] == 2 and p["chunks_per_row"] == 129
+    p = sm.softmax_plan(1, 64 * 32768)
+    assert p["launches"] == 1 and p["chunks_per_row"] == 64
 
 
 def _raw_fwd(x, y, rows, cols):

@@ -293,3 +293,57 @@ def test_host_pointer_is_rejected():
     if rc == 0 and a.type != 0:
         pytest.skip(f"HIP reports host memory type {a.type}")
     assert sm.softmax_fwd_ptr(buf.ctypes.data, buf.ctypes.data, 64, 64, 0) == sm.ERR_NOT_DEVICE
+
+
+def test_split_rows_several_one_pass_launches():
+    """More rows than one launch holds: several one-pass launches that reuse
+    the arrival counters back to back."""
+    log("[parity] split rows, several one-pass launches")
+    p = sm.softmax_plan(65, 262144)
+    assert p["grid"] == 512
+    assert p["kernel_name"] == "split_row" and p["launches"] == 2
+    x = workloads.random_logits(65, 262144, seed=5, kind="offset")
+    y1 = run_gpu(x)
+    check_parity(x, y1, "65x262144")
+    y2 = run_gpu(x)
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
+def test_split_rows_two_pass_fallback():
+    """A row longer than 64 one-pass chunks takes the two-pass path."""
+    log("[parity] split rows, two-pass fallback")
+    cols = 64 * 32768 + 1
+    p = sm.softmax_plan(1, cols)
+    assert p["kernel_name"] == "split_row" and p["launches"] == 2
+    x = workloads.random_logits(1, cols, seed=6, kind="normal")
+    check_parity(x, run_gpu(x), "1x2097153")
+    x = workloads.random_logits(3, cols, seed=7, kind="clip_heavy")
+    check_parity(x, run_gpu(x), "3x2097153 clip-heavy")
+
+
+@pytest.mark.parametrize("rows,cols", [(115200, 50), (4096, 1000), (512, 32768), (64, 262144)])
+def test_graph_capture_replays(rows, cols):
+    """softmax_fwd captured in a HIP graph: every replay, with eager work and
+    synchronisation in between, matches the eager output bit for bit."""
+    torch = _torch()
+    log(f"[parity] graph capture {rows}x{cols}")
+    x = workloads.random_logits(rows, cols, seed=9, kind="clip_heavy" if cols < 1000 else "normal")
+    xt = torch.from_numpy(x).to(_dev())
+    y_eager = sm.softmax_fwd(xt)          # first use (allocates any workspace)
+    torch.cuda.synchronize()
+    want = y_eager.cpu().numpy()
+    check_parity(x, want, f"eager {rows}x{cols}")
+    yg = torch.empty_like(xt)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(g, stream=s):
+        sm.softmax_fwd(xt, out=yg, stream=s)
+    for rep in range(3):
+        yg.fill_(-1.0)
+        sm.softmax_fwd(xt, out=y_eager)   # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = yg.cpu().numpy()
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), rep
