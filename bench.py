@@ -13,9 +13,9 @@ steps; every x_k holds the same seeded matrix.
 Timing: the K steps are captured once into a HIP graph (torch.cuda.CUDAGraph)
 and the graph is replayed: W untimed steps, then exactly K steps between two
 synchronisations, timed with HIP events recorded on the stream the kernels
-run on.  The graph removes host launch overhead (about 3 us per call through
-the C ABI); the same steps launched one by one from Python are reported as
-``eager``.  The roofline object uses the algorithmic traffic of one call
+run on.  The graph removes host launch overhead (about 4 us per call through
+the C ABI plus Python); the same steps launched one by one from Python are
+reported as ``eager``.  All of it runs on a dedicated stream.  The roofline object uses the algorithmic traffic of one call
 (8 bytes per element: one fp32 read of x, one fp32 write of y) divided by the
 average step time.  ``cpu_baseline`` times the float64 oracle on the host,
 ``cpu_fp32_baseline`` a plain single-thread fp32 C loop.
@@ -104,36 +104,37 @@ class Rotation:
 def time_steps(torch, launch, steps: int, warmup: int) -> tuple[float, float]:
     """Capture `steps` calls of launch(i, stream) into one graph; replay it
     once untimed (after `warmup` eager calls), then time one replay.
+    Everything runs on one dedicated stream: HIP's legacy null stream (torch's
+    default) adds a few microseconds of GPU time between kernels.
     Returns (graph ms per step, eager ms per step)."""
-    stream = torch.cuda.current_stream()
-    for i in range(warmup):
-        launch(i, stream)
-    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
-    # eager: one call per step from Python
-    torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(steps):
-        launch(i, stream)
-    stop.record(stream)
-    torch.cuda.synchronize()
-    eager_ms = start.elapsed_time(stop) / steps
-    # graph: the same steps captured once
-    g = torch.cuda.CUDAGraph()
-    cs = torch.cuda.Stream()
-    cs.wait_stream(stream)
-    with torch.cuda.graph(g, stream=cs):
+    with torch.cuda.stream(stream):
+        for i in range(warmup):
+            launch(i, stream)
+        torch.cuda.synchronize()
+        # eager: one call per step from Python
+        start.record(stream)
         for i in range(steps):
-            launch(i, cs)
-    torch.cuda.synchronize()
-    g.replay()                      # warm replay
-    torch.cuda.synchronize()
-    start.record(stream)
-    g.replay()
-    stop.record(stream)
-    torch.cuda.synchronize()
-    graph_ms = start.elapsed_time(stop) / steps
+            launch(i, stream)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        eager_ms = start.elapsed_time(stop) / steps
+        # graph: the same steps captured once, replayed on the same stream
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for i in range(steps):
+                launch(i, stream)
+        torch.cuda.synchronize()
+        g.replay()                  # warm replay
+        torch.cuda.synchronize()
+        start.record(stream)
+        g.replay()
+        stop.record(stream)
+        torch.cuda.synchronize()
+        graph_ms = start.elapsed_time(stop) / steps
     del g
     return graph_ms, eager_ms
 

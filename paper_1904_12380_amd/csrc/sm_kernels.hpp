@@ -138,20 +138,46 @@ __device__ __forceinline__ int seg_len(int64_t cols, int64_t c0, int64_t cap) {
 }
 
 // ---------------------------------------------------------------------------
-// (a) Packed rows, cols <= 16*G, with G lanes per row (G = 1, 2, 4, ...).
+// (a) Packed rows, cols <= G*EPL, with G lanes per row (G = 1, 2 or 4) and
+// EPL <= 16 columns per lane, both compile-time.
 //
-// A 256-thread workgroup owns tiles of kRows = 256/G consecutive rows: one
-// row per group of G lanes, so a tile is done in one pass.  kRows is a
-// multiple of 4, so a tile starts on a 16-byte boundary whenever x and y
-// do, whatever cols is (cols = 50 gives 200-byte rows).  The tile moves
-// HBM -> LDS -> HBM with 128-bit accesses; lane j of a row group handles
-// columns j, j+G, ..., j+(epl-1)G with epl = ceil(cols/G) <= 16.
-template <int G, bool VEC4>
+// A 256-thread workgroup works on tiles of kRows = 256/G consecutive rows:
+// one row per group of G lanes, so a tile is done in one pass.  kRows is a
+// multiple of 4, so a tile starts on a 16-byte boundary whenever x and y do,
+// whatever cols is (cols = 50 gives 200-byte rows).  Tiles move
+// HBM -> registers -> LDS -> HBM with 128-bit accesses; lane j of a row group
+// takes columns j, j+G, ..., j+(EPL-1)G.
+//
+// The grid is persistent (a few workgroups per CU, each looping over tiles)
+// and every workgroup issues the loads of its next tile right after staging
+// the current one, so they are in flight while the current tile computes.
+template <int G, int EPL>
+__device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int r, int j) {
+  const bool active = r < nr;
+  float* tr = tile + r * ccols;
+  float v[EPL];
+#pragma unroll
+  for (int k = 0; k < EPL; ++k) {
+    const int c = j + G * k;
+    v[k] = (active && c < ccols) ? tr[c] : kNegInf;
+  }
+  const RowShift rs = row_shift(seg_max<G>(array_max(v)));
+#pragma unroll
+  for (int k = 0; k < EPL; ++k) v[k] = exp_shift_clip(v[k], rs);
+  const float rcp = 1.0f / seg_sum<G>(tree_sum(v));
+#pragma unroll
+  for (int k = 0; k < EPL; ++k) {
+    const int c = j + G * k;
+    if (active && c < ccols) tr[c] = v[k] * rcp;
+  }
+}
+
+template <int G, int EPL, bool VEC4>
 __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_t rows,
-                                                int64_t cols, int epl) {
+                                                int64_t cols) {
   constexpr int kRows = 256 / G;
-  constexpr int kMaxEpl = 16;
-  constexpr int kTileFloats = kRows * G * kMaxEpl;  // = 4096
+  constexpr int kTileFloats = kRows * G * EPL;  // = 256 * EPL
+  constexpr int kPer = VEC4 ? (kTileFloats / 4 + 255) / 256 : (kTileFloats + 255) / 256;
   __shared__ float tile[kTileFloats];
 
   const int tid = threadIdx.x;
@@ -160,68 +186,60 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
   const int r = tid / G;
   const int j = tid % G;
 
-  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+  // Registers for the next tile: kPer 128-bit (or 32-bit) values per thread.
+  f32x4 q4[VEC4 ? kPer : 1];
+  float q1[VEC4 ? 1 : kPer];
+  auto issue = [&](int64_t t) {
+    const int64_t row0 = t * kRows;
+    const int nr = static_cast<int>(rows - row0 < kRows ? rows - row0 : kRows);
+    const int n = nr * ccols;
+    const float* xs = x + row0 * cols;
+    if constexpr (VEC4) {
+      const int n4 = n >> 2;
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int i = tid + 256 * u;
+        q4[u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (i < n4) q4[u] = ld_stream(xs + 4 * i);
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int i = tid + 256 * u;
+        q1[u] = 0.0f;
+        if (i < n) q1[u] = __builtin_nontemporal_load(xs + i);
+      }
+    }
+  };
+
+  int64_t t = blockIdx.x;
+  if (t < ntiles) issue(t);
+  for (; t < ntiles; t += gridDim.x) {
     const int64_t row0 = t * kRows;
     const int nr = static_cast<int>(rows - row0 < kRows ? rows - row0 : kRows);
     const int n = nr * ccols;
     const float* xs = x + row0 * cols;
     float* ys = y + row0 * cols;
 
-    // Every load of the tile is issued before the first LDS write.
     if constexpr (VEC4) {
-      constexpr int kVecPerThread = kTileFloats / 4 / 256;
       const int n4 = n >> 2;
-      f32x4 q[kVecPerThread];
 #pragma unroll
-      for (int u = 0; u < kVecPerThread; ++u) {
+      for (int u = 0; u < kPer; ++u) {
         const int i = tid + 256 * u;
-        q[u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        if (i < n4) q[u] = ld_stream(xs + 4 * i);
-      }
-#pragma unroll
-      for (int u = 0; u < kVecPerThread; ++u) {
-        const int i = tid + 256 * u;
-        if (i < n4) *reinterpret_cast<f32x4*>(tile + 4 * i) = q[u];
+        if (i < n4) *reinterpret_cast<f32x4*>(tile + 4 * i) = q4[u];
       }
       for (int i = (n4 << 2) + tid; i < n; i += 256) tile[i] = xs[i];
     } else {
-      constexpr int kPerThread = kTileFloats / 256;
-      float q[kPerThread];
 #pragma unroll
-      for (int u = 0; u < kPerThread; ++u) {
+      for (int u = 0; u < kPer; ++u) {
         const int i = tid + 256 * u;
-        q[u] = 0.0f;
-        if (i < n) q[u] = __builtin_nontemporal_load(xs + i);
-      }
-#pragma unroll
-      for (int u = 0; u < kPerThread; ++u) {
-        const int i = tid + 256 * u;
-        if (i < n) tile[i] = q[u];
+        if (i < n) tile[i] = q1[u];
       }
     }
     __syncthreads();
+    if (t + gridDim.x < ntiles) issue(t + gridDim.x);
 
-    {
-      const bool active = r < nr;
-      float* tr = tile + r * ccols;
-      float v[kMaxEpl];
-#pragma unroll
-      for (int k = 0; k < kMaxEpl; ++k) {
-        const int c = j + G * k;
-        v[k] = (k < epl && active && c < ccols) ? tr[c] : kNegInf;
-      }
-      const float m = seg_max<G>(array_max(v));
-      const RowShift rs = row_shift(m);
-#pragma unroll
-      for (int k = 0; k < kMaxEpl; ++k) v[k] = (k < epl) ? exp_shift_clip(v[k], rs) : 0.0f;
-      const float s = seg_sum<G>(tree_sum(v));
-      const float rcp = 1.0f / s;
-#pragma unroll
-      for (int k = 0; k < kMaxEpl; ++k) {
-        const int c = j + G * k;
-        if (k < epl && active && c < ccols) tr[c] = v[k] * rcp;
-      }
-    }
+    packed_rows<G, EPL>(tile, nr, ccols, r, j);
     __syncthreads();
 
     if constexpr (VEC4) {

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <mutex>
+#include <utility>
 #include <vector>
 
 #include "../../include/softmax_mi355x.h"
@@ -18,6 +19,13 @@ constexpr int64_t kMaxGrid = int64_t(1) << 20;
 
 // Bucket limits on cols.
 constexpr int64_t kPackedMaxCols = 64;
+
+// The packed kernel's persistent grid: six 256-thread workgroups per CU on
+// MI355X's 256 CUs.  Measured on 115200 x 50: up to six per CU the
+// prefetched next tile overlaps the current tile's compute (8.6 us); seven
+// or more per CU, or one tile per workgroup, take 10.4-11.2 us.
+constexpr int64_t kPackedBlocksPerCU = 6;
+constexpr int64_t kDeviceCUs = 256;
 constexpr int64_t kWaveRowMaxCols = 4096;
 constexpr int64_t kBlockRowMaxCols = 32768;
 
@@ -148,7 +156,8 @@ softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t c
   const bool a16 = aligned16(x) && aligned16(y);
   const bool vec_rows = a16 && (cols % 4 == 0);
   if (cols <= kPackedMaxCols) {
-    // G lanes per row with at most 16 columns per lane.
+    // G lanes per row with at most 16 columns per lane; a persistent grid of
+    // kPackedBlocksPerCU workgroups per CU loops over tiles of 256/G rows.
     const int64_t g = cols <= 16 ? 1 : cols <= 32 ? 2 : 4;
     p.kernel = SOFTMAX_KERNEL_PACKED;
     p.vec_width = a16 ? 4 : 1;
@@ -156,7 +165,7 @@ softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t c
     p.elems_per_lane = static_cast<int32_t>(ceil_div(cols, g));
     p.block_threads = 256;
     const int64_t tile = 256 / g;
-    p.grid = std::min(ceil_div(rows, tile), kMaxGrid);
+    p.grid = std::min(ceil_div(rows, tile), kPackedBlocksPerCU * kDeviceCUs);
     p.launches = 1;
   } else if (cols <= kWaveRowMaxCols) {
     const int64_t v = pow2_at_least(ceil_div(cols, 256));
@@ -209,22 +218,28 @@ hipError_t launch(const void* fn, int64_t grid, int block, void** args, hipStrea
   return hipLaunchKernel(fn, dim3(static_cast<uint32_t>(grid)), dim3(block), args, 0, s);
 }
 
-template <int G, bool VEC4>
-hipError_t run_packed(const float* x, float* y, int64_t rows, int64_t cols, int epl,
-                      int64_t grid, hipStream_t s) {
-  void* args[] = {&x, &y, &rows, &cols, &epl};
-  return launch(reinterpret_cast<const void*>(&k_packed<G, VEC4>), grid, 256, args, s);
+// k_packed instances: G = 1 with EPL = 1..16, G = 2 and G = 4 with
+// EPL = 9..16 (a plan never asks for fewer columns per lane at G > 1).
+template <int G, bool VEC4, int... E>
+const void* packed_fn(int epl, std::integer_sequence<int, E...>) {
+  static const void* const table[] = {
+      reinterpret_cast<const void*>(&k_packed<G, (G == 1 ? 1 : 9) + E, VEC4>)...};
+  const int idx = epl - (G == 1 ? 1 : 9);
+  return (idx >= 0 && idx < static_cast<int>(sizeof...(E))) ? table[idx] : nullptr;
 }
 
 template <bool VEC4>
 hipError_t dispatch_packed(const softmax_plan_t& p, const float* x, float* y,
                            int64_t rows, int64_t cols, hipStream_t s) {
-  const int epl = p.elems_per_lane;
+  const void* fn = nullptr;
   switch (p.lanes_per_row) {
-    case 1: return run_packed<1, VEC4>(x, y, rows, cols, epl, p.grid, s);
-    case 2: return run_packed<2, VEC4>(x, y, rows, cols, epl, p.grid, s);
-    default: return run_packed<4, VEC4>(x, y, rows, cols, epl, p.grid, s);
+    case 1: fn = packed_fn<1, VEC4>(p.elems_per_lane, std::make_integer_sequence<int, 16>{}); break;
+    case 2: fn = packed_fn<2, VEC4>(p.elems_per_lane, std::make_integer_sequence<int, 8>{}); break;
+    default: fn = packed_fn<4, VEC4>(p.elems_per_lane, std::make_integer_sequence<int, 8>{}); break;
   }
+  if (fn == nullptr) return hipErrorInvalidValue;
+  void* args[] = {&x, &y, &rows, &cols};
+  return launch(fn, p.grid, 256, args, s);
 }
 
 template <int V, bool VEC4>

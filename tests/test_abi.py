@@ -66,7 +66,8 @@ def test_cpu_tensor_is_rejected():
 
 @pytest.mark.parametrize("rows,cols,kernel,vec,extra", [
     (64, 1000, "wave_row", 4, dict(elems_per_lane=16)),
-    (115200, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13, grid=1800)),
+    (115200, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13, grid=1536)),
+    (1000, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13, grid=16)),
     (4096, 1000, "wave_row", 4, dict(grid=1024)),
     (512, 32768, "block_row", 4, dict(elems_per_lane=32, grid=512)),
     (64, 262144, "split_row", 4, dict(chunks_per_row=8, launches=1, grid=512)),

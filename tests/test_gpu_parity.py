@@ -87,6 +87,18 @@ def test_edge_shapes(cols):
             check_parity(x, run_gpu(x), f"{rows}x{cols} {kind}")
 
 
+@pytest.mark.parametrize("rows,cols", [(400001, 7), (200003, 20), (99999, 33), (98305, 64)])
+def test_packed_persistent_tiles(rows, cols):
+    """More tiles than the persistent grid: every workgroup loops over
+    several tiles with the next tile's loads in flight; ragged last tile."""
+    log(f"[parity] packed persistent {rows}x{cols}")
+    p = sm.softmax_plan(rows, cols)
+    tile_rows = 256 // p["lanes_per_row"]
+    assert -(-rows // tile_rows) > p["grid"]
+    x = workloads.random_logits(rows, cols, seed=rows, kind="clip_heavy")
+    check_parity(x, run_gpu(x), f"packed {rows}x{cols}")
+
+
 @pytest.mark.parametrize("rows,cols", [(257, 50), (64, 1000), (33, 1001), (5, 8192), (3, 100003),
                                        (131, 7)])
 def test_misaligned_views(rows, cols):
