@@ -76,8 +76,8 @@ extern "C" {
  * Asynchrony: work is enqueued on `stream` and the call returns without
  * waiting; y is valid once the stream has reached that point.
  *
- * Workspace: rows longer than 32768 columns use a 256 KiB device workspace
- * that the library allocates (hipMalloc, zeroed) on the first such call on
+ * Workspace: rows longer than 32768 columns use a 136 KiB device workspace
+ * that the library allocates (hipMalloc, initialised) on the first such call on
  * each (device, stream) and keeps until the process ends, so calls on
  * different streams never share one.  Up to 64 streams per device get their
  * own; past that the least recently used one is reassigned after a
@@ -88,7 +88,9 @@ extern "C" {
  *
  * Long rows are done in one pass when a row spans at most 64 workgroups
  * (cols <= 2097152): the workgroups of a row exchange partial (max, sum)
- * pairs in the middle of the kernel and wait for each other.  Workgroups are
+ * pairs through the workspace in the middle of the kernel and wait for each
+ * other; the workspace is back in its resting state when the kernel ends.
+ * Workgroups are
  * dispatched in ID order, so this always progresses while 64 workgroups of
  * the launch can be resident; the wait is bounded, and a workgroup that
  * times out writes NaN instead of stalling.  Longer rows use two passes.

@@ -376,17 +376,30 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
 }
 
 // ---------------------------------------------------------------------------
-// (c, split, one pass) All rows*G workgroups of a launch exchange partials
-// in the middle, so x is read from HBM exactly once.
+// (c, split, one pass) The G workgroups of a row exchange partials in the
+// middle of the kernel, so x is read from HBM exactly once.
 //
 // Workgroup (row, g) keeps e = exp(max(x - m_g, -64)) of its chunk in
-// registers, publishes (m_g, s_g) and adds its share to the row's arrival
-// counter; once every chunk of the row has arrived it merges the partials
-// into M and S and writes
+// registers and publishes (m_g, s_g) in its slot part[row*G + g].  Wave 0
+// polls the row's G slots until none holds the sentinel, merges them into M
+// and S, and every thread writes
 //     y = max(e * exp(m_g - M), e^-64) / S.
 // For an element with x - M >= -64 the rescaled e equals exp(x - M) >= e^-64;
 // for x - M < -64 it is below e^-64, so the max is exactly the clip of the
 // definition.  A NaN element makes s_g, hence S and the whole row, NaN.
+//
+// Slots hold kSlotEmpty between launches.  After reading, each workgroup
+// adds 1 to depart[row]; the one that brings it to G puts the row's
+// sentinels back and zeroes the counter.  Every workgroup departs only after
+// its own reads have returned, and the next launch on the same workspace
+// starts after this kernel has finished, so each launch (graph replays
+// included) starts from clean slots.
+//
+// All exchange accesses are device-scope atomics, performed at the device's
+// coherence point rather than in a per-XCD L2, so no cache writeback or
+// invalidate is needed.  A wavefront issues memory operations in program
+// order and not speculatively, so the output work, which depends on the
+// loaded slots, never runs ahead of them.
 //
 // Progress: a row's G workgroups have consecutive IDs and workgroups are
 // dispatched in ID order, so the lowest unfinished row always has all of
@@ -394,13 +407,7 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
 // long as G workgroups of the launch fit on the device at once (G <= 64).
 // The wait is also bounded: a workgroup that gives up writes NaN for its
 // chunk instead of stalling the device.
-//
-// Arrival counters are never reset: every launch adds exactly kArriveQuantum
-// to each counter it uses (chunk 0 adds kArriveQuantum - G + 1, the others 1),
-// so a launch's base is the counter value rounded down to a multiple of
-// kArriveQuantum and it waits for base + kArriveQuantum.  Launches that share
-// the counters must not overlap in time (the host gives each stream its own).
-constexpr unsigned kArriveQuantum = 1024;
+constexpr unsigned long long kSlotEmpty = ~0ull;
 constexpr unsigned kSpinLimit = 1u << 20;
 
 __device__ __forceinline__ unsigned long long pack_pair(float a, float b) {
@@ -409,15 +416,14 @@ __device__ __forceinline__ unsigned long long pack_pair(float a, float b) {
 }
 
 template <int NT, int V, bool VEC4>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_split_onepass(const float* x, float* y,
-                                                   unsigned long long* part,
-                                                   unsigned* arrive, int64_t cols,
-                                                   int chunks) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_split_onepass(
+    const float* x, float* y, unsigned long long* part, unsigned* depart, int64_t cols,
+    int chunks) {
   constexpr int NW = NT / 64;
   constexpr int64_t CH = int64_t(4) * V * NT;
   __shared__ float red_max[NW];
   __shared__ float red_sum[NW];
-  __shared__ float bcast[3];
+  __shared__ float bcast[2];
   const int tid = threadIdx.x;
   const int64_t b = blockIdx.x;
   const int64_t row = b / chunks;
@@ -434,64 +440,47 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_
   float s = block_sum<NW>(exp_strip(v, row_shift(empty_max ? 0.0f : m)), red_sum);
   if (empty_max) s = static_cast<float>(lim);
 
-  // Exchange.  Every access below is a device-scope atomic, performed at the
-  // device's coherence point rather than in a per-XCD L2, so no cache
-  // writeback or invalidate is needed (a release/acquire pair here costs
-  // two whole-L2 operations per workgroup, about 10 us per launch):
-  //  * the partial is published with an atomic exchange, and the arrival
-  //    add is not issued until the exchange has returned (the empty asm
-  //    makes the add's operand depend on the returned value), so the
-  //    partial is in place before the count can include it;
-  //  * a reader issues its partial loads only after a poll has returned the
-  //    full count (the loop exit depends on the loaded value, and a
-  //    wavefront does not issue memory operations speculatively).
   if (tid == 0) {
-    const unsigned long long prev = __hip_atomic_exchange(
-        &part[b], pack_pair(m, s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    unsigned add = (g == 0) ? kArriveQuantum - static_cast<unsigned>(chunks) + 1u : 1u;
-    asm volatile("" : "+v"(add) : "v"(prev));
-    const unsigned old = __hip_atomic_fetch_add(&arrive[row], add, __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT);
-    const unsigned target = (old & ~(kArriveQuantum - 1u)) + kArriveQuantum;
+    unsigned long long val = pack_pair(m, s);
+    if (val == kSlotEmpty) val = pack_pair(__builtin_nanf(""), __builtin_nanf(""));
+    __hip_atomic_store(&part[b], val, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  if (tid < 64) {
+    unsigned long long* pr = part + row * chunks;
+    unsigned long long q = 0;
     unsigned spins = 0;
     bool ok = true;
-    while (static_cast<int>(__hip_atomic_load(&arrive[row], __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT) -
-                            target) < 0) {
+    while (true) {
+      q = (tid < chunks)
+              ? __hip_atomic_load(&pr[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+              : 0ull;
+      if (__builtin_amdgcn_ballot_w64(tid < chunks && q == kSlotEmpty) == 0) break;
       __builtin_amdgcn_s_sleep(2);
       if (++spins > kSpinLimit) {
         ok = false;
         break;
       }
     }
-    bcast[2] = ok ? 1.0f : 0.0f;
-  }
-  __syncthreads();
-
-  // Wave 0 merges the row's partials and broadcasts the two output factors.
-  if (tid < 64) {
-    const unsigned long long* pr = part + row * chunks;
-    float mm = kNegInf;
-    for (int l = tid; l < chunks; l += 64) {
-      const unsigned long long q =
-          __hip_atomic_load(&pr[l], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      mm = fmaxf(mm, __builtin_bit_cast(float, static_cast<unsigned>(q)));
-    }
-    const RowShift rs = row_shift(seg_max<64>(mm));
-    float ss = 0.0f;
-    for (int l = tid; l < chunks; l += 64) {
-      const unsigned long long q =
-          __hip_atomic_load(&pr[l], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const float pm = __builtin_bit_cast(float, static_cast<unsigned>(q));
-      const float ps = __builtin_bit_cast(float, static_cast<unsigned>(q >> 32));
-      ss = ss + ps * exp_shift_clip(pm, rs);
-    }
-    const float rcp = 1.0f / seg_sum<64>(ss);
+    const float pm = (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q)) : kNegInf;
+    const float ps =
+        (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q >> 32)) : 0.0f;
+    const RowShift rs = row_shift(seg_max<64>(pm));
+    const float term = (tid < chunks) ? ps * exp_shift_clip(pm, rs) : 0.0f;
+    const float rcp = 1.0f / seg_sum<64>(term);
     if (tid == 0) {
-      const float scale = exp_shift_clip(m, rs) * rcp;  // e^(m_g - M) / S
-      const bool ok = bcast[2] != 0.0f;
-      bcast[0] = ok ? scale : __builtin_nanf("");
-      bcast[1] = ok ? kExpClipLo * rcp : __builtin_nanf("");  // e^-64 / S
+      bcast[0] = ok ? exp_shift_clip(m, rs) * rcp : __builtin_nanf("");  // e^(m_g - M) / S
+      bcast[1] = ok ? kExpClipLo * rcp : __builtin_nanf("");             // e^-64 / S
+      // Depart once this wave's slot reads have returned (the add's operand
+      // depends on them); the last workgroup of the row restores the slots.
+      unsigned one = 1u;
+      asm volatile("" : "+v"(one) : "v"(q));
+      const unsigned old = __hip_atomic_fetch_add(&depart[row], one, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+      if (old == static_cast<unsigned>(chunks) - 1u) {
+        for (int l = 0; l < chunks; ++l)
+          __hip_atomic_store(&pr[l], kSlotEmpty, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&depart[row], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   }
   __syncthreads();

@@ -38,9 +38,9 @@ constexpr int64_t kOnePassChunk = int64_t(4) * kOnePassV * kOnePassThreads;
 // workgroups: two per CU on MI355X's 256 CUs (the kernel's registers allow
 // two 512-thread workgroups per CU), so all of them are resident together.
 constexpr int64_t kOnePassMaxBlocks = 512;
-// A row may span at most this many workgroups on the one-pass path.
+// A row may span at most this many workgroups on the one-pass path (the
+// exchange is read by one wavefront, one slot per lane).
 constexpr int64_t kOnePassMaxChunks = 64;
-static_assert(kOnePassMaxChunks <= kArriveQuantum, "arrival quantum covers a row");
 
 // Split rows, two-pass fallback for rows longer than kOnePassMaxChunks
 // chunks: 512-thread workgroups holding 32 columns per lane (chunks of
@@ -49,16 +49,19 @@ constexpr int kSplitThreads = 512;
 constexpr int kSplitV = 8;
 constexpr int64_t kSplitChunk = int64_t(4) * kSplitV * kSplitThreads;
 
-// Library-owned workspace for split rows: partials in the first half,
-// arrival counters (one-pass) in the second.  One per (device, stream) for
-// eager calls, so launches that may overlap in time never share one, and
-// one per device shared by captured graphs.
-constexpr int64_t kWorkspaceBytes = int64_t(256) << 10;
-constexpr int64_t kWorkspacePairs = kWorkspaceBytes / 2 / int64_t(sizeof(float2));
-constexpr int64_t kArriveOffset = kWorkspaceBytes / 2;
-constexpr int64_t kArriveCount = kWorkspaceBytes / 2 / int64_t(sizeof(unsigned));
-static_assert(kOnePassMaxBlocks <= kWorkspacePairs, "one-pass partials fit");
-static_assert(kOnePassMaxBlocks <= kArriveCount, "one arrival counter per row");
+// Library-owned workspace for split rows, one per (device, stream) for
+// eager calls (launches that may overlap in time never share one) and one
+// per device shared by captured graphs:
+//   [0, 128 KiB)          two-pass partials, float2
+//   [128 KiB, +4 KiB)     one-pass exchange slots, 64-bit, kSlotEmpty at rest
+//   [132 KiB, +2 KiB)     one-pass departure counters, zero at rest
+constexpr int64_t kWorkspaceBytes = int64_t(136) << 10;
+constexpr int64_t kWorkspacePairs = (int64_t(128) << 10) / int64_t(sizeof(float2));
+constexpr int64_t kSlotsOffset = int64_t(128) << 10;
+constexpr int64_t kSlotsBytes = kOnePassMaxBlocks * 8;
+constexpr int64_t kDepartOffset = kSlotsOffset + kSlotsBytes;
+constexpr int64_t kDepartBytes = kOnePassMaxBlocks * 4;
+static_assert(kDepartOffset + kDepartBytes <= kWorkspaceBytes, "workspace layout fits");
 constexpr int kMaxDevices = 64;
 constexpr int kMaxStreamWorkspaces = 64;  // per device
 
@@ -305,15 +308,15 @@ hipError_t run_split(const float* x, float* y, float2* ws, int64_t rows, int64_t
 template <bool VEC4>
 hipError_t run_onepass(const float* x, float* y, char* ws, int64_t rows, int64_t cols,
                        int64_t chunks, hipStream_t s) {
-  unsigned long long* part = reinterpret_cast<unsigned long long*>(ws);
-  unsigned* arrive = reinterpret_cast<unsigned*>(ws + kArriveOffset);
+  unsigned long long* part = reinterpret_cast<unsigned long long*>(ws + kSlotsOffset);
+  unsigned* depart = reinterpret_cast<unsigned*>(ws + kDepartOffset);
   const int64_t rows_per_launch = kOnePassMaxBlocks / chunks;
   int ichunks = static_cast<int>(chunks);
   for (int64_t r0 = 0; r0 < rows; r0 += rows_per_launch) {
     const int64_t nb = std::min(rows_per_launch, rows - r0);
     const float* xb = x + r0 * cols;
     float* yb = y + r0 * cols;
-    void* args[] = {&xb, &yb, &part, &arrive, &cols, &ichunks};
+    void* args[] = {&xb, &yb, &part, &depart, &cols, &ichunks};
     hipError_t e = launch(
         reinterpret_cast<const void*>(&k_split_onepass<kOnePassThreads, kOnePassV, VEC4>),
         nb * chunks, kOnePassThreads, args, s);
@@ -322,17 +325,19 @@ hipError_t run_onepass(const float* x, float* y, char* ws, int64_t rows, int64_t
   return hipSuccess;
 }
 
-// A zeroed workspace allocation (counters must start at zero once).
+// A workspace in its resting state: exchange slots empty, counters zero.
 hipError_t new_workspace(char** out) {
   void* mem = nullptr;
   hipError_t e = hipMalloc(&mem, kWorkspaceBytes);
   if (e != hipSuccess) return e;
-  e = hipMemset(mem, 0, kWorkspaceBytes);
+  char* ws = static_cast<char*>(mem);
+  e = hipMemset(ws, 0, kWorkspaceBytes);
+  if (e == hipSuccess) e = hipMemset(ws + kSlotsOffset, 0xFF, kSlotsBytes);
   if (e != hipSuccess) {
     (void)hipFree(mem);
     return e;
   }
-  *out = static_cast<char*>(mem);
+  *out = ws;
   return hipSuccess;
 }
 
