@@ -416,7 +416,7 @@ __device__ __forceinline__ unsigned long long pack_pair(float a, float b) {
 }
 
 template <int NT, int V, bool VEC4>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_split_onepass(
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 : 4))) void k_split_onepass(
     const float* x, float* y, unsigned long long* part, unsigned* depart, int64_t cols,
     int chunks) {
   constexpr int NW = NT / 64;

@@ -70,7 +70,8 @@ def test_cpu_tensor_is_rejected():
     (1000, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13, grid=16)),
     (4096, 1000, "wave_row", 4, dict(grid=1024)),
     (512, 32768, "block_row", 4, dict(elems_per_lane=32, grid=512)),
-    (64, 262144, "split_row", 4, dict(chunks_per_row=8, launches=1, grid=512)),
+    (64, 262144, "split_row", 4, dict(chunks_per_row=16, launches=1, grid=1024,
+                                      elems_per_lane=32)),
     (3, 1, "packed", 4, dict(lanes_per_row=1, elems_per_lane=1)),
     (300, 16, "packed", 4, dict(lanes_per_row=1, elems_per_lane=16, grid=2)),
     (300, 17, "packed", 4, dict(lanes_per_row=2, elems_per_lane=9, grid=3)),
@@ -78,8 +79,12 @@ def test_cpu_tensor_is_rejected():
     (3, 65, "wave_row", 1, dict(elems_per_lane=4)),
     (3, 4096, "wave_row", 4, dict(elems_per_lane=64)),
     (3, 4097, "block_row", 1, dict(elems_per_lane=8)),
-    (3, 32769, "split_row", 1, dict(chunks_per_row=2, launches=1)),
-    (300, 262144, "split_row", 4, dict(chunks_per_row=8, launches=5, grid=512)),
+    (3, 32769, "split_row", 1, dict(chunks_per_row=3, launches=1)),
+    (300, 262144, "split_row", 4, dict(chunks_per_row=16, launches=5, grid=1024)),
+    (1, 1048576, "split_row", 4, dict(chunks_per_row=64, elems_per_lane=32, launches=1)),
+    (1, 1048580, "split_row", 4, dict(chunks_per_row=33, elems_per_lane=64, launches=1)),
+    (20, 2097152, "split_row", 4, dict(chunks_per_row=64, elems_per_lane=64, grid=512,
+                                       launches=3)),
     (0, 5, "none", 0, {}),
     (5, 0, "none", 0, {}),
 ])
@@ -104,7 +109,7 @@ def test_plan_vector_width_follows_alignment():
 def test_plan_split_batches_rows_per_one_pass_launch():
     p = sm.softmax_plan(10000, 262144)
     per_launch = p["grid"] // p["chunks_per_row"]
-    assert p["grid"] <= 512 and per_launch * p["chunks_per_row"] == p["grid"]
+    assert p["grid"] <= 1024 and per_launch * p["chunks_per_row"] == p["grid"]
     assert p["launches"] == -(-10000 // per_launch)
 
 

@@ -312,13 +312,23 @@ def test_split_rows_several_one_pass_launches():
     the arrival counters back to back."""
     log("[parity] split rows, several one-pass launches")
     p = sm.softmax_plan(65, 262144)
-    assert p["grid"] == 512
+    assert p["grid"] == 1024
     assert p["kernel_name"] == "split_row" and p["launches"] == 2
     x = workloads.random_logits(65, 262144, seed=5, kind="offset")
     y1 = run_gpu(x)
     check_parity(x, y1, "65x262144")
     y2 = run_gpu(x)
     assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
+@pytest.mark.parametrize("rows,cols", [(3, 1048577), (2, 2097152), (1, 1048576)])
+def test_split_rows_large_chunks(rows, cols):
+    """Rows past 64 chunks of 16384 columns use 32768-column chunks."""
+    log(f"[parity] split rows, large chunks {rows}x{cols}")
+    p = sm.softmax_plan(rows, cols)
+    assert p["kernel_name"] == "split_row" and p["launches"] == 1
+    x = workloads.random_logits(rows, cols, seed=cols % 1000, kind="offset")
+    check_parity(x, run_gpu(x), f"{rows}x{cols}")
 
 
 def test_split_rows_two_pass_fallback():
