@@ -20,10 +20,13 @@ reported as ``eager``.  All of it runs on a dedicated stream.  The roofline obje
 average step time.  ``cpu_baseline`` times the float64 oracle on the host,
 ``cpu_fp32_baseline`` a plain single-thread fp32 C loop.
 
-Counter passes (FETCH_SIZE, WRITE_SIZE) use two extra modes:
+Counter passes (FETCH_SIZE, WRITE_SIZE, and optionally occupancy) use two
+extra modes:
 
     rocprofv3 --pmc FETCH_SIZE -d DIR/fetch -o run -- python3 bench.py --pmc-run --workload KEY
     rocprofv3 --pmc WRITE_SIZE -d DIR/write -o run -- python3 bench.py --pmc-run --workload KEY
+    rocprofv3 --pmc OccupancyPercent SQ_WAVES GRBM_GUI_ACTIVE -d DIR/occ -o run \
+        -- python3 bench.py --pmc-run --workload KEY
     python3 bench.py --summarize-pmc DIR --workload KEY
 
 The summary (profiles/pmc_KEY.json and .md) scales each counter by what it
@@ -140,7 +143,7 @@ def time_steps(torch, launch, steps: int, warmup: int) -> tuple[float, float]:
 
 
 def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, warmup: int,
-             check: bool = True) -> dict:
+             check: bool = True, memcpy: bool = False) -> dict:
     rot = Rotation(torch, x_host)
     plan = sm.softmax_plan(w.rows, w.cols, rot.xs[0].data_ptr(), rot.ys[0].data_ptr())
 
@@ -152,8 +155,13 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         x, y = rot.pair(i)
         sm.softmax_copy_probe(x, out=y, stream=s)
 
+    def d2d(i, s):
+        x, y = rot.pair(i)
+        y.copy_(x)          # hipMemcpyAsync device to device
+
     ms, eager_ms = time_steps(torch, fwd, steps, warmup)
     copy_ms, _ = time_steps(torch, cpy, steps, warmup)
+    memcpy_ms = time_steps(torch, d2d, steps, warmup)[0] if memcpy else None
 
     max_rel = None
     if check:
@@ -186,6 +194,7 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         "copy_ms_per_step": copy_ms,
         "copy_gbps": w.algorithmic_bytes / (copy_ms * 1e-3) / 1e9,
         "softmax_over_copy_time": ms / copy_ms,
+        "memcpy_ms_per_step": memcpy_ms,
         "rotation_buffers": nbuf,
         "plan": plan,
         "sampled_max_rel_err": max_rel,
@@ -293,7 +302,8 @@ def summarize_pmc(directory: str, w: workloads.Workload, command: str) -> dict:
     kernel and of the copy kernel, scaled by the copy kernel's reading for
     its known byte count (4 * elements read, 4 * elements written)."""
     per = {}
-    for sub in ("fetch", "write"):
+    subs = ["fetch", "write"] + (["occ"] if os.path.isdir(os.path.join(directory, "occ")) else [])
+    for sub in subs:
         for name, cname, val in _counter_rows(os.path.join(directory, sub)):
             key = "copy" if "k_copy" in name else ("softmax" if "smx::k_" in name else None)
             if key is None:
@@ -326,6 +336,11 @@ def summarize_pmc(directory: str, w: workloads.Workload, command: str) -> dict:
         "traffic_over_algorithmic": (fetch_b + write_b) / w.algorithmic_bytes,
         "command": command,
     }
+    if "occ" in subs:
+        for key in ("softmax", "copy"):
+            doc[f"{key}_occupancy_percent"] = agg[key].get("OccupancyPercent")
+            doc[f"{key}_sq_waves_per_dispatch"] = agg[key].get("SQ_WAVES")
+            doc[f"{key}_grbm_gui_active_cycles"] = agg[key].get("GRBM_GUI_ACTIVE")
     os.makedirs(PROFILES, exist_ok=True)
     with open(pmc_summary_path(w.key, "json"), "w") as f:
         json.dump(doc, f, indent=1)
@@ -343,37 +358,98 @@ def summarize_pmc(directory: str, w: workloads.Workload, command: str) -> dict:
                 f"fetch {scale_fetch:.4f}, write {scale_write:.4f}.\n\n")
         f.write(f"Scaled traffic per launch: fetch {fetch_b:.0f} B + write {write_b:.0f} B = "
                 f"{fetch_b + write_b:.0f} B; algorithmic {w.algorithmic_bytes} B; ratio "
-                f"{doc['traffic_over_algorithmic']:.4f}.\n\n"
-                f"Kernel sources sha256: {doc['source_sha256']}\n")
+                f"{doc['traffic_over_algorithmic']:.4f}.\n\n")
+        if "occ" in subs:
+            f.write("Occupancy pass (OccupancyPercent = 400 * SQ_WAVE_CYCLES / "
+                    "GRBM_GUI_ACTIVE / CUs / 32, the profiler's derived counter: mean "
+                    "resident waves per CU over the dispatch as % of 32):\n\n"
+                    "| quantity | softmax kernel | copy kernel |\n|---|---|---|\n")
+            for label, k in (("OccupancyPercent (median)", "occupancy_percent"),
+                             ("SQ_WAVES per dispatch", "sq_waves_per_dispatch"),
+                             ("GRBM_GUI_ACTIVE cycles", "grbm_gui_active_cycles")):
+                a, b = doc[f"softmax_{k}"], doc[f"copy_{k}"]
+                f.write(f"| {label} | {a if a is None else round(a, 1)} | "
+                        f"{b if b is None else round(b, 1)} |\n")
+            f.write("\n")
+        f.write(f"Kernel sources sha256: {doc['source_sha256']}\n")
     return doc
+
+
+COPY_THREADS = 256       # launch shape of softmax_copy_probe's 128-bit kernel:
+COPY_UNROLL = 4          # 256 threads, 4 float4 per thread per workgroup
+
+
+def trace_groups(w_all: dict) -> dict:
+    """(kernel base name, grid size in threads) -> the workloads whose
+    launches have that shape: the softmax kernel from softmax_plan(), the copy
+    kernel from its fixed launch shape."""
+    import paper_1904_12380_amd as sm
+    names = {"packed": "k_packed", "wave_row": "k_wave_row", "block_row": "k_block_row",
+             "split_row": "k_split"}
+    out: dict = {}
+    for key, wk in w_all.items():
+        p = sm.softmax_plan(wk.rows, wk.cols)
+        out.setdefault((names[p["kernel_name"]], p["grid"] * p["block_threads"]), []).append(key)
+        blocks = min(-(-(wk.elements // 4) // (COPY_THREADS * COPY_UNROLL)), 1 << 20)
+        out.setdefault(("k_copy4", blocks * COPY_THREADS), []).append(key)
+    return {k: " / ".join(v) for k, v in out.items()}
+
+
+def _base_name(full: str) -> str:
+    head = full.split("(")[0].split("<")[0]
+    return head.split("::")[-1].replace("void ", "").strip()
 
 
 def summarize_trace(directory: str, w: workloads.Workload, command: str,
                     bench_json: str | None) -> str:
     """profiles/<kernel>_<workload>_trace.md from a rocprofv3 --kernel-trace
-    --stats run of this script: per-kernel call counts and durations, next
-    to the step times the same run printed."""
-    files = glob.glob(os.path.join(directory, "**", "*kernel_stats.csv"), recursive=True)
-    if not files:
-        raise SystemExit(f"no kernel_stats.csv under {directory}")
-    with open(files[0]) as f:
+    --stats run of this script: per (kernel, grid) dispatch durations
+    (median, p10, p90, mean) and register / LDS usage, the per-kernel stats
+    table, and the step times the same run printed."""
+    traces = glob.glob(os.path.join(directory, "**", "*kernel_trace.csv"), recursive=True)
+    stats = glob.glob(os.path.join(directory, "**", "*kernel_stats.csv"), recursive=True)
+    if not traces or not stats:
+        raise SystemExit(f"no kernel_trace.csv / kernel_stats.csv under {directory}")
+    labels = trace_groups(workloads.WORKLOADS)
+    groups: dict = {}
+    with open(traces[0]) as f:
+        for r in csv.DictReader(f):
+            base = _base_name(r["Kernel_Name"])
+            if not (base.startswith("k_") and "smx::" in r["Kernel_Name"]):
+                continue
+            key = (r["Kernel_Name"].split("(")[0].replace("void ", ""), int(r["Grid_Size_X"]))
+            g = groups.setdefault(key, {"d": [], "res": r, "base": base})
+            g["d"].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    with open(stats[0]) as f:
         rows = list(csv.DictReader(f))
-    ours = [r for r in rows if "smx::" in r["Name"]]
-    main_k = None
     bench = None
+    main_k = "kernels"
     if bench_json:
         with open(bench_json) as f:
             bench = json.loads(f.read().strip().splitlines()[-1])
-        kname = {"packed": "k_packed", "wave_row": "k_wave_row", "block_row": "k_block_row",
-                 "split_row": "k_split"}[bench["config"]["kernel"]]
-        main_k = kname
-    name = f"{main_k or 'kernels'}_{w.key}_trace.md"
-    path = os.path.join(PROFILES, name)
+        main_k = {"packed": "k_packed", "wave_row": "k_wave_row", "block_row": "k_block_row",
+                  "split_row": "k_split"}[bench["config"]["kernel"]]
+    path = os.path.join(PROFILES, f"{main_k}_{w.key}_trace.md")
     with open(path, "w") as f:
         f.write(f"# Kernel trace: bench.py on {w.key} (and the other workloads it times)\n\n")
         f.write(f"Command (repository root, GPU machine):\n\n```\n{command}\n```\n\n")
+        f.write("Per dispatch, grouped by kernel and grid (eager and graph-replayed "
+                "launches together; durations are the profiler's begin-to-end times):\n\n")
+        f.write("| kernel | grid threads | workload | calls | median us | p10 us | p90 us | "
+                "mean us | VGPR | AGPR | SGPR | LDS B | scratch B |\n"
+                "|---|---|---|---|---|---|---|---|---|---|---|---|---|\n")
+        for (name, grid), g in sorted(groups.items(), key=lambda kv: (kv[0][0], kv[0][1])):
+            d = np.array(g["d"])
+            r = g["res"]
+            lab = labels.get((g["base"] if not g["base"].startswith("k_split") else "k_split",
+                              grid), "")
+            f.write(f"| `{name}` | {grid} | {lab} | {d.size} | {np.median(d):.2f} | "
+                    f"{np.percentile(d, 10):.2f} | {np.percentile(d, 90):.2f} | "
+                    f"{d.mean():.2f} | {r['VGPR_Count']} | {r['Accum_VGPR_Count']} | "
+                    f"{r['SGPR_Count']} | {r['LDS_Block_Size']} | {r['Scratch_Size']} |\n")
+        f.write("\nrocprofv3 --stats table (all kernels of the run):\n\n")
         f.write("| kernel | calls | average us | min us | max us |\n|---|---|---|---|---|\n")
-        for r in ours + [r for r in rows if r not in ours]:
+        for r in rows:
             f.write(f"| `{r['Name'].split('(')[0]}` | {r['Calls']} | "
                     f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
                     f"{float(r['MaxNs']) / 1e3:.2f} |\n")
@@ -383,8 +459,9 @@ def summarize_trace(directory: str, w: workloads.Workload, command: str,
                     f"(graph replay); other workloads: ")
             f.write(", ".join(f"{k} {v['ms_per_step'] * 1e3:.2f} us"
                               for k, v in bench["other_workloads"].items()))
-            f.write(".  Kernel averages include the eager and the graph-replayed "
-                    "launches and the profiler's own per-dispatch overhead.\n")
+            f.write(".  Event time per step includes the gap between consecutive "
+                    "kernels; the profiler's durations do not, and the profiler adds "
+                    "its own per-dispatch overhead.\n")
     return path
 
 
@@ -438,7 +515,7 @@ def main() -> int:
     log(f"[bench] generating {w.key}")
     x = workloads.generate(w.key)
     log(f"[bench] timing {w.key}: {args.warmup} warmup + {args.steps} steps (graph replay)")
-    main_res = time_gpu(sm, torch, w, x, args.steps, args.warmup)
+    main_res = time_gpu(sm, torch, w, x, args.steps, args.warmup, memcpy=True)
     log(f"[bench] {w.key}: {main_res['ms_per_step'] * 1e3:.2f} us/step, "
         f"{main_res['hbm_gbps']:.0f} GB/s")
 
@@ -449,7 +526,7 @@ def main() -> int:
                 continue
             log(f"[bench] timing {key}")
             r = time_gpu(sm, torch, wk, workloads.generate(key), args.steps, args.warmup)
-            extra[key] = {k: (round(v, 6) if isinstance(v, float) else v)
+            extra[key] = {k: (float(f"{v:.6g}") if isinstance(v, float) else v)
                           for k, v in r.items() if k != "plan"}
             extra[key]["kernel"] = r["plan"]["kernel_name"]
             extra[key]["launches_per_step"] = r["plan"]["launches"]
@@ -500,7 +577,10 @@ def main() -> int:
                   "hbm_gbps": main_res["eager_hbm_gbps"]},
         "copy_ceiling": {"gbps": main_res["copy_gbps"],
                          "ms_per_step": main_res["copy_ms_per_step"],
-                         "softmax_over_copy_time": main_res["softmax_over_copy_time"]},
+                         "softmax_over_copy_time": main_res["softmax_over_copy_time"],
+                         "memcpy_d2d_ms_per_step": main_res["memcpy_ms_per_step"],
+                         "memcpy_d2d_gbps": w.algorithmic_bytes
+                         / (main_res["memcpy_ms_per_step"] * 1e-3) / 1e9},
         "cpu_baseline": cpu,
         "cpu_fp32_baseline": cpu32,
         "sampled_max_rel_err": main_res["sampled_max_rel_err"],

@@ -76,7 +76,7 @@ extern "C" {
  * Asynchrony: work is enqueued on `stream` and the call returns without
  * waiting; y is valid once the stream has reached that point.
  *
- * Workspace: rows longer than 32768 columns use a 136 KiB device workspace
+ * Workspace: rows longer than 32768 columns use a 140 KiB device workspace
  * that the library allocates (hipMalloc, initialised) on the first such call on
  * each (device, stream) and keeps until the process ends, so calls on
  * different streams never share one.  Up to 64 streams per device get their

@@ -1,0 +1,92 @@
+"""Host-side logic of bench.py: argument handling that must not touch the GPU,
+the counter-summary arithmetic (scaling each counter by the copy kernel's
+reading for a known byte count) and the labelling of kernel-trace groups."""
+import csv
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+import workloads  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def _write_counters(path, rows):
+    os.makedirs(path, exist_ok=True)
+    with open(os.path.join(path, "run_counter_collection.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Counter_Name", "Counter_Value"])
+        w.writeheader()
+        for name, cname, val in rows:
+            w.writerow({"Kernel_Name": name, "Counter_Name": cname, "Counter_Value": val})
+
+
+def test_summarize_pmc_scales_by_the_copy_kernel(tmp_path, monkeypatch):
+    wl = workloads.WORKLOADS["classifier_4096x1000"]
+    kib_each_way = 4.0 * wl.elements / 1024.0
+    soft = "void smx::k_wave_row<4, true>(float const*, float*, long, long)"
+    copy = "smx::k_copy4(float const*, float*, long)"
+    # FETCH_SIZE reads half the bytes for both kernels; the softmax kernel
+    # fetches 1% more than the copy.  WRITE_SIZE reads the bytes written.
+    _write_counters(tmp_path / "fetch",
+                    [(soft, "FETCH_SIZE", 0.505 * kib_each_way)] * 3
+                    + [(copy, "FETCH_SIZE", 0.5 * kib_each_way)] * 3)
+    _write_counters(tmp_path / "write",
+                    [(soft, "WRITE_SIZE", kib_each_way)] * 3
+                    + [(copy, "WRITE_SIZE", kib_each_way)] * 3)
+    _write_counters(tmp_path / "occ",
+                    [(soft, "OccupancyPercent", 40.0), (soft, "SQ_WAVES", 4096.0),
+                     (soft, "GRBM_GUI_ACTIVE", 1e4), (copy, "OccupancyPercent", 50.0),
+                     (copy, "SQ_WAVES", 4000.0), (copy, "GRBM_GUI_ACTIVE", 1.2e4)])
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path / "profiles"))
+    doc = bench.summarize_pmc(str(tmp_path), wl, "cmd")
+    assert doc["scale_fetch"] == pytest.approx(2.0)
+    assert doc["scale_write"] == pytest.approx(1.0)
+    assert doc["traffic_fetch_bytes_per_launch"] == pytest.approx(1.01 * 4 * wl.elements)
+    assert doc["traffic_write_bytes_per_launch"] == pytest.approx(4 * wl.elements)
+    assert doc["traffic_over_algorithmic"] == pytest.approx(1.005)
+    assert doc["softmax_occupancy_percent"] == 40.0
+    assert doc["copy_sq_waves_per_dispatch"] == 4000.0
+    with open(tmp_path / "profiles" / f"pmc_{wl.key}.json") as f:
+        assert json.load(f)["source_sha256"] == bench.kernel_source_sha256()
+    md = (tmp_path / "profiles" / f"pmc_{wl.key}.md").read_text()
+    assert "k_wave_row" in md and "Occupancy" in md
+
+
+def test_traffic_is_withheld_when_sources_changed(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    with open(tmp_path / "pmc_x.json", "w") as f:
+        json.dump({"source_sha256": "0" * 64, "traffic_bytes_per_launch": 1.0}, f)
+    assert bench.load_traffic("x") == (None, "kernel changed since the counters were taken")
+    with open(tmp_path / "pmc_x.json", "w") as f:
+        json.dump({"source_sha256": bench.kernel_source_sha256(),
+                   "traffic_bytes_per_launch": 5.0}, f)
+    assert bench.load_traffic("x") == (5.0, None)
+    assert bench.load_traffic("missing") == (None, None)
+
+
+def test_trace_groups_name_every_workload():
+    pytest.importorskip("ctypes")
+    import paper_1904_12380_amd as sm
+    try:
+        sm.load_library()
+    except ImportError:
+        pytest.skip("library not built")
+    groups = bench.trace_groups(workloads.WORKLOADS)
+    labelled = " / ".join(groups.values())
+    for key in workloads.WORKLOADS:
+        assert labelled.count(key) == 2, key        # softmax kernel and copy kernel
+    kernels = {k for k, _ in groups}
+    assert {"k_packed", "k_wave_row", "k_block_row", "k_split", "k_copy4"} <= kernels
