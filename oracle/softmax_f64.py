@@ -25,7 +25,10 @@ Sources in the paper:
 Readings where the paper is silent (also listed in the design doc):
   * The clip bound is CLIP_LO = -64 applied to the shifted logit before exp
     (the prose's 1e-60 is not an fp32 value and describes the effect, not the
-    code).
+    code).  Other bounds are a parameter, ``clip_lo``; ``clip_lo = -inf``
+    is no clip at all, the optimised functor of Sec. 2.3 Fig. 4 (Sec. 2.1
+    describes dropping the clip as the first optimisation).  Without a clip
+    an output can be 0 (exp underflows below about -745 in float64).
   * The clip is a compare-select ``d < L ? L : d`` so a NaN stays NaN; a NaN
     anywhere in a row, a +inf element or an all -inf row makes the whole row
     NaN; a -inf element among finite ones clips to e^-64.
@@ -47,7 +50,8 @@ def row_max(x: np.ndarray) -> np.ndarray:
 
 def exp_clipped(d: np.ndarray, clip_lo: float = CLIP_LO) -> np.ndarray:
     """exp of the lower-clipped shifted logit, float64 (Fig. 1: ValueClip
-    then exp).  ``d`` is already x - M; a NaN stays NaN."""
+    then exp; clip_lo = -inf: exp alone, as in Fig. 4).  ``d`` is already
+    x - M; a NaN stays NaN."""
     d64 = np.asarray(d, dtype=np.float64)
     c = np.where(d64 < clip_lo, clip_lo, d64)
     return np.exp(c)
@@ -56,7 +60,8 @@ def exp_clipped(d: np.ndarray, clip_lo: float = CLIP_LO) -> np.ndarray:
 def softmax_clipped(x: np.ndarray, clip_lo: float = CLIP_LO) -> np.ndarray:
     """Row-wise clipped softmax of a 2-D array, returned as float64.
 
-    Sec. 1.1 Eq. (1) with the max shift and the clip of Sec. 1.2 Fig. 1.
+    Sec. 1.1 Eq. (1) with the max shift and the clip of Sec. 1.2 Fig. 1 at
+    ``clip_lo`` (-inf: no clip, Sec. 2.3 Fig. 4).
     """
     x64 = np.asarray(x, dtype=np.float64)
     if x64.ndim != 2:

@@ -10,6 +10,10 @@ and not from the GPU path.  They pin the float64 oracle to the definition:
     Sec. 2.1 used throughout), evaluated as
     y_j = exp(max(x_j - M, -64)) / sum_i exp(max(x_i - M, -64)).
 
+Each row is also evaluated with other clip bounds (``y_clip``): -48, -90,
+-120 and -inf (no clip, the optimised functor of Sec. 2.3 Fig. 4, which
+drops the ValueClip, Sec. 2.1).
+
 Inputs are fp32 values stored as exact hex strings.  Run from the repo root:
     python tests/golden/make_brute_force.py
 """
@@ -23,6 +27,8 @@ import numpy as np
 
 getcontext().prec = 50
 CLIP = Decimal(-64)
+OTHER_CLIPS = {"-48": Decimal(-48), "-90": Decimal(-90), "-120": Decimal(-120),
+               "-inf": Decimal("-Infinity")}
 
 
 def _rows() -> list[list[float]]:
@@ -44,13 +50,17 @@ def _rows() -> list[list[float]]:
     # ties and signed zeros
     rows.append([2.5, 2.5, 2.5, -1.0])
     rows.append([0.0, -0.0, -0.0, 0.0])
+    # rows whose shifted logits reach the denormal and underflow range of
+    # fp32 exponentials (e^-87.3 and e^-103.3), for the lower clip bounds
+    rows.append([0.0, -88.0, -95.5, -103.0, -104.5, -110.0, -1.0e4])
+    rows.append(list(np.float32(rng.uniform(-130.0, 0.0, 8))))
     return [[float(np.float32(v)) for v in r] for r in rows]
 
 
-def clipped_softmax_decimal(row: list[float]) -> list[Decimal]:
+def clipped_softmax_decimal(row: list[float], clip: Decimal = CLIP) -> list[Decimal]:
     xs = [Decimal(v) for v in row]            # exact: fp32 -> Decimal
     m = max(xs)
-    cs = [max(x - m, CLIP) for x in xs]
+    cs = [max(x - m, clip) for x in xs]
     es = [c.exp() for c in cs]
     s = sum(es, Decimal(0))
     return [e / s for e in es]
@@ -73,6 +83,8 @@ def main() -> None:
             "x_hex": [float(v).hex() for v in row],
             "y": [format(v, ".30e") for v in y],
             "clip_active": clip_active,
+            "y_clip": {k: [format(v, ".30e") for v in clipped_softmax_decimal(row, c)]
+                       for k, c in OTHER_CLIPS.items()},
         }
         if not clip_active:
             y1 = eq1_softmax_decimal(row)
@@ -83,7 +95,8 @@ def main() -> None:
     doc = {
         "what": "clipped row softmax of tiny fp32 rows in 50-digit decimal",
         "cites": "Sec. 1.1 Eq. (1); Sec. 1.2 Fig. 1 (clip of the shifted "
-                 "logits, bound -64); Sec. 2.1",
+                 "logits, bound -64; y_clip: other bounds and no clip); "
+                 "Sec. 2.1; Sec. 2.3 Fig. 4",
         "generator": "tests/golden/make_brute_force.py (decimal only)",
         "rows": out,
     }

@@ -204,3 +204,124 @@ def pin_empty(impl):
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
+
+
+# ---------------------------------------------------------------------------
+# Pins for the clip bound as a parameter.  Each ``pinc_*`` function takes
+# ``impl(x: float32 [R, C], clip_lo: float) -> float64 [R, C]``; clip_lo is
+# the lower bound on the shifted logits, and -inf means no clip (the
+# optimised functor of Sec. 2.3 Fig. 4, which drops the ValueClip of Fig. 1;
+# Sec. 2.1 gives the clip's purpose and its removal).  Outputs can then be
+# tiny or 0, so values are compared with a relative bound above 1e-290 and
+# an absolute one below.
+
+def _close(got, want, rel=1e-14, tiny=1e-290) -> bool:
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    big = np.abs(want) >= tiny
+    ok_big = np.all(np.abs(got[big] - want[big]) <= rel * np.abs(want[big]))
+    ok_small = np.all(np.abs(got[~big] - want[~big]) <= tiny)
+    return bool(ok_big and ok_small)
+
+
+def pinc_minus_64_passes_the_default_pins(impl):
+    """At clip_lo = -64 the function satisfies every pin of the default
+    bound (closed forms, brute force, invariants, non-finite reading)."""
+    for pin in ALL_PINS:
+        pin(lambda x: impl(x, -64.0))
+
+
+def pinc_clip_off_matches_library(impl):
+    """With no clip the result is plain softmax: scipy.special.softmax in
+    float64, on rows whose shifted logits go far below -64 (where any clip
+    would change the result) and rows with offsets large enough that exp
+    overflows unless the max is subtracted first."""
+    from scipy.special import softmax as sp_softmax
+    rng = np.random.default_rng(52)
+    rows = [rng.uniform(-700.0, 0.0, 64), rng.uniform(-150.0, 10.0, 64),
+            800.0 + rng.standard_normal(64), -900.0 + 40.0 * rng.standard_normal(64)]
+    x = _f32(np.stack(rows))
+    want = sp_softmax(x.astype(np.float64), axis=1)
+    y = impl(x, -np.inf)
+    assert _close(y, want), "clip off differs from plain softmax"
+    assert np.any(y < math.exp(-64.0) / 64), "some outputs must fall below the -64 clip"
+
+
+def pinc_closed_form(impl):
+    """Row [0, L-1, L, L+0.5, -1e4] with bound L: clipped shifts
+    [0, L, L, L+0.5, L], S = 1 + 3 e^L + e^(L+0.5); with offsets and in every
+    rotation."""
+    for lo in (-48.0, -80.5, -100.0, -120.0):
+        base = np.array([0.0, lo - 1.0, lo, lo + 0.5, -1.0e4])
+        el = math.exp(lo)
+        s = 1.0 + 3.0 * el + math.exp(lo + 0.5)
+        want = np.array([1.0, el, el, math.exp(lo + 0.5), el]) / s
+        for off in (0.0, 37.25, -20.5):
+            for r in range(5):
+                y = impl(_f32(np.roll(base + off, r)[None, :]), lo)[0]
+                assert _close(y, np.roll(want, r)), (lo, off, r)
+
+
+def pinc_two_class(impl):
+    """C = 2 with bound L: the smaller class is e^max(b-a, L) / (1 + that)."""
+    from scipy.special import expit
+    rng = np.random.default_rng(53)
+    a = rng.uniform(-30.0, 30.0, 100)
+    b = a - rng.uniform(0.0, 140.0, 100)
+    x = _f32(np.stack([a, b], axis=1))
+    diff = x[:, 0].astype(np.float64) - x[:, 1].astype(np.float64)
+    for lo in (-48.0, -90.0, -np.inf):
+        y = impl(x, lo)
+        t = np.maximum(-diff, lo)
+        assert _close(y[:, 1], np.exp(t) / (1.0 + np.exp(t)))
+        assert _close(y[:, 0], expit(-t))
+
+
+def pinc_brute_force_decimal(impl):
+    """Tiny rows against 50-digit decimal at bounds -48, -90, -120 and with
+    no clip (tests/golden, y_clip)."""
+    with open(os.path.join(GOLDEN, "brute_force_rows.json")) as f:
+        doc = json.load(f)
+    for rec in doc["rows"]:
+        x = _f32([[float.fromhex(h) for h in rec["x_hex"]]])
+        for key, vals in rec["y_clip"].items():
+            lo = -np.inf if key == "-inf" else float(key)
+            want = np.array([float(Decimal(v)) for v in vals])
+            assert _close(impl(x, lo)[0], want), (rec["x_hex"], key)
+
+
+def pinc_lower_bound(impl):
+    """Every output is at least e^L / C for a finite bound L; with no clip,
+    outputs whose shifted logit is below ln(2^-1074) are exactly 0."""
+    x = random_logits(16, 64, 54, "clip_heavy")
+    for lo in (-48.0, -90.0):
+        assert np.all(impl(x, lo) >= math.exp(lo) / 64 * (1 - 1e-14))
+    y = impl(_f32([[0.0, -800.0, -1.0e4, 0.0]]), -np.inf)[0]
+    assert y[1] == 0.0 and y[2] == 0.0 and y[0] == 0.5 and y[3] == 0.5
+
+
+def pinc_nonfinite_clip_off(impl):
+    """With no clip: a -inf element gives exactly 0; NaN, +inf and all -inf
+    rows are NaN."""
+    x = _f32([[1.0, np.nan, 0.0],
+              [1.0, np.inf, 0.0],
+              [-np.inf, -np.inf, -np.inf],
+              [0.0, -np.inf, 0.0]])
+    y = impl(x, -np.inf)
+    assert np.all(np.isnan(y[:3]))
+    assert y[3, 1] == 0.0 and y[3, 0] == 0.5 and y[3, 2] == 0.5
+
+
+def pinc_bound_is_monotone(impl):
+    """Lowering the bound never raises an output that was clipped, and an
+    element above both bounds keeps its share of the unclipped mass."""
+    x = random_logits(6, 200, 55, "clip_heavy")
+    d = x.astype(np.float64) - x.max(axis=1, keepdims=True)
+    y48, y90 = impl(x, -48.0), impl(x, -90.0)
+    clipped = d < -48.0
+    assert np.all(y90[clipped] <= y48[clipped] * (1 + 1e-14))
+    free = d >= -48.0
+    assert np.all(y90[free] >= y48[free] * (1 - 1e-14))
+
+
+CLIP_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pinc_")]

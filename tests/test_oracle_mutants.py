@@ -103,3 +103,42 @@ def test_mutant_is_caught(name):
         assert failed == [], failed
     else:
         assert failed, f"mutant {name} passed every pin"
+
+
+# Mistakes specific to the clip bound as a parameter (impl(x, clip_lo));
+# they must each fail at least one of pins.CLIP_PINS.  (An IEEE fmax "clip"
+# at -inf is not listed: with no clip a NaN already reaches every shifted
+# logit through the row max, so it is an equivalent form.)
+def _clip_off_only(spec):
+    """Apply the mistake only when the clip is off (clip_lo = -inf)."""
+    return lambda x, lo: _base(x, **spec) if lo == -np.inf else _base(x, clip_lo=lo)
+
+
+MUTANTS_CLIP = {
+    "reference_copy_is_clean": lambda x, lo: _base(x, clip_lo=lo),
+    "ignores_clip_param": lambda x, lo: _base(x),
+    "clip_param_plus_one": lambda x, lo: _base(x, clip_lo=lo + 1.0),
+    "clip_param_on_raw_logits": lambda x, lo: _base(x, clip_lo=lo, clip_on="x"),
+    "clip_off_keeps_minus_64": _clip_off_only(dict(clip_lo=L)),
+    "clip_off_also_drops_shift": _clip_off_only(dict(shift="none", clip_kind="none")),
+    "clip_off_float32": _clip_off_only(dict(clip_lo=-np.inf, dtype=np.float32)),
+}
+
+
+def _clip_failures(impl):
+    failed = []
+    for pin in pins.CLIP_PINS:
+        try:
+            pin(impl)
+        except (AssertionError, ValueError, FloatingPointError, IndexError):
+            failed.append(pin.__name__)
+    return failed
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_CLIP))
+def test_clip_mutant_is_caught(name):
+    failed = _clip_failures(MUTANTS_CLIP[name])
+    if name == "reference_copy_is_clean":
+        assert failed == [], failed
+    else:
+        assert failed, f"mutant {name} passed every clip pin"

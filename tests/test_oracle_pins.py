@@ -11,6 +11,11 @@ def test_oracle_pin(pin):
     pin(oracle.softmax_clipped)
 
 
+@pytest.mark.parametrize("pin", pins.CLIP_PINS, ids=lambda p: p.__name__)
+def test_oracle_clip_pin(pin):
+    pin(oracle.softmax_clipped)
+
+
 def test_row_max_exact_and_nan():
     rng = np.random.default_rng(3)
     x = rng.standard_normal((9, 77)).astype(np.float32)
