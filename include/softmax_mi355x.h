@@ -33,11 +33,20 @@ extern "C" {
 
 #define SOFTMAX_API __attribute__((visibility("default")))
 
-/* Lower bound applied to the shifted logit x - rowmax before exp.  The
- * paper's reference functor clips here (Sec. 1.2 Fig. 1; purpose in
- * Sec. 2.1) without printing the constant; this library fixes it at -64,
- * so no output is 0 and none is denormal for any row length below 2^33. */
+/* Lower bound applied to the shifted logit x - rowmax before exp by
+ * softmax_fwd.  The paper's reference functor clips here (Sec. 1.2 Fig. 1;
+ * purpose in Sec. 2.1) without printing the constant; this library's
+ * default is -64, so no output is 0 and none is denormal for any row length
+ * below 2^33.  softmax_fwd_clip takes the bound as an argument. */
 #define SOFTMAX_CLIP_LO (-64.0f)
+
+/* Largest bound softmax_fwd_clip accepts.  Two parts of the kernels rely on
+ * a clipped exponential being negligible next to a row sum of at least 1:
+ * the padding of a row's last partial vector (under 4096 entries) and the
+ * chunk-local clip inside the partial sums of rows split over several
+ * workgroups (cols entries).  At -48 each adds under cols * e^-48 (below
+ * 1e-10 relative for any row that fits in memory). */
+#define SOFTMAX_CLIP_MAX (-48.0f)
 
 /* Return codes. */
 #define SOFTMAX_OK 0
@@ -105,6 +114,29 @@ extern "C" {
 SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols,
                             hipStream_t stream);
 
+/*
+ * softmax_fwd_clip -- softmax_fwd with the clip bound as an argument:
+ *
+ *     y[i,j] = exp(max(x[i,j] - M_i, clip_lo)) / sum_k exp(max(x[i,k] - M_i, clip_lo))
+ *
+ * clip_lo = -INFINITY turns the clip off, which is the paper's optimised
+ * functor (Sec. 2.3 Fig. 4; dropping the reference functor's ValueClip is
+ * the first optimisation of Sec. 2.1): then a -inf entry among finite ones
+ * gives exactly 0 and outputs may be denormal or 0.  Any clip_lo <=
+ * SOFTMAX_CLIP_MAX is accepted; bounds below -128 give the same fp32
+ * results as no clip.  softmax_fwd(...) is softmax_fwd_clip(..., -64, ...)
+ * bit for bit.
+ *
+ * Accuracy: every output is within 4e-6 relative plus 2^-148 absolute of
+ * the exact value (the absolute term only matters for outputs below 2^-126,
+ * which need clip_lo < -87).  All other arguments, the layout, ownership,
+ * asynchrony, workspace and error codes are those of softmax_fwd; a NaN
+ * clip_lo or one above SOFTMAX_CLIP_MAX returns SOFTMAX_ERR_INVALID_ARG
+ * with nothing launched.
+ */
+SOFTMAX_API int softmax_fwd_clip(const float* x, float* y, int64_t rows, int64_t cols,
+                                 float clip_lo, hipStream_t stream);
+
 /* Static description of a return code.  Never NULL. */
 SOFTMAX_API const char* softmax_strerror(int code);
 
@@ -129,14 +161,15 @@ SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64
                              softmax_plan_t* plan);
 
 /*
- * softmax_exp_probe -- diagnostic: e[i] = exp(max(x[i] - m[i], -64)) for
- * 0 <= i < n, through the same device routine the softmax kernels use for
- * the clipped exp (Sec. 1.2 Fig. 1, the ValueClip then exp).  x, m, e are
- * device fp32 arrays of n elements owned by the caller (e must not overlap
- * x or m).  Same error rules as softmax_fwd.
+ * softmax_exp_probe -- diagnostic: e[i] = exp(max(x[i] - m[i], clip_lo))
+ * for 0 <= i < n, through the same device routine the softmax kernels use
+ * for the clipped exp (Sec. 1.2 Fig. 1, the ValueClip then exp), with the
+ * clip_lo rules of softmax_fwd_clip.  x, m, e are device fp32 arrays of n
+ * elements owned by the caller (e must not overlap x or m).  Same error
+ * rules as softmax_fwd_clip.
  */
 SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int64_t n,
-                                  hipStream_t stream);
+                                  float clip_lo, hipStream_t stream);
 
 /*
  * softmax_copy_probe -- diagnostic: y[i] = x[i] for 0 <= i < n with 128-bit

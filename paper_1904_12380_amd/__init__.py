@@ -9,8 +9,10 @@ Functions keep the C names:
 
     softmax_fwd(x, out=None, stream=None) -> torch.Tensor
     softmax_fwd_ptr(x_ptr, y_ptr, rows, cols, stream_handle) -> int
+    softmax_fwd_clip(x, clip_lo, out=None, stream=None) -> torch.Tensor
+    softmax_fwd_clip_ptr(x_ptr, y_ptr, rows, cols, clip_lo, stream_handle) -> int
     softmax_plan(rows, cols, x_ptr=1 << 44, y_ptr=1 << 45) -> dict
-    softmax_exp_probe(x, m, out=None, stream=None) -> torch.Tensor
+    softmax_exp_probe(x, m, out=None, stream=None, clip_lo=-64.0) -> torch.Tensor
     softmax_copy_probe(x, out=None, stream=None) -> torch.Tensor
     softmax_strerror(code) -> str
     softmax_last_hip_error() -> int
@@ -22,8 +24,9 @@ import os
 
 __all__ = [
     "LIB_PATH", "HEADER_PATH", "SoftmaxError", "load_library", "softmax_fwd",
-    "softmax_fwd_ptr", "softmax_plan", "softmax_exp_probe", "softmax_copy_probe",
-    "softmax_strerror", "softmax_last_hip_error", "CLIP_LO", "KERNEL_NAMES",
+    "softmax_fwd_ptr", "softmax_fwd_clip", "softmax_fwd_clip_ptr", "softmax_plan",
+    "softmax_exp_probe", "softmax_copy_probe", "softmax_strerror", "softmax_last_hip_error",
+    "CLIP_LO", "CLIP_MAX", "KERNEL_NAMES",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -31,6 +34,7 @@ LIB_PATH = os.path.join(_PKG, "lib", "libsoftmax_mi355x.so")
 HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "softmax_mi355x.h")
 
 CLIP_LO = -64.0
+CLIP_MAX = -48.0
 OK, ERR_INVALID_ARG, ERR_HIP, ERR_NOT_DEVICE = 0, 1, 2, 3
 KERNEL_NAMES = {0: "none", 1: "packed", 2: "wave_row", 3: "block_row", 4: "split_row"}
 
@@ -74,13 +78,15 @@ def load_library() -> ctypes.CDLL:
     vp, i64 = ctypes.c_void_p, ctypes.c_int64
     lib.softmax_fwd.argtypes = [vp, vp, i64, i64, vp]
     lib.softmax_fwd.restype = ctypes.c_int
+    lib.softmax_fwd_clip.argtypes = [vp, vp, i64, i64, ctypes.c_float, vp]
+    lib.softmax_fwd_clip.restype = ctypes.c_int
     lib.softmax_strerror.argtypes = [ctypes.c_int]
     lib.softmax_strerror.restype = ctypes.c_char_p
     lib.softmax_last_hip_error.argtypes = []
     lib.softmax_last_hip_error.restype = ctypes.c_int
     lib.softmax_plan.argtypes = [vp, vp, i64, i64, ctypes.POINTER(_Plan)]
     lib.softmax_plan.restype = ctypes.c_int
-    lib.softmax_exp_probe.argtypes = [vp, vp, vp, i64, vp]
+    lib.softmax_exp_probe.argtypes = [vp, vp, vp, i64, ctypes.c_float, vp]
     lib.softmax_exp_probe.restype = ctypes.c_int
     lib.softmax_copy_probe.argtypes = [vp, vp, i64, vp]
     lib.softmax_copy_probe.restype = ctypes.c_int
@@ -139,21 +145,34 @@ def _check_f32_cuda(t, name: str):
         raise ValueError(f"{name} must be contiguous (row-major, leading dim = cols)")
 
 
-def softmax_fwd(x, out=None, stream=None):
-    """Row-wise clipped softmax of a 2-D float32 GPU tensor [rows, cols].
+def softmax_fwd_clip_ptr(x_ptr: int, y_ptr: int, rows: int, cols: int, clip_lo: float,
+                         stream_handle: int = 0) -> int:
+    """Raw C call; returns the C return code."""
+    return int(load_library().softmax_fwd_clip(x_ptr, y_ptr, rows, cols, float(clip_lo),
+                                               stream_handle))
 
-    ``out`` may be ``x`` itself (in place).  Runs on ``stream`` (default: the
-    current torch stream) and returns without synchronising."""
+
+def _out_for(x, out):
     torch = _torch()
     _check_f32_cuda(x, "x")
     if x.dim() != 2:
         raise ValueError("x must be 2-D [rows, cols]")
     if out is None:
-        out = torch.empty_like(x)
-    else:
-        _check_f32_cuda(out, "out")
-        if out.shape != x.shape or out.device != x.device:
-            raise ValueError("out must match x in shape and device")
+        return torch.empty_like(x)
+    _check_f32_cuda(out, "out")
+    if out.shape != x.shape or out.device != x.device:
+        raise ValueError("out must match x in shape and device")
+    return out
+
+
+def softmax_fwd(x, out=None, stream=None):
+    """Row-wise clipped softmax (bound -64) of a 2-D float32 GPU tensor
+    [rows, cols].
+
+    ``out`` may be ``x`` itself (in place).  Runs on ``stream`` (default: the
+    current torch stream) and returns without synchronising."""
+    torch = _torch()
+    out = _out_for(x, out)
     rows, cols = x.shape
     with torch.cuda.device(x.device):
         rc = softmax_fwd_ptr(x.data_ptr(), out.data_ptr(), rows, cols,
@@ -163,8 +182,23 @@ def softmax_fwd(x, out=None, stream=None):
     return out
 
 
-def softmax_exp_probe(x, m, out=None, stream=None):
-    """e = exp(max(x - m, -64)) elementwise through the kernels' exp routine."""
+def softmax_fwd_clip(x, clip_lo: float, out=None, stream=None):
+    """softmax_fwd with the clip bound as an argument: any value <= CLIP_MAX,
+    or -inf for no clip."""
+    torch = _torch()
+    out = _out_for(x, out)
+    rows, cols = x.shape
+    with torch.cuda.device(x.device):
+        rc = softmax_fwd_clip_ptr(x.data_ptr(), out.data_ptr(), rows, cols, clip_lo,
+                                  _stream_handle(stream))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_fwd_clip")
+    return out
+
+
+def softmax_exp_probe(x, m, out=None, stream=None, clip_lo: float = CLIP_LO):
+    """e = exp(max(x - m, clip_lo)) elementwise through the kernels' exp
+    routine."""
     torch = _torch()
     _check_f32_cuda(x, "x")
     _check_f32_cuda(m, "m")
@@ -175,7 +209,8 @@ def softmax_exp_probe(x, m, out=None, stream=None):
     _check_f32_cuda(out, "out")
     with torch.cuda.device(x.device):
         rc = int(load_library().softmax_exp_probe(
-            x.data_ptr(), m.data_ptr(), out.data_ptr(), x.numel(), _stream_handle(stream)))
+            x.data_ptr(), m.data_ptr(), out.data_ptr(), x.numel(), float(clip_lo),
+            _stream_handle(stream)))
     if rc != OK:
         raise SoftmaxError(rc, "softmax_exp_probe")
     return out

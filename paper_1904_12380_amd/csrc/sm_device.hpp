@@ -1,11 +1,12 @@
 // Device primitives for the clipped row softmax on CDNA4 (gfx950, wave64).
 //
-//   * exp_shift_clip(): e = exp(max(x - M, -64)) with the shift and the exp
+//   * exp_shift_clip(): e = exp(max(x - M, lo)) with the shift and the exp
 //     argument in binary64 (full rate on gfx950) and v_exp_f32 on the fp32
 //     part, so the result is within 1.5 ulp of the exact value over the
 //     whole clipped range (the clip is the ValueClip of the paper's
-//     reference functor, Sec. 1.2 Fig. 1; the bound -64 is this library's
-//     documented choice).
+//     reference functor, Sec. 1.2 Fig. 1; the default bound -64 is this
+//     library's documented choice, and lo = -inf, no clip, is the optimised
+//     functor of Sec. 2.3 Fig. 4).
 //   * seg_max / seg_sum: reductions over aligned groups of W lanes using DPP
 //     (quad_perm, row_half_mirror, row_mirror) inside a 16-lane row and the
 //     gfx950 permlane16/permlane32 swaps across rows.  These play the part of
@@ -24,10 +25,25 @@
 
 namespace smx {
 
-// Lower bound applied to the shifted logit x - max before exp.
+// Default lower bound applied to the shifted logit x - max before exp, and
+// RN(e^-64), the value of every exponential it clips.
 constexpr float kClipLo = -64.0f;
-// RN(e^-64): the value of every clipped exponential.
 constexpr float kExpClipLo = 0x1.969d48p-93f;  // 1.6038109e-28
+
+// Other bounds.  Bounds below kClipFloor, and no clip at all, run as
+// kClipFloor with a clipped value of 0: every fp32 exponential below
+// e^-103.98 rounds to 0, so the outputs are the same.  Bounds below
+// kClipWide let unclipped exponentials fall under 2^-126 (denormal or 0),
+// which needs the wide form of exp_shift_clip.
+constexpr float kClipFloor = -128.0f;
+constexpr float kClipWide = -87.0f;
+
+// The clip as a kernel argument: lo in [kClipFloor, 0] and e_lo = RN(e^lo')
+// for the caller's bound lo' (0 when lo' < -103.98 or lo' = -inf).
+struct Clip {
+  float lo;
+  float e_lo;
+};
 
 // RN(log2 e) and RN(ln 2) in binary64.
 constexpr double kLog2e = 0x1.71547652b82fep+0;
@@ -48,50 +64,69 @@ __device__ __forceinline__ void st_stream(float* p, f32x4 v) {
 
 // Per-row constants of the shifted, clipped exponential.
 //   neg_m: -M in binary64.
-//   tc:    the smallest fp32 value >= M - 64 (computed exactly), so that for
-//          every fp32 x:  x < tc  <=>  x - M < -64.  The clip test is then one
+//   tc:    the smallest fp32 value >= M + lo (computed exactly), so that for
+//          every fp32 x:  x < tc  <=>  x - M < lo.  The clip test is then one
 //          fp32 compare per element.  M = NaN gives tc = NaN (no element is
 //          clipped and NaN propagates); M = -inf gives tc = -inf.
+//   e_lo:  the value of a clipped exponential.
 struct RowShift {
   double neg_m;
   float tc;
+  float e_lo;
 };
 
-__device__ __forceinline__ RowShift row_shift(float m) {
+__device__ __forceinline__ RowShift row_shift(float m, Clip clip) {
   RowShift r;
   r.neg_m = -static_cast<double>(m);
-  // M - 64 is exact in binary64 unless |M| < 2^-23, where the rounding is
-  // below 2^-47 and only moves the boundary by that much.
-  const double s = static_cast<double>(m) - 64.0;
+  // M + lo is exact in binary64 unless the exponents of M and lo differ by
+  // more than 29 (|M| < 2^-23 |lo|), where the rounding is below 2^-47 |lo|
+  // and only moves the boundary by that much.
+  const double s = static_cast<double>(m) + static_cast<double>(clip.lo);
   float f = static_cast<float>(s);
   if (static_cast<double>(f) < s) {
-    // next fp32 towards +inf (f < s <= M - 64 <= f + ulp, f finite)
+    // next fp32 towards +inf (f < s <= f + ulp, f finite)
     const unsigned u = __builtin_bit_cast(unsigned, f);
     f = __builtin_bit_cast(float, f < 0.0f ? u - 1u : (f == 0.0f ? 1u : u + 1u));
   }
   r.tc = f;
+  r.e_lo = clip.e_lo;
   return r;
 }
 
-// exp(max(x - M, -64)) for fp32 x, within 1.5 ulp of the exact value.
+// exp(max(x - M, lo)) for fp32 x, within 1.5 ulp of the exact value where
+// that is a normal fp32, and within 2^-150 plus 1.5 ulp-relative (the error
+// carried into the final rounding onto the denormal grid) below it.
 //
 // 1. d = x - M in binary64: exact whenever the exponents of x and M differ by
 //    at most 29; otherwise its relative error is below 2^-53.
 // 2. t = d * log2(e) in binary64, th = RN32(t), and the remainder
 //    r = d - th * ln2 from one binary64 fma (|r| <= 2^-18 * ln2 = 2.6e-6).
 // 3. e = 2^th * e^r = v_exp_f32(th) * (1 + r), rounded once by an fp32 fma;
-//    the dropped r^2/2 is below 4e-12.  For unclipped x, th is in
-//    [-92.34, 0], where 2^th is a normal fp32.
-// 4. Clipped elements (x < tc) return RN(e^-64) exactly; this also covers
-//    x = -inf.  NaN inputs, and rows whose max is +inf or -inf, give NaN.
+//    the dropped r^2/2 is below 4e-12.  With lo >= kClipWide, th stays in
+//    [-125.6, 0], where 2^th is a normal fp32.
+// 4. WIDE (lo < kClipWide): v_exp_f32 returns no denormals, so for
+//    th < -126 the fma works on 2^(th+64) (exact shift, th >= -185 since
+//    lo >= kClipFloor) and one final multiplication by 2^-64 rounds the
+//    result into the denormal range.
+// 5. Clipped elements (x < tc) return e_lo; this also covers x = -inf.
+//    NaN inputs, and rows whose max is +inf or -inf, give NaN.
+template <bool WIDE>
 __device__ __forceinline__ float exp_shift_clip(float x, RowShift rs) {
   const double d = static_cast<double>(x) + rs.neg_m;
   const double t = d * kLog2e;
   const float th = static_cast<float>(t);
   const double r = __builtin_fma(static_cast<double>(th), -kLn2, d);
-  const float e0 = __builtin_amdgcn_exp2f(th);
-  const float e = __builtin_fmaf(e0, static_cast<float>(r), e0);
-  return x < rs.tc ? kExpClipLo : e;
+  float e;
+  if constexpr (WIDE) {
+    const bool tiny = th < -126.0f;
+    const float e0 = __builtin_amdgcn_exp2f(tiny ? th + 64.0f : th);
+    const float ew = __builtin_fmaf(e0, static_cast<float>(r), e0);
+    e = tiny ? ew * 0x1p-64f : ew;
+  } else {
+    const float e0 = __builtin_amdgcn_exp2f(th);
+    e = __builtin_fmaf(e0, static_cast<float>(r), e0);
+  }
+  return x < rs.tc ? rs.e_lo : e;
 }
 
 // ---------------------------------------------------------------------------

@@ -1,20 +1,26 @@
 // HIP kernels for the clipped row softmax on gfx950.
 //
 // Every kernel computes, per row of a row-major [rows, cols] fp32 matrix,
-//   y = exp(max(x - rowmax, -64)) / sum(exp(max(x - rowmax, -64)))
+//   y = exp(max(x - rowmax, lo)) / sum(exp(max(x - rowmax, lo)))
 // in the order of the paper's optimised functor (Sec. 2.3, Fig. 4: row max,
 // subtract, exp, row sum, scale by the reciprocal of the sum) with the clip
-// of the reference functor (Sec. 1.2, Fig. 1).  Unlike that CPU functor, no
-// kernel uses y as scratch: x is read from HBM once (twice for split rows)
+// of the reference functor (Sec. 1.2, Fig. 1) at a bound lo given as a
+// kernel argument (default -64; no clip runs as the floor bound with a
+// clipped value of 0).  WIDE instances handle bounds whose unclipped
+// exponentials can be denormal.  Unlike the CPU functor, no kernel uses y
+// as scratch: x is read from HBM once (twice for rows over 2^21 columns)
 // and y is written once.
 //
-//   k_packed      cols <= 64: a workgroup stages a tile of whole rows in LDS
-//                 with 128-bit loads, then groups of G lanes reduce one row
-//                 each with DPP, then the tile goes back out with 128-bit
-//                 stores.
+//   k_packed      cols <= 64: a persistent workgroup stages tiles of whole
+//                 rows in LDS with 128-bit loads, groups of G lanes reduce
+//                 one row each with DPP, and the tile goes back out with
+//                 128-bit stores; the next tile's loads are issued early.
 //   k_wave_row    cols <= 4096: one wavefront per row, the row held in VGPRs.
 //   k_block_row   cols <= 32768: one workgroup per row, the row held in
 //                 VGPRs, per-wave partials combined through LDS.
+//   k_split_onepass   rows of up to 64 chunks: one workgroup per chunk,
+//                 partials exchanged between the row's workgroups in the
+//                 middle of the kernel, x read once.
 //   k_split_stats / k_split_apply   longer rows: G workgroups per row; the
 //                 first pass writes a (max, sum) partial per chunk, the
 //                 second merges them and writes the chunk's outputs.
@@ -64,8 +70,9 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 // 32-bit (a segment is at most 2^20 columns), so the address is one base
 // register plus a 32-bit lane offset.  Columns at or past `lim` read as
 // -inf: they take part in the max as a neutral value and their clipped
-// exponential (e^-64) changes a row sum of at least 1 by under 1e-24
-// relative, so no per-element mask is needed later.  Strip j covers
+// exponential (e^lo with lo <= -48, or 0 with no clip) changes a row sum of
+// at least 1 by under 4096 e^-48 < 1e-17 relative, so no per-element mask
+// is needed later.  Strip j covers
 // [4*stride*j, 4*stride*(j+1)); when all of it is inside the segment (a
 // uniform test) no lane is masked.
 template <int V, bool VEC4>
@@ -101,10 +108,10 @@ __device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* p, in
 
 // Replaces v by the clipped exponentials and returns this lane's pairwise
 // partial sum.
-template <int N>
+template <bool WIDE, int N>
 __device__ __forceinline__ float exp_strip(float (&v)[N], RowShift rs) {
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = exp_shift_clip(v[i], rs);
+  for (int i = 0; i < N; ++i) v[i] = exp_shift_clip<WIDE>(v[i], rs);
   return tree_sum(v);
 }
 
@@ -151,8 +158,9 @@ __device__ __forceinline__ int seg_len(int64_t cols, int64_t c0, int64_t cap) {
 // The grid is persistent (a few workgroups per CU, each looping over tiles)
 // and every workgroup issues the loads of its next tile right after staging
 // the current one, so they are in flight while the current tile computes.
-template <int G, int EPL>
-__device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int r, int j) {
+template <int G, int EPL, bool WIDE>
+__device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int r, int j,
+                                            Clip clip) {
   const bool active = r < nr;
   float* tr = tile + r * ccols;
   float v[EPL];
@@ -161,9 +169,9 @@ __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int 
     const int c = j + G * k;
     v[k] = (active && c < ccols) ? tr[c] : kNegInf;
   }
-  const RowShift rs = row_shift(seg_max<G>(array_max(v)));
+  const RowShift rs = row_shift(seg_max<G>(array_max(v)), clip);
 #pragma unroll
-  for (int k = 0; k < EPL; ++k) v[k] = exp_shift_clip(v[k], rs);
+  for (int k = 0; k < EPL; ++k) v[k] = exp_shift_clip<WIDE>(v[k], rs);
   const float rcp = 1.0f / seg_sum<G>(tree_sum(v));
 #pragma unroll
   for (int k = 0; k < EPL; ++k) {
@@ -172,9 +180,9 @@ __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int 
   }
 }
 
-template <int G, int EPL, bool VEC4>
+template <int G, int EPL, bool VEC4, bool WIDE>
 __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_t rows,
-                                                int64_t cols) {
+                                                int64_t cols, Clip clip) {
   constexpr int kRows = 256 / G;
   constexpr int kTileFloats = kRows * G * EPL;  // = 256 * EPL
   constexpr int kPer = VEC4 ? (kTileFloats / 4 + 255) / 256 : (kTileFloats + 255) / 256;
@@ -239,7 +247,7 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
     __syncthreads();
     if (t + gridDim.x < ntiles) issue(t + gridDim.x);
 
-    packed_rows<G, EPL>(tile, nr, ccols, r, j);
+    packed_rows<G, EPL, WIDE>(tile, nr, ccols, r, j, clip);
     __syncthreads();
 
     if constexpr (VEC4) {
@@ -257,9 +265,9 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
 // ---------------------------------------------------------------------------
 // (b) One wavefront per row, cols <= 256*V (4*V elements per lane).
 // Four wavefronts per workgroup work on four rows independently.
-template <int V, bool VEC4>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_wave_row(const float* x, float* y, int64_t rows,
-                                                  int64_t cols) {
+template <int V, bool VEC4, bool WIDE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_wave_row(
+    const float* x, float* y, int64_t rows, int64_t cols, Clip clip) {
   const int lane = __lane_id();
   const int wave = threadIdx.x >> 6;
   for (int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wave; row < rows;
@@ -269,8 +277,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
     const int lim = static_cast<int>(cols);
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, lane, 64, lim);
-    const RowShift rs = row_shift(seg_max<64>(array_max(v)));
-    const float s = seg_sum<64>(exp_strip(v, rs));
+    const RowShift rs = row_shift(seg_max<64>(array_max(v)), clip);
+    const float s = seg_sum<64>(exp_strip<WIDE>(v, rs));
     const float rcp = 1.0f / s;
     store_strip<V, VEC4>(v, rcp, yr, lane, 64, lim);
   }
@@ -278,9 +286,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
 
 // ---------------------------------------------------------------------------
 // (c) One workgroup of NT threads per row, cols <= 4*V*NT.
-template <int NT, int V, bool VEC4>
+template <int NT, int V, bool VEC4, bool WIDE>
 __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int64_t rows,
-                                                  int64_t cols) {
+                                                  int64_t cols, Clip clip) {
   constexpr int NW = NT / 64;
   __shared__ float red_max[NW];
   __shared__ float red_sum[NW];
@@ -291,8 +299,8 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int6
     const int lim = static_cast<int>(cols);
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, tid, NT, lim);
-    const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max));
-    const float s = block_sum<NW>(exp_strip(v, rs), red_sum);
+    const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max), clip);
+    const float s = block_sum<NW>(exp_strip<WIDE>(v, rs), red_sum);
     const float rcp = 1.0f / s;
     store_strip<V, VEC4>(v, rcp, yr, tid, NT, lim);
   }
@@ -303,20 +311,20 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int6
 // workgroups per row, CH = 4*V*NT columns each.
 //
 // Pass 1 writes part[row*G + g] = (m_g, s_g): the chunk max and the chunk's
-// sum of exp(max(x - m_g, -64)).  A chunk whose max is -inf stores s_g = its
-// element count, so that the merge below gives count * e^-64, the clipped
+// sum of exp(max(x - m_g, lo)).  A chunk whose max is -inf stores s_g = its
+// element count, so that the merge below gives count * e_lo, the clipped
 // value of its -inf elements.
 //
 // Pass 2 merges a row's partials (every wavefront of the workgroup does the
 // same merge, so all hold the same bits):  M = max_g m_g,
-// S = sum_g s_g * exp(max(m_g - M, -64)), then writes
-// y = exp(max(x - M, -64)) / S.  Using the clip relative to m_g inside a
-// partial changes S by at most cols * e^-64 relative (below 1e-22 at any
-// supported length), far under fp32 resolution.
-template <int NT, int V, bool VEC4>
+// S = sum_g s_g * exp(max(m_g - M, lo)), then writes
+// y = exp(max(x - M, lo)) / S.  Using the clip relative to m_g inside a
+// partial changes S by at most cols * e^lo relative (below 1e-10 for any
+// row that fits in memory, since lo <= -48), far under fp32 resolution.
+template <int NT, int V, bool VEC4, bool WIDE>
 __global__ __launch_bounds__(NT) void k_split_stats(const float* x, float2* part,
                                                     int64_t rows, int64_t cols,
-                                                    int64_t chunks) {
+                                                    int64_t chunks, Clip clip) {
   constexpr int NW = NT / 64;
   constexpr int64_t CH = int64_t(4) * V * NT;
   __shared__ float red_max[NW];
@@ -333,17 +341,17 @@ __global__ __launch_bounds__(NT) void k_split_stats(const float* x, float2* part
     load_strip<V, VEC4>(v, xr, tid, NT, lim);
     const float m = block_max<NW>(array_max(v), red_max);
     const bool empty_max = (m == kNegInf);
-    const RowShift rs = row_shift(empty_max ? 0.0f : m);
-    float s = block_sum<NW>(exp_strip(v, rs), red_sum);
+    const RowShift rs = row_shift(empty_max ? 0.0f : m, clip);
+    float s = block_sum<NW>(exp_strip<WIDE>(v, rs), red_sum);
     if (empty_max) s = static_cast<float>(lim);
     if (tid == 0) part[b] = make_float2(m, s);
   }
 }
 
-template <int NT, int V, bool VEC4>
+template <int NT, int V, bool VEC4, bool WIDE>
 __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
                                                     const float2* part, int64_t rows,
-                                                    int64_t cols, int64_t chunks) {
+                                                    int64_t cols, int64_t chunks, Clip clip) {
   constexpr int64_t CH = int64_t(4) * V * NT;
   const int tid = threadIdx.x;
   const int lane = __lane_id();
@@ -361,16 +369,16 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
     const float2* pr = part + row * chunks;
     float mm = kNegInf;
     for (int64_t l = lane; l < chunks; l += 64) mm = fmaxf(mm, pr[l].x);
-    const RowShift rs = row_shift(seg_max<64>(mm));
+    const RowShift rs = row_shift(seg_max<64>(mm), clip);
     float ss = 0.0f;
     for (int64_t l = lane; l < chunks; l += 64) {
       const float2 p = pr[l];
-      ss = ss + p.y * exp_shift_clip(p.x, rs);
+      ss = ss + p.y * exp_shift_clip<WIDE>(p.x, rs);
     }
     const float rcp = 1.0f / seg_sum<64>(ss);
 
 #pragma unroll
-    for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip(v[i], rs);
+    for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip<WIDE>(v[i], rs);
     store_strip<V, VEC4>(v, rcp, yr, tid, NT, lim);
   }
 }
@@ -379,13 +387,13 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
 // (c, split, one pass) The G workgroups of a row exchange partials in the
 // middle of the kernel, so x is read from HBM exactly once.
 //
-// Workgroup (row, g) keeps e = exp(max(x - m_g, -64)) of its chunk in
+// Workgroup (row, g) keeps e = exp(max(x - m_g, lo)) of its chunk in
 // registers and publishes (m_g, s_g) in its slot part[row*G + g].  Wave 0
 // polls the row's G slots until none holds the sentinel, merges them into M
 // and S, and every thread writes
-//     y = max(e * exp(m_g - M), e^-64) / S.
-// For an element with x - M >= -64 the rescaled e equals exp(x - M) >= e^-64;
-// for x - M < -64 it is below e^-64, so the max is exactly the clip of the
+//     y = max(e * exp(m_g - M), e_lo) / S.
+// For an element with x - M >= lo the rescaled e equals exp(x - M) >= e^lo;
+// for x - M < lo it is below e^lo, so the max is exactly the clip of the
 // definition.  A NaN element makes s_g, hence S and the whole row, NaN.
 //
 // Slots hold kSlotEmpty between launches.  After reading, each workgroup
@@ -415,10 +423,10 @@ __device__ __forceinline__ unsigned long long pack_pair(float a, float b) {
          (static_cast<unsigned long long>(__builtin_bit_cast(unsigned, b)) << 32);
 }
 
-template <int NT, int V, bool VEC4>
+template <int NT, int V, bool VEC4, bool WIDE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 : 4))) void k_split_onepass(
     const float* x, float* y, unsigned long long* part, unsigned* depart, int64_t cols,
-    int chunks) {
+    int chunks, Clip clip) {
   constexpr int NW = NT / 64;
   constexpr int64_t CH = int64_t(4) * V * NT;
   __shared__ float red_max[NW];
@@ -437,7 +445,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 :
   load_strip<V, VEC4>(v, xr, tid, NT, lim);
   const float m = block_max<NW>(array_max(v), red_max);
   const bool empty_max = (m == kNegInf);
-  float s = block_sum<NW>(exp_strip(v, row_shift(empty_max ? 0.0f : m)), red_sum);
+  float s = block_sum<NW>(exp_strip<WIDE>(v, row_shift(empty_max ? 0.0f : m, clip)), red_sum);
   if (empty_max) s = static_cast<float>(lim);
 
   if (tid == 0) {
@@ -464,12 +472,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 :
     const float pm = (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q)) : kNegInf;
     const float ps =
         (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q >> 32)) : 0.0f;
-    const RowShift rs = row_shift(seg_max<64>(pm));
-    const float term = (tid < chunks) ? ps * exp_shift_clip(pm, rs) : 0.0f;
+    const RowShift rs = row_shift(seg_max<64>(pm), clip);
+    const float term = (tid < chunks) ? ps * exp_shift_clip<WIDE>(pm, rs) : 0.0f;
     const float rcp = 1.0f / seg_sum<64>(term);
     if (tid == 0) {
-      bcast[0] = ok ? exp_shift_clip(m, rs) * rcp : __builtin_nanf("");  // e^(m_g - M) / S
-      bcast[1] = ok ? kExpClipLo * rcp : __builtin_nanf("");             // e^-64 / S
+      bcast[0] = ok ? exp_shift_clip<WIDE>(m, rs) * rcp : __builtin_nanf("");  // e^(m_g - M) / S
+      bcast[1] = ok ? clip.e_lo * rcp : __builtin_nanf("");                    // e_lo / S
       // Depart once this wave's slot reads have returned (the add's operand
       // depends on them); the last workgroup of the row restores the slots.
       unsigned one = 1u;
@@ -494,13 +502,14 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 :
 // ---------------------------------------------------------------------------
 // Diagnostics.
 
-// e[i] = exp(max(x[i] - m[i], -64)), through the same device routine the
+// e[i] = exp(max(x[i] - m[i], lo)), through the same device routine the
 // softmax kernels use.
+template <bool WIDE>
 __global__ __launch_bounds__(256) void k_exp_probe(const float* x, const float* m,
-                                                   float* e, int64_t n) {
+                                                   float* e, int64_t n, Clip clip) {
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
        i += static_cast<int64_t>(gridDim.x) * 256)
-    e[i] = exp_shift_clip(x[i], row_shift(m[i]));
+    e[i] = exp_shift_clip<WIDE>(x[i], row_shift(m[i], clip));
 }
 
 // Plain copy with 128-bit streaming accesses: the memory-bound ceiling that

@@ -3,6 +3,7 @@
 // include/softmax_mi355x.h.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <mutex>
 #include <utility>
 #include <vector>
@@ -233,91 +234,99 @@ hipError_t launch(const void* fn, int64_t grid, int block, void** args, hipStrea
 
 // k_packed instances: G = 1 with EPL = 1..16, G = 2 and G = 4 with
 // EPL = 9..16 (a plan never asks for fewer columns per lane at G > 1).
-template <int G, bool VEC4, int... E>
+template <int G, bool VEC4, bool WIDE, int... E>
 const void* packed_fn(int epl, std::integer_sequence<int, E...>) {
   static const void* const table[] = {
-      reinterpret_cast<const void*>(&k_packed<G, (G == 1 ? 1 : 9) + E, VEC4>)...};
+      reinterpret_cast<const void*>(&k_packed<G, (G == 1 ? 1 : 9) + E, VEC4, WIDE>)...};
   const int idx = epl - (G == 1 ? 1 : 9);
   return (idx >= 0 && idx < static_cast<int>(sizeof...(E))) ? table[idx] : nullptr;
 }
 
-template <bool VEC4>
+template <bool VEC4, bool WIDE>
 hipError_t dispatch_packed(const softmax_plan_t& p, const float* x, float* y,
-                           int64_t rows, int64_t cols, hipStream_t s) {
+                           int64_t rows, int64_t cols, Clip c, hipStream_t s) {
   const void* fn = nullptr;
   switch (p.lanes_per_row) {
-    case 1: fn = packed_fn<1, VEC4>(p.elems_per_lane, std::make_integer_sequence<int, 16>{}); break;
-    case 2: fn = packed_fn<2, VEC4>(p.elems_per_lane, std::make_integer_sequence<int, 8>{}); break;
-    default: fn = packed_fn<4, VEC4>(p.elems_per_lane, std::make_integer_sequence<int, 8>{}); break;
+    case 1:
+      fn = packed_fn<1, VEC4, WIDE>(p.elems_per_lane, std::make_integer_sequence<int, 16>{});
+      break;
+    case 2:
+      fn = packed_fn<2, VEC4, WIDE>(p.elems_per_lane, std::make_integer_sequence<int, 8>{});
+      break;
+    default:
+      fn = packed_fn<4, VEC4, WIDE>(p.elems_per_lane, std::make_integer_sequence<int, 8>{});
+      break;
   }
   if (fn == nullptr) return hipErrorInvalidValue;
-  void* args[] = {&x, &y, &rows, &cols};
+  void* args[] = {&x, &y, &rows, &cols, &c};
   return launch(fn, p.grid, 256, args, s);
 }
 
-template <int V, bool VEC4>
-hipError_t run_wave(const float* x, float* y, int64_t rows, int64_t cols, int64_t grid,
-                    hipStream_t s) {
-  void* args[] = {&x, &y, &rows, &cols};
-  return launch(reinterpret_cast<const void*>(&k_wave_row<V, VEC4>), grid, 256, args, s);
+template <int V, bool VEC4, bool WIDE>
+hipError_t run_wave(const float* x, float* y, int64_t rows, int64_t cols, Clip c,
+                    int64_t grid, hipStream_t s) {
+  void* args[] = {&x, &y, &rows, &cols, &c};
+  return launch(reinterpret_cast<const void*>(&k_wave_row<V, VEC4, WIDE>), grid, 256, args,
+                s);
 }
 
-template <bool VEC4>
+template <bool VEC4, bool WIDE>
 hipError_t dispatch_wave(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
-                         int64_t cols, hipStream_t s) {
+                         int64_t cols, Clip c, hipStream_t s) {
   switch (p.elems_per_lane / 4) {
-    case 1: return run_wave<1, VEC4>(x, y, rows, cols, p.grid, s);
-    case 2: return run_wave<2, VEC4>(x, y, rows, cols, p.grid, s);
-    case 4: return run_wave<4, VEC4>(x, y, rows, cols, p.grid, s);
-    case 8: return run_wave<8, VEC4>(x, y, rows, cols, p.grid, s);
-    default: return run_wave<16, VEC4>(x, y, rows, cols, p.grid, s);
+    case 1: return run_wave<1, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
+    case 2: return run_wave<2, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
+    case 4: return run_wave<4, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
+    case 8: return run_wave<8, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
+    default: return run_wave<16, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
   }
 }
 
-template <int V, bool VEC4>
-hipError_t run_block(const float* x, float* y, int64_t rows, int64_t cols, int64_t grid,
-                     hipStream_t s) {
-  void* args[] = {&x, &y, &rows, &cols};
-  return launch(reinterpret_cast<const void*>(&k_block_row<1024, V, VEC4>), grid, 1024,
+template <int V, bool VEC4, bool WIDE>
+hipError_t run_block(const float* x, float* y, int64_t rows, int64_t cols, Clip c,
+                     int64_t grid, hipStream_t s) {
+  void* args[] = {&x, &y, &rows, &cols, &c};
+  return launch(reinterpret_cast<const void*>(&k_block_row<1024, V, VEC4, WIDE>), grid, 1024,
                 args, s);
 }
 
-template <bool VEC4>
+template <bool VEC4, bool WIDE>
 hipError_t dispatch_block(const softmax_plan_t& p, const float* x, float* y,
-                          int64_t rows, int64_t cols, hipStream_t s) {
+                          int64_t rows, int64_t cols, Clip c, hipStream_t s) {
   switch (p.elems_per_lane / 4) {
-    case 2: return run_block<2, VEC4>(x, y, rows, cols, p.grid, s);
-    case 4: return run_block<4, VEC4>(x, y, rows, cols, p.grid, s);
-    default: return run_block<8, VEC4>(x, y, rows, cols, p.grid, s);
+    case 2: return run_block<2, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
+    case 4: return run_block<4, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
+    default: return run_block<8, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
   }
 }
 
-template <bool VEC4>
+template <bool VEC4, bool WIDE>
 hipError_t run_split(const float* x, float* y, float2* ws, int64_t rows, int64_t cols,
-                     int64_t chunks, hipStream_t s) {
+                     int64_t chunks, Clip c, hipStream_t s) {
   const int64_t rows_per_batch = std::max<int64_t>(1, kWorkspacePairs / chunks);
   for (int64_t r0 = 0; r0 < rows; r0 += rows_per_batch) {
     int64_t nb = std::min(rows_per_batch, rows - r0);
     const float* xb = x + r0 * cols;
     float* yb = y + r0 * cols;
     const int64_t grid = std::min(nb * chunks, kMaxGrid);
-    void* a1[] = {&xb, &ws, &nb, &cols, &chunks};
+    void* a1[] = {&xb, &ws, &nb, &cols, &chunks, &c};
     hipError_t e = launch(
-        reinterpret_cast<const void*>(&k_split_stats<kSplitThreads, kSplitV, VEC4>), grid,
-        kSplitThreads, a1, s);
+        reinterpret_cast<const void*>(&k_split_stats<kSplitThreads, kSplitV, VEC4, WIDE>),
+        grid, kSplitThreads, a1, s);
     if (e != hipSuccess) return e;
     const float2* wsc = ws;
-    void* a2[] = {&xb, &yb, &wsc, &nb, &cols, &chunks};
-    e = launch(reinterpret_cast<const void*>(&k_split_apply<kSplitThreads, kSplitV, VEC4>),
-               grid, kSplitThreads, a2, s);
+    void* a2[] = {&xb, &yb, &wsc, &nb, &cols, &chunks, &c};
+    e = launch(
+        reinterpret_cast<const void*>(&k_split_apply<kSplitThreads, kSplitV, VEC4, WIDE>),
+        grid, kSplitThreads, a2, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
-template <int V, bool VEC4>
+template <int V, bool VEC4, bool WIDE>
 hipError_t run_onepass(const float* x, float* y, char* ws, int64_t rows, int64_t cols,
-                       int64_t chunks, int64_t max_blocks, hipStream_t s) {
+                       int64_t chunks, int64_t max_blocks, Clip c, hipStream_t s) {
   unsigned long long* part = reinterpret_cast<unsigned long long*>(ws + kSlotsOffset);
   unsigned* depart = reinterpret_cast<unsigned*>(ws + kDepartOffset);
   const int64_t rows_per_launch = max_blocks / chunks;
@@ -326,9 +335,9 @@ hipError_t run_onepass(const float* x, float* y, char* ws, int64_t rows, int64_t
     const int64_t nb = std::min(rows_per_launch, rows - r0);
     const float* xb = x + r0 * cols;
     float* yb = y + r0 * cols;
-    void* args[] = {&xb, &yb, &part, &depart, &cols, &ichunks};
+    void* args[] = {&xb, &yb, &part, &depart, &cols, &ichunks, &c};
     hipError_t e = launch(
-        reinterpret_cast<const void*>(&k_split_onepass<kOnePassThreads, V, VEC4>),
+        reinterpret_cast<const void*>(&k_split_onepass<kOnePassThreads, V, VEC4, WIDE>),
         nb * chunks, kOnePassThreads, args, s);
     if (e != hipSuccess) return e;
   }
@@ -396,8 +405,23 @@ int workspace_for(int dev, hipStream_t s, bool capturing, char** out) {
   return SOFTMAX_OK;
 }
 
+template <bool VEC4, bool WIDE>
+hipError_t split_launch(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
+                        int64_t cols, char* ws, Clip c, hipStream_t s) {
+  // Plans with at most kOnePassMaxChunks chunks per row are one-pass (their
+  // chunk size is told by elems_per_lane); longer rows are two-pass.
+  const int64_t g = p.chunks_per_row;
+  if (g <= kOnePassMaxChunks && p.elems_per_lane == 4 * kOnePassVSmall)
+    return run_onepass<kOnePassVSmall, VEC4, WIDE>(x, y, ws, rows, cols, g,
+                                                   kOnePassMaxBlocksSmall, c, s);
+  if (g <= kOnePassMaxChunks)
+    return run_onepass<kOnePassVLarge, VEC4, WIDE>(x, y, ws, rows, cols, g,
+                                                   kOnePassMaxBlocksLarge, c, s);
+  return run_split<VEC4, WIDE>(x, y, reinterpret_cast<float2*>(ws), rows, cols, g, c, s);
+}
+
 int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
-               int64_t cols, int dev, hipStream_t s) {
+               int64_t cols, int dev, Clip c, bool wide, hipStream_t s) {
   if (dev < 0 || dev >= kMaxDevices) return SOFTMAX_ERR_INVALID_ARG;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
   hipError_t e = hipStreamIsCapturing(s, &cap);
@@ -408,23 +432,43 @@ int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
     const int rc = workspace_for(dev, s, cap != hipStreamCaptureStatusNone, &ws);
     if (rc != SOFTMAX_OK) return rc;
   }
-  // Plans with at most kOnePassMaxChunks chunks per row are one-pass (their
-  // chunk size is told by elems_per_lane); longer rows are two-pass.
-  const int64_t g = p.chunks_per_row;
-  if (g <= kOnePassMaxChunks && p.elems_per_lane == 4 * kOnePassVSmall) {
-    e = p.vec_width == 4
-            ? run_onepass<kOnePassVSmall, true>(x, y, ws, rows, cols, g, kOnePassMaxBlocksSmall, s)
-            : run_onepass<kOnePassVSmall, false>(x, y, ws, rows, cols, g, kOnePassMaxBlocksSmall, s);
-  } else if (g <= kOnePassMaxChunks) {
-    e = p.vec_width == 4
-            ? run_onepass<kOnePassVLarge, true>(x, y, ws, rows, cols, g, kOnePassMaxBlocksLarge, s)
-            : run_onepass<kOnePassVLarge, false>(x, y, ws, rows, cols, g, kOnePassMaxBlocksLarge, s);
-  } else {
-    float2* part = reinterpret_cast<float2*>(ws);
-    e = p.vec_width == 4 ? run_split<true>(x, y, part, rows, cols, p.chunks_per_row, s)
-                         : run_split<false>(x, y, part, rows, cols, p.chunks_per_row, s);
-  }
+  if (p.vec_width == 4)
+    e = wide ? split_launch<true, true>(p, x, y, rows, cols, ws, c, s)
+             : split_launch<true, false>(p, x, y, rows, cols, ws, c, s);
+  else
+    e = wide ? split_launch<false, true>(p, x, y, rows, cols, ws, c, s)
+             : split_launch<false, false>(p, x, y, rows, cols, ws, c, s);
   return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
+}
+
+// The clip as the kernels take it, from the caller's bound: NaN and bounds
+// above SOFTMAX_CLIP_MAX are rejected; bounds below kClipFloor (and -inf)
+// run at kClipFloor with clipped value RN(e^bound) = 0.
+int make_clip(float clip_lo, Clip* c, bool* wide) {
+  if (!(clip_lo <= SOFTMAX_CLIP_MAX)) return SOFTMAX_ERR_INVALID_ARG;  // NaN too
+  c->lo = clip_lo < kClipFloor ? kClipFloor : clip_lo;
+  c->e_lo = clip_lo == kClipLo ? kExpClipLo
+                               : static_cast<float>(std::exp(static_cast<double>(clip_lo)));
+  *wide = c->lo < kClipWide;
+  return SOFTMAX_OK;
+}
+
+template <bool WIDE>
+hipError_t launch_rows(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
+                       int64_t cols, Clip c, hipStream_t s) {
+  switch (p.kernel) {
+    case SOFTMAX_KERNEL_PACKED:
+      return p.vec_width == 4 ? dispatch_packed<true, WIDE>(p, x, y, rows, cols, c, s)
+                              : dispatch_packed<false, WIDE>(p, x, y, rows, cols, c, s);
+    case SOFTMAX_KERNEL_WAVE_ROW:
+      return p.vec_width == 4 ? dispatch_wave<true, WIDE>(p, x, y, rows, cols, c, s)
+                              : dispatch_wave<false, WIDE>(p, x, y, rows, cols, c, s);
+    case SOFTMAX_KERNEL_BLOCK_ROW:
+      return p.vec_width == 4 ? dispatch_block<true, WIDE>(p, x, y, rows, cols, c, s)
+                              : dispatch_block<false, WIDE>(p, x, y, rows, cols, c, s);
+    default:
+      return hipSuccess;
+  }
 }
 
 int check_pointers(const float* x, const float* y, int64_t n_elems, int* dev) {
@@ -456,9 +500,13 @@ SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64
   return SOFTMAX_OK;
 }
 
-SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols,
-                            hipStream_t stream) {
-  int rc = check_sizes(rows, cols);
+SOFTMAX_API int softmax_fwd_clip(const float* x, float* y, int64_t rows, int64_t cols,
+                                 float clip_lo, hipStream_t stream) {
+  Clip c;
+  bool wide = false;
+  int rc = make_clip(clip_lo, &c, &wide);
+  if (rc != SOFTMAX_OK) return rc;
+  rc = check_sizes(rows, cols);
   if (rc != SOFTMAX_OK) return rc;
   if (rows == 0 || cols == 0) return SOFTMAX_OK;
   int dev = 0;
@@ -466,27 +514,16 @@ SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols
   if (rc != SOFTMAX_OK) return rc;
 
   const softmax_plan_t p = make_plan(x, y, rows, cols);
-  hipError_t e = hipSuccess;
-  switch (p.kernel) {
-    case SOFTMAX_KERNEL_PACKED:
-      e = p.vec_width == 4 ? dispatch_packed<true>(p, x, y, rows, cols, stream)
-                           : dispatch_packed<false>(p, x, y, rows, cols, stream);
-      break;
-    case SOFTMAX_KERNEL_WAVE_ROW:
-      e = p.vec_width == 4 ? dispatch_wave<true>(p, x, y, rows, cols, stream)
-                           : dispatch_wave<false>(p, x, y, rows, cols, stream);
-      break;
-    case SOFTMAX_KERNEL_BLOCK_ROW:
-      e = p.vec_width == 4 ? dispatch_block<true>(p, x, y, rows, cols, stream)
-                           : dispatch_block<false>(p, x, y, rows, cols, stream);
-      break;
-    case SOFTMAX_KERNEL_SPLIT_ROW:
-      return split_call(p, x, y, rows, cols, dev, stream);
-    default:
-      return SOFTMAX_OK;
-  }
-  if (e != hipSuccess) return fail_hip(e);
-  return SOFTMAX_OK;
+  if (p.kernel == SOFTMAX_KERNEL_SPLIT_ROW)
+    return split_call(p, x, y, rows, cols, dev, c, wide, stream);
+  const hipError_t e = wide ? launch_rows<true>(p, x, y, rows, cols, c, stream)
+                            : launch_rows<false>(p, x, y, rows, cols, c, stream);
+  return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
+}
+
+SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols,
+                            hipStream_t stream) {
+  return softmax_fwd_clip(x, y, rows, cols, SOFTMAX_CLIP_LO, stream);
 }
 
 SOFTMAX_API const char* softmax_strerror(int code) {
@@ -494,7 +531,8 @@ SOFTMAX_API const char* softmax_strerror(int code) {
     case SOFTMAX_OK: return "success";
     case SOFTMAX_ERR_INVALID_ARG:
       return "invalid argument (negative or overflowing size, null pointer, "
-             "or partially overlapping x and y)";
+             "partially overlapping x and y, or a clip bound that is NaN or above "
+             "SOFTMAX_CLIP_MAX)";
     case SOFTMAX_ERR_HIP: return "HIP call or kernel launch failed";
     case SOFTMAX_ERR_NOT_DEVICE:
       return "pointer is not memory the current device can use, or the range "
@@ -506,7 +544,10 @@ SOFTMAX_API const char* softmax_strerror(int code) {
 SOFTMAX_API int softmax_last_hip_error(void) { return tl_last_hip_error; }
 
 SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int64_t n,
-                                  hipStream_t stream) {
+                                  float clip_lo, hipStream_t stream) {
+  Clip c;
+  bool wide = false;
+  if (make_clip(clip_lo, &c, &wide) != SOFTMAX_OK) return SOFTMAX_ERR_INVALID_ARG;
   if (n < 0 || n > INT64_MAX / 4) return SOFTMAX_ERR_INVALID_ARG;
   if (n == 0) return SOFTMAX_OK;
   if (x == nullptr || m == nullptr || e == nullptr) return SOFTMAX_ERR_INVALID_ARG;
@@ -519,8 +560,10 @@ SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int6
   if (rc == SOFTMAX_OK) rc = check_device_range(e, n * 4, dev);
   if (rc != SOFTMAX_OK) return rc;
   const int64_t grid = std::min(ceil_div(n, 256), kMaxGrid);
-  void* args[] = {&x, &m, &e, &n};
-  he = launch(reinterpret_cast<const void*>(&k_exp_probe), grid, 256, args, stream);
+  void* args[] = {&x, &m, &e, &n, &c};
+  he = launch(wide ? reinterpret_cast<const void*>(&k_exp_probe<true>)
+                   : reinterpret_cast<const void*>(&k_exp_probe<false>),
+              grid, 256, args, stream);
   return he == hipSuccess ? SOFTMAX_OK : fail_hip(he);
 }
 
