@@ -9,6 +9,8 @@ Contents
 --------
 ``softmax_f64``          float64 definition of the clipped row softmax
                           (plain numpy; the parity reference).
+``attention_f64``        float64 softmax attention, softmax(scale Q K^T) V
+                          per batch element, built on ``softmax_f64``.
 ``cpu_fp32_baseline.c``  a straightforward single-thread fp32 C softmax in the
                           loop shape of the paper's MKL-era functor; it is a
                           timed CPU baseline, never a parity reference.
@@ -17,6 +19,7 @@ Every function here is pinned by ``tests/test_oracle_pins.py`` to facts that
 do not come from this code: closed forms, the logistic special case, a
 50-digit ``decimal`` brute force, a library cross-check and invariants.
 """
+from .attention_f64 import attention_clipped
 from .softmax_f64 import CLIP_LO, exp_clipped, row_max, softmax_clipped
 
-__all__ = ["CLIP_LO", "row_max", "exp_clipped", "softmax_clipped"]
+__all__ = ["CLIP_LO", "row_max", "exp_clipped", "softmax_clipped", "attention_clipped"]

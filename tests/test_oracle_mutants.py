@@ -142,3 +142,53 @@ def test_clip_mutant_is_caught(name):
         assert failed == [], failed
     else:
         assert failed, f"mutant {name} passed every clip pin"
+
+
+# Mistakes in the attention oracle: each must fail at least one of
+# pins_attention.ATTN_PINS.
+def _attn(q, k, v, scale, lo, axis=-1, scale_pow=1, use_k_as_v=False, clip=True,
+          shift=True, normalise=True, v_transposed=False):
+    q64, k64, v64 = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
+    if q64.shape[0] * q64.shape[1] == 0 or v64.shape[2] == 0:
+        return np.zeros((q64.shape[0], q64.shape[1], v64.shape[2]))
+    s = np.matmul(q64, k64.transpose(0, 2, 1)) * float(scale) ** scale_pow
+    with np.errstate(all="ignore"):
+        m = np.max(s, axis=axis, keepdims=True) if shift else 0.0
+        d = s - m
+        if clip:
+            d = np.where(d < lo, lo, d)
+        e = np.exp(d)
+        p = e / np.sum(e, axis=axis, keepdims=True) if normalise else e
+        vv = k64 if use_k_as_v else v64
+        if v_transposed and vv.shape[1] == vv.shape[2]:
+            vv = vv.transpose(0, 2, 1)
+        return np.matmul(p, vv) if p.shape[2] == vv.shape[1] else np.matmul(p, v64)
+
+
+MUTANTS_ATTN = {
+    "reference_copy_is_clean": {},
+    "softmax_over_queries": dict(axis=1),
+    "scale_not_applied": dict(scale_pow=0),
+    "scale_applied_twice": dict(scale_pow=2),
+    "keys_used_as_values": dict(use_k_as_v=True),
+    "no_clip": dict(clip=False),
+    "no_max_shift": dict(shift=False),
+    "weights_not_normalised": dict(normalise=False),
+    "values_transposed": dict(v_transposed=True),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_ATTN))
+def test_attention_mutant_is_caught(name):
+    from tests import pins_attention
+    impl = lambda q, k, v, s, lo: _attn(q, k, v, s, lo, **MUTANTS_ATTN[name])  # noqa: E731
+    failed = []
+    for pin in pins_attention.ATTN_PINS:
+        try:
+            pin(impl)
+        except (AssertionError, ValueError, FloatingPointError, IndexError):
+            failed.append(pin.__name__)
+    if name == "reference_copy_is_clean":
+        assert failed == [], failed
+    else:
+        assert failed, f"mutant {name} passed every attention pin"

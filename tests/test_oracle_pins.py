@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 
 import oracle
-from tests import pins
+from tests import pins, pins_attention
 
 
 @pytest.mark.parametrize("pin", pins.ALL_PINS, ids=lambda p: p.__name__)
@@ -50,3 +50,15 @@ def test_workloads_oracle_invariants():
         assert np.all(np.isfinite(y))
         assert np.max(np.abs(y.sum(axis=1) - 1.0)) < 1e-12
         assert np.all(y >= np.exp(-64.0) / x.shape[1] * (1 - 1e-12))
+
+
+@pytest.mark.parametrize("pin", pins_attention.ATTN_PINS, ids=lambda p: p.__name__)
+def test_attention_oracle_pin(pin):
+    pin(oracle.attention_clipped)
+
+
+def test_attention_oracle_rejects_zero_keys():
+    import workloads
+    q, k, v = workloads.random_qkv(2, 3, 0, 4, 5, 1)
+    with pytest.raises(ValueError):
+        oracle.attention_clipped(q, k, v, 1.0)

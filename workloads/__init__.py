@@ -25,7 +25,8 @@ from dataclasses import dataclass
 
 import numpy as np
 
-__all__ = ["Workload", "WORKLOADS", "generate", "sha256_f32", "random_logits"]
+__all__ = ["Workload", "WORKLOADS", "generate", "sha256_f32", "random_logits",
+           "AttentionWorkload", "ATTENTION_WORKLOADS", "generate_qkv", "random_qkv"]
 
 
 @dataclass(frozen=True)
@@ -74,12 +75,20 @@ def _resolve(key) -> Workload:
     return WORKLOADS[key]
 
 
-def _dam_scores(rng: np.random.Generator) -> np.ndarray:
+def _dam_qk(rng: np.random.Generator) -> tuple[np.ndarray, np.ndarray]:
+    """DAM query and key vectors, [2304, 50, 200] each, standard normal
+    rounded to multiples of 2^-10 (exact in fp32)."""
     batch_turns, q, k, dim = 2304, 50, 50, 200
     qv = rng.standard_normal((batch_turns, q, dim))
     kv = rng.standard_normal((batch_turns, k, dim))
     qv = np.round(qv * 1024.0) / 1024.0
     kv = np.round(kv * 1024.0) / 1024.0
+    return qv, kv
+
+
+def _dam_scores(rng: np.random.Generator) -> np.ndarray:
+    batch_turns, q, k = 2304, 50, 50
+    qv, kv = _dam_qk(rng)
     s = np.matmul(qv, kv.transpose(0, 2, 1))
     s = s / np.sqrt(200.0)
     return s.reshape(batch_turns * q, k)
@@ -152,3 +161,69 @@ def random_logits(rows: int, cols: int, seed: int, kind: str = "normal",
     else:
         raise ValueError(kind)
     return np.ascontiguousarray(x.astype(np.float32))
+
+
+# ---------------------------------------------------------------------------
+# Attention inputs (Q, K, V) for the fused attention path: softmax over the
+# keys of scale * Q.K^T, then the product with V, per batch element.
+
+@dataclass(frozen=True)
+class AttentionWorkload:
+    key: str
+    batch: int
+    lq: int
+    lk: int
+    d: int
+    dv: int
+    seed: int
+    description: str
+
+    @property
+    def scale(self) -> float:
+        """1/sqrt(d) rounded to fp32, the scale applied to Q.K^T."""
+        return float(np.float32(1.0 / np.sqrt(self.d)))
+
+    @property
+    def algorithmic_bytes(self) -> int:
+        """One fp32 read of Q, K and V and one fp32 write of the output."""
+        return 4 * self.batch * (self.lq * self.d + self.lk * self.d
+                                 + self.lk * self.dv + self.lq * self.dv)
+
+    @property
+    def flops(self) -> int:
+        """Multiply-adds of Q.K^T and P.V, two flops each."""
+        return 2 * self.batch * self.lq * self.lk * (self.d + self.dv)
+
+
+ATTENTION_WORKLOADS: dict[str, AttentionWorkload] = {
+    w.key: w
+    for w in (
+        AttentionWorkload("dam_fused_attention_2304x50x50x200", 2304, 50, 50, 200, 200, 1,
+                          "DAM attention, 256 batch x 9 turns: 50 queries over 50 keys "
+                          "of dimension 200; Q and K are the vectors behind "
+                          "dam_attention_115200x50, V is drawn after them"),
+    )
+}
+
+
+def generate_qkv(key: str) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """float32 Q [batch, lq, d], K [batch, lk, d], V [batch, lk, dv].
+
+    Q and K are the same draws as the DAM scores workload (seed 1), so the
+    scores of this workload are that workload's logits before rounding; V is
+    drawn next, standard normal rounded to multiples of 2^-10."""
+    w = ATTENTION_WORKLOADS[key]
+    rng = np.random.default_rng(w.seed)
+    qv, kv = _dam_qk(rng)
+    vv = np.round(rng.standard_normal((w.batch, w.lk, w.dv)) * 1024.0) / 1024.0
+    return tuple(np.ascontiguousarray(a.astype(np.float32)) for a in (qv, kv, vv))
+
+
+def random_qkv(batch: int, lq: int, lk: int, d: int, dv: int, seed: int,
+               scale: float = 1.0) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Seeded float32 Q, K, V of N(0, scale^2) entries for edge-shape tests."""
+    rng = np.random.default_rng(seed)
+    q = scale * rng.standard_normal((batch, lq, d))
+    k = scale * rng.standard_normal((batch, lk, d))
+    v = rng.standard_normal((batch, lk, dv))
+    return tuple(np.ascontiguousarray(a.astype(np.float32)) for a in (q, k, v))
