@@ -208,6 +208,67 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
     }
 
 
+FP32_MATRIX_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix-core peak
+
+
+def time_attention(sm, torch, key: str, steps: int, warmup: int) -> dict:
+    """The fused attention on the DAM Q, K, V: graph-replayed steps over a
+    rotation of at least 1 GiB of (Q, K, V, O) sets, plus the same problem
+    done unfused for comparison (hipBLAS batched products around
+    softmax_fwd, with K^T made contiguous outside the timed region)."""
+    wa = workloads.ATTENTION_WORKLOADS[key]
+    q, k, v = workloads.generate_qkv(key)
+    dev = torch.device("cuda:0")
+    nset = max(2, math.ceil(ROTATE_BYTES / wa.algorithmic_bytes))
+    q0, k0, v0 = (torch.from_numpy(a).to(dev) for a in (q, k, v))
+    sets = [(q0.clone(), k0.clone(), v0.clone(),
+             torch.empty((wa.batch, wa.lq, wa.dv), device=dev)) for _ in range(nset)]
+
+    def fused(i, s):
+        qq, kk, vv, oo = sets[i % nset]
+        sm.softmax_attention_fwd(qq, kk, vv, scale=wa.scale, out=oo, stream=s)
+
+    ms, eager_ms = time_steps(torch, fused, steps, warmup)
+    # parity of the timed output on sampled batch elements
+    import oracle
+    torch.cuda.synchronize()
+    pick = np.random.default_rng(0).choice(wa.batch, 32, replace=False)
+    got = sets[0][3][torch.from_numpy(pick).to(dev)].cpu().numpy().astype(np.float64)
+    want = oracle.attention_clipped(q[pick], k[pick], v[pick], wa.scale)
+    err = float(np.max(np.abs(got - want)) / np.max(np.abs(want)))
+    if err > 1e-4:
+        raise SystemExit(f"attention output failed parity: normwise {err:.3e}")
+
+    # unfused: S = bmm(Q, K^T) * scale, P = softmax_fwd(S), O = bmm(P, V)
+    kt = [st[1].transpose(1, 2).contiguous() for st in sets]
+    ss = [torch.empty((wa.batch, wa.lq, wa.lk), device=dev) for _ in range(nset)]
+
+    def unfused(i, s):
+        qq, _, vv, oo = sets[i % nset]
+        sc = ss[i % nset]
+        torch.bmm(qq, kt[i % nset], out=sc)
+        sc.mul_(wa.scale)
+        sm.softmax_fwd(sc.view(-1, wa.lk), out=sc.view(-1, wa.lk), stream=s)
+        torch.bmm(sc, vv, out=oo)
+
+    unfused_ms, _ = time_steps(torch, unfused, steps, warmup)
+    del sets, kt, ss
+    torch.cuda.empty_cache()
+    gbps = wa.algorithmic_bytes / (ms * 1e-3) / 1e9
+    tflops = wa.flops / (ms * 1e-3) / 1e12
+    return {
+        "workload": key, "batch": wa.batch, "lq": wa.lq, "lk": wa.lk, "d": wa.d, "dv": wa.dv,
+        "ms_per_step": ms, "eager_ms_per_step": eager_ms,
+        "batches_per_s": wa.batch / (ms * 1e-3),
+        "algorithmic_bytes_per_launch": wa.algorithmic_bytes, "hbm_gbps": gbps,
+        "frac_of_hbm_peak": gbps / HBM_PEAK_GBPS,
+        "flops_per_launch": wa.flops, "tflops": tflops,
+        "frac_of_fp32_matrix_peak": tflops / FP32_MATRIX_PEAK_TFLOPS,
+        "unfused_ms_per_step": unfused_ms, "fused_speedup": unfused_ms / ms,
+        "sampled_normwise_err": err, "rotation_sets": nset,
+    }
+
+
 def time_cpu_oracle(x: np.ndarray, budget_s: float) -> dict:
     """float64 oracle (numpy, one thread) on whole passes over the matrix,
     repeated until `budget_s` of wall time is spent."""
@@ -540,6 +601,15 @@ def main() -> int:
             log(f"[bench] {key}: {r['ms_per_step'] * 1e3:.2f} us/step, {r['hbm_gbps']:.0f} GB/s "
                 f"(no clip {r['noclip_ms_per_step'] * 1e3:.2f} us)")
 
+    attention = None
+    if not args.no_extra_workloads:
+        akey = next(iter(workloads.ATTENTION_WORKLOADS))
+        log(f"[bench] timing fused attention {akey}")
+        attention = time_attention(sm, torch, akey, args.steps, args.warmup)
+        log(f"[bench] {akey}: {attention['ms_per_step'] * 1e3:.2f} us/step, "
+            f"{attention['hbm_gbps']:.0f} GB/s, {attention['tflops']:.1f} TFLOP/s; unfused "
+            f"{attention['unfused_ms_per_step'] * 1e3:.2f} us")
+
     cpu = None
     cpu32 = None
     if not args.no_cpu_baseline:
@@ -596,6 +666,7 @@ def main() -> int:
         "cpu_fp32_baseline": cpu32,
         "sampled_max_rel_err": main_res["sampled_max_rel_err"],
         "other_workloads": extra,
+        "fused_attention": attention,
     }
     print(json.dumps(out), flush=True)
     return 0

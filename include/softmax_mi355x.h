@@ -137,6 +137,52 @@ SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols
 SOFTMAX_API int softmax_fwd_clip(const float* x, float* y, int64_t rows, int64_t cols,
                                  float clip_lo, hipStream_t stream);
 
+/* Limits of softmax_attention_fwd. */
+#define SOFTMAX_ATTN_MAX_KEYS 64     /* lk: the keys of one row fit one set of tiles */
+#define SOFTMAX_ATTN_MAX_DIM 65536   /* d and dv */
+
+/*
+ * softmax_attention_fwd -- fused softmax attention over small tiles, the
+ * attention of the DAM model whose softmax the paper optimises (Sec. 1;
+ * softmax is 18.5% of that model's time in Sec. 1.2 Fig. 2):
+ *
+ *   for every batch element b:
+ *     S = scale * Q_b K_b^T                       [lq, lk]
+ *     P = row-wise clipped softmax of S over the keys, bound clip_lo
+ *         (the operation of softmax_fwd_clip, Sec. 1.1 Eq. (1), Sec. 1.2
+ *         Fig. 1; -INFINITY for no clip, Sec. 2.3 Fig. 4)
+ *     O_b = P V_b                                  [lq, dv]
+ *
+ *   q      device pointer, batch x lq x d fp32, row-major, contiguous
+ *   k      device pointer, batch x lk x d fp32
+ *   v      device pointer, batch x lk x dv fp32
+ *   o      device pointer, batch x lq x dv fp32; written.  o may not overlap
+ *          q, k or v.
+ *   batch, lq >= 0; 1 <= lk <= SOFTMAX_ATTN_MAX_KEYS (when there is work);
+ *   0 <= d, dv <= SOFTMAX_ATTN_MAX_DIM.  q and k may be NULL when d == 0
+ *   (every score is then 0).
+ *   scale  finite fp32 multiplier of Q K^T (1/sqrt(d) for the DAM model).
+ *   clip_lo as for softmax_fwd_clip.
+ *
+ * The scores and weights never leave the registers: the two products run
+ * on the matrix cores in fp32 (v_mfma_f32_16x16x4f32) and the softmax runs
+ * on their accumulators.  Accuracy: each score carries the rounding of a
+ * d-term fp32 dot product, so each weight is within a relative
+ * 2*(d+1)*2^-24 * max_k |scale| sum_t |Q_it K_kt| (plus 4e-6) of the exact
+ * weight, and each output within that relative error, plus (lk+1)*2^-24,
+ * of sum_k P_ik |V_kc|.
+ *
+ * Ownership, asynchrony and error codes follow softmax_fwd: caller-owned
+ * device memory, work enqueued on `stream`, SOFTMAX_ERR_INVALID_ARG for bad
+ * sizes, a non-finite scale, a bad clip_lo, null or overlapping pointers,
+ * SOFTMAX_ERR_NOT_DEVICE for memory the device cannot use.  batch, lq or
+ * dv of 0 returns SOFTMAX_OK with nothing launched.  No workspace.
+ */
+SOFTMAX_API int softmax_attention_fwd(const float* q, const float* k, const float* v,
+                                      float* o, int64_t batch, int64_t lq, int64_t lk,
+                                      int64_t d, int64_t dv, float scale, float clip_lo,
+                                      hipStream_t stream);
+
 /* Static description of a return code.  Never NULL. */
 SOFTMAX_API const char* softmax_strerror(int code);
 

@@ -11,6 +11,9 @@ Functions keep the C names:
     softmax_fwd_ptr(x_ptr, y_ptr, rows, cols, stream_handle) -> int
     softmax_fwd_clip(x, clip_lo, out=None, stream=None) -> torch.Tensor
     softmax_fwd_clip_ptr(x_ptr, y_ptr, rows, cols, clip_lo, stream_handle) -> int
+    softmax_attention_fwd(q, k, v, scale=None, clip_lo=-64.0, out=None, stream=None)
+    softmax_attention_fwd_ptr(q_ptr, k_ptr, v_ptr, o_ptr, batch, lq, lk, d, dv,
+                              scale, clip_lo, stream_handle) -> int
     softmax_plan(rows, cols, x_ptr=1 << 44, y_ptr=1 << 45) -> dict
     softmax_exp_probe(x, m, out=None, stream=None, clip_lo=-64.0) -> torch.Tensor
     softmax_copy_probe(x, out=None, stream=None) -> torch.Tensor
@@ -25,6 +28,7 @@ import os
 __all__ = [
     "LIB_PATH", "HEADER_PATH", "SoftmaxError", "load_library", "softmax_fwd",
     "softmax_fwd_ptr", "softmax_fwd_clip", "softmax_fwd_clip_ptr", "softmax_plan",
+    "softmax_attention_fwd", "softmax_attention_fwd_ptr", "ATTN_MAX_KEYS", "ATTN_MAX_DIM",
     "softmax_exp_probe", "softmax_copy_probe", "softmax_strerror", "softmax_last_hip_error",
     "CLIP_LO", "CLIP_MAX", "KERNEL_NAMES",
 ]
@@ -35,6 +39,8 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "softmax_mi355x.h")
 
 CLIP_LO = -64.0
 CLIP_MAX = -48.0
+ATTN_MAX_KEYS = 64
+ATTN_MAX_DIM = 65536
 OK, ERR_INVALID_ARG, ERR_HIP, ERR_NOT_DEVICE = 0, 1, 2, 3
 KERNEL_NAMES = {0: "none", 1: "packed", 2: "wave_row", 3: "block_row", 4: "split_row"}
 
@@ -80,6 +86,9 @@ def load_library() -> ctypes.CDLL:
     lib.softmax_fwd.restype = ctypes.c_int
     lib.softmax_fwd_clip.argtypes = [vp, vp, i64, i64, ctypes.c_float, vp]
     lib.softmax_fwd_clip.restype = ctypes.c_int
+    f32 = ctypes.c_float
+    lib.softmax_attention_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i64, f32, f32, vp]
+    lib.softmax_attention_fwd.restype = ctypes.c_int
     lib.softmax_strerror.argtypes = [ctypes.c_int]
     lib.softmax_strerror.restype = ctypes.c_char_p
     lib.softmax_last_hip_error.argtypes = []
@@ -193,6 +202,45 @@ def softmax_fwd_clip(x, clip_lo: float, out=None, stream=None):
                                   _stream_handle(stream))
     if rc != OK:
         raise SoftmaxError(rc, "softmax_fwd_clip")
+    return out
+
+
+def softmax_attention_fwd_ptr(q_ptr: int, k_ptr: int, v_ptr: int, o_ptr: int, batch: int,
+                              lq: int, lk: int, d: int, dv: int, scale: float,
+                              clip_lo: float = CLIP_LO, stream_handle: int = 0) -> int:
+    """Raw C call; returns the C return code."""
+    return int(load_library().softmax_attention_fwd(
+        q_ptr, k_ptr, v_ptr, o_ptr, batch, lq, lk, d, dv, float(scale), float(clip_lo),
+        stream_handle))
+
+
+def softmax_attention_fwd(q, k, v, scale=None, clip_lo: float = CLIP_LO, out=None,
+                          stream=None):
+    """O = softmax_clip(scale * Q K^T) V per batch element, on the matrix
+    cores, for float32 GPU tensors q [B, lq, d], k [B, lk, d], v [B, lk, dv].
+    ``scale`` defaults to 1/sqrt(d) rounded to float32."""
+    torch = _torch()
+    for t, name in ((q, "q"), (k, "k"), (v, "v")):
+        _check_f32_cuda(t, name)
+        if t.dim() != 3:
+            raise ValueError(f"{name} must be 3-D [batch, len, dim]")
+    b, lq, d = q.shape
+    if k.shape[0] != b or k.shape[2] != d or v.shape[:2] != k.shape[:2]:
+        raise ValueError("q, k, v shapes do not match")
+    lk, dv = k.shape[1], v.shape[2]
+    if scale is None:
+        scale = float(torch.tensor(1.0 / max(d, 1) ** 0.5, dtype=torch.float32))
+    if out is None:
+        out = torch.empty((b, lq, dv), dtype=torch.float32, device=q.device)
+    else:
+        _check_f32_cuda(out, "out")
+        if tuple(out.shape) != (b, lq, dv):
+            raise ValueError("out must be [batch, lq, dv]")
+    with torch.cuda.device(q.device):
+        rc = softmax_attention_fwd_ptr(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                       b, lq, lk, d, dv, scale, clip_lo, _stream_handle(stream))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_attention_fwd")
     return out
 
 

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "libsoftmax_mi355x.so")
-SOURCES = [os.path.join(CSRC, "softmax_api.hip")]
+SOURCES = [os.path.join(CSRC, "softmax_api.hip"), os.path.join(CSRC, "attention_api.hip")]
 
 ARCH = "gfx950"
 HIPCC_FLAGS = [

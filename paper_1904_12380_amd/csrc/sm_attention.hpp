@@ -1,0 +1,471 @@
+// Fused softmax attention over small tiles on gfx950 matrix cores:
+//
+//   O_b = softmax_clip(scale * Q_b K_b^T) V_b        for every batch element b
+//
+// with Q_b [lq, d], K_b [lk, d], V_b [lk, dv], O_b [lq, dv], fp32, row-major
+// and contiguous per batch.  The softmax step is the library's clipped row
+// softmax over the keys (Sec. 1.1 Eq. (1), the clip of Sec. 1.2 Fig. 1, no
+// clip as in Sec. 2.3 Fig. 4); around it are the two products of the DAM
+// model's attention, whose softmax the paper optimises (Sec. 1).  The scores
+// never leave registers: they are produced by one matrix-core product,
+// normalised in place and consumed as the operand of the next.
+//
+// Mapping (v_mfma_f32_16x16x4f32: C[i][j] += sum_k A[i][k] B[k][j], with
+// A[i][k] in lane i + 16k, B[k][j] in lane j + 16k, and C[i][j] in lane
+// j + 16 (i / 4), register i % 4):
+//
+//   * A workgroup of 4 wavefronts takes one batch element and a block of up
+//     to 64 queries; wavefront w takes queries 16w .. 16w+15 of the block.
+//     Write lane = j + 16 g (j = lane % 16, g = lane / 16).
+//   * Scores, transposed: S^T[key][query] = sum_t K[key][t] Q[query][t],
+//     for NKT key tiles of 16.  The contraction index runs over d in blocks
+//     of 16; within a block, lane g of step s holds t = 16 blk + 4 g + s, so
+//     each lane loads 4 consecutive t of its key (A) and its query (B) with
+//     one 128-bit load per block.  The order of the terms of a dot product
+//     is a permutation of t; every product is still taken once.
+//   * Accumulator register r of key tile kt in lane (j, g) holds the score
+//     of query j and key 16 kt + 4 g + r.  A query's keys are spread over its
+//     4 registers x NKT tiles and the 4 lanes j, j+16, j+32, j+48, so the
+//     row max and row sum take a lane-local reduction and two cross-lane
+//     swaps (permlane16, permlane32).  Keys past lk are masked out of both.
+//   * The normalised weights are then exactly the A operand of P.V for the
+//     contraction step (kt, r): lane (j, g) holds P[query j][key 16kt+4g+r],
+//     and the B operand is V[key 16kt+4g+r][column 16 nt + j].  The output
+//     accumulator of column tile nt holds O[query 4g + r][column 16 nt + j].
+//
+// Padding: queries past lq load zeros and store nothing; keys past lk get
+// weight exactly 0 and load zero value rows; t past d loads zeros; columns
+// past dv load zeros and store nothing.
+#pragma once
+
+#include "sm_device.hpp"
+
+namespace smx {
+
+typedef float f32x4m __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4m mfma16x16x4(float a, float b, f32x4m c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Buffer resources.  Every operand is addressed through a raw buffer
+// resource over the batch element's (or the wave's) own rows with a 32-bit
+// byte offset per lane, so a load needs one offset register and no 64-bit
+// pointer arithmetic.  The hardware checks each access against the
+// resource's size: loads past it return 0 and stores past it are dropped,
+// which is how rows past lq and lk are padded and skipped.  Offsets are
+// kept below 2^31: a resource never spans more than 64 rows of at most
+// 65536 floats.
+constexpr int kBufDword3 = 0x00020000;  // raw buffer, 32-bit data format
+constexpr int kBufOff = 0x7ffffff0;     // an offset past any resource here
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), static_cast<short>(0), bytes,
+                                           kBufDword3);
+}
+
+// Four consecutive floats of a row at byte offset `off` (128-bit when VEC4,
+// else four 32-bit loads), zero when `ok` is false, past the resource, or
+// (32-bit loads) at or past the row's `left` remaining columns.  With VEC4
+// the row length is a multiple of 4, so the four are all in the row or all
+// out of it.
+template <bool VEC4>
+__device__ __forceinline__ f32x4m buf_load4(__amdgpu_buffer_rsrc_t r, int off, bool ok,
+                                            int left = 4) {
+  if constexpr (VEC4) {
+    const int o = ok ? off : kBufOff;
+    return __builtin_bit_cast(f32x4m, __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, 0));
+  } else {
+    f32x4m x;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int o = (ok & (i < left)) ? off + 4 * i : kBufOff;
+      x[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, o, 0, 0));
+    }
+    return x;
+  }
+}
+
+template <int NKT, bool VEC4, bool WIDE>
+__global__ __launch_bounds__(256) void k_attention(const float* q, const float* k,
+                                                   const float* v, float* o, int64_t batch,
+                                                   int lq, int lk, int d, int dv, float scale,
+                                                   Clip clip) {
+  const int lane = __lane_id();
+  const int j = lane & 15;
+  const int g = lane >> 4;
+  // The wave index is uniform across the wave; saying so keeps the buffer
+  // resources built from it in scalar registers.
+  const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int qblocks = (lq + 63) >> 6;
+  const int64_t items = batch * qblocks;
+
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    const int64_t b = item / qblocks;
+    const int q0 = static_cast<int>(item - b * qblocks) * 64 + 16 * w;  // this wave's queries
+    if (q0 >= lq) continue;                       // wave-uniform; no barriers below
+    const int nq = lq - q0 < 16 ? lq - q0 : 16;   // valid queries of this wave
+    // The wave's 16 query rows of Q and O, and the batch element's K and V.
+    const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + (b * lq + q0) * static_cast<int64_t>(d), nq * d * 4);
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + b * lk * static_cast<int64_t>(d), lk * d * 4);
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + b * lk * static_cast<int64_t>(dv), lk * dv * 4);
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
+
+    // ---- scores S^T = K Q^T for this wave's 16 queries --------------------
+    // Lane (j, g) reads query j and key 16 kt + j at columns t0 .. t0+3,
+    // t0 = 16 blk + 4 g; columns past d (last block only) read as zero.
+    const int qoff = (j * d + 4 * g) * 4;
+    const int koff = (j * d + 4 * g) * 4;
+    const int kstride = 16 * d * 4;               // one key tile
+    f32x4m acc[NKT];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) acc[kt] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+    const int nblk = (d + 15) >> 4;               // uniform trip count for the matrix ops
+    if (nblk > 0) {
+      // Operands of blocks blk, blk+1 are in registers while block blk+2 is
+      // loaded: two blocks of loads stay in flight behind the matrix ops.
+      const int left0 = d - 4 * g, left1 = d - 16 - 4 * g;
+      f32x4m qf0 = buf_load4<VEC4>(rq, qoff, left0 > 0, left0);
+      f32x4m qf1 = buf_load4<VEC4>(rq, qoff + 64, (nblk > 1) & (left1 > 0), left1);
+      f32x4m kf0[NKT], kf1[NKT];
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        kf0[kt] = buf_load4<VEC4>(rk, koff + kt * kstride, left0 > 0, left0);
+        kf1[kt] = buf_load4<VEC4>(rk, koff + kt * kstride + 64, (nblk > 1) & (left1 > 0), left1);
+      }
+      for (int blk = 0; blk < nblk; ++blk) {
+        const int left = d - 16 * (blk + 2) - 4 * g;
+        const bool more = (blk + 2 < nblk) & (left > 0);
+        const int step = 64 * (blk + 2);
+        const f32x4m qn = buf_load4<VEC4>(rq, qoff + step, more, left);
+        f32x4m kn[NKT];
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+          kn[kt] = buf_load4<VEC4>(rk, koff + kt * kstride + step, more, left);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+#pragma unroll
+          for (int kt = 0; kt < NKT; ++kt) acc[kt] = mfma16x16x4(kf0[kt][s], qf0[s], acc[kt]);
+        }
+        qf0 = qf1;
+        qf1 = qn;
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt) {
+          kf0[kt] = kf1[kt];
+          kf1[kt] = kn[kt];
+        }
+      }
+    }
+
+    // ---- clipped softmax over the keys of query j -------------------------
+    // Only the last key tile can hold keys past lk (NKT = ceil(lk / 16)).
+    float e[4 * NKT];
+    float m = -__builtin_inff();
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
+        const float sv = acc[kt][r] * scale;
+        e[4 * kt + r] = sv;
+        m = key_ok ? fmaxf(m, sv) : m;
+      }
+    }
+    m = fmaxf(m, row16_partner(m));
+    m = fmaxf(m, half32_partner(m));
+    const RowShift rs = row_shift(m, clip);
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
+        const float ev = exp_shift_clip<WIDE>(e[4 * kt + r], rs);
+        e[4 * kt + r] = key_ok ? ev : 0.0f;
+      }
+    }
+    float sum = tree_sum(e);
+    sum = sum + row16_partner(sum);
+    sum = sum + half32_partner(sum);
+    const float rcp = 1.0f / sum;
+#pragma unroll
+    for (int i = 0; i < 4 * NKT; ++i) e[i] = e[i] * rcp;
+
+    // ---- O = P V ----------------------------------------------------------
+    // Contraction step i = 4 kt + r takes key 16 kt + 4 g + r in lane
+    // (j, g): byte offset vlane + i' * dv * 4 with i' = 16 kt + r.  Keys past
+    // lk fall outside the resource and read as zero.
+    const int vlane = 4 * g * dv * 4;
+    const int orow = 4 * g * dv * 4;              // O row 4 g + r of the wave
+    // Full 64-column blocks with 128-bit access (VEC4): lane j takes
+    // columns c0 + 4 j .. c0 + 4 j + 3, one per column tile u, so a lane's
+    // four tiles are one 128-bit load of V and one 128-bit store of O.  The
+    // block is done in two halves of 2 NKT contraction steps; the next
+    // half's loads are in flight while this half's matrix ops run.
+    constexpr int H = 2 * NKT;
+    const int nfull = VEC4 ? dv >> 6 : 0;
+    if (nfull > 0) {
+      f32x4m va[H], vh[H];
+#pragma unroll
+      for (int i = 0; i < H; ++i)
+        va[i] = buf_load4<true>(rv, vlane + ((16 * (i >> 2) + (i & 3)) * dv + 4 * j) * 4, true);
+      for (int cb = 0; cb < nfull; ++cb) {
+        const int c = 64 * cb + 4 * j;
+#pragma unroll
+        for (int i = 0; i < H; ++i) {
+          const int ii = H + i;
+          vh[i] = buf_load4<true>(rv, vlane + ((16 * (ii >> 2) + (ii & 3)) * dv + c) * 4, true);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        f32x4m oacc[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) oacc[u] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int i = 0; i < H; ++i) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) oacc[u] = mfma16x16x4(e[i], va[i][u], oacc[u]);
+        }
+        const bool next = cb + 1 < nfull;
+#pragma unroll
+        for (int i = 0; i < H; ++i)
+          va[i] = buf_load4<true>(rv, vlane + ((16 * (i >> 2) + (i & 3)) * dv + c + 64) * 4, next);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < H; ++i) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) oacc[u] = mfma16x16x4(e[H + i], vh[i][u], oacc[u]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const f32x4m ov = {oacc[0][r], oacc[1][r], oacc[2][r], oacc[3][r]};
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(
+              __attribute__((ext_vector_type(4))) unsigned, ov), ro, orow + (r * dv + c) * 4, 0, 0);
+        }
+      }
+    }
+    // The remaining columns (all of them without 128-bit access), one plain
+    // 16-column tile at a time: lane j takes column c0 + j.  Columns past dv
+    // would land in the next row, so their loads use an offset past the
+    // resource, and their stores are skipped.
+    for (int c0 = 64 * nfull; c0 < dv; c0 += 16) {
+      const int c = c0 + j;
+      const bool c_ok = c < dv;
+      float vs[4 * NKT];
+#pragma unroll
+      for (int i = 0; i < 4 * NKT; ++i) {
+        const int off = c_ok ? vlane + ((16 * (i >> 2) + (i & 3)) * dv + c) * 4 : kBufOff;
+        vs[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rv, off, 0, 0));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      f32x4m oa = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int i = 0; i < 4 * NKT; ++i) oa = mfma16x16x4(e[i], vs[i], oa);
+      // Plain stores here: a 32-bit buffer store of an accumulator element
+      // was compiled to store element 0 for every r by this toolchain.
+      float* orow_p = o + (b * lq + q0 + 4 * g) * static_cast<int64_t>(dv) + c;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if ((q0 + 4 * g + r < lq) & c_ok)
+          __builtin_nontemporal_store(oa[r], orow_p + static_cast<int64_t>(r) * dv);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The same computation with K_b and V_b staged in LDS, for problems whose
+// lk * (d + dv) floats fit in kAttnLdsBytes and whose rows allow 128-bit
+// access (d % 4 == dv % 4 == 0, 16-byte aligned operands).  A workgroup of
+// 4 wavefronts takes one batch element (and one block of 64 queries):
+//
+//   1. the 4 wavefronts copy K_b and V_b, which are contiguous, into LDS
+//      with LDS-DMA loads (global_load_lds_dwordx4: 1 KiB per wavefront
+//      instruction, no registers), while each wavefront loads its 16 query
+//      rows into registers;
+//   2. the score product reads its K operands from LDS, the weights stay in
+//      registers as before, and the P.V product reads V from LDS;
+//   3. a barrier ends the item before the next one overwrites the LDS.
+//
+// Each batch element's K and V cross HBM and L2 once, instead of once per
+// wavefront, and the matrix-op operands come from LDS.  Two workgroups fit
+// per CU, so one copies while the other computes.
+constexpr int kAttnLdsBytes = 80 * 1024;
+constexpr int kAttnMaxDQ = 256;  // d up to this keeps Q in registers
+
+template <int NKT, bool WIDE>
+__global__ __launch_bounds__(256) void k_attention_lds(const float* q, const float* k,
+                                                       const float* v, float* o,
+                                                       int64_t batch, int lq, int lk, int d,
+                                                       int dv, float scale, Clip clip) {
+  __shared__ __attribute__((aligned(16))) float lds[kAttnLdsBytes / 4];
+  float* lk_s = lds;                       // K_b: lk x d
+  float* lv_s = lds + lk * d;              // V_b: lk x dv (16-byte aligned: d % 4 == 0)
+  const int lane = __lane_id();
+  const int j = lane & 15;
+  const int g = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int qblocks = (lq + 63) >> 6;
+  const int64_t items = batch * qblocks;
+  const int kbytes = lk * d * 4;
+  const int vbytes = lk * dv * 4;
+
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    const int64_t b = item / qblocks;
+    const int q0 = static_cast<int>(item - b * qblocks) * 64 + 16 * w;
+
+    // ---- 1. K_b and V_b into LDS; Q rows into registers --------------------
+    {
+      // Each instruction writes its 64 lanes' 16 bytes to consecutive LDS
+      // bytes from the (uniform) destination; lanes past the end are off.
+      typedef __attribute__((address_space(3))) char lds_char;
+      lds_char* dk = (lds_char*)lk_s;
+      lds_char* dvs = (lds_char*)lv_s;
+      const char* gk = reinterpret_cast<const char*>(k + b * lk * static_cast<int64_t>(d));
+      const char* gv = reinterpret_cast<const char*>(v + b * lk * static_cast<int64_t>(dv));
+      for (int c = 1024 * w; c < kbytes; c += 4096) {
+        if (c + 16 * lane < kbytes)
+          __builtin_amdgcn_global_load_lds(gk + c + 16 * lane, dk + c, 16, 0, 0);
+      }
+      for (int c = 1024 * w; c < vbytes; c += 4096) {
+        if (c + 16 * lane < vbytes)
+          __builtin_amdgcn_global_load_lds(gv + c + 16 * lane, dvs + c, 16, 0, 0);
+      }
+    }
+    const bool active = q0 < lq;                 // wave-uniform
+    const int nq = active ? (lq - q0 < 16 ? lq - q0 : 16) : 0;
+    constexpr int QB = kAttnMaxDQ / 16;          // d blocks held in registers
+    f32x4m qf[QB];
+    const int nblk = (d + 15) >> 4;
+    if (active) {
+      const __amdgpu_buffer_rsrc_t rq =
+          make_rsrc(q + (b * lq + q0) * static_cast<int64_t>(d), nq * d * 4);
+      const int qoff = (j * d + 4 * g) * 4;
+#pragma unroll
+      for (int blk = 0; blk < QB; ++blk)
+        qf[blk] = buf_load4<true>(rq, qoff + 64 * blk, (blk < nblk) & (16 * blk + 4 * g < d));
+    }
+    __builtin_amdgcn_s_waitcnt(0);               // this wave's copies and loads
+    __syncthreads();                             // everyone's copies
+
+    if (active) {
+      // ---- 2a. scores S^T = K Q^T, K from LDS -------------------------------
+      f32x4m acc[NKT];
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) acc[kt] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+      int krow[NKT];
+      bool k_ok[NKT];
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        const int key = 16 * kt + j;
+        k_ok[kt] = kt < NKT - 1 || key < lk;
+        krow[kt] = (k_ok[kt] ? key : 0) * d + 4 * g;
+      }
+#pragma unroll
+      for (int blk = 0; blk < QB; ++blk) {
+        if (blk < nblk) {                        // uniform
+          const bool t_ok = 16 * blk + 4 * g < d;
+          f32x4m kf[NKT];
+#pragma unroll
+          for (int kt = 0; kt < NKT; ++kt) {
+            const f32x4m x = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt] + 16 * blk);
+            kf[kt] = (k_ok[kt] & t_ok) ? x : f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+          }
+#pragma unroll
+          for (int s = 0; s < 4; ++s) {
+#pragma unroll
+            for (int kt = 0; kt < NKT; ++kt)
+              acc[kt] = mfma16x16x4(kf[kt][s], qf[blk][s], acc[kt]);
+          }
+        }
+      }
+
+      // ---- 2b. clipped softmax over the keys of query j ---------------------
+      float e[4 * NKT];
+      float m = -__builtin_inff();
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
+          const float sv = acc[kt][r] * scale;
+          e[4 * kt + r] = sv;
+          m = key_ok ? fmaxf(m, sv) : m;
+        }
+      }
+      m = fmaxf(m, row16_partner(m));
+      m = fmaxf(m, half32_partner(m));
+      const RowShift rs = row_shift(m, clip);
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
+          const float ev = exp_shift_clip<WIDE>(e[4 * kt + r], rs);
+          e[4 * kt + r] = key_ok ? ev : 0.0f;
+        }
+      }
+      float sum = tree_sum(e);
+      sum = sum + row16_partner(sum);
+      sum = sum + half32_partner(sum);
+      const float rcp = 1.0f / sum;
+#pragma unroll
+      for (int i = 0; i < 4 * NKT; ++i) e[i] = e[i] * rcp;
+
+      // ---- 2c. O = P V, V from LDS ------------------------------------------
+      // Contraction step i = 4 kt + r: key 16 kt + 4 g + r.  Keys past lk
+      // read row 0 and are zeroed (their weight is 0, but a stale value
+      // could be NaN).
+      int vrow[4 * NKT];
+      bool v_ok[4 * NKT];
+#pragma unroll
+      for (int i = 0; i < 4 * NKT; ++i) {
+        const int key = 16 * (i >> 2) + 4 * g + (i & 3);
+        v_ok[i] = (i >> 2) < NKT - 1 || key < lk;
+        vrow[i] = (v_ok[i] ? key : 0) * dv;
+      }
+      const __amdgpu_buffer_rsrc_t ro =
+          make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
+      const int orow = 4 * g * dv * 4;
+      const int nfull = dv >> 6;
+      for (int cb = 0; cb < nfull; ++cb) {
+        const int c = 64 * cb + 4 * j;
+        f32x4m oacc[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) oacc[u] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int i = 0; i < 4 * NKT; ++i) {
+          const f32x4m x = *reinterpret_cast<const f32x4m*>(lv_s + vrow[i] + c);
+          const f32x4m vf = v_ok[i] ? x : f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) oacc[u] = mfma16x16x4(e[i], vf[u], oacc[u]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const f32x4m ov = {oacc[0][r], oacc[1][r], oacc[2][r], oacc[3][r]};
+          __builtin_amdgcn_raw_buffer_store_b128(
+              __builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, ov), ro,
+              orow + (r * dv + c) * 4, 0, 0);
+        }
+      }
+      for (int c0 = 64 * nfull; c0 < dv; c0 += 16) {
+        const int c = c0 + j;
+        const bool c_ok = c < dv;
+        f32x4m oa = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int i = 0; i < 4 * NKT; ++i) {
+          const float x = lv_s[vrow[i] + (c_ok ? c : 0)];
+          oa = mfma16x16x4(e[i], (v_ok[i] & c_ok) ? x : 0.0f, oa);
+        }
+        float* orow_p = o + (b * lq + q0 + 4 * g) * static_cast<int64_t>(dv) + c;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if ((q0 + 4 * g + r < lq) & c_ok)
+            __builtin_nontemporal_store(oa[r], orow_p + static_cast<int64_t>(r) * dv);
+        }
+      }
+    }
+    __syncthreads();                             // LDS is free for the next item
+  }
+}
+
+}  // namespace smx

@@ -9,14 +9,13 @@
 #include <vector>
 
 #include "../../include/softmax_mi355x.h"
+#include "sm_host.hpp"
 #include "sm_kernels.hpp"
 
 namespace {
 
 using namespace smx;
-
-// Largest grid any launch uses; the kernels loop over the rest.
-constexpr int64_t kMaxGrid = int64_t(1) << 20;
+using namespace smx_host;
 
 // Bucket limits on cols.
 constexpr int64_t kPackedMaxCols = 64;
@@ -72,8 +71,6 @@ static_assert(kDepartOffset + kDepartBytes <= kWorkspaceBytes, "workspace layout
 constexpr int kMaxDevices = 64;
 constexpr int kMaxStreamWorkspaces = 64;  // per device
 
-thread_local int tl_last_hip_error = 0;
-
 struct StreamWorkspace {
   hipStream_t stream;
   char* mem;
@@ -87,21 +84,10 @@ struct DeviceState {
 std::mutex g_mu;
 DeviceState g_dev[kMaxDevices];
 
-inline bool aligned16(const void* p) {
-  return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
-}
-
-inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
-
 inline int64_t pow2_at_least(int64_t v) {
   int64_t p = 1;
   while (p < v) p <<= 1;
   return p;
-}
-
-int fail_hip(hipError_t e) {
-  tl_last_hip_error = static_cast<int>(e);
-  return SOFTMAX_ERR_HIP;
 }
 
 // rows*cols*4 must fit in int64 and both counts must be non-negative.
@@ -110,50 +96,6 @@ int check_sizes(int64_t rows, int64_t cols) {
   if (rows == 0 || cols == 0) return SOFTMAX_OK;
   if (rows > INT64_MAX / 4 / cols) return SOFTMAX_ERR_INVALID_ARG;
   return SOFTMAX_OK;
-}
-
-// Byte ranges [a, a+n) and [b, b+n) overlap without being identical.
-bool partial_overlap(const void* a, const void* b, int64_t n) {
-  const uintptr_t pa = reinterpret_cast<uintptr_t>(a);
-  const uintptr_t pb = reinterpret_cast<uintptr_t>(b);
-  if (pa == pb) return false;
-  return pa < pb + static_cast<uintptr_t>(n) && pb < pa + static_cast<uintptr_t>(n);
-}
-
-bool any_overlap(const void* a, const void* b, int64_t n) {
-  const uintptr_t pa = reinterpret_cast<uintptr_t>(a);
-  const uintptr_t pb = reinterpret_cast<uintptr_t>(b);
-  return pa < pb + static_cast<uintptr_t>(n) && pb < pa + static_cast<uintptr_t>(n);
-}
-
-// The device can use [p, p+bytes): memory registered with HIP, on the
-// current device when it is device memory, and inside one allocation.
-int check_device_range(const void* p, int64_t bytes, int dev) {
-  hipPointerAttribute_t a;
-  hipError_t e = hipPointerGetAttributes(&a, p);
-  if (e != hipSuccess) {
-    (void)hipGetLastError();
-    return SOFTMAX_ERR_NOT_DEVICE;
-  }
-  if (a.type == hipMemoryTypeDevice) {
-    if (a.device != dev) return SOFTMAX_ERR_NOT_DEVICE;
-    hipDeviceptr_t base = nullptr;
-    size_t size = 0;
-    e = hipMemGetAddressRange(&base, &size, const_cast<void*>(p));
-    if (e != hipSuccess) {
-      (void)hipGetLastError();
-      return SOFTMAX_ERR_NOT_DEVICE;
-    }
-    const uintptr_t lo = reinterpret_cast<uintptr_t>(base);
-    const uintptr_t pp = reinterpret_cast<uintptr_t>(p);
-    if (pp < lo || pp + static_cast<uintptr_t>(bytes) > lo + size)
-      return SOFTMAX_ERR_NOT_DEVICE;
-    return SOFTMAX_OK;
-  }
-  // Pinned (registered) host memory and managed memory are usable by the
-  // device; unregistered pageable memory is not.
-  if (a.type == hipMemoryTypeHost || a.type == hipMemoryTypeManaged) return SOFTMAX_OK;
-  return SOFTMAX_ERR_NOT_DEVICE;
 }
 
 softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t cols) {
@@ -226,10 +168,6 @@ softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t c
     }
   }
   return p;
-}
-
-hipError_t launch(const void* fn, int64_t grid, int block, void** args, hipStream_t s) {
-  return hipLaunchKernel(fn, dim3(static_cast<uint32_t>(grid)), dim3(block), args, 0, s);
 }
 
 // k_packed instances: G = 1 with EPL = 1..16, G = 2 and G = 4 with
@@ -441,18 +379,6 @@ int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
   return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
 }
 
-// The clip as the kernels take it, from the caller's bound: NaN and bounds
-// above SOFTMAX_CLIP_MAX are rejected; bounds below kClipFloor (and -inf)
-// run at kClipFloor with clipped value RN(e^bound) = 0.
-int make_clip(float clip_lo, Clip* c, bool* wide) {
-  if (!(clip_lo <= SOFTMAX_CLIP_MAX)) return SOFTMAX_ERR_INVALID_ARG;  // NaN too
-  c->lo = clip_lo < kClipFloor ? kClipFloor : clip_lo;
-  c->e_lo = clip_lo == kClipLo ? kExpClipLo
-                               : static_cast<float>(std::exp(static_cast<double>(clip_lo)));
-  *wide = c->lo < kClipWide;
-  return SOFTMAX_OK;
-}
-
 template <bool WIDE>
 hipError_t launch_rows(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
                        int64_t cols, Clip c, hipStream_t s) {
@@ -541,7 +467,7 @@ SOFTMAX_API const char* softmax_strerror(int code) {
   }
 }
 
-SOFTMAX_API int softmax_last_hip_error(void) { return tl_last_hip_error; }
+SOFTMAX_API int softmax_last_hip_error(void) { return smx_host::tl_last_hip_error; }
 
 SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int64_t n,
                                   float clip_lo, hipStream_t stream) {

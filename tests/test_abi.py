@@ -24,8 +24,9 @@ def declared_functions():
 
 def test_header_declares_entry_points():
     names = declared_functions()
-    for n in ("softmax_fwd", "softmax_fwd_clip", "softmax_strerror", "softmax_last_hip_error",
-              "softmax_plan", "softmax_exp_probe", "softmax_copy_probe"):
+    for n in ("softmax_fwd", "softmax_fwd_clip", "softmax_attention_fwd", "softmax_strerror",
+              "softmax_last_hip_error", "softmax_plan", "softmax_exp_probe",
+              "softmax_copy_probe"):
         assert n in names
 
 
@@ -176,3 +177,33 @@ def test_clip_bound_checked_before_any_hip_call():
     text = open(os.path.join(ROOT, "include", "softmax_mi355x.h")).read()
     assert re.search(r"#define SOFTMAX_CLIP_MAX \((-?[\d.]+)f\)", text).group(1) == "-48.0"
     assert sm.CLIP_MAX == -48.0
+
+
+def _attn(q, k, v, o, b, lq, lk, d, dv, scale=0.5, lo=-64.0):
+    return sm.softmax_attention_fwd_ptr(q, k, v, o, b, lq, lk, d, dv, scale, lo, 0)
+
+
+def test_attention_arguments_rejected_before_any_hip_call():
+    """Bad sizes, scales, bounds, null or overlapping pointers return
+    SOFTMAX_ERR_INVALID_ARG from checks that run before any HIP call."""
+    Q, K, V, O = 1 << 32, 2 << 32, 3 << 32, 4 << 32     # far apart, never dereferenced
+    bad = sm.ERR_INVALID_ARG
+    assert _attn(Q, K, V, O, -1, 50, 50, 200, 200) == bad
+    assert _attn(Q, K, V, O, 2, -1, 50, 200, 200) == bad
+    assert _attn(Q, K, V, O, 2, 50, 65, 200, 200) == bad          # more keys than one tile set
+    assert _attn(Q, K, V, O, 2, 50, 0, 200, 200) == bad           # softmax over no keys
+    assert _attn(Q, K, V, O, 2, 50, 50, 65537, 200) == bad
+    assert _attn(Q, K, V, O, 2, 50, 50, 200, 65537) == bad
+    assert _attn(Q, K, V, O, 2, 50, 50, 200, 200, scale=float("nan")) == bad
+    assert _attn(Q, K, V, O, 2, 50, 50, 200, 200, scale=float("inf")) == bad
+    assert _attn(Q, K, V, O, 2, 50, 50, 200, 200, lo=-1.0) == bad
+    assert _attn(Q, K, V, O, 2, 50, 50, 200, 200, lo=float("nan")) == bad
+    assert _attn(0, K, V, O, 2, 50, 50, 200, 200) == bad
+    assert _attn(Q, K, 0, O, 2, 50, 50, 200, 200) == bad
+    assert _attn(Q, K, V, 0, 2, 50, 50, 200, 200) == bad
+    assert _attn(Q, K, V, Q + 400, 2, 50, 50, 200, 200) == bad    # o overlaps q
+    assert _attn(Q, K, V, V - 4, 2, 50, 50, 200, 200) == bad      # o overlaps v
+    # nothing to do: success with no HIP call, even with null pointers
+    assert _attn(0, 0, 0, 0, 0, 50, 50, 200, 200) == sm.OK
+    assert _attn(0, 0, 0, 0, 2, 0, 50, 200, 200) == sm.OK
+    assert _attn(0, 0, 0, 0, 2, 50, 50, 200, 0) == sm.OK
