@@ -137,6 +137,25 @@ SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols
 SOFTMAX_API int softmax_fwd_clip(const float* x, float* y, int64_t rows, int64_t cols,
                                  float clip_lo, hipStream_t stream);
 
+/*
+ * softmax_fwd_approx -- softmax_fwd_clip with the cheap exponential the
+ * paper proposes as further work (Sec. 4: approximations that trade a little
+ * accuracy for speed): each e = exp(max(x - M, clip_lo)) is the single
+ * instruction v_exp_f32(RN(RN(x - M) * RN(log2 e))) in fp32 instead of the
+ * extended-precision argument of softmax_fwd.
+ *
+ * Accuracy (the stated, looser bound): every output y with exact value
+ * y* >= 2^-126 satisfies |y - y*| <= (2e-6 + 1.5e-7 * min(|x - M|, |clip_lo|)) * y*:
+ * the fp32 argument carries a relative error of about 1.33e-7 that the
+ * exponential turns into 1.33e-7 * |x - M|, so it grows with the distance
+ * from the row max (about 1.2e-5 at the -64 clip).  Outputs whose exact
+ * value is below 2^-126 (only possible with clip_lo < -87) may be flushed
+ * to 0.  Arguments, layout, errors and everything else are those of
+ * softmax_fwd_clip.
+ */
+SOFTMAX_API int softmax_fwd_approx(const float* x, float* y, int64_t rows, int64_t cols,
+                                   float clip_lo, hipStream_t stream);
+
 /* Limits of softmax_attention_fwd. */
 #define SOFTMAX_ATTN_MAX_KEYS 64     /* lk: the keys of one row fit one set of tiles */
 #define SOFTMAX_ATTN_MAX_DIM 65536   /* d and dv */
@@ -210,12 +229,13 @@ SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64
  * softmax_exp_probe -- diagnostic: e[i] = exp(max(x[i] - m[i], clip_lo))
  * for 0 <= i < n, through the same device routine the softmax kernels use
  * for the clipped exp (Sec. 1.2 Fig. 1, the ValueClip then exp), with the
- * clip_lo rules of softmax_fwd_clip.  x, m, e are device fp32 arrays of n
- * elements owned by the caller (e must not overlap x or m).  Same error
- * rules as softmax_fwd_clip.
+ * clip_lo rules of softmax_fwd_clip: the routine of softmax_fwd_clip when
+ * approx == 0, that of softmax_fwd_approx otherwise.  x, m, e are device
+ * fp32 arrays of n elements owned by the caller (e must not overlap x or
+ * m).  Same error rules as softmax_fwd_clip.
  */
 SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int64_t n,
-                                  float clip_lo, hipStream_t stream);
+                                  float clip_lo, int approx, hipStream_t stream);
 
 /*
  * softmax_copy_probe -- diagnostic: y[i] = x[i] for 0 <= i < n with 128-bit

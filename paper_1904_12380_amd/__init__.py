@@ -11,6 +11,8 @@ Functions keep the C names:
     softmax_fwd_ptr(x_ptr, y_ptr, rows, cols, stream_handle) -> int
     softmax_fwd_clip(x, clip_lo, out=None, stream=None) -> torch.Tensor
     softmax_fwd_clip_ptr(x_ptr, y_ptr, rows, cols, clip_lo, stream_handle) -> int
+    softmax_fwd_approx(x, clip_lo=-64.0, out=None, stream=None) -> torch.Tensor
+    softmax_fwd_approx_ptr(x_ptr, y_ptr, rows, cols, clip_lo, stream_handle) -> int
     softmax_attention_fwd(q, k, v, scale=None, clip_lo=-64.0, out=None, stream=None)
     softmax_attention_fwd_ptr(q_ptr, k_ptr, v_ptr, o_ptr, batch, lq, lk, d, dv,
                               scale, clip_lo, stream_handle) -> int
@@ -28,6 +30,7 @@ import os
 __all__ = [
     "LIB_PATH", "HEADER_PATH", "SoftmaxError", "load_library", "softmax_fwd",
     "softmax_fwd_ptr", "softmax_fwd_clip", "softmax_fwd_clip_ptr", "softmax_plan",
+    "softmax_fwd_approx", "softmax_fwd_approx_ptr",
     "softmax_attention_fwd", "softmax_attention_fwd_ptr", "ATTN_MAX_KEYS", "ATTN_MAX_DIM",
     "softmax_exp_probe", "softmax_copy_probe", "softmax_strerror", "softmax_last_hip_error",
     "CLIP_LO", "CLIP_MAX", "KERNEL_NAMES",
@@ -95,7 +98,9 @@ def load_library() -> ctypes.CDLL:
     lib.softmax_last_hip_error.restype = ctypes.c_int
     lib.softmax_plan.argtypes = [vp, vp, i64, i64, ctypes.POINTER(_Plan)]
     lib.softmax_plan.restype = ctypes.c_int
-    lib.softmax_exp_probe.argtypes = [vp, vp, vp, i64, ctypes.c_float, vp]
+    lib.softmax_exp_probe.argtypes = [vp, vp, vp, i64, ctypes.c_float, ctypes.c_int, vp]
+    lib.softmax_fwd_approx.argtypes = [vp, vp, i64, i64, ctypes.c_float, vp]
+    lib.softmax_fwd_approx.restype = ctypes.c_int
     lib.softmax_exp_probe.restype = ctypes.c_int
     lib.softmax_copy_probe.argtypes = [vp, vp, i64, vp]
     lib.softmax_copy_probe.restype = ctypes.c_int
@@ -205,6 +210,27 @@ def softmax_fwd_clip(x, clip_lo: float, out=None, stream=None):
     return out
 
 
+def softmax_fwd_approx_ptr(x_ptr: int, y_ptr: int, rows: int, cols: int, clip_lo: float,
+                           stream_handle: int = 0) -> int:
+    """Raw C call; returns the C return code."""
+    return int(load_library().softmax_fwd_approx(x_ptr, y_ptr, rows, cols, float(clip_lo),
+                                                 stream_handle))
+
+
+def softmax_fwd_approx(x, clip_lo: float = CLIP_LO, out=None, stream=None):
+    """softmax_fwd_clip with the fast fp32 exponential (looser, stated
+    bound: 2e-6 + 1.5e-7 |x - max| relative)."""
+    torch = _torch()
+    out = _out_for(x, out)
+    rows, cols = x.shape
+    with torch.cuda.device(x.device):
+        rc = softmax_fwd_approx_ptr(x.data_ptr(), out.data_ptr(), rows, cols, clip_lo,
+                                    _stream_handle(stream))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_fwd_approx")
+    return out
+
+
 def softmax_attention_fwd_ptr(q_ptr: int, k_ptr: int, v_ptr: int, o_ptr: int, batch: int,
                               lq: int, lk: int, d: int, dv: int, scale: float,
                               clip_lo: float = CLIP_LO, stream_handle: int = 0) -> int:
@@ -244,9 +270,10 @@ def softmax_attention_fwd(q, k, v, scale=None, clip_lo: float = CLIP_LO, out=Non
     return out
 
 
-def softmax_exp_probe(x, m, out=None, stream=None, clip_lo: float = CLIP_LO):
+def softmax_exp_probe(x, m, out=None, stream=None, clip_lo: float = CLIP_LO,
+                      approx: bool = False):
     """e = exp(max(x - m, clip_lo)) elementwise through the kernels' exp
-    routine."""
+    routine (the fast approximation of softmax_fwd_approx if ``approx``)."""
     torch = _torch()
     _check_f32_cuda(x, "x")
     _check_f32_cuda(m, "m")
@@ -258,7 +285,7 @@ def softmax_exp_probe(x, m, out=None, stream=None, clip_lo: float = CLIP_LO):
     with torch.cuda.device(x.device):
         rc = int(load_library().softmax_exp_probe(
             x.data_ptr(), m.data_ptr(), out.data_ptr(), x.numel(), float(clip_lo),
-            _stream_handle(stream)))
+            int(bool(approx)), _stream_handle(stream)))
     if rc != OK:
         raise SoftmaxError(rc, "softmax_exp_probe")
     return out

@@ -180,7 +180,7 @@ __global__ __launch_bounds__(256) void k_attention(const float* q, const float* 
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
-        const float ev = exp_shift_clip<WIDE>(e[4 * kt + r], rs);
+        const float ev = exp_shift_clip<WIDE ? kExpWide : kExpAccurate>(e[4 * kt + r], rs);
         e[4 * kt + r] = key_ok ? ev : 0.0f;
       }
     }
@@ -400,7 +400,7 @@ __global__ __launch_bounds__(256) void k_attention_lds(const float* q, const flo
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
-          const float ev = exp_shift_clip<WIDE>(e[4 * kt + r], rs);
+          const float ev = exp_shift_clip<WIDE ? kExpWide : kExpAccurate>(e[4 * kt + r], rs);
           e[4 * kt + r] = key_ok ? ev : 0.0f;
         }
       }

@@ -38,6 +38,20 @@ constexpr float kExpClipLo = 0x1.969d48p-93f;  // 1.6038109e-28
 constexpr float kClipFloor = -128.0f;
 constexpr float kClipWide = -87.0f;
 
+// How a kernel evaluates the clipped exponential (a template argument):
+//   kExpAccurate  binary64 argument, v_exp_f32 on the fp32 part (results
+//                 normal: bounds >= kClipWide);
+//   kExpWide      the same, plus the range below 2^-126 (bounds < kClipWide);
+//   kExpFast      the single-instruction exponential on an fp32 argument,
+//                 v_exp_f32(RN(RN(x - M) * RN(log2 e))): the cheaper
+//                 approximation the paper suggests as further work (Sec. 4).
+//                 Its relative error grows with |x - M|: below
+//                 1.5e-7 |x - M| + 1.2e-7 where the result is normal; results
+//                 under 2^-126 are flushed to 0.
+constexpr int kExpAccurate = 0;
+constexpr int kExpWide = 1;
+constexpr int kExpFast = 2;
+
 // The clip as a kernel argument: lo in [kClipFloor, 0] and e_lo = RN(e^lo')
 // for the caller's bound lo' (0 when lo' < -103.98 or lo' = -inf).
 struct Clip {
@@ -71,6 +85,7 @@ __device__ __forceinline__ void st_stream(float* p, f32x4 v) {
 //   e_lo:  the value of a clipped exponential.
 struct RowShift {
   double neg_m;
+  float m;
   float tc;
   float e_lo;
 };
@@ -78,6 +93,7 @@ struct RowShift {
 __device__ __forceinline__ RowShift row_shift(float m, Clip clip) {
   RowShift r;
   r.neg_m = -static_cast<double>(m);
+  r.m = m;
   // M + lo is exact in binary64 unless the exponents of M and lo differ by
   // more than 29 (|M| < 2^-23 |lo|), where the rounding is below 2^-47 |lo|
   // and only moves the boundary by that much.
@@ -104,20 +120,25 @@ __device__ __forceinline__ RowShift row_shift(float m, Clip clip) {
 // 3. e = 2^th * e^r = v_exp_f32(th) * (1 + r), rounded once by an fp32 fma;
 //    the dropped r^2/2 is below 4e-12.  With lo >= kClipWide, th stays in
 //    [-125.6, 0], where 2^th is a normal fp32.
-// 4. WIDE (lo < kClipWide): v_exp_f32 returns no denormals, so for
+// 4. kExpWide (lo < kClipWide): v_exp_f32 returns no denormals, so for
 //    th < -126 the fma works on 2^(th+64) (exact shift, th >= -185 since
 //    lo >= kClipFloor) and one final multiplication by 2^-64 rounds the
 //    result into the denormal range.
 // 5. Clipped elements (x < tc) return e_lo; this also covers x = -inf.
 //    NaN inputs, and rows whose max is +inf or -inf, give NaN.
-template <bool WIDE>
+template <int EM>
 __device__ __forceinline__ float exp_shift_clip(float x, RowShift rs) {
+  if constexpr (EM == kExpFast) {
+    const float t = (x - rs.m) * 0x1.715476p+0f;     // RN(log2 e) in fp32
+    const float e = __builtin_amdgcn_exp2f(t);
+    return x < rs.tc ? rs.e_lo : e;
+  }
   const double d = static_cast<double>(x) + rs.neg_m;
   const double t = d * kLog2e;
   const float th = static_cast<float>(t);
   const double r = __builtin_fma(static_cast<double>(th), -kLn2, d);
   float e;
-  if constexpr (WIDE) {
+  if constexpr (EM == kExpWide) {
     const bool tiny = th < -126.0f;
     const float e0 = __builtin_amdgcn_exp2f(tiny ? th + 64.0f : th);
     const float ew = __builtin_fmaf(e0, static_cast<float>(r), e0);

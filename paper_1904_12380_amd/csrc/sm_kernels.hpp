@@ -6,8 +6,8 @@
 // subtract, exp, row sum, scale by the reciprocal of the sum) with the clip
 // of the reference functor (Sec. 1.2, Fig. 1) at a bound lo given as a
 // kernel argument (default -64; no clip runs as the floor bound with a
-// clipped value of 0).  WIDE instances handle bounds whose unclipped
-// exponentials can be denormal.  Unlike the CPU functor, no kernel uses y
+// clipped value of 0).  The exponential is evaluated as the template argument EM says
+// (accurate, accurate into the denormal range, or the fast approximation).  Unlike the CPU functor, no kernel uses y
 // as scratch: x is read from HBM once (twice for rows over 2^21 columns)
 // and y is written once.
 //
@@ -108,10 +108,10 @@ __device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* p, in
 
 // Replaces v by the clipped exponentials and returns this lane's pairwise
 // partial sum.
-template <bool WIDE, int N>
+template <int EM, int N>
 __device__ __forceinline__ float exp_strip(float (&v)[N], RowShift rs) {
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = exp_shift_clip<WIDE>(v[i], rs);
+  for (int i = 0; i < N; ++i) v[i] = exp_shift_clip<EM>(v[i], rs);
   return tree_sum(v);
 }
 
@@ -158,7 +158,7 @@ __device__ __forceinline__ int seg_len(int64_t cols, int64_t c0, int64_t cap) {
 // The grid is persistent (a few workgroups per CU, each looping over tiles)
 // and every workgroup issues the loads of its next tile right after staging
 // the current one, so they are in flight while the current tile computes.
-template <int G, int EPL, bool WIDE>
+template <int G, int EPL, int EM>
 __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int r, int j,
                                             Clip clip) {
   const bool active = r < nr;
@@ -171,7 +171,7 @@ __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int 
   }
   const RowShift rs = row_shift(seg_max<G>(array_max(v)), clip);
 #pragma unroll
-  for (int k = 0; k < EPL; ++k) v[k] = exp_shift_clip<WIDE>(v[k], rs);
+  for (int k = 0; k < EPL; ++k) v[k] = exp_shift_clip<EM>(v[k], rs);
   const float rcp = 1.0f / seg_sum<G>(tree_sum(v));
 #pragma unroll
   for (int k = 0; k < EPL; ++k) {
@@ -180,7 +180,7 @@ __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int 
   }
 }
 
-template <int G, int EPL, bool VEC4, bool WIDE>
+template <int G, int EPL, bool VEC4, int EM>
 __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_t rows,
                                                 int64_t cols, Clip clip) {
   constexpr int kRows = 256 / G;
@@ -247,7 +247,7 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
     __syncthreads();
     if (t + gridDim.x < ntiles) issue(t + gridDim.x);
 
-    packed_rows<G, EPL, WIDE>(tile, nr, ccols, r, j, clip);
+    packed_rows<G, EPL, EM>(tile, nr, ccols, r, j, clip);
     __syncthreads();
 
     if constexpr (VEC4) {
@@ -265,7 +265,7 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
 // ---------------------------------------------------------------------------
 // (b) One wavefront per row, cols <= 256*V (4*V elements per lane).
 // Four wavefronts per workgroup work on four rows independently.
-template <int V, bool VEC4, bool WIDE>
+template <int V, bool VEC4, int EM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_wave_row(
     const float* x, float* y, int64_t rows, int64_t cols, Clip clip) {
   const int lane = __lane_id();
@@ -278,7 +278,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, lane, 64, lim);
     const RowShift rs = row_shift(seg_max<64>(array_max(v)), clip);
-    const float s = seg_sum<64>(exp_strip<WIDE>(v, rs));
+    const float s = seg_sum<64>(exp_strip<EM>(v, rs));
     const float rcp = 1.0f / s;
     store_strip<V, VEC4>(v, rcp, yr, lane, 64, lim);
   }
@@ -286,7 +286,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
 
 // ---------------------------------------------------------------------------
 // (c) One workgroup of NT threads per row, cols <= 4*V*NT.
-template <int NT, int V, bool VEC4, bool WIDE>
+template <int NT, int V, bool VEC4, int EM>
 __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int64_t rows,
                                                   int64_t cols, Clip clip) {
   constexpr int NW = NT / 64;
@@ -300,7 +300,7 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int6
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, tid, NT, lim);
     const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max), clip);
-    const float s = block_sum<NW>(exp_strip<WIDE>(v, rs), red_sum);
+    const float s = block_sum<NW>(exp_strip<EM>(v, rs), red_sum);
     const float rcp = 1.0f / s;
     store_strip<V, VEC4>(v, rcp, yr, tid, NT, lim);
   }
@@ -321,7 +321,7 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int6
 // y = exp(max(x - M, lo)) / S.  Using the clip relative to m_g inside a
 // partial changes S by at most cols * e^lo relative (below 1e-10 for any
 // row that fits in memory, since lo <= -48), far under fp32 resolution.
-template <int NT, int V, bool VEC4, bool WIDE>
+template <int NT, int V, bool VEC4, int EM>
 __global__ __launch_bounds__(NT) void k_split_stats(const float* x, float2* part,
                                                     int64_t rows, int64_t cols,
                                                     int64_t chunks, Clip clip) {
@@ -342,13 +342,13 @@ __global__ __launch_bounds__(NT) void k_split_stats(const float* x, float2* part
     const float m = block_max<NW>(array_max(v), red_max);
     const bool empty_max = (m == kNegInf);
     const RowShift rs = row_shift(empty_max ? 0.0f : m, clip);
-    float s = block_sum<NW>(exp_strip<WIDE>(v, rs), red_sum);
+    float s = block_sum<NW>(exp_strip<EM>(v, rs), red_sum);
     if (empty_max) s = static_cast<float>(lim);
     if (tid == 0) part[b] = make_float2(m, s);
   }
 }
 
-template <int NT, int V, bool VEC4, bool WIDE>
+template <int NT, int V, bool VEC4, int EM>
 __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
                                                     const float2* part, int64_t rows,
                                                     int64_t cols, int64_t chunks, Clip clip) {
@@ -373,12 +373,12 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
     float ss = 0.0f;
     for (int64_t l = lane; l < chunks; l += 64) {
       const float2 p = pr[l];
-      ss = ss + p.y * exp_shift_clip<WIDE>(p.x, rs);
+      ss = ss + p.y * exp_shift_clip<EM>(p.x, rs);
     }
     const float rcp = 1.0f / seg_sum<64>(ss);
 
 #pragma unroll
-    for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip<WIDE>(v[i], rs);
+    for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip<EM>(v[i], rs);
     store_strip<V, VEC4>(v, rcp, yr, tid, NT, lim);
   }
 }
@@ -423,7 +423,7 @@ __device__ __forceinline__ unsigned long long pack_pair(float a, float b) {
          (static_cast<unsigned long long>(__builtin_bit_cast(unsigned, b)) << 32);
 }
 
-template <int NT, int V, bool VEC4, bool WIDE>
+template <int NT, int V, bool VEC4, int EM>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 : 4))) void k_split_onepass(
     const float* x, float* y, unsigned long long* part, unsigned* depart, int64_t cols,
     int chunks, Clip clip) {
@@ -445,7 +445,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 :
   load_strip<V, VEC4>(v, xr, tid, NT, lim);
   const float m = block_max<NW>(array_max(v), red_max);
   const bool empty_max = (m == kNegInf);
-  float s = block_sum<NW>(exp_strip<WIDE>(v, row_shift(empty_max ? 0.0f : m, clip)), red_sum);
+  float s = block_sum<NW>(exp_strip<EM>(v, row_shift(empty_max ? 0.0f : m, clip)), red_sum);
   if (empty_max) s = static_cast<float>(lim);
 
   if (tid == 0) {
@@ -473,10 +473,10 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 :
     const float ps =
         (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q >> 32)) : 0.0f;
     const RowShift rs = row_shift(seg_max<64>(pm), clip);
-    const float term = (tid < chunks) ? ps * exp_shift_clip<WIDE>(pm, rs) : 0.0f;
+    const float term = (tid < chunks) ? ps * exp_shift_clip<EM>(pm, rs) : 0.0f;
     const float rcp = 1.0f / seg_sum<64>(term);
     if (tid == 0) {
-      bcast[0] = ok ? exp_shift_clip<WIDE>(m, rs) * rcp : __builtin_nanf("");  // e^(m_g - M) / S
+      bcast[0] = ok ? exp_shift_clip<EM>(m, rs) * rcp : __builtin_nanf("");  // e^(m_g - M) / S
       bcast[1] = ok ? clip.e_lo * rcp : __builtin_nanf("");                    // e_lo / S
       // Depart once this wave's slot reads have returned (the add's operand
       // depends on them); the last workgroup of the row restores the slots.
@@ -504,12 +504,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 :
 
 // e[i] = exp(max(x[i] - m[i], lo)), through the same device routine the
 // softmax kernels use.
-template <bool WIDE>
+template <int EM>
 __global__ __launch_bounds__(256) void k_exp_probe(const float* x, const float* m,
                                                    float* e, int64_t n, Clip clip) {
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
        i += static_cast<int64_t>(gridDim.x) * 256)
-    e[i] = exp_shift_clip<WIDE>(x[i], row_shift(m[i], clip));
+    e[i] = exp_shift_clip<EM>(x[i], row_shift(m[i], clip));
 }
 
 // Plain copy with 128-bit streaming accesses: the memory-bound ceiling that

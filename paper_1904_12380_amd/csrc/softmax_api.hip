@@ -172,27 +172,27 @@ softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t c
 
 // k_packed instances: G = 1 with EPL = 1..16, G = 2 and G = 4 with
 // EPL = 9..16 (a plan never asks for fewer columns per lane at G > 1).
-template <int G, bool VEC4, bool WIDE, int... E>
+template <int G, bool VEC4, int EM, int... E>
 const void* packed_fn(int epl, std::integer_sequence<int, E...>) {
   static const void* const table[] = {
-      reinterpret_cast<const void*>(&k_packed<G, (G == 1 ? 1 : 9) + E, VEC4, WIDE>)...};
+      reinterpret_cast<const void*>(&k_packed<G, (G == 1 ? 1 : 9) + E, VEC4, EM>)...};
   const int idx = epl - (G == 1 ? 1 : 9);
   return (idx >= 0 && idx < static_cast<int>(sizeof...(E))) ? table[idx] : nullptr;
 }
 
-template <bool VEC4, bool WIDE>
+template <bool VEC4, int EM>
 hipError_t dispatch_packed(const softmax_plan_t& p, const float* x, float* y,
                            int64_t rows, int64_t cols, Clip c, hipStream_t s) {
   const void* fn = nullptr;
   switch (p.lanes_per_row) {
     case 1:
-      fn = packed_fn<1, VEC4, WIDE>(p.elems_per_lane, std::make_integer_sequence<int, 16>{});
+      fn = packed_fn<1, VEC4, EM>(p.elems_per_lane, std::make_integer_sequence<int, 16>{});
       break;
     case 2:
-      fn = packed_fn<2, VEC4, WIDE>(p.elems_per_lane, std::make_integer_sequence<int, 8>{});
+      fn = packed_fn<2, VEC4, EM>(p.elems_per_lane, std::make_integer_sequence<int, 8>{});
       break;
     default:
-      fn = packed_fn<4, VEC4, WIDE>(p.elems_per_lane, std::make_integer_sequence<int, 8>{});
+      fn = packed_fn<4, VEC4, EM>(p.elems_per_lane, std::make_integer_sequence<int, 8>{});
       break;
   }
   if (fn == nullptr) return hipErrorInvalidValue;
@@ -200,45 +200,45 @@ hipError_t dispatch_packed(const softmax_plan_t& p, const float* x, float* y,
   return launch(fn, p.grid, 256, args, s);
 }
 
-template <int V, bool VEC4, bool WIDE>
+template <int V, bool VEC4, int EM>
 hipError_t run_wave(const float* x, float* y, int64_t rows, int64_t cols, Clip c,
                     int64_t grid, hipStream_t s) {
   void* args[] = {&x, &y, &rows, &cols, &c};
-  return launch(reinterpret_cast<const void*>(&k_wave_row<V, VEC4, WIDE>), grid, 256, args,
+  return launch(reinterpret_cast<const void*>(&k_wave_row<V, VEC4, EM>), grid, 256, args,
                 s);
 }
 
-template <bool VEC4, bool WIDE>
+template <bool VEC4, int EM>
 hipError_t dispatch_wave(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
                          int64_t cols, Clip c, hipStream_t s) {
   switch (p.elems_per_lane / 4) {
-    case 1: return run_wave<1, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
-    case 2: return run_wave<2, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
-    case 4: return run_wave<4, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
-    case 8: return run_wave<8, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
-    default: return run_wave<16, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
+    case 1: return run_wave<1, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
+    case 2: return run_wave<2, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
+    case 4: return run_wave<4, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
+    case 8: return run_wave<8, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
+    default: return run_wave<16, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
   }
 }
 
-template <int V, bool VEC4, bool WIDE>
+template <int V, bool VEC4, int EM>
 hipError_t run_block(const float* x, float* y, int64_t rows, int64_t cols, Clip c,
                      int64_t grid, hipStream_t s) {
   void* args[] = {&x, &y, &rows, &cols, &c};
-  return launch(reinterpret_cast<const void*>(&k_block_row<1024, V, VEC4, WIDE>), grid, 1024,
+  return launch(reinterpret_cast<const void*>(&k_block_row<1024, V, VEC4, EM>), grid, 1024,
                 args, s);
 }
 
-template <bool VEC4, bool WIDE>
+template <bool VEC4, int EM>
 hipError_t dispatch_block(const softmax_plan_t& p, const float* x, float* y,
                           int64_t rows, int64_t cols, Clip c, hipStream_t s) {
   switch (p.elems_per_lane / 4) {
-    case 2: return run_block<2, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
-    case 4: return run_block<4, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
-    default: return run_block<8, VEC4, WIDE>(x, y, rows, cols, c, p.grid, s);
+    case 2: return run_block<2, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
+    case 4: return run_block<4, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
+    default: return run_block<8, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
   }
 }
 
-template <bool VEC4, bool WIDE>
+template <bool VEC4, int EM>
 hipError_t run_split(const float* x, float* y, float2* ws, int64_t rows, int64_t cols,
                      int64_t chunks, Clip c, hipStream_t s) {
   const int64_t rows_per_batch = std::max<int64_t>(1, kWorkspacePairs / chunks);
@@ -249,20 +249,20 @@ hipError_t run_split(const float* x, float* y, float2* ws, int64_t rows, int64_t
     const int64_t grid = std::min(nb * chunks, kMaxGrid);
     void* a1[] = {&xb, &ws, &nb, &cols, &chunks, &c};
     hipError_t e = launch(
-        reinterpret_cast<const void*>(&k_split_stats<kSplitThreads, kSplitV, VEC4, WIDE>),
+        reinterpret_cast<const void*>(&k_split_stats<kSplitThreads, kSplitV, VEC4, EM>),
         grid, kSplitThreads, a1, s);
     if (e != hipSuccess) return e;
     const float2* wsc = ws;
     void* a2[] = {&xb, &yb, &wsc, &nb, &cols, &chunks, &c};
     e = launch(
-        reinterpret_cast<const void*>(&k_split_apply<kSplitThreads, kSplitV, VEC4, WIDE>),
+        reinterpret_cast<const void*>(&k_split_apply<kSplitThreads, kSplitV, VEC4, EM>),
         grid, kSplitThreads, a2, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
-template <int V, bool VEC4, bool WIDE>
+template <int V, bool VEC4, int EM>
 hipError_t run_onepass(const float* x, float* y, char* ws, int64_t rows, int64_t cols,
                        int64_t chunks, int64_t max_blocks, Clip c, hipStream_t s) {
   unsigned long long* part = reinterpret_cast<unsigned long long*>(ws + kSlotsOffset);
@@ -275,7 +275,7 @@ hipError_t run_onepass(const float* x, float* y, char* ws, int64_t rows, int64_t
     float* yb = y + r0 * cols;
     void* args[] = {&xb, &yb, &part, &depart, &cols, &ichunks, &c};
     hipError_t e = launch(
-        reinterpret_cast<const void*>(&k_split_onepass<kOnePassThreads, V, VEC4, WIDE>),
+        reinterpret_cast<const void*>(&k_split_onepass<kOnePassThreads, V, VEC4, EM>),
         nb * chunks, kOnePassThreads, args, s);
     if (e != hipSuccess) return e;
   }
@@ -343,23 +343,23 @@ int workspace_for(int dev, hipStream_t s, bool capturing, char** out) {
   return SOFTMAX_OK;
 }
 
-template <bool VEC4, bool WIDE>
+template <bool VEC4, int EM>
 hipError_t split_launch(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
                         int64_t cols, char* ws, Clip c, hipStream_t s) {
   // Plans with at most kOnePassMaxChunks chunks per row are one-pass (their
   // chunk size is told by elems_per_lane); longer rows are two-pass.
   const int64_t g = p.chunks_per_row;
   if (g <= kOnePassMaxChunks && p.elems_per_lane == 4 * kOnePassVSmall)
-    return run_onepass<kOnePassVSmall, VEC4, WIDE>(x, y, ws, rows, cols, g,
+    return run_onepass<kOnePassVSmall, VEC4, EM>(x, y, ws, rows, cols, g,
                                                    kOnePassMaxBlocksSmall, c, s);
   if (g <= kOnePassMaxChunks)
-    return run_onepass<kOnePassVLarge, VEC4, WIDE>(x, y, ws, rows, cols, g,
+    return run_onepass<kOnePassVLarge, VEC4, EM>(x, y, ws, rows, cols, g,
                                                    kOnePassMaxBlocksLarge, c, s);
-  return run_split<VEC4, WIDE>(x, y, reinterpret_cast<float2*>(ws), rows, cols, g, c, s);
+  return run_split<VEC4, EM>(x, y, reinterpret_cast<float2*>(ws), rows, cols, g, c, s);
 }
 
 int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
-               int64_t cols, int dev, Clip c, bool wide, hipStream_t s) {
+               int64_t cols, int dev, Clip c, int em, hipStream_t s) {
   if (dev < 0 || dev >= kMaxDevices) return SOFTMAX_ERR_INVALID_ARG;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
   hipError_t e = hipStreamIsCapturing(s, &cap);
@@ -370,28 +370,36 @@ int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
     const int rc = workspace_for(dev, s, cap != hipStreamCaptureStatusNone, &ws);
     if (rc != SOFTMAX_OK) return rc;
   }
-  if (p.vec_width == 4)
-    e = wide ? split_launch<true, true>(p, x, y, rows, cols, ws, c, s)
-             : split_launch<true, false>(p, x, y, rows, cols, ws, c, s);
-  else
-    e = wide ? split_launch<false, true>(p, x, y, rows, cols, ws, c, s)
-             : split_launch<false, false>(p, x, y, rows, cols, ws, c, s);
+  switch (em) {
+    case kExpWide:
+      e = p.vec_width == 4 ? split_launch<true, kExpWide>(p, x, y, rows, cols, ws, c, s)
+                           : split_launch<false, kExpWide>(p, x, y, rows, cols, ws, c, s);
+      break;
+    case kExpFast:
+      e = p.vec_width == 4 ? split_launch<true, kExpFast>(p, x, y, rows, cols, ws, c, s)
+                           : split_launch<false, kExpFast>(p, x, y, rows, cols, ws, c, s);
+      break;
+    default:
+      e = p.vec_width == 4 ? split_launch<true, kExpAccurate>(p, x, y, rows, cols, ws, c, s)
+                           : split_launch<false, kExpAccurate>(p, x, y, rows, cols, ws, c, s);
+      break;
+  }
   return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
 }
 
-template <bool WIDE>
+template <int EM>
 hipError_t launch_rows(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
                        int64_t cols, Clip c, hipStream_t s) {
   switch (p.kernel) {
     case SOFTMAX_KERNEL_PACKED:
-      return p.vec_width == 4 ? dispatch_packed<true, WIDE>(p, x, y, rows, cols, c, s)
-                              : dispatch_packed<false, WIDE>(p, x, y, rows, cols, c, s);
+      return p.vec_width == 4 ? dispatch_packed<true, EM>(p, x, y, rows, cols, c, s)
+                              : dispatch_packed<false, EM>(p, x, y, rows, cols, c, s);
     case SOFTMAX_KERNEL_WAVE_ROW:
-      return p.vec_width == 4 ? dispatch_wave<true, WIDE>(p, x, y, rows, cols, c, s)
-                              : dispatch_wave<false, WIDE>(p, x, y, rows, cols, c, s);
+      return p.vec_width == 4 ? dispatch_wave<true, EM>(p, x, y, rows, cols, c, s)
+                              : dispatch_wave<false, EM>(p, x, y, rows, cols, c, s);
     case SOFTMAX_KERNEL_BLOCK_ROW:
-      return p.vec_width == 4 ? dispatch_block<true, WIDE>(p, x, y, rows, cols, c, s)
-                              : dispatch_block<false, WIDE>(p, x, y, rows, cols, c, s);
+      return p.vec_width == 4 ? dispatch_block<true, EM>(p, x, y, rows, cols, c, s)
+                              : dispatch_block<false, EM>(p, x, y, rows, cols, c, s);
     default:
       return hipSuccess;
   }
@@ -407,6 +415,28 @@ int check_pointers(const float* x, const float* y, int64_t n_elems, int* dev) {
   if (rc != SOFTMAX_OK) return rc;
   if (y != x) rc = check_device_range(y, bytes, *dev);
   return rc;
+}
+
+// The row softmax with exponential mode em (kExpAccurate, kExpWide or
+// kExpFast) after the clip and size checks.
+int softmax_rows(const float* x, float* y, int64_t rows, int64_t cols, Clip c, int em,
+                 hipStream_t stream) {
+  int rc = check_sizes(rows, cols);
+  if (rc != SOFTMAX_OK) return rc;
+  if (rows == 0 || cols == 0) return SOFTMAX_OK;
+  int dev = 0;
+  rc = check_pointers(x, y, rows * cols, &dev);
+  if (rc != SOFTMAX_OK) return rc;
+
+  const softmax_plan_t p = make_plan(x, y, rows, cols);
+  if (p.kernel == SOFTMAX_KERNEL_SPLIT_ROW) return split_call(p, x, y, rows, cols, dev, c, em, stream);
+  hipError_t e;
+  switch (em) {
+    case kExpWide: e = launch_rows<kExpWide>(p, x, y, rows, cols, c, stream); break;
+    case kExpFast: e = launch_rows<kExpFast>(p, x, y, rows, cols, c, stream); break;
+    default: e = launch_rows<kExpAccurate>(p, x, y, rows, cols, c, stream); break;
+  }
+  return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
 }
 
 }  // namespace
@@ -430,21 +460,18 @@ SOFTMAX_API int softmax_fwd_clip(const float* x, float* y, int64_t rows, int64_t
                                  float clip_lo, hipStream_t stream) {
   Clip c;
   bool wide = false;
-  int rc = make_clip(clip_lo, &c, &wide);
+  const int rc = make_clip(clip_lo, &c, &wide);
   if (rc != SOFTMAX_OK) return rc;
-  rc = check_sizes(rows, cols);
-  if (rc != SOFTMAX_OK) return rc;
-  if (rows == 0 || cols == 0) return SOFTMAX_OK;
-  int dev = 0;
-  rc = check_pointers(x, y, rows * cols, &dev);
-  if (rc != SOFTMAX_OK) return rc;
+  return softmax_rows(x, y, rows, cols, c, wide ? kExpWide : kExpAccurate, stream);
+}
 
-  const softmax_plan_t p = make_plan(x, y, rows, cols);
-  if (p.kernel == SOFTMAX_KERNEL_SPLIT_ROW)
-    return split_call(p, x, y, rows, cols, dev, c, wide, stream);
-  const hipError_t e = wide ? launch_rows<true>(p, x, y, rows, cols, c, stream)
-                            : launch_rows<false>(p, x, y, rows, cols, c, stream);
-  return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
+SOFTMAX_API int softmax_fwd_approx(const float* x, float* y, int64_t rows, int64_t cols,
+                                   float clip_lo, hipStream_t stream) {
+  Clip c;
+  bool wide = false;
+  const int rc = make_clip(clip_lo, &c, &wide);
+  if (rc != SOFTMAX_OK) return rc;
+  return softmax_rows(x, y, rows, cols, c, kExpFast, stream);
 }
 
 SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols,
@@ -470,7 +497,7 @@ SOFTMAX_API const char* softmax_strerror(int code) {
 SOFTMAX_API int softmax_last_hip_error(void) { return smx_host::tl_last_hip_error; }
 
 SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int64_t n,
-                                  float clip_lo, hipStream_t stream) {
+                                  float clip_lo, int approx, hipStream_t stream) {
   Clip c;
   bool wide = false;
   if (make_clip(clip_lo, &c, &wide) != SOFTMAX_OK) return SOFTMAX_ERR_INVALID_ARG;
@@ -487,9 +514,10 @@ SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int6
   if (rc != SOFTMAX_OK) return rc;
   const int64_t grid = std::min(ceil_div(n, 256), kMaxGrid);
   void* args[] = {&x, &m, &e, &n, &c};
-  he = launch(wide ? reinterpret_cast<const void*>(&k_exp_probe<true>)
-                   : reinterpret_cast<const void*>(&k_exp_probe<false>),
-              grid, 256, args, stream);
+  const void* fn = approx ? reinterpret_cast<const void*>(&k_exp_probe<kExpFast>)
+                  : wide  ? reinterpret_cast<const void*>(&k_exp_probe<kExpWide>)
+                          : reinterpret_cast<const void*>(&k_exp_probe<kExpAccurate>);
+  he = launch(fn, grid, 256, args, stream);
   return he == hipSuccess ? SOFTMAX_OK : fail_hip(he);
 }
 

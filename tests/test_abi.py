@@ -24,7 +24,8 @@ def declared_functions():
 
 def test_header_declares_entry_points():
     names = declared_functions()
-    for n in ("softmax_fwd", "softmax_fwd_clip", "softmax_attention_fwd", "softmax_strerror",
+    for n in ("softmax_fwd", "softmax_fwd_clip", "softmax_fwd_approx", "softmax_attention_fwd",
+              "softmax_strerror",
               "softmax_last_hip_error", "softmax_plan", "softmax_exp_probe",
               "softmax_copy_probe"):
         assert n in names
@@ -158,9 +159,9 @@ def test_probes_reject_bad_arguments():
     assert lib.softmax_copy_probe(0x1000, 0x1000, 16, None) == sm.ERR_INVALID_ARG
     assert lib.softmax_copy_probe(0x1000, 0x2000, -1, None) == sm.ERR_INVALID_ARG
     assert lib.softmax_copy_probe(None, 0x2000, 4, None) == sm.ERR_INVALID_ARG
-    assert lib.softmax_exp_probe(0x1000, 0x8000, 0x1004, 16, -64.0, None) == sm.ERR_INVALID_ARG
-    assert lib.softmax_exp_probe(0x1000, 0x8000, 0x10000, 0, -64.0, None) == sm.OK
-    assert lib.softmax_exp_probe(0x1000, 0x8000, 0x10000, 0, -1.0, None) == sm.ERR_INVALID_ARG
+    assert lib.softmax_exp_probe(0x1000, 0x8000, 0x1004, 16, -64.0, 0, None) == sm.ERR_INVALID_ARG
+    assert lib.softmax_exp_probe(0x1000, 0x8000, 0x10000, 0, -64.0, 0, None) == sm.OK
+    assert lib.softmax_exp_probe(0x1000, 0x8000, 0x10000, 0, -1.0, 1, None) == sm.ERR_INVALID_ARG
 
 
 def test_clip_bound_checked_before_any_hip_call():
@@ -169,6 +170,7 @@ def test_clip_bound_checked_before_any_hip_call():
     nan, inf = float("nan"), float("inf")
     for lo in (nan, -47.99, -1.0, 0.0, 5.0, inf):
         assert sm.softmax_fwd_clip_ptr(0x1000, 0x2000000, 4, 4, lo, 0) == sm.ERR_INVALID_ARG
+        assert sm.softmax_fwd_approx_ptr(0x1000, 0x2000000, 4, 4, lo, 0) == sm.ERR_INVALID_ARG
     # accepted bounds fall through to the size checks (negative rows here)
     for lo in (-48.0, -64.0, -87.5, -120.0, -1e30, -inf):
         assert sm.softmax_fwd_clip_ptr(0x1000, 0x2000000, -1, 4, lo, 0) == sm.ERR_INVALID_ARG

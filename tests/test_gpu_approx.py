@@ -1,0 +1,102 @@
+"""GPU parity for the fast-exponential softmax (softmax_fwd_approx), through
+the C ABI, against the float64 oracle, to the looser bound the header
+states: per element
+
+    |y - y*| <= (2e-6 + 1.5e-7 * min(|x - M|, |clip_lo|)) * y*
+
+(the fp32 argument of the single-instruction exponential carries a relative
+error of about 1.33e-7, which the exponential turns into 1.33e-7 |x - M|),
+and |sum_j y_ij - 1| <= 1e-5 per row.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_1904_12380_amd as sm
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_approx(x, lo=-64.0):
+    import torch
+    xt = torch.from_numpy(np.ascontiguousarray(x)).to("cuda:0")
+    y = sm.softmax_fwd_approx(xt, lo)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+def check_approx(x, y, lo, what):
+    want = oracle.softmax_clipped(x, lo)
+    y64 = y.astype(np.float64)
+    assert np.array_equal(np.isnan(y64), np.isnan(want)), what
+    fin = np.isfinite(want)
+    d = np.abs(x.astype(np.float64) - x.astype(np.float64).max(axis=1, keepdims=True))
+    bound = (2e-6 + 1.5e-7 * np.minimum(d, abs(lo))) * want
+    err = np.abs(y64 - want)
+    bad = fin & (err > bound)
+    if bad.any():
+        idx = tuple(np.argwhere(bad)[0])
+        pytest.fail(f"{what}: err {err[idx]:.3e} > bound {bound[idx]:.3e} at {idx}, "
+                    f"d = {d[idx]:.3f}")
+    rows_ok = np.all(fin, axis=1)
+    if rows_ok.any():
+        assert float(np.abs(y64[rows_ok].sum(axis=1) - 1.0).max()) <= 1e-5, what
+    rel = err[fin] / want[fin]
+    return float(rel.max()) if rel.size else 0.0
+
+
+@pytest.mark.parametrize("key", list(workloads.WORKLOADS))
+def test_workloads(key):
+    log(f"[approx] {key}")
+    x = workloads.generate(key)
+    worst = check_approx(x, run_approx(x), -64.0, key)
+    log(f"[approx] {key}: max rel err {worst:.3e}")
+
+
+# one shape per kernel family and path, two input kinds
+SHAPES = [(1000, 50), (257, 7), (64, 1000), (5, 8192), (3, 100003), (2, 1048577), (1, 2097153)]
+
+
+@pytest.mark.parametrize("rows,cols", SHAPES)
+def test_shapes(rows, cols):
+    for kind in ("clip_heavy", "normal", "offset"):
+        x = workloads.random_logits(rows, cols, seed=rows * 31 + cols, kind=kind, scale=10.0)
+        worst = check_approx(x, run_approx(x), -64.0, f"{rows}x{cols} {kind}")
+        log(f"[approx] {rows}x{cols} {kind}: max rel err {worst:.3e}")
+
+
+def test_uniform_rows_and_clip_rows():
+    """Uniform rows are exact (every exponential is e^0 = 1); clipped
+    elements take the exact clipped value."""
+    for n in (1, 3, 50, 1000, 4096, 32768, 262144):
+        y = run_approx(np.full((2, n), 7.25, dtype=np.float32))
+        assert np.all(y == np.float32(1.0 / n)), n
+    x = np.array([[0.0, -100.0, -64.0, -63.5, -1.0e4]], dtype=np.float32)
+    check_approx(x, run_approx(x), -64.0, "clip row")
+
+
+def test_exp_probe_fast_bound():
+    """The fast exponential alone: relative error within 1.5e-7 |x - m| +
+    1.2e-7 over the clipped domain."""
+    import torch
+    rng = np.random.default_rng(97)
+    n = 1 << 21
+    m = rng.uniform(-60.0, 60.0, n).astype(np.float32)
+    d = rng.uniform(-64.0, 0.0, n)
+    x = (m.astype(np.float64) + d).astype(np.float32)
+    e = sm.softmax_exp_probe(torch.from_numpy(x).to("cuda:0"), torch.from_numpy(m).to("cuda:0"),
+                             approx=True).cpu().numpy().astype(np.float64)
+    dd = x.astype(np.float64) - m.astype(np.float64)
+    want = oracle.exp_clipped(dd)
+    rel = np.abs(e - want) / want
+    bound = 1.5e-7 * np.minimum(np.abs(dd), 64.0) + 1.2e-7
+    assert np.all(rel <= bound), float((rel / bound).max())
+    log(f"[approx] exp probe: max rel err {rel.max():.3e}, worst / bound {(rel / bound).max():.3f}")
