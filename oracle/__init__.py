@@ -7,8 +7,9 @@ no code, header, constant or helper with it.
 
 Contents
 --------
-``softmax_f64``          float64 definition of the clipped row softmax
-                          (plain numpy; the parity reference).
+``softmax_f64``          float64 definition of the clipped row softmax and
+                          of its logarithm (plain numpy; the parity
+                          references).
 ``attention_f64``        float64 softmax attention, softmax(scale Q K^T) V
                           per batch element, built on ``softmax_f64``.
 ``cpu_fp32_baseline.c``  a straightforward single-thread fp32 C softmax in the
@@ -20,6 +21,7 @@ do not come from this code: closed forms, the logistic special case, a
 50-digit ``decimal`` brute force, a library cross-check and invariants.
 """
 from .attention_f64 import attention_clipped
-from .softmax_f64 import CLIP_LO, exp_clipped, row_max, softmax_clipped
+from .softmax_f64 import CLIP_LO, exp_clipped, log_softmax_clipped, row_max, softmax_clipped
 
-__all__ = ["CLIP_LO", "row_max", "exp_clipped", "softmax_clipped", "attention_clipped"]
+__all__ = ["CLIP_LO", "row_max", "exp_clipped", "softmax_clipped", "log_softmax_clipped",
+           "attention_clipped"]

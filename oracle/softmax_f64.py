@@ -75,3 +75,29 @@ def softmax_clipped(x: np.ndarray, clip_lo: float = CLIP_LO) -> np.ndarray:
         e = exp_clipped(d, clip_lo)
         s = np.sum(e, axis=1, keepdims=True)
         return e / s
+
+
+def log_softmax_clipped(x: np.ndarray, clip_lo: float = CLIP_LO) -> np.ndarray:
+    """Row-wise log of the clipped softmax, float64:
+
+        y_ij = c_ij - log(sum_k exp(c_ik)),   c_ij = max(x_ij - M_i, clip_lo)
+
+    which is log(softmax_clipped(x, clip_lo)) written so that it stays exact
+    where the probability underflows.  The log after softmax is why the
+    reference functor clips at all (Sec. 2.1: softmax must not return 0 for
+    the log that follows in training); with clip_lo = -inf this is the plain
+    log-softmax of the shifted logits (Sec. 1.1 Eq. (1), logarithm taken).
+    A -inf entry gives -inf when there is no clip.
+    """
+    x64 = np.asarray(x, dtype=np.float64)
+    if x64.ndim != 2:
+        raise ValueError("expected a 2-D [rows, classes] array")
+    rows, cols = x64.shape
+    if rows == 0 or cols == 0:
+        return np.zeros((rows, cols), dtype=np.float64)
+    m = row_max(x64)
+    with np.errstate(invalid="ignore", over="ignore", divide="ignore"):
+        d = x64 - m
+        c = np.where(d < clip_lo, clip_lo, d)
+        s = np.sum(np.exp(c), axis=1, keepdims=True)
+        return c - np.log(s)

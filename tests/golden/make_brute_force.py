@@ -12,7 +12,9 @@ and not from the GPU path.  They pin the float64 oracle to the definition:
 
 Each row is also evaluated with other clip bounds (``y_clip``): -48, -90,
 -120 and -inf (no clip, the optimised functor of Sec. 2.3 Fig. 4, which
-drops the ValueClip, Sec. 2.1).
+drops the ValueClip, Sec. 2.1), and its logarithm ``logy_clip``,
+c_j - ln(sum_k exp(c_k)), at those bounds and at -64 (the log that the clip
+exists for, Sec. 2.1).
 
 Inputs are fp32 values stored as exact hex strings.  Run from the repo root:
     python tests/golden/make_brute_force.py
@@ -66,6 +68,16 @@ def clipped_softmax_decimal(row: list[float], clip: Decimal = CLIP) -> list[Deci
     return [e / s for e in es]
 
 
+def log_softmax_decimal(row: list[float], clip: Decimal = CLIP) -> list[Decimal]:
+    """c_j - ln(sum_k exp(c_k)) with c = max(x - M, clip), in decimal."""
+    xs = [Decimal(v) for v in row]
+    m = max(xs)
+    cs = [max(x - m, clip) for x in xs]
+    s = sum((c.exp() for c in cs), Decimal(0))
+    ls = s.ln()
+    return [c - ls for c in cs]
+
+
 def eq1_softmax_decimal(row: list[float]) -> list[Decimal]:
     xs = [Decimal(v) for v in row]
     es = [x.exp() for x in xs]
@@ -85,6 +97,8 @@ def main() -> None:
             "clip_active": clip_active,
             "y_clip": {k: [format(v, ".30e") for v in clipped_softmax_decimal(row, c)]
                        for k, c in OTHER_CLIPS.items()},
+            "logy_clip": {k: [format(v, ".30e") for v in log_softmax_decimal(row, c)]
+                          for k, c in dict(OTHER_CLIPS, **{"-64": CLIP}).items()},
         }
         if not clip_active:
             y1 = eq1_softmax_decimal(row)

@@ -325,3 +325,123 @@ def pinc_bound_is_monotone(impl):
 
 
 CLIP_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pinc_")]
+
+
+# ---------------------------------------------------------------------------
+# Pins for the log of the clipped softmax.  Each ``pinl_*`` function takes
+# ``impl(x: float32 [R, C], clip_lo: float) -> float64 [R, C]``, the row-wise
+# log of softmax_clipped (the log that follows softmax in training is why
+# the reference functor clips, Sec. 2.1).
+
+def _close_abs(got, want, tol=1e-13):
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    both_inf = np.isneginf(got) & np.isneginf(want)
+    ok = both_inf | (np.abs(got - want) <= tol * np.maximum(1.0, np.abs(want)))
+    return bool(np.all(ok))
+
+
+def pinl_library_log_softmax(impl):
+    """No clip: scipy.special.log_softmax in float64, on rows whose shifted
+    logits reach -800 (where exp underflows but the log must not) and rows
+    with large offsets."""
+    from scipy.special import log_softmax
+    rng = np.random.default_rng(61)
+    rows = [rng.uniform(-800.0, 0.0, 64), rng.uniform(-150.0, 10.0, 64),
+            800.0 + rng.standard_normal(64), 3.0 * rng.standard_normal(64)]
+    x = _f32(np.stack(rows))
+    assert _close_abs(impl(x, -np.inf), log_softmax(x.astype(np.float64), axis=1))
+    # where no shifted logit is below -64 the -64 clip changes nothing
+    x = random_logits(5, 300, 62, "normal", 4.0)
+    assert _close_abs(impl(x, -64.0), log_softmax(x.astype(np.float64), axis=1))
+
+
+def pinl_is_log_of_softmax(impl):
+    """exp of the result is the pinned clipped softmax (math.exp per entry,
+    where the probability is a normal float64)."""
+    x = random_logits(6, 257, 63, "clip_heavy")
+    for lo in (-64.0, -90.0):
+        y = impl(x, lo)
+        p = np.exp(y)
+        want = _softmax_reference(x, lo)
+        assert np.all(np.abs(p - want) <= 1e-13 * want)
+
+
+def _softmax_reference(x, lo):
+    """Plain loops over the definition (math.fsum), independent of numpy's
+    reductions, for the consistency pin."""
+    out = np.empty(x.shape)
+    for i, row in enumerate(x.astype(np.float64)):
+        m = max(row)
+        e = [math.exp(max(v - m, lo)) for v in row]
+        s = math.fsum(e)
+        out[i] = [t / s for t in e]
+    return out
+
+
+def pinl_uniform_and_two_class(impl):
+    """Uniform rows give -log N; two classes give the log-sigmoid
+    (scipy.special.log_expit of the difference)."""
+    from scipy.special import log_expit
+    for n in (1, 2, 7, 1000):
+        y = impl(_f32(np.full((2, n), 3.5)), -64.0)
+        assert _close_abs(y, np.full((2, n), -math.log(n)), 1e-15)
+    rng = np.random.default_rng(64)
+    a, b = rng.uniform(-30.0, 30.0, 100), rng.uniform(-30.0, 30.0, 100)
+    x = _f32(np.stack([a, b], axis=1))
+    diff = x[:, 0].astype(np.float64) - x[:, 1].astype(np.float64)
+    y = impl(x, -np.inf)
+    assert _close_abs(y[:, 0], log_expit(diff)) and _close_abs(y[:, 1], log_expit(-diff))
+
+
+def pinl_closed_form_clip(impl):
+    """Row [0, -100, -64, -63.5, -1e4] at the -64 clip:
+    y = c - log(1 + 3 e^-64 + e^-63.5) with c = [0, -64, -64, -63.5, -64];
+    rows at a bound of -1 where the clipped terms dominate the sum."""
+    x = _f32([[0.0, -100.0, -64.0, -63.5, -1.0e4]])
+    ls = math.log1p(3.0 * E64 + math.exp(-63.5))
+    want = np.array([[0.0, -64.0, -64.0, -63.5, -64.0]]) - ls
+    assert _close_abs(impl(x, -64.0), want, 1e-15)
+    # a bound close to the max makes the clip's share of the sum visible:
+    # [0, -3, -5] at -1 gives c = [0, -1, -1] and S = 1 + 2/e
+    x = _f32([[0.0, -3.0, -5.0], [7.0, 4.0, 2.0]])
+    want = np.array([[0.0, -1.0, -1.0]] * 2) - math.log1p(2.0 * math.exp(-1.0))
+    assert _close_abs(impl(x, -1.0), want, 1e-15)
+
+
+def pinl_brute_force_decimal(impl):
+    """Tiny rows against 50-digit decimal logs at bounds -48, -64, -90, -120
+    and with no clip (tests/golden, logy_clip)."""
+    with open(os.path.join(GOLDEN, "brute_force_rows.json")) as f:
+        doc = json.load(f)
+    for rec in doc["rows"]:
+        x = _f32([[float.fromhex(h) for h in rec["x_hex"]]])
+        for key, vals in rec["logy_clip"].items():
+            lo = -np.inf if key == "-inf" else float(key)
+            want = np.array([float(Decimal(v)) for v in vals])
+            assert _close_abs(impl(x, lo)[0], want, 1e-14), (rec["x_hex"], key)
+
+
+def pinl_nonfinite(impl):
+    """NaN, +inf and all -inf rows are NaN; a -inf entry gives the clipped
+    value c - log S, or -inf with no clip."""
+    x = _f32([[1.0, np.nan, 0.0], [1.0, np.inf, 0.0], [-np.inf] * 3, [0.0, -np.inf, 0.0]])
+    y = impl(x, -64.0)
+    assert np.all(np.isnan(y[:3]))
+    ls = math.log(2.0 + E64)
+    assert _close_abs(y[3], [-ls, -64.0 - ls, -ls], 1e-15)
+    y = impl(x, -np.inf)
+    assert np.all(np.isnan(y[:3])) and y[3, 1] == -np.inf
+    assert _close_abs(y[3, [0, 2]], [-math.log(2.0)] * 2, 1e-15)
+
+
+def pinl_shift_invariance(impl):
+    """Adding k to a dyadic row leaves every output bit-identical."""
+    x = random_logits(4, 129, 65, "dyadic")
+    y0 = impl(x, -64.0)
+    for k in (0.5, 64.0, -256.0):
+        xk = _f32(x.astype(np.float64) + k)
+        assert np.array_equal(impl(xk, -64.0), y0), k
+
+
+LOG_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pinl_")]

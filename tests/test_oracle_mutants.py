@@ -192,3 +192,47 @@ def test_attention_mutant_is_caught(name):
         assert failed == [], failed
     else:
         assert failed, f"mutant {name} passed every attention pin"
+
+
+# Mistakes in the log of the clipped softmax; each must fail one of
+# pins.LOG_PINS.
+def _logsm(x, lo, shift=True, clip_sum=True, clip_out=True, base=np.e, via_prob=False,
+           sign=1.0):
+    x64 = np.asarray(x, dtype=np.float64)
+    if x64.size == 0:
+        return np.zeros(x64.shape)
+    with np.errstate(all="ignore"):
+        m = np.max(x64, axis=1, keepdims=True) if shift else 0.0
+        d = x64 - m
+        c = np.where(d < lo, lo, d)
+        s = np.sum(np.exp(c if clip_sum else d), axis=1, keepdims=True)
+        if via_prob:
+            return np.log(np.exp(c) / s)
+        out = c if clip_out else d
+        return sign * (out - np.log(s) / np.log(base))
+
+
+MUTANTS_LOG = {
+    "reference_copy_is_clean": {},
+    "no_max_shift": dict(shift=False),
+    "log_base_2": dict(base=2.0),
+    "log_of_underflowed_probability": dict(via_prob=True),
+    "output_not_clipped": dict(clip_out=False),
+    "sum_not_clipped": dict(clip_sum=False),
+    "negated": dict(sign=-1.0),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_LOG))
+def test_log_mutant_is_caught(name):
+    impl = lambda x, lo: _logsm(x, lo, **MUTANTS_LOG[name])  # noqa: E731
+    failed = []
+    for pin in pins.LOG_PINS:
+        try:
+            pin(impl)
+        except (AssertionError, ValueError, FloatingPointError, IndexError):
+            failed.append(pin.__name__)
+    if name == "reference_copy_is_clean":
+        assert failed == [], failed
+    else:
+        assert failed, f"mutant {name} passed every log pin"

@@ -62,3 +62,8 @@ def test_attention_oracle_rejects_zero_keys():
     q, k, v = workloads.random_qkv(2, 3, 0, 4, 5, 1)
     with pytest.raises(ValueError):
         oracle.attention_clipped(q, k, v, 1.0)
+
+
+@pytest.mark.parametrize("pin", pins.LOG_PINS, ids=lambda p: p.__name__)
+def test_log_oracle_pin(pin):
+    pin(oracle.log_softmax_clipped)
