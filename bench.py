@@ -167,11 +167,16 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         x, y = rot.pair(i)
         sm.softmax_fwd_approx(x, out=y, stream=s)
 
+    def fwd_log(i, s):
+        x, y = rot.pair(i)
+        sm.softmax_log_fwd(x, out=y, stream=s)
+
     ms, eager_ms = time_steps(torch, fwd, steps, warmup)
     copy_ms, _ = time_steps(torch, cpy, steps, warmup)
     memcpy_ms = time_steps(torch, d2d, steps, warmup)[0] if memcpy else None
     noclip_ms, _ = time_steps(torch, fwd_noclip, steps, warmup)
     approx_ms, _ = time_steps(torch, fwd_approx, steps, warmup)
+    log_ms, _ = time_steps(torch, fwd_log, steps, warmup)
 
     max_rel = None
     if check:
@@ -209,6 +214,8 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         "noclip_hbm_gbps": w.algorithmic_bytes / (noclip_ms * 1e-3) / 1e9,
         "approx_exp_ms_per_step": approx_ms,
         "approx_exp_hbm_gbps": w.algorithmic_bytes / (approx_ms * 1e-3) / 1e9,
+        "log_softmax_ms_per_step": log_ms,
+        "log_softmax_hbm_gbps": w.algorithmic_bytes / (log_ms * 1e-3) / 1e9,
         "rotation_buffers": nbuf,
         "plan": plan,
         "sampled_max_rel_err": max_rel,
@@ -593,7 +600,8 @@ def main() -> int:
     main_res = time_gpu(sm, torch, w, x, args.steps, args.warmup, memcpy=True)
     log(f"[bench] {w.key}: {main_res['ms_per_step'] * 1e3:.2f} us/step, "
         f"{main_res['hbm_gbps']:.0f} GB/s (no clip {main_res['noclip_ms_per_step'] * 1e3:.2f} us, "
-        f"approx exp {main_res['approx_exp_ms_per_step'] * 1e3:.2f} us)")
+        f"approx exp {main_res['approx_exp_ms_per_step'] * 1e3:.2f} us, "
+        f"log {main_res['log_softmax_ms_per_step'] * 1e3:.2f} us)")
 
     extra = {}
     if not args.no_extra_workloads:
@@ -608,7 +616,8 @@ def main() -> int:
             extra[key]["launches_per_step"] = r["plan"]["launches"]
             log(f"[bench] {key}: {r['ms_per_step'] * 1e3:.2f} us/step, {r['hbm_gbps']:.0f} GB/s "
                 f"(no clip {r['noclip_ms_per_step'] * 1e3:.2f} us, approx exp "
-                f"{r['approx_exp_ms_per_step'] * 1e3:.2f} us)")
+                f"{r['approx_exp_ms_per_step'] * 1e3:.2f} us, log "
+                f"{r['log_softmax_ms_per_step'] * 1e3:.2f} us)")
 
     attention = None
     if not args.no_extra_workloads:
@@ -671,6 +680,10 @@ def main() -> int:
         "no_clip": {"ms_per_step": main_res["noclip_ms_per_step"],
                     "hbm_gbps": main_res["noclip_hbm_gbps"],
                     "what": "softmax_fwd_clip with clip_lo = -inf, same rotation and timing"},
+        "log_softmax": {"ms_per_step": main_res["log_softmax_ms_per_step"],
+                        "hbm_gbps": main_res["log_softmax_hbm_gbps"],
+                        "what": "softmax_log_fwd (log of the clipped softmax), same rotation "
+                                "and timing"},
         "approx_exp": {"ms_per_step": main_res["approx_exp_ms_per_step"],
                        "hbm_gbps": main_res["approx_exp_hbm_gbps"],
                        "what": "softmax_fwd_approx (single-instruction fp32 exponential), "

@@ -156,6 +156,26 @@ SOFTMAX_API int softmax_fwd_clip(const float* x, float* y, int64_t rows, int64_t
 SOFTMAX_API int softmax_fwd_approx(const float* x, float* y, int64_t rows, int64_t cols,
                                    float clip_lo, hipStream_t stream);
 
+/*
+ * softmax_log_fwd -- the logarithm of the clipped row softmax:
+ *
+ *     y[i,j] = c_ij - ln(sum_k exp(c_ik)),   c_ij = max(x[i,j] - M_i, clip_lo)
+ *
+ * the log that follows softmax in training and that the reference functor's
+ * clip exists for (Sec. 2.1), computed directly so that it stays exact
+ * where the probability itself would underflow.  clip_lo as for
+ * softmax_fwd_clip (-INFINITY: plain log-softmax; a -inf entry then gives
+ * -inf).  The row sum uses the accurate exponential, ln S comes from
+ * v_log_f32 in binary64, and c - ln S is formed in binary64 and rounded once.
+ *
+ * Accuracy: |y - y*| <= 2e-6 + 2.5e-7 * (|y*| + ln(cols)) against the exact
+ * value y* (the sum's rounding and the logarithm's 1 ulp on log2 S).
+ * Arguments, layout, NaN rules, errors and everything else are those of
+ * softmax_fwd_clip; y == x (in place) is allowed.
+ */
+SOFTMAX_API int softmax_log_fwd(const float* x, float* y, int64_t rows, int64_t cols,
+                                float clip_lo, hipStream_t stream);
+
 /* Limits of softmax_attention_fwd. */
 #define SOFTMAX_ATTN_MAX_KEYS 64     /* lk: the keys of one row fit one set of tiles */
 #define SOFTMAX_ATTN_MAX_DIM 65536   /* d and dv */

@@ -13,6 +13,8 @@ Functions keep the C names:
     softmax_fwd_clip_ptr(x_ptr, y_ptr, rows, cols, clip_lo, stream_handle) -> int
     softmax_fwd_approx(x, clip_lo=-64.0, out=None, stream=None) -> torch.Tensor
     softmax_fwd_approx_ptr(x_ptr, y_ptr, rows, cols, clip_lo, stream_handle) -> int
+    softmax_log_fwd(x, clip_lo=-64.0, out=None, stream=None) -> torch.Tensor
+    softmax_log_fwd_ptr(x_ptr, y_ptr, rows, cols, clip_lo, stream_handle) -> int
     softmax_attention_fwd(q, k, v, scale=None, clip_lo=-64.0, out=None, stream=None)
     softmax_attention_fwd_ptr(q_ptr, k_ptr, v_ptr, o_ptr, batch, lq, lk, d, dv,
                               scale, clip_lo, stream_handle) -> int
@@ -30,7 +32,7 @@ import os
 __all__ = [
     "LIB_PATH", "HEADER_PATH", "SoftmaxError", "load_library", "softmax_fwd",
     "softmax_fwd_ptr", "softmax_fwd_clip", "softmax_fwd_clip_ptr", "softmax_plan",
-    "softmax_fwd_approx", "softmax_fwd_approx_ptr",
+    "softmax_fwd_approx", "softmax_fwd_approx_ptr", "softmax_log_fwd", "softmax_log_fwd_ptr",
     "softmax_attention_fwd", "softmax_attention_fwd_ptr", "ATTN_MAX_KEYS", "ATTN_MAX_DIM",
     "softmax_exp_probe", "softmax_copy_probe", "softmax_strerror", "softmax_last_hip_error",
     "CLIP_LO", "CLIP_MAX", "KERNEL_NAMES",
@@ -101,6 +103,8 @@ def load_library() -> ctypes.CDLL:
     lib.softmax_exp_probe.argtypes = [vp, vp, vp, i64, ctypes.c_float, ctypes.c_int, vp]
     lib.softmax_fwd_approx.argtypes = [vp, vp, i64, i64, ctypes.c_float, vp]
     lib.softmax_fwd_approx.restype = ctypes.c_int
+    lib.softmax_log_fwd.argtypes = [vp, vp, i64, i64, ctypes.c_float, vp]
+    lib.softmax_log_fwd.restype = ctypes.c_int
     lib.softmax_exp_probe.restype = ctypes.c_int
     lib.softmax_copy_probe.argtypes = [vp, vp, i64, vp]
     lib.softmax_copy_probe.restype = ctypes.c_int
@@ -228,6 +232,26 @@ def softmax_fwd_approx(x, clip_lo: float = CLIP_LO, out=None, stream=None):
                                     _stream_handle(stream))
     if rc != OK:
         raise SoftmaxError(rc, "softmax_fwd_approx")
+    return out
+
+
+def softmax_log_fwd_ptr(x_ptr: int, y_ptr: int, rows: int, cols: int, clip_lo: float,
+                        stream_handle: int = 0) -> int:
+    """Raw C call; returns the C return code."""
+    return int(load_library().softmax_log_fwd(x_ptr, y_ptr, rows, cols, float(clip_lo),
+                                              stream_handle))
+
+
+def softmax_log_fwd(x, clip_lo: float = CLIP_LO, out=None, stream=None):
+    """Row-wise log of the clipped softmax, y = max(x - M, clip_lo) - ln S."""
+    torch = _torch()
+    out = _out_for(x, out)
+    rows, cols = x.shape
+    with torch.cuda.device(x.device):
+        rc = softmax_log_fwd_ptr(x.data_ptr(), out.data_ptr(), rows, cols, clip_lo,
+                                 _stream_handle(stream))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_log_fwd")
     return out
 
 

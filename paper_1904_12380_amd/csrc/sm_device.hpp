@@ -51,12 +51,19 @@ constexpr float kClipWide = -87.0f;
 constexpr int kExpAccurate = 0;
 constexpr int kExpWide = 1;
 constexpr int kExpFast = 2;
+// A fourth kernel mode: the output is the log of the clipped softmax,
+// y = c - ln S with c = max(x - M, lo), instead of e / S.  Its row sums use
+// the accurate exponential (terms under 2^-126 do not matter next to S >= 1).
+constexpr int kLogOut = 3;
+template <int MODE>
+constexpr int exp_mode() { return MODE == kLogOut ? kExpAccurate : MODE; }
 
 // The clip as a kernel argument: lo in [kClipFloor, 0] and e_lo = RN(e^lo')
 // for the caller's bound lo' (0 when lo' < -103.98 or lo' = -inf).
 struct Clip {
   float lo;
   float e_lo;
+  float lo_out;  // the caller's bound itself (may be -inf), for log outputs
 };
 
 // RN(log2 e) and RN(ln 2) in binary64.
@@ -88,7 +95,20 @@ struct RowShift {
   float m;
   float tc;
   float e_lo;
+  float tc_out;  // as tc, for the caller's bound (log outputs)
+  float lo_out;
 };
+
+// The smallest fp32 value >= s (s in binary64).
+__device__ __forceinline__ float round_up_f32(double s) {
+  float f = static_cast<float>(s);
+  if (static_cast<double>(f) < s) {
+    // next fp32 towards +inf (f < s <= f + ulp, f finite)
+    const unsigned u = __builtin_bit_cast(unsigned, f);
+    f = __builtin_bit_cast(float, f < 0.0f ? u - 1u : (f == 0.0f ? 1u : u + 1u));
+  }
+  return f;
+}
 
 __device__ __forceinline__ RowShift row_shift(float m, Clip clip) {
   RowShift r;
@@ -97,16 +117,26 @@ __device__ __forceinline__ RowShift row_shift(float m, Clip clip) {
   // M + lo is exact in binary64 unless the exponents of M and lo differ by
   // more than 29 (|M| < 2^-23 |lo|), where the rounding is below 2^-47 |lo|
   // and only moves the boundary by that much.
-  const double s = static_cast<double>(m) + static_cast<double>(clip.lo);
-  float f = static_cast<float>(s);
-  if (static_cast<double>(f) < s) {
-    // next fp32 towards +inf (f < s <= f + ulp, f finite)
-    const unsigned u = __builtin_bit_cast(unsigned, f);
-    f = __builtin_bit_cast(float, f < 0.0f ? u - 1u : (f == 0.0f ? 1u : u + 1u));
-  }
-  r.tc = f;
+  r.tc = round_up_f32(static_cast<double>(m) + static_cast<double>(clip.lo));
   r.e_lo = clip.e_lo;
+  r.tc_out = round_up_f32(static_cast<double>(m) + static_cast<double>(clip.lo_out));
+  r.lo_out = clip.lo_out;
   return r;
+}
+
+// ln S in binary64 from v_log_f32 (log2, within 1 ulp) times RN(ln 2);
+// S >= 1 for every row with a finite max.
+__device__ __forceinline__ double log_of_sum(float s) {
+  return static_cast<double>(__builtin_amdgcn_logf(s)) * kLn2;
+}
+
+// One log-softmax output: y = RN32(c - ln S), c = max(x - M, lo) formed in
+// binary64 (exact for fp32 x and M within 29 binades) against the caller's
+// bound; with no clip a -inf entry gives -inf.
+__device__ __forceinline__ float log_out(float x, RowShift rs, double log_s) {
+  const double c = x < rs.tc_out ? static_cast<double>(rs.lo_out)
+                                 : static_cast<double>(x) + rs.neg_m;
+  return static_cast<float>(c - log_s);
 }
 
 // exp(max(x - M, lo)) for fp32 x, within 1.5 ulp of the exact value where

@@ -92,6 +92,7 @@ inline int make_clip(float clip_lo, Clip* c, bool* wide) {
   c->lo = clip_lo < kClipFloor ? kClipFloor : clip_lo;
   c->e_lo = clip_lo == kClipLo ? kExpClipLo
                                : static_cast<float>(std::exp(static_cast<double>(clip_lo)));
+  c->lo_out = clip_lo;
   *wide = c->lo < kClipWide;
   return SOFTMAX_OK;
 }

@@ -106,35 +106,65 @@ __device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* p, in
   }
 }
 
-// Replaces v by the clipped exponentials and returns this lane's pairwise
-// partial sum.
-template <int EM, int N>
+// This lane's pairwise partial sum of the clipped exponentials.  For
+// probability outputs v is replaced by the exponentials; for log outputs
+// (MODE == kLogOut) v keeps the logits, which the output step needs.
+template <int MODE, int N>
 __device__ __forceinline__ float exp_strip(float (&v)[N], RowShift rs) {
+  if constexpr (MODE == kLogOut) {
+    // Eight interleaved partial sums, then their tree: no second array of N
+    // registers next to the logits.
+    constexpr int P = N < 8 ? N : 8;
+    float t[P];
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = exp_shift_clip<EM>(v[i], rs);
-  return tree_sum(v);
+    for (int i = 0; i < P; ++i) t[i] = exp_shift_clip<kExpAccurate>(v[i], rs);
+#pragma unroll
+    for (int i = P; i < N; ++i) t[i % P] = t[i % P] + exp_shift_clip<kExpAccurate>(v[i], rs);
+    return tree_sum(t);
+  } else {
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = exp_shift_clip<MODE>(v[i], rs);
+    return tree_sum(v);
+  }
 }
 
-template <int V, bool VEC4>
-__device__ __forceinline__ void store_strip(const float (&v)[4 * V], float scale, float* p,
+// Stores out(v[i]) for the columns of the strip that are inside the row.
+template <int V, bool VEC4, typename F>
+__device__ __forceinline__ void store_strip(const float (&v)[4 * V], F out, float* p,
                                             int lane_off, int stride, int lim) {
   if constexpr (VEC4) {
 #pragma unroll
     for (int j = 0; j < V; ++j) {
       const int c = 4 * (lane_off + stride * j);
       f32x4 q;
-      q.x = v[4 * j + 0] * scale;
-      q.y = v[4 * j + 1] * scale;
-      q.z = v[4 * j + 2] * scale;
-      q.w = v[4 * j + 3] * scale;
+      q.x = out(v[4 * j + 0]);
+      q.y = out(v[4 * j + 1]);
+      q.z = out(v[4 * j + 2]);
+      q.w = out(v[4 * j + 3]);
       if (4 * stride * (j + 1) <= lim || c < lim) st_stream(p + c, q);
     }
   } else {
 #pragma unroll
     for (int i = 0; i < 4 * V; ++i) {
       const int c = lane_off + stride * i;
-      if (stride * (i + 1) <= lim || c < lim) __builtin_nontemporal_store(v[i] * scale, p + c);
+      if (stride * (i + 1) <= lim || c < lim) __builtin_nontemporal_store(out(v[i]), p + c);
     }
+  }
+}
+
+// The output step of a row whose shift is rs and whose sum of clipped
+// exponentials is s: v holds e (probabilities, y = e / S) or x (log
+// outputs, y = c - ln S).
+template <int V, bool VEC4, int MODE>
+__device__ __forceinline__ void store_row(const float (&v)[4 * V], RowShift rs, float s,
+                                          float* p, int lane_off, int stride, int lim) {
+  if constexpr (MODE == kLogOut) {
+    const double ls = log_of_sum(s);
+    store_strip<V, VEC4>(v, [&](float xv) { return log_out(xv, rs, ls); }, p, lane_off, stride,
+                         lim);
+  } else {
+    const float rcp = 1.0f / s;
+    store_strip<V, VEC4>(v, [&](float ev) { return ev * rcp; }, p, lane_off, stride, lim);
   }
 }
 
@@ -158,7 +188,7 @@ __device__ __forceinline__ int seg_len(int64_t cols, int64_t c0, int64_t cap) {
 // The grid is persistent (a few workgroups per CU, each looping over tiles)
 // and every workgroup issues the loads of its next tile right after staging
 // the current one, so they are in flight while the current tile computes.
-template <int G, int EPL, int EM>
+template <int G, int EPL, int MODE>
 __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int r, int j,
                                             Clip clip) {
   const bool active = r < nr;
@@ -170,17 +200,25 @@ __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int 
     v[k] = (active && c < ccols) ? tr[c] : kNegInf;
   }
   const RowShift rs = row_shift(seg_max<G>(array_max(v)), clip);
+  const float s = seg_sum<G>(exp_strip<MODE>(v, rs));
+  if constexpr (MODE == kLogOut) {
+    const double ls = log_of_sum(s);
 #pragma unroll
-  for (int k = 0; k < EPL; ++k) v[k] = exp_shift_clip<EM>(v[k], rs);
-  const float rcp = 1.0f / seg_sum<G>(tree_sum(v));
+    for (int k = 0; k < EPL; ++k) {
+      const int c = j + G * k;
+      if (active && c < ccols) tr[c] = log_out(v[k], rs, ls);
+    }
+  } else {
+    const float rcp = 1.0f / s;
 #pragma unroll
-  for (int k = 0; k < EPL; ++k) {
-    const int c = j + G * k;
-    if (active && c < ccols) tr[c] = v[k] * rcp;
+    for (int k = 0; k < EPL; ++k) {
+      const int c = j + G * k;
+      if (active && c < ccols) tr[c] = v[k] * rcp;
+    }
   }
 }
 
-template <int G, int EPL, bool VEC4, int EM>
+template <int G, int EPL, bool VEC4, int MODE>
 __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_t rows,
                                                 int64_t cols, Clip clip) {
   constexpr int kRows = 256 / G;
@@ -247,7 +285,7 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
     __syncthreads();
     if (t + gridDim.x < ntiles) issue(t + gridDim.x);
 
-    packed_rows<G, EPL, EM>(tile, nr, ccols, r, j, clip);
+    packed_rows<G, EPL, MODE>(tile, nr, ccols, r, j, clip);
     __syncthreads();
 
     if constexpr (VEC4) {
@@ -262,11 +300,21 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
   }
 }
 
+// Occupancy targets (waves per SIMD) for the register-resident kernels: 4
+// (128 VGPRs) up to 32 values per lane with 128-bit access and probability
+// outputs; 2 (256 VGPRs) otherwise, where 32-bit access needs more address
+// registers and log outputs keep the logits next to the exponentials, so
+// nothing spills to scratch.  The one-pass split kernel runs at twice
+// these (its chunks hold half as many values per lane).
+template <int V, bool VEC4, int MODE>
+constexpr int kRowWaves = (V <= 8 && VEC4 && MODE != kLogOut) ? 4 : 2;
+
 // ---------------------------------------------------------------------------
 // (b) One wavefront per row, cols <= 256*V (4*V elements per lane).
 // Four wavefronts per workgroup work on four rows independently.
-template <int V, bool VEC4, int EM>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_wave_row(
+template <int V, bool VEC4, int MODE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
+    kRowWaves<V, VEC4, MODE>))) void k_wave_row(
     const float* x, float* y, int64_t rows, int64_t cols, Clip clip) {
   const int lane = __lane_id();
   const int wave = threadIdx.x >> 6;
@@ -278,15 +326,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, lane, 64, lim);
     const RowShift rs = row_shift(seg_max<64>(array_max(v)), clip);
-    const float s = seg_sum<64>(exp_strip<EM>(v, rs));
-    const float rcp = 1.0f / s;
-    store_strip<V, VEC4>(v, rcp, yr, lane, 64, lim);
+    const float s = seg_sum<64>(exp_strip<MODE>(v, rs));
+    store_row<V, VEC4, MODE>(v, rs, s, yr, lane, 64, lim);
   }
 }
 
 // ---------------------------------------------------------------------------
 // (c) One workgroup of NT threads per row, cols <= 4*V*NT.
-template <int NT, int V, bool VEC4, int EM>
+template <int NT, int V, bool VEC4, int MODE>
 __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int64_t rows,
                                                   int64_t cols, Clip clip) {
   constexpr int NW = NT / 64;
@@ -300,9 +347,8 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int6
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, tid, NT, lim);
     const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max), clip);
-    const float s = block_sum<NW>(exp_strip<EM>(v, rs), red_sum);
-    const float rcp = 1.0f / s;
-    store_strip<V, VEC4>(v, rcp, yr, tid, NT, lim);
+    const float s = block_sum<NW>(exp_strip<MODE>(v, rs), red_sum);
+    store_row<V, VEC4, MODE>(v, rs, s, yr, tid, NT, lim);
   }
 }
 
@@ -318,10 +364,11 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int6
 // Pass 2 merges a row's partials (every wavefront of the workgroup does the
 // same merge, so all hold the same bits):  M = max_g m_g,
 // S = sum_g s_g * exp(max(m_g - M, lo)), then writes
-// y = exp(max(x - M, lo)) / S.  Using the clip relative to m_g inside a
+// y = exp(max(x - M, lo)) / S (or c - ln S for log outputs).  Using the
+// clip relative to m_g inside a
 // partial changes S by at most cols * e^lo relative (below 1e-10 for any
 // row that fits in memory, since lo <= -48), far under fp32 resolution.
-template <int NT, int V, bool VEC4, int EM>
+template <int NT, int V, bool VEC4, int MODE>
 __global__ __launch_bounds__(NT) void k_split_stats(const float* x, float2* part,
                                                     int64_t rows, int64_t cols,
                                                     int64_t chunks, Clip clip) {
@@ -342,13 +389,13 @@ __global__ __launch_bounds__(NT) void k_split_stats(const float* x, float2* part
     const float m = block_max<NW>(array_max(v), red_max);
     const bool empty_max = (m == kNegInf);
     const RowShift rs = row_shift(empty_max ? 0.0f : m, clip);
-    float s = block_sum<NW>(exp_strip<EM>(v, rs), red_sum);
+    float s = block_sum<NW>(exp_strip<MODE>(v, rs), red_sum);
     if (empty_max) s = static_cast<float>(lim);
     if (tid == 0) part[b] = make_float2(m, s);
   }
 }
 
-template <int NT, int V, bool VEC4, int EM>
+template <int NT, int V, bool VEC4, int MODE>
 __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
                                                     const float2* part, int64_t rows,
                                                     int64_t cols, int64_t chunks, Clip clip) {
@@ -373,13 +420,14 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
     float ss = 0.0f;
     for (int64_t l = lane; l < chunks; l += 64) {
       const float2 p = pr[l];
-      ss = ss + p.y * exp_shift_clip<EM>(p.x, rs);
+      ss = ss + p.y * exp_shift_clip<exp_mode<MODE>()>(p.x, rs);
     }
-    const float rcp = 1.0f / seg_sum<64>(ss);
-
+    const float s = seg_sum<64>(ss);
+    if constexpr (MODE != kLogOut) {
 #pragma unroll
-    for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip<EM>(v[i], rs);
-    store_strip<V, VEC4>(v, rcp, yr, tid, NT, lim);
+      for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip<MODE>(v[i], rs);
+    }
+    store_row<V, VEC4, MODE>(v, rs, s, yr, tid, NT, lim);
   }
 }
 
@@ -391,7 +439,8 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
 // registers and publishes (m_g, s_g) in its slot part[row*G + g].  Wave 0
 // polls the row's G slots until none holds the sentinel, merges them into M
 // and S, and every thread writes
-//     y = max(e * exp(m_g - M), e_lo) / S.
+//     y = max(e * exp(m_g - M), e_lo) / S
+// (log outputs keep x instead of e and write y = max(x - M, lo) - ln S).
 // For an element with x - M >= lo the rescaled e equals exp(x - M) >= e^lo;
 // for x - M < lo it is below e^lo, so the max is exactly the clip of the
 // definition.  A NaN element makes s_g, hence S and the whole row, NaN.
@@ -423,8 +472,9 @@ __device__ __forceinline__ unsigned long long pack_pair(float a, float b) {
          (static_cast<unsigned long long>(__builtin_bit_cast(unsigned, b)) << 32);
 }
 
-template <int NT, int V, bool VEC4, int EM>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 : 4))) void k_split_onepass(
+template <int NT, int V, bool VEC4, int MODE>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
+    2 * kRowWaves<V, VEC4, MODE>))) void k_split_onepass(
     const float* x, float* y, unsigned long long* part, unsigned* depart, int64_t cols,
     int chunks, Clip clip) {
   constexpr int NW = NT / 64;
@@ -445,7 +495,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 :
   load_strip<V, VEC4>(v, xr, tid, NT, lim);
   const float m = block_max<NW>(array_max(v), red_max);
   const bool empty_max = (m == kNegInf);
-  float s = block_sum<NW>(exp_strip<EM>(v, row_shift(empty_max ? 0.0f : m, clip)), red_sum);
+  float s = block_sum<NW>(exp_strip<MODE>(v, row_shift(empty_max ? 0.0f : m, clip)), red_sum);
   if (empty_max) s = static_cast<float>(lim);
 
   if (tid == 0) {
@@ -472,12 +522,19 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 :
     const float pm = (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q)) : kNegInf;
     const float ps =
         (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q >> 32)) : 0.0f;
-    const RowShift rs = row_shift(seg_max<64>(pm), clip);
-    const float term = (tid < chunks) ? ps * exp_shift_clip<EM>(pm, rs) : 0.0f;
-    const float rcp = 1.0f / seg_sum<64>(term);
+    const float mrow = seg_max<64>(pm);
+    const RowShift rs = row_shift(mrow, clip);
+    const float term = (tid < chunks) ? ps * exp_shift_clip<exp_mode<MODE>()>(pm, rs) : 0.0f;
+    const float srow = seg_sum<64>(term);
+    const float rcp = 1.0f / srow;
     if (tid == 0) {
-      bcast[0] = ok ? exp_shift_clip<EM>(m, rs) * rcp : __builtin_nanf("");  // e^(m_g - M) / S
-      bcast[1] = ok ? clip.e_lo * rcp : __builtin_nanf("");                    // e_lo / S
+      if constexpr (MODE == kLogOut) {
+        bcast[0] = ok ? mrow : __builtin_nanf("");  // M
+        bcast[1] = ok ? srow : __builtin_nanf("");  // S
+      } else {
+        bcast[0] = ok ? exp_shift_clip<MODE>(m, rs) * rcp : __builtin_nanf("");  // e^(m_g - M) / S
+        bcast[1] = ok ? clip.e_lo * rcp : __builtin_nanf("");                    // e_lo / S
+      }
       // Depart once this wave's slot reads have returned (the add's operand
       // depends on them); the last workgroup of the row restores the slots.
       unsigned one = 1u;
@@ -492,11 +549,16 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 :
     }
   }
   __syncthreads();
-  const float scale = bcast[0];
-  const float floor_y = bcast[1];
+  if constexpr (MODE == kLogOut) {
+    // v still holds the logits: y = c - ln S against the row's M.
+    store_row<V, VEC4, MODE>(v, row_shift(bcast[0], clip), bcast[1], yr, tid, NT, lim);
+  } else {
+    const float scale = bcast[0];
+    const float floor_y = bcast[1];
 #pragma unroll
-  for (int i = 0; i < 4 * V; ++i) v[i] = fmaxf(v[i] * scale, floor_y);
-  store_strip<V, VEC4>(v, 1.0f, yr, tid, NT, lim);
+    for (int i = 0; i < 4 * V; ++i) v[i] = fmaxf(v[i] * scale, floor_y);
+    store_strip<V, VEC4>(v, [](float ev) { return ev; }, yr, tid, NT, lim);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -504,12 +566,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(V <= 8 ? 8 :
 
 // e[i] = exp(max(x[i] - m[i], lo)), through the same device routine the
 // softmax kernels use.
-template <int EM>
+template <int MODE>
 __global__ __launch_bounds__(256) void k_exp_probe(const float* x, const float* m,
                                                    float* e, int64_t n, Clip clip) {
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
        i += static_cast<int64_t>(gridDim.x) * 256)
-    e[i] = exp_shift_clip<EM>(x[i], row_shift(m[i], clip));
+    e[i] = exp_shift_clip<MODE>(x[i], row_shift(m[i], clip));
 }
 
 // Plain copy with 128-bit streaming accesses: the memory-bound ceiling that

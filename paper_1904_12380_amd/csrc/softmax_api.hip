@@ -379,6 +379,10 @@ int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
       e = p.vec_width == 4 ? split_launch<true, kExpFast>(p, x, y, rows, cols, ws, c, s)
                            : split_launch<false, kExpFast>(p, x, y, rows, cols, ws, c, s);
       break;
+    case kLogOut:
+      e = p.vec_width == 4 ? split_launch<true, kLogOut>(p, x, y, rows, cols, ws, c, s)
+                           : split_launch<false, kLogOut>(p, x, y, rows, cols, ws, c, s);
+      break;
     default:
       e = p.vec_width == 4 ? split_launch<true, kExpAccurate>(p, x, y, rows, cols, ws, c, s)
                            : split_launch<false, kExpAccurate>(p, x, y, rows, cols, ws, c, s);
@@ -417,8 +421,8 @@ int check_pointers(const float* x, const float* y, int64_t n_elems, int* dev) {
   return rc;
 }
 
-// The row softmax with exponential mode em (kExpAccurate, kExpWide or
-// kExpFast) after the clip and size checks.
+// The row softmax with kernel mode em (kExpAccurate, kExpWide, kExpFast,
+// or kLogOut for log outputs) after the clip and size checks.
 int softmax_rows(const float* x, float* y, int64_t rows, int64_t cols, Clip c, int em,
                  hipStream_t stream) {
   int rc = check_sizes(rows, cols);
@@ -434,6 +438,7 @@ int softmax_rows(const float* x, float* y, int64_t rows, int64_t cols, Clip c, i
   switch (em) {
     case kExpWide: e = launch_rows<kExpWide>(p, x, y, rows, cols, c, stream); break;
     case kExpFast: e = launch_rows<kExpFast>(p, x, y, rows, cols, c, stream); break;
+    case kLogOut: e = launch_rows<kLogOut>(p, x, y, rows, cols, c, stream); break;
     default: e = launch_rows<kExpAccurate>(p, x, y, rows, cols, c, stream); break;
   }
   return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
@@ -472,6 +477,15 @@ SOFTMAX_API int softmax_fwd_approx(const float* x, float* y, int64_t rows, int64
   const int rc = make_clip(clip_lo, &c, &wide);
   if (rc != SOFTMAX_OK) return rc;
   return softmax_rows(x, y, rows, cols, c, kExpFast, stream);
+}
+
+SOFTMAX_API int softmax_log_fwd(const float* x, float* y, int64_t rows, int64_t cols,
+                                float clip_lo, hipStream_t stream) {
+  Clip c;
+  bool wide = false;
+  const int rc = make_clip(clip_lo, &c, &wide);
+  if (rc != SOFTMAX_OK) return rc;
+  return softmax_rows(x, y, rows, cols, c, kLogOut, stream);
 }
 
 SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols,

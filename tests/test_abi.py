@@ -24,7 +24,8 @@ def declared_functions():
 
 def test_header_declares_entry_points():
     names = declared_functions()
-    for n in ("softmax_fwd", "softmax_fwd_clip", "softmax_fwd_approx", "softmax_attention_fwd",
+    for n in ("softmax_fwd", "softmax_fwd_clip", "softmax_fwd_approx", "softmax_log_fwd",
+              "softmax_attention_fwd",
               "softmax_strerror",
               "softmax_last_hip_error", "softmax_plan", "softmax_exp_probe",
               "softmax_copy_probe"):
@@ -171,6 +172,7 @@ def test_clip_bound_checked_before_any_hip_call():
     for lo in (nan, -47.99, -1.0, 0.0, 5.0, inf):
         assert sm.softmax_fwd_clip_ptr(0x1000, 0x2000000, 4, 4, lo, 0) == sm.ERR_INVALID_ARG
         assert sm.softmax_fwd_approx_ptr(0x1000, 0x2000000, 4, 4, lo, 0) == sm.ERR_INVALID_ARG
+        assert sm.softmax_log_fwd_ptr(0x1000, 0x2000000, 4, 4, lo, 0) == sm.ERR_INVALID_ARG
     # accepted bounds fall through to the size checks (negative rows here)
     for lo in (-48.0, -64.0, -87.5, -120.0, -1e30, -inf):
         assert sm.softmax_fwd_clip_ptr(0x1000, 0x2000000, -1, 4, lo, 0) == sm.ERR_INVALID_ARG
