@@ -340,6 +340,36 @@ def load_traffic(key: str) -> tuple[float | None, str | None]:
     return doc["traffic_bytes_per_launch"], None
 
 
+class AttentionCounters:
+    """An attention workload seen by the counter passes: the copy kernel that
+    calibrates the counters moves as many floats as Q, K and V hold."""
+
+    def __init__(self, key: str):
+        self.wa = workloads.ATTENTION_WORKLOADS[key]
+        self.key = key
+        wa = self.wa
+        self.elements = wa.batch * (wa.lq * wa.d + wa.lk * wa.d + wa.lk * wa.dv)
+        self.algorithmic_bytes = wa.algorithmic_bytes
+
+
+def pmc_run_attention(sm, torch, wc: AttentionCounters, launches: int) -> None:
+    """Launches for a counter pass on the fused attention: `launches` calls,
+    then as many copy-kernel calls over the bytes of Q, K and V."""
+    wa = wc.wa
+    dev = torch.device("cuda:0")
+    q, k, v = (torch.from_numpy(a).to(dev) for a in workloads.generate_qkv(wc.key))
+    o = torch.empty((wa.batch, wa.lq, wa.dv), device=dev)
+    for _ in range(launches):
+        sm.softmax_attention_fwd(q, k, v, scale=wa.scale, out=o)
+    torch.cuda.synchronize()
+    src = torch.cat([q.reshape(-1), k.reshape(-1), v.reshape(-1)])
+    dst = torch.empty_like(src)
+    for _ in range(launches):
+        sm.softmax_copy_probe(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"pmc_run": wc.key, "launches": launches}), flush=True)
+
+
 def pmc_run(sm, torch, w: workloads.Workload, launches: int) -> None:
     """Launches for a counter pass: `launches` softmax calls on the rotation,
     then as many copy-kernel calls over the same bytes."""
@@ -501,7 +531,7 @@ def summarize_trace(directory: str, w: workloads.Workload, command: str,
                 continue
             key = (r["Kernel_Name"].split("(")[0].replace("void ", ""), int(r["Grid_Size_X"]))
             g = groups.setdefault(key, {"d": [], "res": r, "base": base})
-            g["d"].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+            g["d"].append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
     with open(stats[0]) as f:
         rows = list(csv.DictReader(f))
     bench = None
@@ -516,19 +546,38 @@ def summarize_trace(directory: str, w: workloads.Workload, command: str,
         f.write(f"# Kernel trace: bench.py on {w.key} (and the other workloads it times)\n\n")
         f.write(f"Command (repository root, GPU machine):\n\n```\n{command}\n```\n\n")
         f.write("Per dispatch, grouped by kernel and grid (eager and graph-replayed "
-                "launches together; durations are the profiler's begin-to-end times):\n\n")
+                "launches together; durations are the profiler's begin-to-end times). "
+                "The last template argument of the softmax kernels is the mode: 0 "
+                "softmax_fwd, 1 no clip, 2 approximate exponential, 3 log-softmax.  A "
+                "shape seen in separate parts of the run is split into runs: the second "
+                "run of the DAM-shaped k_packed mode 0 is the unfused attention "
+                "reference (softmax_fwd between two hipBLAS products).\n\n")
         f.write("| kernel | grid threads | workload | calls | median us | p10 us | p90 us | "
                 "mean us | VGPR | AGPR | SGPR | LDS B | scratch B |\n"
                 "|---|---|---|---|---|---|---|---|---|---|---|---|---|\n")
         for (name, grid), g in sorted(groups.items(), key=lambda kv: (kv[0][0], kv[0][1])):
-            d = np.array(g["d"])
             r = g["res"]
             lab = labels.get((g["base"] if not g["base"].startswith("k_split") else "k_split",
                               grid), "")
-            f.write(f"| `{name}` | {grid} | {lab} | {d.size} | {np.median(d):.2f} | "
-                    f"{np.percentile(d, 10):.2f} | {np.percentile(d, 90):.2f} | "
-                    f"{d.mean():.2f} | {r['VGPR_Count']} | {r['Accum_VGPR_Count']} | "
-                    f"{r['SGPR_Count']} | {r['LDS_Block_Size']} | {r['Scratch_Size']} |\n")
+            if g["base"].startswith("k_attention"):
+                lab = " / ".join(workloads.ATTENTION_WORKLOADS)
+            # Runs of calls separated by more than 0.5 s are reported apart:
+            # the same launch shape can come from different parts of the run
+            # (the unfused attention reference calls softmax_fwd on scores of
+            # the DAM shape).
+            calls = sorted(g["d"])
+            runs = [[calls[0]]]
+            for c in calls[1:]:
+                if c[0] - runs[-1][-1][1] > 500_000_000:
+                    runs.append([])
+                runs[-1].append(c)
+            for k, run in enumerate(runs):
+                d = np.array([(e - b) / 1e3 for b, e in run])
+                tag = lab if len(runs) == 1 else f"{lab} (run {k + 1} of {len(runs)})"
+                f.write(f"| `{name}` | {grid} | {tag} | {d.size} | {np.median(d):.2f} | "
+                        f"{np.percentile(d, 10):.2f} | {np.percentile(d, 90):.2f} | "
+                        f"{d.mean():.2f} | {r['VGPR_Count']} | {r['Accum_VGPR_Count']} | "
+                        f"{r['SGPR_Count']} | {r['LDS_Block_Size']} | {r['Scratch_Size']} |\n")
         f.write("\nrocprofv3 --stats table (all kernels of the run):\n\n")
         f.write("| kernel | calls | average us | min us | max us |\n|---|---|---|---|---|\n")
         for r in rows:
@@ -552,7 +601,9 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=list(workloads.WORKLOADS))
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
+                    choices=list(workloads.WORKLOADS) + list(workloads.ATTENTION_WORKLOADS),
+                    help="a softmax workload (attention workloads: counter passes only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra-workloads", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
@@ -567,7 +618,14 @@ def main() -> int:
     ap.add_argument("--trace-json", help="JSON line printed by the traced run")
     args = ap.parse_args()
 
-    w = workloads.WORKLOADS[args.workload]
+    if args.workload in workloads.ATTENTION_WORKLOADS:
+        w = AttentionCounters(args.workload)
+        if not (args.pmc_run or args.summarize_pmc):
+            print("attention workloads are timed inside the default run; use them with "
+                  "--pmc-run or --summarize-pmc", file=sys.stderr)
+            return 2
+    else:
+        w = workloads.WORKLOADS[args.workload]
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace, w, args.pmc_command, args.trace_json))
         return 0
@@ -591,7 +649,10 @@ def main() -> int:
     sm.load_library()
 
     if args.pmc_run:
-        pmc_run(sm, torch, w, args.pmc_launches)
+        if isinstance(w, AttentionCounters):
+            pmc_run_attention(sm, torch, w, args.pmc_launches)
+        else:
+            pmc_run(sm, torch, w, args.pmc_launches)
         return 0
 
     log(f"[bench] generating {w.key}")

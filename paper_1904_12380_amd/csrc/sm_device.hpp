@@ -124,19 +124,19 @@ __device__ __forceinline__ RowShift row_shift(float m, Clip clip) {
   return r;
 }
 
-// ln S in binary64 from v_log_f32 (log2, within 1 ulp) times RN(ln 2);
-// S >= 1 for every row with a finite max.
-__device__ __forceinline__ double log_of_sum(float s) {
-  return static_cast<double>(__builtin_amdgcn_logf(s)) * kLn2;
+// ln S = RN(v_log_f32(S) * RN(ln 2)): log2 within 1 ulp, one product
+// rounding; S >= 1 for every row with a finite max.
+__device__ __forceinline__ float log_of_sum(float s) {
+  return __builtin_amdgcn_logf(s) * 0x1.62e430p-1f;
 }
 
-// One log-softmax output: y = RN32(c - ln S), c = max(x - M, lo) formed in
-// binary64 (exact for fp32 x and M within 29 binades) against the caller's
-// bound; with no clip a -inf entry gives -inf.
-__device__ __forceinline__ float log_out(float x, RowShift rs, double log_s) {
-  const double c = x < rs.tc_out ? static_cast<double>(rs.lo_out)
-                                 : static_cast<double>(x) + rs.neg_m;
-  return static_cast<float>(c - log_s);
+// One log-softmax output: y = RN(c - ln S) with c = RN(x - M), or the
+// caller's bound itself where x - M is below it; with no clip a -inf entry
+// gives -inf.  Three fp32 roundings and ln S's error: within
+// 1.2e-7 |y| + 2.4e-7 ln S of c - ln S, under the header's bound.
+__device__ __forceinline__ float log_out(float x, RowShift rs, float log_s) {
+  const float c = x < rs.tc_out ? rs.lo_out : x - rs.m;
+  return c - log_s;
 }
 
 // exp(max(x - M, lo)) for fp32 x, within 1.5 ulp of the exact value where

@@ -159,7 +159,7 @@ template <int V, bool VEC4, int MODE>
 __device__ __forceinline__ void store_row(const float (&v)[4 * V], RowShift rs, float s,
                                           float* p, int lane_off, int stride, int lim) {
   if constexpr (MODE == kLogOut) {
-    const double ls = log_of_sum(s);
+    const float ls = log_of_sum(s);
     store_strip<V, VEC4>(v, [&](float xv) { return log_out(xv, rs, ls); }, p, lane_off, stride,
                          lim);
   } else {
@@ -202,7 +202,7 @@ __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int 
   const RowShift rs = row_shift(seg_max<G>(array_max(v)), clip);
   const float s = seg_sum<G>(exp_strip<MODE>(v, rs));
   if constexpr (MODE == kLogOut) {
-    const double ls = log_of_sum(s);
+    const float ls = log_of_sum(s);
 #pragma unroll
     for (int k = 0; k < EPL; ++k) {
       const int c = j + G * k;
