@@ -159,6 +159,14 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         x, y = rot.pair(i)
         y.copy_(x)          # hipMemcpyAsync device to device
 
+    # The fixed cost of one launch that reads and then writes: the copy
+    # kernel on 4 KiB, same stream and graph timing.
+    tiny_x = torch.zeros(1024, device=rot.xs[0].device)
+    tiny_y = torch.empty_like(tiny_x)
+
+    def tiny(i, s):
+        sm.softmax_copy_probe(tiny_x, out=tiny_y, stream=s)
+
     def fwd_noclip(i, s):
         x, y = rot.pair(i)
         sm.softmax_fwd_clip(x, float("-inf"), out=y, stream=s)
@@ -174,6 +182,7 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
     ms, eager_ms = time_steps(torch, fwd, steps, warmup)
     copy_ms, _ = time_steps(torch, cpy, steps, warmup)
     memcpy_ms = time_steps(torch, d2d, steps, warmup)[0] if memcpy else None
+    floor_ms = time_steps(torch, tiny, steps, warmup)[0] if memcpy else None
     noclip_ms, _ = time_steps(torch, fwd_noclip, steps, warmup)
     approx_ms, _ = time_steps(torch, fwd_approx, steps, warmup)
     log_ms, _ = time_steps(torch, fwd_log, steps, warmup)
@@ -210,6 +219,7 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         "copy_gbps": w.algorithmic_bytes / (copy_ms * 1e-3) / 1e9,
         "softmax_over_copy_time": ms / copy_ms,
         "memcpy_ms_per_step": memcpy_ms,
+        "launch_floor_ms_per_step": floor_ms,
         "noclip_ms_per_step": noclip_ms,
         "noclip_hbm_gbps": w.algorithmic_bytes / (noclip_ms * 1e-3) / 1e9,
         "approx_exp_ms_per_step": approx_ms,
@@ -737,7 +747,16 @@ def main() -> int:
                          "softmax_over_copy_time": main_res["softmax_over_copy_time"],
                          "memcpy_d2d_ms_per_step": main_res["memcpy_ms_per_step"],
                          "memcpy_d2d_gbps": w.algorithmic_bytes
-                         / (main_res["memcpy_ms_per_step"] * 1e-3) / 1e9},
+                         / (main_res["memcpy_ms_per_step"] * 1e-3) / 1e9,
+                         "launch_floor_ms_per_step": main_res["launch_floor_ms_per_step"],
+                         "launch_floor_what": "softmax_copy_probe on 4 KiB: the fixed cost "
+                                              "of one graph-replayed launch that reads, "
+                                              "then writes",
+                         "softmax_gbps_above_launch_floor": w.algorithmic_bytes
+                         / ((ms - main_res["launch_floor_ms_per_step"]) * 1e-3) / 1e9,
+                         "copy_gbps_above_launch_floor": w.algorithmic_bytes
+                         / ((main_res["copy_ms_per_step"]
+                             - main_res["launch_floor_ms_per_step"]) * 1e-3) / 1e9},
         "no_clip": {"ms_per_step": main_res["noclip_ms_per_step"],
                     "hbm_gbps": main_res["noclip_hbm_gbps"],
                     "what": "softmax_fwd_clip with clip_lo = -inf, same rotation and timing"},
