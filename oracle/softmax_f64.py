@@ -101,3 +101,33 @@ def log_softmax_clipped(x: np.ndarray, clip_lo: float = CLIP_LO) -> np.ndarray:
         c = np.where(d < clip_lo, clip_lo, d)
         s = np.sum(np.exp(c), axis=1, keepdims=True)
         return c - np.log(s)
+
+
+def nll_clipped(x: np.ndarray, labels: np.ndarray, clip_lo: float = CLIP_LO) -> np.ndarray:
+    """Per-row negative log-likelihood of a label under the clipped softmax,
+    float64 [rows]:
+
+        loss_i = log(sum_k exp(c_ik)) - c_{i, t_i},   c_ij = max(x_ij - M_i, clip_lo)
+
+    that is -log_softmax_clipped(x, clip_lo)[i, t_i] for the label t_i of
+    row i: the training loss that the log after softmax feeds, and the
+    reason the reference functor clips (Sec. 2.1).  ``labels`` holds one
+    integer per row; a label outside [0, cols) gives NaN.  Rows of zero
+    columns have no valid label and are rejected.
+    """
+    x64 = np.asarray(x, dtype=np.float64)
+    if x64.ndim != 2:
+        raise ValueError("expected a 2-D [rows, classes] array")
+    rows, cols = x64.shape
+    t = np.asarray(labels)
+    if t.shape != (rows,) or not np.issubdtype(t.dtype, np.integer):
+        raise ValueError("expected one integer label per row")
+    if rows == 0:
+        return np.zeros(0, dtype=np.float64)
+    if cols == 0:
+        raise ValueError("rows of zero classes have no label")
+    logp = log_softmax_clipped(x64, clip_lo)
+    t64 = t.astype(np.int64)
+    valid = (t64 >= 0) & (t64 < cols)
+    picked = logp[np.arange(rows), np.where(valid, t64, 0)]
+    return np.where(valid, -picked, np.nan)

@@ -445,3 +445,111 @@ def pinl_shift_invariance(impl):
 
 
 LOG_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pinl_")]
+
+
+# ---------------------------------------------------------------------------
+# Pins for the per-row negative log-likelihood of a label under the clipped
+# softmax.  Each ``pinn_*`` function takes
+# ``impl(x: float32 [R, C], labels: int64 [R], clip_lo: float) -> float64 [R]``.
+
+def _labels(*v):
+    return np.asarray(v, dtype=np.int64)
+
+
+def pinn_library_cross_entropy(impl):
+    """No clip: torch's cross_entropy in float64 (reduction 'none'), on rows
+    whose shifted logits reach -800 and rows with offsets of +-800; with the
+    -64 clip on rows where no shifted logit is below -64."""
+    import torch
+    import torch.nn.functional as F
+    rng = np.random.default_rng(71)
+    rows = [rng.uniform(-800.0, 0.0, 64), rng.uniform(-150.0, 10.0, 64),
+            800.0 + rng.standard_normal(64), -800.0 + 3.0 * rng.standard_normal(64)]
+    x = _f32(np.stack(rows))
+    t = rng.integers(0, 64, size=4)
+    want = F.cross_entropy(torch.from_numpy(x.astype(np.float64)), torch.from_numpy(t),
+                           reduction="none").numpy()
+    assert _close_abs(impl(x, t, -np.inf), want)
+    x = random_logits(6, 300, 72, "normal", 4.0)
+    t = rng.integers(0, 300, size=6)
+    want = F.cross_entropy(torch.from_numpy(x.astype(np.float64)), torch.from_numpy(t),
+                           reduction="none").numpy()
+    assert _close_abs(impl(x, t, -64.0), want)
+
+
+def pinn_uniform_and_two_class(impl):
+    """Uniform rows give log N for any label; two classes give the softplus
+    of the other class's margin (-log_expit of the label's margin)."""
+    from scipy.special import log_expit
+    for n in (1, 2, 7, 1000):
+        for lab in sorted({0, n // 2, n - 1}):
+            y = impl(_f32(np.full((2, n), -2.25)), _labels(lab, lab), -64.0)
+            assert _close_abs(y, [math.log(n)] * 2, 1e-15), (n, lab)
+    rng = np.random.default_rng(73)
+    a, b = rng.uniform(-30.0, 30.0, 100), rng.uniform(-30.0, 30.0, 100)
+    x = _f32(np.stack([a, b], axis=1))
+    diff = x[:, 0].astype(np.float64) - x[:, 1].astype(np.float64)
+    t = rng.integers(0, 2, size=100)
+    want = np.where(t == 0, -log_expit(diff), -log_expit(-diff))
+    assert _close_abs(impl(x, t, -np.inf), want)
+
+
+def pinn_closed_form_clip(impl):
+    """Row [0, -100, -64, -63.5, -1e4] at the -64 clip, every label:
+    loss = log(1 + 3 e^-64 + e^-63.5) - c_label with
+    c = [0, -64, -64, -63.5, -64]; and at a bound of -1, where the clipped
+    terms change the sum: [0, -3, -5] gives log(1 + 2/e) - c_label with
+    c = [0, -1, -1]."""
+    x = _f32([[0.0, -100.0, -64.0, -63.5, -1.0e4]] * 5)
+    ls = math.log1p(3.0 * E64 + math.exp(-63.5))
+    want = ls - np.array([0.0, -64.0, -64.0, -63.5, -64.0])
+    assert _close_abs(impl(x, _labels(0, 1, 2, 3, 4), -64.0), want, 1e-15)
+    x = _f32([[0.0, -3.0, -5.0]] * 3)
+    ls = math.log1p(2.0 * math.exp(-1.0))
+    assert _close_abs(impl(x, _labels(0, 1, 2), -1.0), ls - np.array([0.0, -1.0, -1.0]), 1e-15)
+
+
+def pinn_brute_force_decimal(impl):
+    """Tiny rows against the 50-digit decimal logs (tests/golden, logy_clip):
+    the loss of label j is minus the log-probability of column j, at every
+    stored bound and every label."""
+    with open(os.path.join(GOLDEN, "brute_force_rows.json")) as f:
+        doc = json.load(f)
+    for rec in doc["rows"]:
+        row = [float.fromhex(h) for h in rec["x_hex"]]
+        n = len(row)
+        x = _f32([row] * n)
+        t = np.arange(n, dtype=np.int64)
+        for key, vals in rec["logy_clip"].items():
+            lo = -np.inf if key == "-inf" else float(key)
+            want = -np.array([float(Decimal(v)) for v in vals])
+            assert _close_abs(impl(x, t, lo), want, 1e-14), (rec["x_hex"], key)
+
+
+def pinn_label_picks_its_column(impl):
+    """For unclipped columns j and k of one row the losses differ by exactly
+    x_k - x_j (the shared log-sum cancels); labels are per row, not shared."""
+    x = random_logits(1, 40, 74, "normal", 2.0)
+    xs = _f32(np.repeat(x, 40, axis=0))
+    losses = impl(xs, np.arange(40, dtype=np.int64), -64.0)
+    x64 = x[0].astype(np.float64)
+    assert np.all(np.abs((losses - losses[0]) - (x64[0] - x64)) <= 1e-12)
+    y = impl(_f32([[5.0, 0.0, 0.0], [0.0, 5.0, 0.0]]), _labels(0, 0), -64.0)
+    assert y[0] < 0.02 and y[1] > 4.9
+
+
+def pinn_out_of_range_and_nonfinite(impl):
+    """Labels below 0 or at or past the class count give NaN (never a
+    wrapped index); a NaN row gives NaN; with no clip a -inf label entry
+    gives +inf, with the -64 clip it gives 64 + log S."""
+    x = _f32([[1.0, 2.0, 3.0]] * 4)
+    y = impl(x, _labels(-1, 3, 1 << 40, 2), -64.0)
+    assert np.all(np.isnan(y[:3])) and np.isfinite(y[3])
+    x = _f32([[1.0, np.nan, 0.0], [1.0, np.inf, 0.0], [0.0, -np.inf, 0.0], [0.0, -np.inf, 0.0]])
+    y = impl(x, _labels(0, 0, 1, 1), -np.inf)
+    assert np.isnan(y[0]) and np.isnan(y[1]) and y[2] == np.inf and y[3] == np.inf
+    y = impl(x[2:], _labels(1, 0), -64.0)
+    assert _close_abs(y, [64.0 + math.log(2.0 + E64), math.log(2.0 + E64)], 1e-15)
+
+
+NLL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pinn_")]

@@ -236,3 +236,56 @@ def test_log_mutant_is_caught(name):
         assert failed == [], failed
     else:
         assert failed, f"mutant {name} passed every log pin"
+
+
+# Mistakes in the per-row negative log-likelihood; each must fail one of
+# pins.NLL_PINS.
+def _nll(x, labels, lo, shift=True, clip_sum=True, clip_label=True, via_prob=False,
+         sign=1.0, label_shift=0, wrap_negative=False, row_mean=False, check_range=True):
+    x64 = np.asarray(x, dtype=np.float64)
+    t = np.asarray(labels).astype(np.int64)
+    rows, cols = x64.shape
+    with np.errstate(all="ignore"):
+        m = np.max(x64, axis=1, keepdims=True) if shift else 0.0
+        d = x64 - m
+        c = np.where(d < lo, lo, d)
+        s = np.sum(np.exp(c if clip_sum else d), axis=1)
+        logp = (np.log(np.exp(c) / s[:, None]) if via_prob
+                else (c if clip_label else d) - np.log(s)[:, None])
+        if row_mean:
+            return sign * -np.mean(logp, axis=1)
+        tt = (t + label_shift) % cols if label_shift else t
+        if wrap_negative:
+            tt = np.where(tt < 0, tt % cols, tt)
+        valid = (tt >= 0) & (tt < cols) if check_range else np.ones(rows, bool)
+        picked = logp[np.arange(rows), np.clip(tt, 0, cols - 1)]
+        return np.where(valid, sign * -picked, np.nan)
+
+
+MUTANTS_NLL = {
+    "reference_copy_is_clean": {},
+    "no_max_shift": dict(shift=False),
+    "sum_not_clipped": dict(clip_sum=False),
+    "label_term_not_clipped": dict(clip_label=False),
+    "log_of_underflowed_probability": dict(via_prob=True),
+    "log_probability_not_negated": dict(sign=-1.0),
+    "label_off_by_one": dict(label_shift=1),
+    "negative_label_wraps": dict(wrap_negative=True),
+    "out_of_range_label_clamped": dict(check_range=False),
+    "mean_over_classes": dict(row_mean=True),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_NLL))
+def test_nll_mutant_is_caught(name):
+    impl = lambda x, t, lo: _nll(x, t, lo, **MUTANTS_NLL[name])  # noqa: E731
+    failed = []
+    for pin in pins.NLL_PINS:
+        try:
+            pin(impl)
+        except (AssertionError, ValueError, FloatingPointError, IndexError):
+            failed.append(pin.__name__)
+    if name == "reference_copy_is_clean":
+        assert failed == [], failed
+    else:
+        assert failed, f"mutant {name} passed every NLL pin"

@@ -67,3 +67,18 @@ def test_attention_oracle_rejects_zero_keys():
 @pytest.mark.parametrize("pin", pins.LOG_PINS, ids=lambda p: p.__name__)
 def test_log_oracle_pin(pin):
     pin(oracle.log_softmax_clipped)
+
+
+@pytest.mark.parametrize("pin", pins.NLL_PINS, ids=lambda p: p.__name__)
+def test_nll_oracle_pin(pin):
+    pin(oracle.nll_clipped)
+
+
+def test_nll_oracle_rejects_bad_labels():
+    with pytest.raises(ValueError):
+        oracle.nll_clipped(np.zeros((2, 3), np.float32), np.zeros(3, np.int64))
+    with pytest.raises(ValueError):
+        oracle.nll_clipped(np.zeros((2, 3), np.float32), np.zeros(2, np.float64))
+    with pytest.raises(ValueError):
+        oracle.nll_clipped(np.zeros((2, 0), np.float32), np.zeros(2, np.int64))
+    assert oracle.nll_clipped(np.zeros((0, 3), np.float32), np.zeros(0, np.int64)).shape == (0,)
