@@ -145,6 +145,8 @@ def time_steps(torch, launch, steps: int, warmup: int) -> tuple[float, float]:
 def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, warmup: int,
              check: bool = True, memcpy: bool = False) -> dict:
     rot = Rotation(torch, x_host)
+    labels = torch.from_numpy(workloads.generate_labels(w.key)).to(rot.xs[0].device)
+    losses = [torch.empty(w.rows, device=rot.xs[0].device) for _ in range(rot.n)]
     plan = sm.softmax_plan(w.rows, w.cols, rot.xs[0].data_ptr(), rot.ys[0].data_ptr())
 
     def fwd(i, s):
@@ -179,6 +181,10 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         x, y = rot.pair(i)
         sm.softmax_log_fwd(x, out=y, stream=s)
 
+    def fwd_nll(i, s):
+        x, _ = rot.pair(i)
+        sm.softmax_nll_fwd(x, labels, out=losses[i % rot.n], stream=s)
+
     ms, eager_ms = time_steps(torch, fwd, steps, warmup)
     copy_ms, _ = time_steps(torch, cpy, steps, warmup)
     memcpy_ms = time_steps(torch, d2d, steps, warmup)[0] if memcpy else None
@@ -186,6 +192,8 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
     noclip_ms, _ = time_steps(torch, fwd_noclip, steps, warmup)
     approx_ms, _ = time_steps(torch, fwd_approx, steps, warmup)
     log_ms, _ = time_steps(torch, fwd_log, steps, warmup)
+    nll_ms, _ = time_steps(torch, fwd_nll, steps, warmup)
+    nll_bytes = 4 * w.rows * w.cols + 12 * w.rows   # x read, labels read, losses written
 
     max_rel = None
     if check:
@@ -226,6 +234,9 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         "approx_exp_hbm_gbps": w.algorithmic_bytes / (approx_ms * 1e-3) / 1e9,
         "log_softmax_ms_per_step": log_ms,
         "log_softmax_hbm_gbps": w.algorithmic_bytes / (log_ms * 1e-3) / 1e9,
+        "nll_ms_per_step": nll_ms,
+        "nll_algorithmic_bytes": nll_bytes,
+        "nll_hbm_gbps": nll_bytes / (nll_ms * 1e-3) / 1e9,
         "rotation_buffers": nbuf,
         "plan": plan,
         "sampled_max_rel_err": max_rel,
@@ -672,7 +683,8 @@ def main() -> int:
     log(f"[bench] {w.key}: {main_res['ms_per_step'] * 1e3:.2f} us/step, "
         f"{main_res['hbm_gbps']:.0f} GB/s (no clip {main_res['noclip_ms_per_step'] * 1e3:.2f} us, "
         f"approx exp {main_res['approx_exp_ms_per_step'] * 1e3:.2f} us, "
-        f"log {main_res['log_softmax_ms_per_step'] * 1e3:.2f} us)")
+        f"log {main_res['log_softmax_ms_per_step'] * 1e3:.2f} us, "
+        f"nll {main_res['nll_ms_per_step'] * 1e3:.2f} us)")
 
     extra = {}
     if not args.no_extra_workloads:
@@ -688,7 +700,8 @@ def main() -> int:
             log(f"[bench] {key}: {r['ms_per_step'] * 1e3:.2f} us/step, {r['hbm_gbps']:.0f} GB/s "
                 f"(no clip {r['noclip_ms_per_step'] * 1e3:.2f} us, approx exp "
                 f"{r['approx_exp_ms_per_step'] * 1e3:.2f} us, log "
-                f"{r['log_softmax_ms_per_step'] * 1e3:.2f} us)")
+                f"{r['log_softmax_ms_per_step'] * 1e3:.2f} us, nll "
+                f"{r['nll_ms_per_step'] * 1e3:.2f} us)")
 
     attention = None
     if not args.no_extra_workloads:
@@ -764,6 +777,11 @@ def main() -> int:
                         "hbm_gbps": main_res["log_softmax_hbm_gbps"],
                         "what": "softmax_log_fwd (log of the clipped softmax), same rotation "
                                 "and timing"},
+        "nll": {"ms_per_step": main_res["nll_ms_per_step"],
+                "hbm_gbps": main_res["nll_hbm_gbps"],
+                "algorithmic_bytes_per_launch": main_res["nll_algorithmic_bytes"],
+                "what": "softmax_nll_fwd (per-row loss of a label; x read once, 4 B "
+                        "written per row), same rotation and timing"},
         "approx_exp": {"ms_per_step": main_res["approx_exp_ms_per_step"],
                        "hbm_gbps": main_res["approx_exp_hbm_gbps"],
                        "what": "softmax_fwd_approx (single-instruction fp32 exponential), "

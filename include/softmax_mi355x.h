@@ -176,6 +176,38 @@ SOFTMAX_API int softmax_fwd_approx(const float* x, float* y, int64_t rows, int64
 SOFTMAX_API int softmax_log_fwd(const float* x, float* y, int64_t rows, int64_t cols,
                                 float clip_lo, hipStream_t stream);
 
+/*
+ * softmax_nll_fwd -- the negative log-likelihood of one label per row under
+ * the clipped softmax, fused so that no probability or log is written:
+ *
+ *     loss[i] = ln(sum_k exp(c_ik)) - c_{i, labels[i]},
+ *     c_ij = max(x[i,j] - M_i, clip_lo)
+ *
+ * that is minus softmax_log_fwd's output at the label: the training loss
+ * that the log after softmax feeds, and the reason the reference functor
+ * clips (Sec. 2.1).
+ *
+ *   x       device pointer, rows x cols fp32, row-major (as softmax_fwd)
+ *   labels  device pointer, rows int64 class indices
+ *   loss    device pointer, rows fp32; written.  May not overlap x or
+ *           labels.
+ *   clip_lo as for softmax_fwd_clip (-INFINITY: plain cross-entropy; a
+ *           -inf logit at the label then gives +inf).
+ *
+ * A label outside [0, cols) gives a NaN loss (no error: labels are device
+ * data).  A NaN in the row, a +inf, or a row of all -inf gives NaN.  x is
+ * read once; the call writes 4 bytes per row.  rows == 0 returns SOFTMAX_OK
+ * with nothing launched; cols == 0 with rows > 0 is SOFTMAX_ERR_INVALID_ARG
+ * (no row can have a valid label).
+ *
+ * Accuracy: |loss - loss*| <= 2e-6 + 2.5e-7 * (|loss*| + ln(cols)), as for
+ * softmax_log_fwd.  Ownership, asynchrony, workspace (rows longer than
+ * 32768 columns) and error codes follow softmax_fwd_clip.
+ */
+SOFTMAX_API int softmax_nll_fwd(const float* x, const int64_t* labels, float* loss,
+                                int64_t rows, int64_t cols, float clip_lo,
+                                hipStream_t stream);
+
 /* Limits of softmax_attention_fwd. */
 #define SOFTMAX_ATTN_MAX_KEYS 64     /* lk: the keys of one row fit one set of tiles */
 #define SOFTMAX_ATTN_MAX_DIM 65536   /* d and dv */

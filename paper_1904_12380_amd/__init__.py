@@ -33,6 +33,7 @@ __all__ = [
     "LIB_PATH", "HEADER_PATH", "SoftmaxError", "load_library", "softmax_fwd",
     "softmax_fwd_ptr", "softmax_fwd_clip", "softmax_fwd_clip_ptr", "softmax_plan",
     "softmax_fwd_approx", "softmax_fwd_approx_ptr", "softmax_log_fwd", "softmax_log_fwd_ptr",
+    "softmax_nll_fwd", "softmax_nll_fwd_ptr",
     "softmax_attention_fwd", "softmax_attention_fwd_ptr", "ATTN_MAX_KEYS", "ATTN_MAX_DIM",
     "softmax_exp_probe", "softmax_copy_probe", "softmax_strerror", "softmax_last_hip_error",
     "CLIP_LO", "CLIP_MAX", "KERNEL_NAMES",
@@ -105,6 +106,8 @@ def load_library() -> ctypes.CDLL:
     lib.softmax_fwd_approx.restype = ctypes.c_int
     lib.softmax_log_fwd.argtypes = [vp, vp, i64, i64, ctypes.c_float, vp]
     lib.softmax_log_fwd.restype = ctypes.c_int
+    lib.softmax_nll_fwd.argtypes = [vp, vp, vp, i64, i64, ctypes.c_float, vp]
+    lib.softmax_nll_fwd.restype = ctypes.c_int
     lib.softmax_exp_probe.restype = ctypes.c_int
     lib.softmax_copy_probe.argtypes = [vp, vp, i64, vp]
     lib.softmax_copy_probe.restype = ctypes.c_int
@@ -252,6 +255,40 @@ def softmax_log_fwd(x, clip_lo: float = CLIP_LO, out=None, stream=None):
                                  _stream_handle(stream))
     if rc != OK:
         raise SoftmaxError(rc, "softmax_log_fwd")
+    return out
+
+
+def softmax_nll_fwd_ptr(x_ptr: int, labels_ptr: int, loss_ptr: int, rows: int, cols: int,
+                        clip_lo: float, stream_handle: int = 0) -> int:
+    """Raw C call; returns the C return code."""
+    return int(load_library().softmax_nll_fwd(x_ptr, labels_ptr, loss_ptr, rows, cols,
+                                              float(clip_lo), stream_handle))
+
+
+def softmax_nll_fwd(x, labels, clip_lo: float = CLIP_LO, out=None, stream=None):
+    """Per-row negative log-likelihood of ``labels`` (int64 GPU tensor
+    [rows]) under the clipped softmax of ``x`` [rows, cols]:
+    loss = ln S - max(x[label] - M, clip_lo).  Returns float32 [rows]; a
+    label outside [0, cols) gives NaN."""
+    torch = _torch()
+    _check_f32_cuda(x, "x")
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [rows, cols]")
+    rows, cols = x.shape
+    if not isinstance(labels, torch.Tensor) or labels.dtype != torch.int64:
+        raise TypeError("labels must be an int64 torch.Tensor")
+    if labels.shape != (rows,) or labels.device != x.device or not labels.is_contiguous():
+        raise ValueError("labels must be contiguous [rows] on x's device")
+    if out is None:
+        out = torch.empty(rows, dtype=torch.float32, device=x.device)
+    _check_f32_cuda(out, "out")
+    if out.shape != (rows,) or out.device != x.device:
+        raise ValueError("out must be [rows] on x's device")
+    with torch.cuda.device(x.device):
+        rc = softmax_nll_fwd_ptr(x.data_ptr(), labels.data_ptr(), out.data_ptr(), rows, cols,
+                                 clip_lo, _stream_handle(stream))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_nll_fwd")
     return out
 
 

@@ -55,8 +55,14 @@ constexpr int kExpFast = 2;
 // y = c - ln S with c = max(x - M, lo), instead of e / S.  Its row sums use
 // the accurate exponential (terms under 2^-126 do not matter next to S >= 1).
 constexpr int kLogOut = 3;
+// A fifth: one value per row, the negative log-likelihood of the row's
+// label, ln S - c_label (minus the label's log output); sums as kLogOut.
+constexpr int kNllOut = 4;
+// Modes whose output step needs the logits rather than the exponentials.
 template <int MODE>
-constexpr int exp_mode() { return MODE == kLogOut ? kExpAccurate : MODE; }
+constexpr bool keeps_logits() { return MODE == kLogOut || MODE == kNllOut; }
+template <int MODE>
+constexpr int exp_mode() { return keeps_logits<MODE>() ? kExpAccurate : MODE; }
 
 // The clip as a kernel argument: lo in [kClipFloor, 0] and e_lo = RN(e^lo')
 // for the caller's bound lo' (0 when lo' < -103.98 or lo' = -inf).

@@ -44,6 +44,14 @@ inline bool partial_overlap(const void* a, const void* b, int64_t n) {
   return pa < pb + static_cast<uintptr_t>(n) && pb < pa + static_cast<uintptr_t>(n);
 }
 
+// Byte ranges [a, a+na) and [b, b+nb) share a byte (empty ranges never do).
+inline bool ranges_overlap(const void* a, int64_t na, const void* b, int64_t nb) {
+  const uintptr_t pa = reinterpret_cast<uintptr_t>(a);
+  const uintptr_t pb = reinterpret_cast<uintptr_t>(b);
+  return na > 0 && nb > 0 && pa < pb + static_cast<uintptr_t>(nb) &&
+         pb < pa + static_cast<uintptr_t>(na);
+}
+
 inline bool any_overlap(const void* a, const void* b, int64_t n) {
   const uintptr_t pa = reinterpret_cast<uintptr_t>(a);
   const uintptr_t pb = reinterpret_cast<uintptr_t>(b);

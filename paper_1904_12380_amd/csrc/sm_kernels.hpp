@@ -107,11 +107,11 @@ __device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* p, in
 }
 
 // This lane's pairwise partial sum of the clipped exponentials.  For
-// probability outputs v is replaced by the exponentials; for log outputs
-// (MODE == kLogOut) v keeps the logits, which the output step needs.
+// probability outputs v is replaced by the exponentials; for log and NLL
+// outputs (keeps_logits) v keeps the logits, which the output step needs.
 template <int MODE, int N>
 __device__ __forceinline__ float exp_strip(float (&v)[N], RowShift rs) {
-  if constexpr (MODE == kLogOut) {
+  if constexpr (keeps_logits<MODE>()) {
     // Eight interleaved partial sums, then their tree: no second array of N
     // registers next to the logits.
     constexpr int P = N < 8 ? N : 8;
@@ -168,6 +168,69 @@ __device__ __forceinline__ void store_row(const float (&v)[4 * V], RowShift rs, 
   }
 }
 
+// The row's label as a column of the segment [c0, c0 + lim), or -1 when it
+// lies outside the segment (or outside the row).
+__device__ __forceinline__ int seg_label(int64_t label, int64_t c0, int lim) {
+  const int64_t l = label - c0;
+  return (l >= 0 && l < lim) ? static_cast<int>(l) : -1;
+}
+
+// Index into this lane's v (laid out as in load_strip) of segment column
+// lc, or -1 when this lane does not hold it (or lc < 0).
+template <int V, bool VEC4>
+__device__ __forceinline__ int held_index(int lc, int lane_off, int stride) {
+  if (lc < 0) return -1;
+  const int t = (VEC4 ? lc >> 2 : lc) - lane_off;
+  if (t < 0 || t % stride != 0) return -1;
+  const int i = t / stride;
+  if constexpr (VEC4) {
+    return i < V ? 4 * i + (lc & 3) : -1;
+  } else {
+    return i < 4 * V ? i : -1;
+  }
+}
+
+// NLL output: the lane holding segment column lc writes *out = ln S - c,
+// minus that column's log output.  Other lanes store nothing.
+template <int V, bool VEC4>
+__device__ __forceinline__ void nll_strip(const float (&v)[4 * V], RowShift rs, float s, int lc,
+                                          float* out, int lane_off, int stride) {
+  const int idx = held_index<V, VEC4>(lc, lane_off, stride);
+  float xl = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4 * V; ++i) xl = idx == i ? v[i] : xl;
+  if (idx >= 0) *out = -log_out(xl, rs, log_of_sum(s));
+}
+
+// The output step of the segment [c0, c0 + lim) of `row`: the row's
+// outputs (probabilities or logs) into y + row * cols + c0, or for NLL
+// outputs the one loss y[row], written by the lane that holds the label's
+// column; `first` (one thread of the row's first segment) writes NaN for a
+// label outside [0, cols).
+template <int V, bool VEC4, int MODE>
+__device__ __forceinline__ void finish_row(const float (&v)[4 * V], RowShift rs, float s,
+                                           float* y, int64_t row, int64_t cols, int64_t c0,
+                                           int lim, int64_t label, int lane_off, int stride,
+                                           bool first) {
+  if constexpr (MODE == kNllOut) {
+    nll_strip<V, VEC4>(v, rs, s, seg_label(label, c0, lim), y + row, lane_off, stride);
+    if (first && (label < 0 || label >= cols)) y[row] = __builtin_nanf("");
+  } else {
+    store_row<V, VEC4, MODE>(v, rs, s, y + row * cols + c0, lane_off, stride, lim);
+  }
+}
+
+// The label of `row` for NLL outputs (0 in the other modes, where labels
+// is null).
+template <int MODE>
+__device__ __forceinline__ int64_t row_label(const int64_t* labels, int64_t row) {
+  if constexpr (MODE == kNllOut) {
+    return labels[row];
+  } else {
+    return 0;
+  }
+}
+
 // Columns of a row segment that starts at column c0: min(cols - c0, cap).
 __device__ __forceinline__ int seg_len(int64_t cols, int64_t c0, int64_t cap) {
   const int64_t left = cols - c0;
@@ -190,7 +253,7 @@ __device__ __forceinline__ int seg_len(int64_t cols, int64_t c0, int64_t cap) {
 // the current one, so they are in flight while the current tile computes.
 template <int G, int EPL, int MODE>
 __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int r, int j,
-                                            Clip clip) {
+                                            Clip clip, int64_t label, float* yl) {
   const bool active = r < nr;
   float* tr = tile + r * ccols;
   float v[EPL];
@@ -201,7 +264,14 @@ __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int 
   }
   const RowShift rs = row_shift(seg_max<G>(array_max(v)), clip);
   const float s = seg_sum<G>(exp_strip<MODE>(v, rs));
-  if constexpr (MODE == kLogOut) {
+  if constexpr (MODE == kNllOut) {
+    // One loss per row into yl[r], by lane 0 of the row: the label's logit
+    // is still in the tile; a label outside the row gives NaN.
+    if (active && j == 0) {
+      const bool ok = label >= 0 && label < ccols;
+      yl[r] = ok ? -log_out(tr[ok ? label : 0], rs, log_of_sum(s)) : __builtin_nanf("");
+    }
+  } else if constexpr (MODE == kLogOut) {
     const float ls = log_of_sum(s);
 #pragma unroll
     for (int k = 0; k < EPL; ++k) {
@@ -219,7 +289,8 @@ __device__ __forceinline__ void packed_rows(float* tile, int nr, int ccols, int 
 }
 
 template <int G, int EPL, bool VEC4, int MODE>
-__global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_t rows,
+__global__ __launch_bounds__(256) void k_packed(const float* x, float* y,
+                                                const int64_t* labels, int64_t rows,
                                                 int64_t cols, Clip clip) {
   constexpr int kRows = 256 / G;
   constexpr int kTileFloats = kRows * G * EPL;  // = 256 * EPL
@@ -232,14 +303,19 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
   const int r = tid / G;
   const int j = tid % G;
 
-  // Registers for the next tile: kPer 128-bit (or 32-bit) values per thread.
+  // Registers for the next tile: kPer 128-bit (or 32-bit) values per thread,
+  // and (NLL outputs) the label of this thread's row of it.
   f32x4 q4[VEC4 ? kPer : 1];
   float q1[VEC4 ? 1 : kPer];
+  int64_t lab_next = -1;
   auto issue = [&](int64_t t) {
     const int64_t row0 = t * kRows;
     const int nr = static_cast<int>(rows - row0 < kRows ? rows - row0 : kRows);
     const int n = nr * ccols;
     const float* xs = x + row0 * cols;
+    if constexpr (MODE == kNllOut) {
+      if (r < nr) lab_next = labels[row0 + r];
+    }
     if constexpr (VEC4) {
       const int n4 = n >> 2;
 #pragma unroll
@@ -265,7 +341,6 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
     const int nr = static_cast<int>(rows - row0 < kRows ? rows - row0 : kRows);
     const int n = nr * ccols;
     const float* xs = x + row0 * cols;
-    float* ys = y + row0 * cols;
 
     if constexpr (VEC4) {
       const int n4 = n >> 2;
@@ -283,18 +358,22 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
       }
     }
     __syncthreads();
+    const int64_t label = lab_next;
     if (t + gridDim.x < ntiles) issue(t + gridDim.x);
 
-    packed_rows<G, EPL, MODE>(tile, nr, ccols, r, j, clip);
+    packed_rows<G, EPL, MODE>(tile, nr, ccols, r, j, clip, label, y + row0);
     __syncthreads();
 
-    if constexpr (VEC4) {
-      const int n4 = n >> 2;
-      for (int i = tid; i < n4; i += 256)
-        st_stream(ys + 4 * i, *reinterpret_cast<const f32x4*>(tile + 4 * i));
-      for (int i = (n4 << 2) + tid; i < n; i += 256) ys[i] = tile[i];
-    } else {
-      for (int i = tid; i < n; i += 256) __builtin_nontemporal_store(tile[i], ys + i);
+    if constexpr (MODE != kNllOut) {
+      float* ys = y + row0 * cols;
+      if constexpr (VEC4) {
+        const int n4 = n >> 2;
+        for (int i = tid; i < n4; i += 256)
+          st_stream(ys + 4 * i, *reinterpret_cast<const f32x4*>(tile + 4 * i));
+        for (int i = (n4 << 2) + tid; i < n; i += 256) ys[i] = tile[i];
+      } else {
+        for (int i = tid; i < n; i += 256) __builtin_nontemporal_store(tile[i], ys + i);
+      }
     }
     __syncthreads();
   }
@@ -307,7 +386,7 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y, int64_
 // nothing spills to scratch.  The one-pass split kernel runs at twice
 // these (its chunks hold half as many values per lane).
 template <int V, bool VEC4, int MODE>
-constexpr int kRowWaves = (V <= 8 && VEC4 && MODE != kLogOut) ? 4 : 2;
+constexpr int kRowWaves = (V <= 8 && VEC4 && !keeps_logits<MODE>()) ? 4 : 2;
 
 // ---------------------------------------------------------------------------
 // (b) One wavefront per row, cols <= 256*V (4*V elements per lane).
@@ -315,26 +394,27 @@ constexpr int kRowWaves = (V <= 8 && VEC4 && MODE != kLogOut) ? 4 : 2;
 template <int V, bool VEC4, int MODE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     kRowWaves<V, VEC4, MODE>))) void k_wave_row(
-    const float* x, float* y, int64_t rows, int64_t cols, Clip clip) {
+    const float* x, float* y, const int64_t* labels, int64_t rows, int64_t cols, Clip clip) {
   const int lane = __lane_id();
   const int wave = threadIdx.x >> 6;
   for (int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wave; row < rows;
        row += static_cast<int64_t>(gridDim.x) * 4) {
     const float* xr = x + row * cols;
-    float* yr = y + row * cols;
+    const int64_t label = row_label<MODE>(labels, row);
     const int lim = static_cast<int>(cols);
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, lane, 64, lim);
     const RowShift rs = row_shift(seg_max<64>(array_max(v)), clip);
     const float s = seg_sum<64>(exp_strip<MODE>(v, rs));
-    store_row<V, VEC4, MODE>(v, rs, s, yr, lane, 64, lim);
+    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, label, lane, 64, lane == 0);
   }
 }
 
 // ---------------------------------------------------------------------------
 // (c) One workgroup of NT threads per row, cols <= 4*V*NT.
 template <int NT, int V, bool VEC4, int MODE>
-__global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int64_t rows,
+__global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y,
+                                                  const int64_t* labels, int64_t rows,
                                                   int64_t cols, Clip clip) {
   constexpr int NW = NT / 64;
   __shared__ float red_max[NW];
@@ -342,13 +422,13 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y, int6
   const int tid = threadIdx.x;
   for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
     const float* xr = x + row * cols;
-    float* yr = y + row * cols;
+    const int64_t label = row_label<MODE>(labels, row);
     const int lim = static_cast<int>(cols);
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, tid, NT, lim);
     const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max), clip);
     const float s = block_sum<NW>(exp_strip<MODE>(v, rs), red_sum);
-    store_row<V, VEC4, MODE>(v, rs, s, yr, tid, NT, lim);
+    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, label, tid, NT, tid == 0);
   }
 }
 
@@ -397,6 +477,7 @@ __global__ __launch_bounds__(NT) void k_split_stats(const float* x, float2* part
 
 template <int NT, int V, bool VEC4, int MODE>
 __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
+                                                    const int64_t* labels,
                                                     const float2* part, int64_t rows,
                                                     int64_t cols, int64_t chunks, Clip clip) {
   constexpr int64_t CH = int64_t(4) * V * NT;
@@ -408,7 +489,7 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
     const int64_t g = b - row * chunks;
     const int64_t c0 = g * CH;
     const float* xr = x + row * cols + c0;
-    float* yr = y + row * cols + c0;
+    const int64_t label = row_label<MODE>(labels, row);
     const int lim = seg_len(cols, c0, CH);
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, tid, NT, lim);
@@ -423,11 +504,12 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
       ss = ss + p.y * exp_shift_clip<exp_mode<MODE>()>(p.x, rs);
     }
     const float s = seg_sum<64>(ss);
-    if constexpr (MODE != kLogOut) {
+    if constexpr (!keeps_logits<MODE>()) {
 #pragma unroll
       for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip<MODE>(v[i], rs);
     }
-    store_row<V, VEC4, MODE>(v, rs, s, yr, tid, NT, lim);
+    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, c0, lim, label, tid, NT,
+                              g == 0 && tid == 0);
   }
 }
 
@@ -475,8 +557,8 @@ __device__ __forceinline__ unsigned long long pack_pair(float a, float b) {
 template <int NT, int V, bool VEC4, int MODE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     2 * kRowWaves<V, VEC4, MODE>))) void k_split_onepass(
-    const float* x, float* y, unsigned long long* part, unsigned* depart, int64_t cols,
-    int chunks, Clip clip) {
+    const float* x, float* y, const int64_t* labels, unsigned long long* part,
+    unsigned* depart, int64_t cols, int chunks, Clip clip) {
   constexpr int NW = NT / 64;
   constexpr int64_t CH = int64_t(4) * V * NT;
   __shared__ float red_max[NW];
@@ -488,7 +570,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
   const int g = static_cast<int>(b - row * chunks);
   const int64_t c0 = g * CH;
   const float* xr = x + row * cols + c0;
-  float* yr = y + row * cols + c0;
+  const int64_t label = row_label<MODE>(labels, row);
   const int lim = seg_len(cols, c0, CH);
 
   float v[4 * V];
@@ -528,7 +610,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     const float srow = seg_sum<64>(term);
     const float rcp = 1.0f / srow;
     if (tid == 0) {
-      if constexpr (MODE == kLogOut) {
+      if constexpr (keeps_logits<MODE>()) {
         bcast[0] = ok ? mrow : __builtin_nanf("");  // M
         bcast[1] = ok ? srow : __builtin_nanf("");  // S
       } else {
@@ -549,10 +631,13 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     }
   }
   __syncthreads();
-  if constexpr (MODE == kLogOut) {
-    // v still holds the logits: y = c - ln S against the row's M.
-    store_row<V, VEC4, MODE>(v, row_shift(bcast[0], clip), bcast[1], yr, tid, NT, lim);
+  if constexpr (keeps_logits<MODE>()) {
+    // v still holds the logits: y = c - ln S (or the label's loss) against
+    // the row's M.
+    finish_row<V, VEC4, MODE>(v, row_shift(bcast[0], clip), bcast[1], y, row, cols, c0, lim,
+                              label, tid, NT, g == 0 && tid == 0);
   } else {
+    float* yr = y + row * cols + c0;
     const float scale = bcast[0];
     const float floor_y = bcast[1];
 #pragma unroll

@@ -182,7 +182,8 @@ const void* packed_fn(int epl, std::integer_sequence<int, E...>) {
 
 template <bool VEC4, int EM>
 hipError_t dispatch_packed(const softmax_plan_t& p, const float* x, float* y,
-                           int64_t rows, int64_t cols, Clip c, hipStream_t s) {
+                           const int64_t* labels, int64_t rows, int64_t cols, Clip c,
+                           hipStream_t s) {
   const void* fn = nullptr;
   switch (p.lanes_per_row) {
     case 1:
@@ -196,56 +197,71 @@ hipError_t dispatch_packed(const softmax_plan_t& p, const float* x, float* y,
       break;
   }
   if (fn == nullptr) return hipErrorInvalidValue;
-  void* args[] = {&x, &y, &rows, &cols, &c};
+  void* args[] = {&x, &y, &labels, &rows, &cols, &c};
   return launch(fn, p.grid, 256, args, s);
 }
 
 template <int V, bool VEC4, int EM>
-hipError_t run_wave(const float* x, float* y, int64_t rows, int64_t cols, Clip c,
-                    int64_t grid, hipStream_t s) {
-  void* args[] = {&x, &y, &rows, &cols, &c};
+hipError_t run_wave(const float* x, float* y, const int64_t* labels, int64_t rows,
+                    int64_t cols, Clip c, int64_t grid, hipStream_t s) {
+  void* args[] = {&x, &y, &labels, &rows, &cols, &c};
   return launch(reinterpret_cast<const void*>(&k_wave_row<V, VEC4, EM>), grid, 256, args,
                 s);
 }
 
 template <bool VEC4, int EM>
-hipError_t dispatch_wave(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
-                         int64_t cols, Clip c, hipStream_t s) {
+hipError_t dispatch_wave(const softmax_plan_t& p, const float* x, float* y,
+                         const int64_t* labels, int64_t rows, int64_t cols, Clip c,
+                         hipStream_t s) {
   switch (p.elems_per_lane / 4) {
-    case 1: return run_wave<1, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
-    case 2: return run_wave<2, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
-    case 4: return run_wave<4, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
-    case 8: return run_wave<8, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
-    default: return run_wave<16, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
+    case 1: return run_wave<1, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
+    case 2: return run_wave<2, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
+    case 4: return run_wave<4, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
+    case 8: return run_wave<8, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
+    default: return run_wave<16, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
   }
 }
 
 template <int V, bool VEC4, int EM>
-hipError_t run_block(const float* x, float* y, int64_t rows, int64_t cols, Clip c,
-                     int64_t grid, hipStream_t s) {
-  void* args[] = {&x, &y, &rows, &cols, &c};
+hipError_t run_block(const float* x, float* y, const int64_t* labels, int64_t rows,
+                     int64_t cols, Clip c, int64_t grid, hipStream_t s) {
+  void* args[] = {&x, &y, &labels, &rows, &cols, &c};
   return launch(reinterpret_cast<const void*>(&k_block_row<1024, V, VEC4, EM>), grid, 1024,
                 args, s);
 }
 
 template <bool VEC4, int EM>
 hipError_t dispatch_block(const softmax_plan_t& p, const float* x, float* y,
-                          int64_t rows, int64_t cols, Clip c, hipStream_t s) {
+                          const int64_t* labels, int64_t rows, int64_t cols, Clip c,
+                          hipStream_t s) {
   switch (p.elems_per_lane / 4) {
-    case 2: return run_block<2, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
-    case 4: return run_block<4, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
-    default: return run_block<8, VEC4, EM>(x, y, rows, cols, c, p.grid, s);
+    case 2: return run_block<2, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
+    case 4: return run_block<4, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
+    default: return run_block<8, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
   }
 }
 
+// The output and labels of rows r0.. of a call: y advances by a row of
+// outputs, or by one loss per row for NLL outputs (whose labels advance
+// with it).
+template <int EM>
+float* out_rows(float* y, int64_t r0, int64_t cols) {
+  return EM == kNllOut ? y + r0 : y + r0 * cols;
+}
+template <int EM>
+const int64_t* label_rows(const int64_t* labels, int64_t r0) {
+  return EM == kNllOut ? labels + r0 : labels;
+}
+
 template <bool VEC4, int EM>
-hipError_t run_split(const float* x, float* y, float2* ws, int64_t rows, int64_t cols,
-                     int64_t chunks, Clip c, hipStream_t s) {
+hipError_t run_split(const float* x, float* y, const int64_t* labels, float2* ws,
+                     int64_t rows, int64_t cols, int64_t chunks, Clip c, hipStream_t s) {
   const int64_t rows_per_batch = std::max<int64_t>(1, kWorkspacePairs / chunks);
   for (int64_t r0 = 0; r0 < rows; r0 += rows_per_batch) {
     int64_t nb = std::min(rows_per_batch, rows - r0);
     const float* xb = x + r0 * cols;
-    float* yb = y + r0 * cols;
+    float* yb = out_rows<EM>(y, r0, cols);
+    const int64_t* lb = label_rows<EM>(labels, r0);
     const int64_t grid = std::min(nb * chunks, kMaxGrid);
     void* a1[] = {&xb, &ws, &nb, &cols, &chunks, &c};
     hipError_t e = launch(
@@ -253,7 +269,7 @@ hipError_t run_split(const float* x, float* y, float2* ws, int64_t rows, int64_t
         grid, kSplitThreads, a1, s);
     if (e != hipSuccess) return e;
     const float2* wsc = ws;
-    void* a2[] = {&xb, &yb, &wsc, &nb, &cols, &chunks, &c};
+    void* a2[] = {&xb, &yb, &lb, &wsc, &nb, &cols, &chunks, &c};
     e = launch(
         reinterpret_cast<const void*>(&k_split_apply<kSplitThreads, kSplitV, VEC4, EM>),
         grid, kSplitThreads, a2, s);
@@ -263,8 +279,9 @@ hipError_t run_split(const float* x, float* y, float2* ws, int64_t rows, int64_t
 }
 
 template <int V, bool VEC4, int EM>
-hipError_t run_onepass(const float* x, float* y, char* ws, int64_t rows, int64_t cols,
-                       int64_t chunks, int64_t max_blocks, Clip c, hipStream_t s) {
+hipError_t run_onepass(const float* x, float* y, const int64_t* labels, char* ws,
+                       int64_t rows, int64_t cols, int64_t chunks, int64_t max_blocks, Clip c,
+                       hipStream_t s) {
   unsigned long long* part = reinterpret_cast<unsigned long long*>(ws + kSlotsOffset);
   unsigned* depart = reinterpret_cast<unsigned*>(ws + kDepartOffset);
   const int64_t rows_per_launch = max_blocks / chunks;
@@ -272,8 +289,9 @@ hipError_t run_onepass(const float* x, float* y, char* ws, int64_t rows, int64_t
   for (int64_t r0 = 0; r0 < rows; r0 += rows_per_launch) {
     const int64_t nb = std::min(rows_per_launch, rows - r0);
     const float* xb = x + r0 * cols;
-    float* yb = y + r0 * cols;
-    void* args[] = {&xb, &yb, &part, &depart, &cols, &ichunks, &c};
+    float* yb = out_rows<EM>(y, r0, cols);
+    const int64_t* lb = label_rows<EM>(labels, r0);
+    void* args[] = {&xb, &yb, &lb, &part, &depart, &cols, &ichunks, &c};
     hipError_t e = launch(
         reinterpret_cast<const void*>(&k_split_onepass<kOnePassThreads, V, VEC4, EM>),
         nb * chunks, kOnePassThreads, args, s);
@@ -344,22 +362,32 @@ int workspace_for(int dev, hipStream_t s, bool capturing, char** out) {
 }
 
 template <bool VEC4, int EM>
-hipError_t split_launch(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
-                        int64_t cols, char* ws, Clip c, hipStream_t s) {
+hipError_t split_launch(const softmax_plan_t& p, const float* x, float* y,
+                        const int64_t* labels, int64_t rows, int64_t cols, char* ws, Clip c,
+                        hipStream_t s) {
   // Plans with at most kOnePassMaxChunks chunks per row are one-pass (their
   // chunk size is told by elems_per_lane); longer rows are two-pass.
   const int64_t g = p.chunks_per_row;
   if (g <= kOnePassMaxChunks && p.elems_per_lane == 4 * kOnePassVSmall)
-    return run_onepass<kOnePassVSmall, VEC4, EM>(x, y, ws, rows, cols, g,
+    return run_onepass<kOnePassVSmall, VEC4, EM>(x, y, labels, ws, rows, cols, g,
                                                    kOnePassMaxBlocksSmall, c, s);
   if (g <= kOnePassMaxChunks)
-    return run_onepass<kOnePassVLarge, VEC4, EM>(x, y, ws, rows, cols, g,
+    return run_onepass<kOnePassVLarge, VEC4, EM>(x, y, labels, ws, rows, cols, g,
                                                    kOnePassMaxBlocksLarge, c, s);
-  return run_split<VEC4, EM>(x, y, reinterpret_cast<float2*>(ws), rows, cols, g, c, s);
+  return run_split<VEC4, EM>(x, y, labels, reinterpret_cast<float2*>(ws), rows, cols, g, c,
+                             s);
 }
 
-int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
-               int64_t cols, int dev, Clip c, int em, hipStream_t s) {
+template <int EM>
+hipError_t split_mode(const softmax_plan_t& p, const float* x, float* y,
+                      const int64_t* labels, int64_t rows, int64_t cols, char* ws, Clip c,
+                      hipStream_t s) {
+  return p.vec_width == 4 ? split_launch<true, EM>(p, x, y, labels, rows, cols, ws, c, s)
+                          : split_launch<false, EM>(p, x, y, labels, rows, cols, ws, c, s);
+}
+
+int split_call(const softmax_plan_t& p, const float* x, float* y, const int64_t* labels,
+               int64_t rows, int64_t cols, int dev, Clip c, int em, hipStream_t s) {
   if (dev < 0 || dev >= kMaxDevices) return SOFTMAX_ERR_INVALID_ARG;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
   hipError_t e = hipStreamIsCapturing(s, &cap);
@@ -371,42 +399,48 @@ int split_call(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
     if (rc != SOFTMAX_OK) return rc;
   }
   switch (em) {
-    case kExpWide:
-      e = p.vec_width == 4 ? split_launch<true, kExpWide>(p, x, y, rows, cols, ws, c, s)
-                           : split_launch<false, kExpWide>(p, x, y, rows, cols, ws, c, s);
-      break;
-    case kExpFast:
-      e = p.vec_width == 4 ? split_launch<true, kExpFast>(p, x, y, rows, cols, ws, c, s)
-                           : split_launch<false, kExpFast>(p, x, y, rows, cols, ws, c, s);
-      break;
-    case kLogOut:
-      e = p.vec_width == 4 ? split_launch<true, kLogOut>(p, x, y, rows, cols, ws, c, s)
-                           : split_launch<false, kLogOut>(p, x, y, rows, cols, ws, c, s);
-      break;
-    default:
-      e = p.vec_width == 4 ? split_launch<true, kExpAccurate>(p, x, y, rows, cols, ws, c, s)
-                           : split_launch<false, kExpAccurate>(p, x, y, rows, cols, ws, c, s);
-      break;
+    case kExpWide: e = split_mode<kExpWide>(p, x, y, labels, rows, cols, ws, c, s); break;
+    case kExpFast: e = split_mode<kExpFast>(p, x, y, labels, rows, cols, ws, c, s); break;
+    case kLogOut: e = split_mode<kLogOut>(p, x, y, labels, rows, cols, ws, c, s); break;
+    case kNllOut: e = split_mode<kNllOut>(p, x, y, labels, rows, cols, ws, c, s); break;
+    default: e = split_mode<kExpAccurate>(p, x, y, labels, rows, cols, ws, c, s); break;
   }
   return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
 }
 
 template <int EM>
-hipError_t launch_rows(const softmax_plan_t& p, const float* x, float* y, int64_t rows,
-                       int64_t cols, Clip c, hipStream_t s) {
+hipError_t launch_rows(const softmax_plan_t& p, const float* x, float* y,
+                       const int64_t* labels, int64_t rows, int64_t cols, Clip c,
+                       hipStream_t s) {
   switch (p.kernel) {
     case SOFTMAX_KERNEL_PACKED:
-      return p.vec_width == 4 ? dispatch_packed<true, EM>(p, x, y, rows, cols, c, s)
-                              : dispatch_packed<false, EM>(p, x, y, rows, cols, c, s);
+      return p.vec_width == 4 ? dispatch_packed<true, EM>(p, x, y, labels, rows, cols, c, s)
+                              : dispatch_packed<false, EM>(p, x, y, labels, rows, cols, c, s);
     case SOFTMAX_KERNEL_WAVE_ROW:
-      return p.vec_width == 4 ? dispatch_wave<true, EM>(p, x, y, rows, cols, c, s)
-                              : dispatch_wave<false, EM>(p, x, y, rows, cols, c, s);
+      return p.vec_width == 4 ? dispatch_wave<true, EM>(p, x, y, labels, rows, cols, c, s)
+                              : dispatch_wave<false, EM>(p, x, y, labels, rows, cols, c, s);
     case SOFTMAX_KERNEL_BLOCK_ROW:
-      return p.vec_width == 4 ? dispatch_block<true, EM>(p, x, y, rows, cols, c, s)
-                              : dispatch_block<false, EM>(p, x, y, rows, cols, c, s);
+      return p.vec_width == 4 ? dispatch_block<true, EM>(p, x, y, labels, rows, cols, c, s)
+                              : dispatch_block<false, EM>(p, x, y, labels, rows, cols, c, s);
     default:
       return hipSuccess;
   }
+}
+
+// Every launch of one call in mode em, on a plan made for it.
+int launch_mode(const softmax_plan_t& p, const float* x, float* y, const int64_t* labels,
+                int64_t rows, int64_t cols, int dev, Clip c, int em, hipStream_t stream) {
+  if (p.kernel == SOFTMAX_KERNEL_SPLIT_ROW)
+    return split_call(p, x, y, labels, rows, cols, dev, c, em, stream);
+  hipError_t e;
+  switch (em) {
+    case kExpWide: e = launch_rows<kExpWide>(p, x, y, labels, rows, cols, c, stream); break;
+    case kExpFast: e = launch_rows<kExpFast>(p, x, y, labels, rows, cols, c, stream); break;
+    case kLogOut: e = launch_rows<kLogOut>(p, x, y, labels, rows, cols, c, stream); break;
+    case kNllOut: e = launch_rows<kNllOut>(p, x, y, labels, rows, cols, c, stream); break;
+    default: e = launch_rows<kExpAccurate>(p, x, y, labels, rows, cols, c, stream); break;
+  }
+  return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
 }
 
 int check_pointers(const float* x, const float* y, int64_t n_elems, int* dev) {
@@ -431,17 +465,8 @@ int softmax_rows(const float* x, float* y, int64_t rows, int64_t cols, Clip c, i
   int dev = 0;
   rc = check_pointers(x, y, rows * cols, &dev);
   if (rc != SOFTMAX_OK) return rc;
-
-  const softmax_plan_t p = make_plan(x, y, rows, cols);
-  if (p.kernel == SOFTMAX_KERNEL_SPLIT_ROW) return split_call(p, x, y, rows, cols, dev, c, em, stream);
-  hipError_t e;
-  switch (em) {
-    case kExpWide: e = launch_rows<kExpWide>(p, x, y, rows, cols, c, stream); break;
-    case kExpFast: e = launch_rows<kExpFast>(p, x, y, rows, cols, c, stream); break;
-    case kLogOut: e = launch_rows<kLogOut>(p, x, y, rows, cols, c, stream); break;
-    default: e = launch_rows<kExpAccurate>(p, x, y, rows, cols, c, stream); break;
-  }
-  return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
+  return launch_mode(make_plan(x, y, rows, cols), x, y, nullptr, rows, cols, dev, c, em,
+                     stream);
 }
 
 }  // namespace
@@ -486,6 +511,35 @@ SOFTMAX_API int softmax_log_fwd(const float* x, float* y, int64_t rows, int64_t 
   const int rc = make_clip(clip_lo, &c, &wide);
   if (rc != SOFTMAX_OK) return rc;
   return softmax_rows(x, y, rows, cols, c, kLogOut, stream);
+}
+
+SOFTMAX_API int softmax_nll_fwd(const float* x, const int64_t* labels, float* loss,
+                                int64_t rows, int64_t cols, float clip_lo,
+                                hipStream_t stream) {
+  Clip c;
+  bool wide = false;
+  int rc = make_clip(clip_lo, &c, &wide);
+  if (rc != SOFTMAX_OK) return rc;
+  rc = check_sizes(rows, cols);
+  if (rc != SOFTMAX_OK) return rc;
+  if (rows == 0) return SOFTMAX_OK;
+  if (cols == 0) return SOFTMAX_ERR_INVALID_ARG;  // no row has a valid label
+  if (x == nullptr || labels == nullptr || loss == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+  if (rows > INT64_MAX / 8) return SOFTMAX_ERR_INVALID_ARG;
+  const int64_t xbytes = rows * cols * 4;
+  const int64_t lbytes = rows * 8;
+  const int64_t obytes = rows * 4;
+  if (ranges_overlap(loss, obytes, x, xbytes) || ranges_overlap(loss, obytes, labels, lbytes))
+    return SOFTMAX_ERR_INVALID_ARG;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e);
+  if ((rc = check_device_range(x, xbytes, dev)) != SOFTMAX_OK) return rc;
+  if ((rc = check_device_range(labels, lbytes, dev)) != SOFTMAX_OK) return rc;
+  if ((rc = check_device_range(loss, obytes, dev)) != SOFTMAX_OK) return rc;
+  // The plan's access width follows x alone: the losses are 32-bit stores.
+  return launch_mode(make_plan(x, x, rows, cols), x, loss, labels, rows, cols, dev, c, kNllOut,
+                     stream);
 }
 
 SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols,

@@ -25,7 +25,7 @@ def declared_functions():
 def test_header_declares_entry_points():
     names = declared_functions()
     for n in ("softmax_fwd", "softmax_fwd_clip", "softmax_fwd_approx", "softmax_log_fwd",
-              "softmax_attention_fwd",
+              "softmax_nll_fwd", "softmax_attention_fwd",
               "softmax_strerror",
               "softmax_last_hip_error", "softmax_plan", "softmax_exp_probe",
               "softmax_copy_probe"):
@@ -211,3 +211,24 @@ def test_attention_arguments_rejected_before_any_hip_call():
     assert _attn(0, 0, 0, 0, 0, 50, 50, 200, 200) == sm.OK
     assert _attn(0, 0, 0, 0, 2, 0, 50, 200, 200) == sm.OK
     assert _attn(0, 0, 0, 0, 2, 50, 50, 200, 0) == sm.OK
+
+
+def test_nll_arguments_rejected_before_any_hip_call():
+    """Bad sizes, bounds, null or overlapping pointers, and rows with no
+    classes return SOFTMAX_ERR_INVALID_ARG before any HIP call."""
+    X, L, O = 1 << 32, 2 << 32, 3 << 32     # far apart, never dereferenced
+    bad = sm.ERR_INVALID_ARG
+    nll = sm.softmax_nll_fwd_ptr
+    assert nll(X, L, O, -1, 10, -64.0, 0) == bad
+    assert nll(X, L, O, 10, -1, -64.0, 0) == bad
+    assert nll(X, L, O, 10, 0, -64.0, 0) == bad                 # no valid label exists
+    assert nll(X, L, O, 1 << 62, 2, -64.0, 0) == bad            # bytes overflow
+    assert nll(X, L, O, 10, 10, -1.0, 0) == bad                 # clip bound above -48
+    assert nll(X, L, O, 10, 10, float("nan"), 0) == bad
+    assert nll(0, L, O, 10, 10, -64.0, 0) == bad
+    assert nll(X, 0, O, 10, 10, -64.0, 0) == bad
+    assert nll(X, L, 0, 10, 10, -64.0, 0) == bad
+    assert nll(X, L, X + 396, 10, 10, -64.0, 0) == bad          # loss overlaps x
+    assert nll(X, L, L + 76, 10, 10, -64.0, 0) == bad           # loss overlaps labels
+    assert nll(0, 0, 0, 0, 10, -64.0, 0) == sm.OK               # no rows: nothing to do
+    assert nll(0, 0, 0, 0, 0, float("-inf"), 0) == sm.OK

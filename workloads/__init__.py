@@ -26,7 +26,8 @@ from dataclasses import dataclass
 import numpy as np
 
 __all__ = ["Workload", "WORKLOADS", "generate", "sha256_f32", "random_logits",
-           "AttentionWorkload", "ATTENTION_WORKLOADS", "generate_qkv", "random_qkv"]
+           "generate_labels", "AttentionWorkload", "ATTENTION_WORKLOADS", "generate_qkv",
+           "random_qkv"]
 
 
 @dataclass(frozen=True)
@@ -131,6 +132,15 @@ def sha256_f32(x: np.ndarray) -> str:
     """SHA-256 of the little-endian float32 bytes of a C-contiguous array."""
     a = np.ascontiguousarray(x, dtype="<f4")
     return hashlib.sha256(a.tobytes()).hexdigest()
+
+
+def generate_labels(key, seed_offset: int = 1000) -> np.ndarray:
+    """int64 [rows] class labels for a workload, uniform over [0, cols), from
+    their own seeded stream (the workload's seed + seed_offset), so that the
+    logits are the same with or without labels."""
+    w = _resolve(key)
+    rng = np.random.default_rng(w.seed + seed_offset)
+    return np.ascontiguousarray(rng.integers(0, w.cols, size=w.rows, dtype=np.int64))
 
 
 def random_logits(rows: int, cols: int, seed: int, kind: str = "normal",
