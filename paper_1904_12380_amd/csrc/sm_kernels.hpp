@@ -72,9 +72,8 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 // -inf: they take part in the max as a neutral value and their clipped
 // exponential (e^lo with lo <= -48, or 0 with no clip) changes a row sum of
 // at least 1 by under 4096 e^-48 < 1e-17 relative, so no per-element mask
-// is needed later.  Strip j covers
-// [4*stride*j, 4*stride*(j+1)); when all of it is inside the segment (a
-// uniform test) no lane is masked.
+// is needed later.  Strip j covers [4*stride*j, 4*stride*(j+1)); when all
+// of it is inside the segment (a uniform test) no lane is masked.
 template <int V, bool VEC4>
 __device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* p, int lane_off,
                                            int stride, int lim) {
@@ -106,6 +105,37 @@ __device__ __forceinline__ void load_strip(float (&v)[4 * V], const float* p, in
   }
 }
 
+// The same loads with no control flow between them (a column past the
+// segment loads column 0 and is then replaced by -inf), for the online
+// reduction below: each use then waits only for its own loads, not for the
+// whole strip.  It keeps one offset register per strip live, so it is used
+// only where the registers allow.  With 128-bit access lim is a multiple of
+// 4 (a segment's four columns are all inside it or all past it).
+template <int V, bool VEC4>
+__device__ __forceinline__ void load_strip_flat(float (&v)[4 * V], const float* p,
+                                                int lane_off, int stride, int lim) {
+  if constexpr (VEC4) {
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const int c = 4 * (lane_off + stride * j);
+      const bool in = c < lim;
+      const f32x4 q = ld_stream(p + (in ? c : 0));
+      v[4 * j + 0] = in ? q.x : kNegInf;
+      v[4 * j + 1] = in ? q.y : kNegInf;
+      v[4 * j + 2] = in ? q.z : kNegInf;
+      v[4 * j + 3] = in ? q.w : kNegInf;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4 * V; ++i) {
+      const int c = lane_off + stride * i;
+      const bool in = c < lim;
+      const float q = __builtin_nontemporal_load(p + (in ? c : 0));
+      v[i] = in ? q : kNegInf;
+    }
+  }
+}
+
 // This lane's pairwise partial sum of the clipped exponentials.  For
 // probability outputs v is replaced by the exponentials; for log and NLL
 // outputs (keeps_logits) v keeps the logits, which the output step needs.
@@ -126,6 +156,63 @@ __device__ __forceinline__ float exp_strip(float (&v)[N], RowShift rs) {
     for (int i = 0; i < N; ++i) v[i] = exp_shift_clip<MODE>(v[i], rs);
     return tree_sum(v);
   }
+}
+
+// Lane-local online reduction of the logits in v, for the modes that keep
+// them (log and NLL outputs) in the one-pass split kernel, whose chunks
+// hold 32 values per lane (on shorter strips the extra rescaling costs more
+// than the overlap gains): v is taken in sub-strips of 8 elements (two
+// 128-bit loads) in load order, each reduced against the running lane max
+// as soon as its own loads have returned, so the exponentials of the first
+// columns overlap the arrival of the last instead of waiting for the whole
+// row.  Returns the lane max m (-inf when every element is) and
+// s = sum exp(max(x - m, lo)) over the lane's elements (shift 0 while m is
+// -inf, where every term is the clipped value).  When the max grows the
+// running sum is rescaled by the clipped exponential of the step; like a
+// clip taken against a partial max, that changes S by at most cols * e^lo
+// relative (under 1e-10 for lo <= -48).
+template <int N, int SUB_MAX = 8>
+__device__ __forceinline__ float2 lane_online(const float (&v)[N], Clip clip) {
+  constexpr int SUB = N < SUB_MAX ? N : SUB_MAX;
+  static_assert(N % SUB == 0, "whole sub-strips");
+  float m = kNegInf;
+  float s = 0.0f;
+#pragma unroll
+  for (int k0 = 0; k0 < N; k0 += SUB) {
+    float mk = v[k0];
+#pragma unroll
+    for (int i = 1; i < SUB; ++i) mk = fmaxf(mk, v[k0 + i]);
+    const float m_new = fmaxf(m, mk);
+    const RowShift rs = row_shift(m_new == kNegInf ? 0.0f : m_new, clip);
+    // two interleaved partials keep few exponentials live at once
+    float p0 = exp_shift_clip<kExpAccurate>(v[k0], rs);
+    float p1 = SUB > 1 ? exp_shift_clip<kExpAccurate>(v[k0 + 1], rs) : 0.0f;
+#pragma unroll
+    for (int i = 2; i < SUB; i += 2) {
+      p0 = p0 + exp_shift_clip<kExpAccurate>(v[k0 + i], rs);
+      if (i + 1 < SUB) p1 = p1 + exp_shift_clip<kExpAccurate>(v[k0 + i + 1], rs);
+    }
+    const float sk = p0 + p1;
+    if (k0 == 0) {
+      s = sk;
+    } else {
+      const float f = m == kNegInf ? 1.0f : exp_shift_clip<kExpAccurate>(m, rs);
+      s = s * f + sk;
+    }
+    m = m_new;
+    // Materialise this sub-strip's running (m, s) here: otherwise the
+    // compiler sinks its exponentials to the next sub-strip and takes every
+    // max first, which waits for all of the row's loads.
+    asm volatile("" : "+v"(s), "+v"(m));
+  }
+  return make_float2(m, s);
+}
+
+// This lane's share of the row sum against the row max M (rs), from its
+// lane_online result: s * exp(max(m - M, lo)), or s itself for a lane with
+// no finite element.
+__device__ __forceinline__ float lane_share(float2 ms, RowShift rs) {
+  return ms.x == kNegInf ? ms.y : ms.y * exp_shift_clip<kExpAccurate>(ms.x, rs);
 }
 
 // Stores out(v[i]) for the columns of the strip that are inside the row.
@@ -190,31 +277,44 @@ __device__ __forceinline__ int held_index(int lc, int lane_off, int stride) {
   }
 }
 
-// NLL output: the lane holding segment column lc writes *out = ln S - c,
-// minus that column's log output.  Other lanes store nothing.
-template <int V, bool VEC4>
-__device__ __forceinline__ void nll_strip(const float (&v)[4 * V], RowShift rs, float s, int lc,
-                                          float* out, int lane_off, int stride) {
-  const int idx = held_index<V, VEC4>(lc, lane_off, stride);
-  float xl = 0.0f;
+// What a lane contributes to an NLL output: the label's logit, if this lane
+// holds its column (`found`), and whether it must write NaN for a label
+// outside the row (`bad`: one thread of the row's first segment).
+struct LabelPick {
+  float x;
+  bool found;
+  bool bad;
+};
+
+// Picks the label's logit out of this lane's v (laid out as in load_strip)
+// for the segment [c0, c0 + lim).  Taken right after the loads, so that v
+// need not stay live through the row reductions.  Other modes pick nothing.
+template <int V, bool VEC4, int MODE>
+__device__ __forceinline__ LabelPick pick_label(const float (&v)[4 * V], int64_t label,
+                                                int64_t cols, int64_t c0, int lim, int lane_off,
+                                                int stride, bool first) {
+  LabelPick p{0.0f, false, false};
+  if constexpr (MODE == kNllOut) {
+    const int idx = held_index<V, VEC4>(seg_label(label, c0, lim), lane_off, stride);
 #pragma unroll
-  for (int i = 0; i < 4 * V; ++i) xl = idx == i ? v[i] : xl;
-  if (idx >= 0) *out = -log_out(xl, rs, log_of_sum(s));
+    for (int i = 0; i < 4 * V; ++i) p.x = idx == i ? v[i] : p.x;
+    p.found = idx >= 0;
+    p.bad = first && (label < 0 || label >= cols);
+  }
+  return p;
 }
 
 // The output step of the segment [c0, c0 + lim) of `row`: the row's
 // outputs (probabilities or logs) into y + row * cols + c0, or for NLL
-// outputs the one loss y[row], written by the lane that holds the label's
-// column; `first` (one thread of the row's first segment) writes NaN for a
-// label outside [0, cols).
+// outputs the one loss y[row] = ln S - c_label, written by the lane that
+// picked the label's logit (NaN for a label outside [0, cols)).
 template <int V, bool VEC4, int MODE>
 __device__ __forceinline__ void finish_row(const float (&v)[4 * V], RowShift rs, float s,
                                            float* y, int64_t row, int64_t cols, int64_t c0,
-                                           int lim, int64_t label, int lane_off, int stride,
-                                           bool first) {
+                                           int lim, LabelPick pick, int lane_off, int stride) {
   if constexpr (MODE == kNllOut) {
-    nll_strip<V, VEC4>(v, rs, s, seg_label(label, c0, lim), y + row, lane_off, stride);
-    if (first && (label < 0 || label >= cols)) y[row] = __builtin_nanf("");
+    if (pick.found) y[row] = -log_out(pick.x, rs, log_of_sum(s));
+    if (pick.bad) y[row] = __builtin_nanf("");
   } else {
     store_row<V, VEC4, MODE>(v, rs, s, y + row * cols + c0, lane_off, stride, lim);
   }
@@ -404,9 +504,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     const int lim = static_cast<int>(cols);
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, lane, 64, lim);
+    const LabelPick pick = pick_label<V, VEC4, MODE>(v, label, cols, 0, lim, lane, 64, lane == 0);
     const RowShift rs = row_shift(seg_max<64>(array_max(v)), clip);
     const float s = seg_sum<64>(exp_strip<MODE>(v, rs));
-    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, label, lane, 64, lane == 0);
+    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, pick, lane, 64);
   }
 }
 
@@ -426,9 +527,10 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y,
     const int lim = static_cast<int>(cols);
     float v[4 * V];
     load_strip<V, VEC4>(v, xr, tid, NT, lim);
+    const LabelPick pick = pick_label<V, VEC4, MODE>(v, label, cols, 0, lim, tid, NT, tid == 0);
     const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max), clip);
     const float s = block_sum<NW>(exp_strip<MODE>(v, rs), red_sum);
-    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, label, tid, NT, tid == 0);
+    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, pick, tid, NT);
   }
 }
 
@@ -508,8 +610,9 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
 #pragma unroll
       for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip<MODE>(v[i], rs);
     }
-    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, c0, lim, label, tid, NT,
-                              g == 0 && tid == 0);
+    const LabelPick pick =
+        pick_label<V, VEC4, MODE>(v, label, cols, c0, lim, tid, NT, g == 0 && tid == 0);
+    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, c0, lim, pick, tid, NT);
   }
 }
 
@@ -574,10 +677,23 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
   const int lim = seg_len(cols, c0, CH);
 
   float v[4 * V];
-  load_strip<V, VEC4>(v, xr, tid, NT, lim);
-  const float m = block_max<NW>(array_max(v), red_max);
+  if constexpr (keeps_logits<MODE>())
+    load_strip_flat<V, VEC4>(v, xr, tid, NT, lim);
+  else
+    load_strip<V, VEC4>(v, xr, tid, NT, lim);
+  float m;
+  float s;
+  LabelPick pick{0.0f, false, false};
+  if constexpr (keeps_logits<MODE>()) {
+    const float2 ms = lane_online(v, clip);
+    pick = pick_label<V, VEC4, MODE>(v, label, cols, c0, lim, tid, NT, g == 0 && tid == 0);
+    m = block_max<NW>(ms.x, red_max);
+    s = block_sum<NW>(lane_share(ms, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
+  } else {
+    m = block_max<NW>(array_max(v), red_max);
+    s = block_sum<NW>(exp_strip<MODE>(v, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
+  }
   const bool empty_max = (m == kNegInf);
-  float s = block_sum<NW>(exp_strip<MODE>(v, row_shift(empty_max ? 0.0f : m, clip)), red_sum);
   if (empty_max) s = static_cast<float>(lim);
 
   if (tid == 0) {
@@ -635,7 +751,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     // v still holds the logits: y = c - ln S (or the label's loss) against
     // the row's M.
     finish_row<V, VEC4, MODE>(v, row_shift(bcast[0], clip), bcast[1], y, row, cols, c0, lim,
-                              label, tid, NT, g == 0 && tid == 0);
+                              pick, tid, NT);
   } else {
     float* yr = y + row * cols + c0;
     const float scale = bcast[0];
