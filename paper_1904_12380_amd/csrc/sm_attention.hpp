@@ -290,13 +290,12 @@ __global__ __launch_bounds__(256) void k_attention(const float* q, const float* 
 // wavefront, and the matrix-op operands come from LDS.  Two workgroups fit
 // per CU, so one copies while the other computes.
 constexpr int kAttnLdsBytes = 80 * 1024;
-constexpr int kAttnMaxDQ = 256;  // d up to this keeps Q in registers
+constexpr int kAttnMaxDQ = 224;  // d up to this keeps Q in registers (14 blocks)
 
 template <int NKT, bool WIDE>
-__global__ __launch_bounds__(256) void k_attention_lds(const float* q, const float* k,
-                                                       const float* v, float* o,
-                                                       int64_t batch, int lq, int lk, int d,
-                                                       int dv, float scale, Clip clip) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_attention_lds(
+    const float* q, const float* k, const float* v, float* o, int64_t batch, int lq, int lk,
+    int d, int dv, float scale, Clip clip) {
   __shared__ __attribute__((aligned(16))) float lds[kAttnLdsBytes / 4];
   float* lk_s = lds;                       // K_b: lk x d
   float* lv_s = lds + lk * d;              // V_b: lk x dv (16-byte aligned: d % 4 == 0)
@@ -352,30 +351,41 @@ __global__ __launch_bounds__(256) void k_attention_lds(const float* q, const flo
       f32x4m acc[NKT];
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt) acc[kt] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+      // Keys past lk read row 0: their scores are garbage (even NaN) but
+      // the softmax below masks them.  Columns t past d would read the next
+      // row, and 0 * NaN is NaN, so those operands are zeroed.
       int krow[NKT];
-      bool k_ok[NKT];
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt) {
         const int key = 16 * kt + j;
-        k_ok[kt] = kt < NKT - 1 || key < lk;
-        krow[kt] = (k_ok[kt] ? key : 0) * d + 4 * g;
+        krow[kt] = ((kt < NKT - 1 || key < lk) ? key : 0) * d + 4 * g;
+      }
+      // The next block's K operands are read while this block's matrix ops
+      // run; the d mask is applied at use, so no wait comes early.
+      f32x4m kc[NKT], kn[NKT];
+      if (nblk > 0) {
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+          kc[kt] = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt]);
       }
 #pragma unroll
       for (int blk = 0; blk < QB; ++blk) {
         if (blk < nblk) {                        // uniform
-          const bool t_ok = 16 * blk + 4 * g < d;
-          f32x4m kf[NKT];
+          if (blk + 1 < nblk) {
 #pragma unroll
-          for (int kt = 0; kt < NKT; ++kt) {
-            const f32x4m x = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt] + 16 * blk);
-            kf[kt] = (k_ok[kt] & t_ok) ? x : f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int kt = 0; kt < NKT; ++kt)
+              kn[kt] = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt] + 16 * (blk + 1));
           }
+          __builtin_amdgcn_sched_barrier(0);
+          const bool t_ok = 16 * blk + 4 * g < d;
 #pragma unroll
           for (int s = 0; s < 4; ++s) {
 #pragma unroll
             for (int kt = 0; kt < NKT; ++kt)
-              acc[kt] = mfma16x16x4(kf[kt][s], qf[blk][s], acc[kt]);
+              acc[kt] = mfma16x16x4(t_ok ? kc[kt][s] : 0.0f, qf[blk][s], acc[kt]);
           }
+#pragma unroll
+          for (int kt = 0; kt < NKT; ++kt) kc[kt] = kn[kt];
         }
       }
 
@@ -413,31 +423,49 @@ __global__ __launch_bounds__(256) void k_attention_lds(const float* q, const flo
 
       // ---- 2c. O = P V, V from LDS ------------------------------------------
       // Contraction step i = 4 kt + r: key 16 kt + 4 g + r.  Keys past lk
-      // read row 0 and are zeroed (their weight is 0, but a stale value
-      // could be NaN).
-      int vrow[4 * NKT];
-      bool v_ok[4 * NKT];
-#pragma unroll
-      for (int i = 0; i < 4 * NKT; ++i) {
-        const int key = 16 * (i >> 2) + 4 * g + (i & 3);
-        v_ok[i] = (i >> 2) < NKT - 1 || key < lk;
-        vrow[i] = (v_ok[i] ? key : 0) * dv;
-      }
+      // (only in the last key tile) read row 0 and are zeroed: their weight
+      // is 0, but a stale value could be NaN.
+      auto v_ok = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + 4 * g + (i & 3) < lk; };
+      auto vrow = [&](int i) { return (v_ok(i) ? 16 * (i >> 2) + 4 * g + (i & 3) : 0) * dv; };
       const __amdgpu_buffer_rsrc_t ro =
           make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
       const int orow = 4 * g * dv * 4;
       const int nfull = dv >> 6;
+      // Each 64-column block in four quarters of NKT contraction steps: the
+      // next quarter's V rows (the next block's first, after the last) are
+      // read while this quarter's matrix ops run; the key mask is applied
+      // at use.
+      f32x4m vq[2][NKT];
+      if (nfull > 0) {
+#pragma unroll
+        for (int i = 0; i < NKT; ++i)
+          vq[0][i] = *reinterpret_cast<const f32x4m*>(lv_s + vrow(i) + 4 * j);
+      }
       for (int cb = 0; cb < nfull; ++cb) {
         const int c = 64 * cb + 4 * j;
         f32x4m oacc[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) oacc[u] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int i = 0; i < 4 * NKT; ++i) {
-          const f32x4m x = *reinterpret_cast<const f32x4m*>(lv_s + vrow[i] + c);
-          const f32x4m vf = v_ok[i] ? x : f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int qi = 0; qi < 4; ++qi) {
+          if (qi < 3) {
 #pragma unroll
-          for (int u = 0; u < 4; ++u) oacc[u] = mfma16x16x4(e[i], vf[u], oacc[u]);
+            for (int i = 0; i < NKT; ++i)
+              vq[(qi + 1) & 1][i] =
+                  *reinterpret_cast<const f32x4m*>(lv_s + vrow((qi + 1) * NKT + i) + c);
+          } else if (cb + 1 < nfull) {
+#pragma unroll
+            for (int i = 0; i < NKT; ++i)
+              vq[0][i] = *reinterpret_cast<const f32x4m*>(lv_s + vrow(i) + c + 64);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int i = 0; i < NKT; ++i) {
+            const int st = qi * NKT + i;
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+              oacc[u] = mfma16x16x4(e[st], v_ok(st) ? vq[qi & 1][i][u] : 0.0f, oacc[u]);
+          }
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -453,8 +481,8 @@ __global__ __launch_bounds__(256) void k_attention_lds(const float* q, const flo
         f32x4m oa = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int i = 0; i < 4 * NKT; ++i) {
-          const float x = lv_s[vrow[i] + (c_ok ? c : 0)];
-          oa = mfma16x16x4(e[i], (v_ok[i] & c_ok) ? x : 0.0f, oa);
+          const float x = lv_s[vrow(i) + (c_ok ? c : 0)];
+          oa = mfma16x16x4(e[i], (v_ok(i) & c_ok) ? x : 0.0f, oa);
         }
         float* orow_p = o + (b * lq + q0 + 4 * g) * static_cast<int64_t>(dv) + c;
 #pragma unroll
