@@ -27,6 +27,9 @@ constexpr int64_t kPackedMaxCols = 64;
 constexpr int64_t kPackedBlocksPerCU = 6;
 constexpr int64_t kDeviceCUs = 256;
 constexpr int64_t kWaveRowMaxCols = 4096;
+// With 32-bit access, 64 values per lane need more registers than a
+// wavefront has (the kernel would spill): such rows go to k_block_row.
+constexpr int64_t kWaveRowMaxColsScalar = 2048;
 constexpr int64_t kBlockRowMaxCols = 32768;
 
 // Split rows, one-pass kernel: 512-thread workgroups holding 32 columns per
@@ -119,7 +122,7 @@ softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t c
     const int64_t tile = 256 / g;
     p.grid = std::min(ceil_div(rows, tile), kPackedBlocksPerCU * kDeviceCUs);
     p.launches = 1;
-  } else if (cols <= kWaveRowMaxCols) {
+  } else if (cols <= (vec_rows ? kWaveRowMaxCols : kWaveRowMaxColsScalar)) {
     const int64_t v = pow2_at_least(ceil_div(cols, 256));
     p.kernel = SOFTMAX_KERNEL_WAVE_ROW;
     p.vec_width = vec_rows ? 4 : 1;
@@ -143,7 +146,10 @@ softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t c
     p.workspace_bytes = kWorkspaceBytes;
     const int64_t gs = ceil_div(cols, kOnePassChunkSmall);
     const int64_t gl = ceil_div(cols, kOnePassChunkLarge);
-    if (gs <= kOnePassMaxChunks || gl <= kOnePassMaxChunks) {
+    // The large chunks (64 values per lane) are taken with 128-bit access
+    // only: with 32-bit access they would spill, and such rows take the
+    // two-pass path instead.
+    if (gs <= kOnePassMaxChunks || (vec_rows && gl <= kOnePassMaxChunks)) {
       // One pass: whole rows per launch, all workgroups resident together.
       const bool small = gs <= kOnePassMaxChunks;
       const int64_t g1 = small ? gs : gl;
@@ -218,7 +224,10 @@ hipError_t dispatch_wave(const softmax_plan_t& p, const float* x, float* y,
     case 2: return run_wave<2, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
     case 4: return run_wave<4, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
     case 8: return run_wave<8, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
-    default: return run_wave<16, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
+    default:
+      // 64 values per lane only with 128-bit access (see make_plan).
+      if constexpr (VEC4) return run_wave<16, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
+      return hipErrorInvalidValue;
   }
 }
 
@@ -371,9 +380,11 @@ hipError_t split_launch(const softmax_plan_t& p, const float* x, float* y,
   if (g <= kOnePassMaxChunks && p.elems_per_lane == 4 * kOnePassVSmall)
     return run_onepass<kOnePassVSmall, VEC4, EM>(x, y, labels, ws, rows, cols, g,
                                                    kOnePassMaxBlocksSmall, c, s);
-  if (g <= kOnePassMaxChunks)
-    return run_onepass<kOnePassVLarge, VEC4, EM>(x, y, labels, ws, rows, cols, g,
-                                                   kOnePassMaxBlocksLarge, c, s);
+  if constexpr (VEC4) {
+    if (g <= kOnePassMaxChunks)
+      return run_onepass<kOnePassVLarge, VEC4, EM>(x, y, labels, ws, rows, cols, g,
+                                                     kOnePassMaxBlocksLarge, c, s);
+  }
   return run_split<VEC4, EM>(x, y, labels, reinterpret_cast<float2*>(ws), rows, cols, g, c,
                              s);
 }

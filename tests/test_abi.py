@@ -82,6 +82,12 @@ def test_cpu_tensor_is_rejected():
     (3, 65, "wave_row", 1, dict(elems_per_lane=4)),
     (3, 4096, "wave_row", 4, dict(elems_per_lane=64)),
     (3, 4097, "block_row", 1, dict(elems_per_lane=8)),
+    # 32-bit access: at most 32 values per lane in a wavefront, and no
+    # one-pass large chunks (both would spill)
+    (3, 2047, "wave_row", 1, dict(elems_per_lane=32)),
+    (3, 2049, "block_row", 1, dict(elems_per_lane=8)),
+    (3, 4095, "block_row", 1, dict(elems_per_lane=8)),
+    (1, 1048579, "split_row", 1, dict(chunks_per_row=65, elems_per_lane=32, launches=2)),
     (3, 32769, "split_row", 1, dict(chunks_per_row=3, launches=1)),
     (300, 262144, "split_row", 4, dict(chunks_per_row=16, launches=5, grid=1024)),
     (1, 1048576, "split_row", 4, dict(chunks_per_row=64, elems_per_lane=32, launches=1)),

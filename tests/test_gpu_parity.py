@@ -321,9 +321,10 @@ def test_split_rows_several_one_pass_launches():
     assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
 
 
-@pytest.mark.parametrize("rows,cols", [(3, 1048577), (2, 2097152), (1, 1048576)])
+@pytest.mark.parametrize("rows,cols", [(3, 1048580), (2, 2097152), (1, 1048576)])
 def test_split_rows_large_chunks(rows, cols):
-    """Rows past 64 chunks of 16384 columns use 32768-column chunks."""
+    """Rows past 64 chunks of 16384 columns use 32768-column chunks (with
+    128-bit access; a ragged 128-bit tail at 1048580)."""
     log(f"[parity] split rows, large chunks {rows}x{cols}")
     p = sm.softmax_plan(rows, cols)
     assert p["kernel_name"] == "split_row" and p["launches"] == 1
@@ -341,6 +342,13 @@ def test_split_rows_two_pass_fallback():
     check_parity(x, run_gpu(x), "1x2097153")
     x = workloads.random_logits(3, cols, seed=7, kind="clip_heavy")
     check_parity(x, run_gpu(x), "3x2097153 clip-heavy")
+    # With 32-bit access (cols % 4 != 0) rows past 64 small chunks take the
+    # two-pass path rather than the large chunks.
+    cols = 1048577
+    p = sm.softmax_plan(3, cols)
+    assert p["kernel_name"] == "split_row" and p["launches"] == 2 and p["vec_width"] == 1
+    x = workloads.random_logits(3, cols, seed=8, kind="offset")
+    check_parity(x, run_gpu(x), "3x1048577 32-bit")
 
 
 @pytest.mark.parametrize("rows,cols", [(115200, 50), (4096, 1000), (512, 32768), (64, 262144)])
