@@ -427,6 +427,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       // is 0, but a stale value could be NaN.
       auto v_ok = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + 4 * g + (i & 3) < lk; };
       auto vrow = [&](int i) { return (v_ok(i) ? 16 * (i >> 2) + 4 * g + (i & 3) : 0) * dv; };
+      // A step whose smallest key (lane group 0) is past lk has zero weight
+      // in every lane: its matrix ops are skipped (a uniform branch; for
+      // DAM's 50 keys, 2 of the 16 steps).
+      auto step_live = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + (i & 3) < lk; };
       const __amdgpu_buffer_rsrc_t ro =
           make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
       const int orow = 4 * g * dv * 4;
@@ -462,9 +466,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
           for (int i = 0; i < NKT; ++i) {
             const int st = qi * NKT + i;
+            if (step_live(st)) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-              oacc[u] = mfma16x16x4(e[st], v_ok(st) ? vq[qi & 1][i][u] : 0.0f, oacc[u]);
+              for (int u = 0; u < 4; ++u)
+                oacc[u] = mfma16x16x4(e[st], v_ok(st) ? vq[qi & 1][i][u] : 0.0f, oacc[u]);
+            }
           }
         }
 #pragma unroll
@@ -481,8 +487,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         f32x4m oa = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int i = 0; i < 4 * NKT; ++i) {
-          const float x = lv_s[vrow(i) + (c_ok ? c : 0)];
-          oa = mfma16x16x4(e[i], (v_ok(i) & c_ok) ? x : 0.0f, oa);
+          if (step_live(i)) {
+            const float x = lv_s[vrow(i) + (c_ok ? c : 0)];
+            oa = mfma16x16x4(e[i], (v_ok(i) & c_ok) ? x : 0.0f, oa);
+          }
         }
         float* orow_p = o + (b * lq + q0 + 4 * g) * static_cast<int64_t>(dv) + c;
 #pragma unroll
