@@ -89,10 +89,12 @@ def test_dam_workload():
 
 # (batch, lq, lk, d, dv): DAM tile, every key-tile count, query blocks past
 # 64, d and dv that are not multiples of 4 or 16 (32-bit loads), one-element
-# problems and long value rows.
+# problems and long value rows; last key tiles of 1 to 4 keys (scores of
+# those keys on the VALU) and of more (matrix ops).
 SHAPES = [(3, 50, 50, 200, 200), (2, 64, 64, 64, 64), (4, 16, 16, 16, 16), (5, 65, 17, 33, 7),
           (7, 3, 5, 8, 250), (2, 100, 64, 128, 16), (1, 1, 64, 1, 1), (1, 1, 1, 1, 1),
-          (9, 48, 32, 20, 3), (2, 130, 49, 12, 70), (3, 7, 33, 300, 5)]
+          (9, 48, 32, 20, 3), (2, 130, 49, 12, 70), (3, 7, 33, 300, 5),
+          (2, 40, 52, 64, 64), (3, 17, 35, 24, 40), (2, 33, 4, 16, 8)]
 
 
 @pytest.mark.parametrize("b,lq,lk,d,dv", SHAPES)
