@@ -238,10 +238,10 @@ SOFTMAX_API int softmax_nll_fwd(const float* x, const int64_t* labels, float* lo
  * The scores and weights never leave the registers: the two products run
  * on the matrix cores in fp32 (v_mfma_f32_16x16x4f32) and the softmax runs
  * on their accumulators.  Accuracy: each score carries the rounding of a
- * d-term fp32 dot product, so each weight is within a relative
- * 2*(d+1)*2^-24 * max_k |scale| sum_t |Q_it K_kt| (plus 4e-6) of the exact
- * weight, and each output within that relative error, plus (lk+1)*2^-24,
- * of sum_k P_ik |V_kc|.
+ * d-term fp32 dot product, delta_i = (d+2)*2^-24 * max_k |scale| sum_t
+ * |Q_it K_kt| for query i, so each weight is within a relative
+ * 2*delta_i + 4e-6 of the exact weight, and each output within
+ * (2*delta_i + 4e-6 + (lk+2)*2^-24) * sum_k P_ik |V_kc| + 2^-148.
  *
  * Ownership, asynchrony and error codes follow softmax_fwd: caller-owned
  * device memory, work enqueued on `stream`, SOFTMAX_ERR_INVALID_ARG for bad
