@@ -165,8 +165,9 @@ SOFTMAX_API int softmax_fwd_approx(const float* x, float* y, int64_t rows, int64
  * clip exists for (Sec. 2.1), computed directly so that it stays exact
  * where the probability itself would underflow.  clip_lo as for
  * softmax_fwd_clip (-INFINITY: plain log-softmax; a -inf entry then gives
- * -inf).  The row sum uses the accurate exponential, ln S comes from
- * v_log_f32, and c = x - M and c - ln S are fp32 operations.
+ * -inf).  The row sum takes the single-instruction exponential per term
+ * (its error, weighted by the softmax, stays within the bound below), ln S
+ * comes from v_log_f32, and c = x - M and c - ln S are fp32 operations.
  *
  * Accuracy: |y - y*| <= 2e-6 + 2.5e-7 * (|y*| + ln(cols)) against the exact
  * value y* (the sum's rounding and the logarithm's 1 ulp on log2 S).

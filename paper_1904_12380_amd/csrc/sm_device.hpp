@@ -52,8 +52,10 @@ constexpr int kExpAccurate = 0;
 constexpr int kExpWide = 1;
 constexpr int kExpFast = 2;
 // A fourth kernel mode: the output is the log of the clipped softmax,
-// y = c - ln S with c = max(x - M, lo), instead of e / S.  Its row sums use
-// the accurate exponential (terms under 2^-126 do not matter next to S >= 1).
+// y = c - ln S with c = max(x - M, lo), instead of e / S.  Its row sums
+// take the cheap exponential term by term (the bound that allows it is at
+// kSumExp; terms under 2^-126 do not matter next to S >= 1) and the
+// accurate one to merge partial sums.
 constexpr int kLogOut = 3;
 // A fifth: one value per row, the negative log-likelihood of the row's
 // label, ln S - c_label (minus the label's log output); sums as kLogOut.

@@ -136,10 +136,24 @@ __device__ __forceinline__ void load_strip_flat(float (&v)[4 * V], const float* 
   }
 }
 
+// The exponential of the row-sum terms for log and NLL outputs.  Those
+// outputs need ln S, not the terms, and the cheap exponential keeps ln S
+// within their bound: a term at x - M = d has relative error at most
+// 1.5e-7 |d| + 1.2e-7, and averaged with the softmax weights p,
+// E_p[-d] = H(p) - ln S <= ln C - ln S (H the entropy).  So S is off by at
+// most 1.5e-7 (ln C - ln S) + 1.2e-7 relative; with ln S's own 1.8e-7 ln S
+// (v_log_f32 and the product by ln 2) and the sum's rounding, ln S stays
+// within 2.5e-7 ln C + 2e-6.  For a row in chunks the terms are taken
+// against the chunk max m_g <= M, so |x - m_g| <= |d| and the same average
+// applies; merges of partial sums keep the accurate exponential (exp_mode).
+constexpr int kSumExp = kExpFast;
+
 // This lane's pairwise partial sum of the clipped exponentials.  For
 // probability outputs v is replaced by the exponentials; for log and NLL
 // outputs (keeps_logits) v keeps the logits, which the output step needs.
-template <int MODE, int N>
+// SE: the exponential of the sum terms for log and NLL outputs (kSumExp,
+// or the accurate one where the cheap one costs registers).
+template <int MODE, int N, int SE = kSumExp>
 __device__ __forceinline__ float exp_strip(float (&v)[N], RowShift rs) {
   if constexpr (keeps_logits<MODE>()) {
     // Eight interleaved partial sums, then their tree: no second array of N
@@ -147,9 +161,9 @@ __device__ __forceinline__ float exp_strip(float (&v)[N], RowShift rs) {
     constexpr int P = N < 8 ? N : 8;
     float t[P];
 #pragma unroll
-    for (int i = 0; i < P; ++i) t[i] = exp_shift_clip<kExpAccurate>(v[i], rs);
+    for (int i = 0; i < P; ++i) t[i] = exp_shift_clip<SE>(v[i], rs);
 #pragma unroll
-    for (int i = P; i < N; ++i) t[i % P] = t[i % P] + exp_shift_clip<kExpAccurate>(v[i], rs);
+    for (int i = P; i < N; ++i) t[i % P] = t[i % P] + exp_shift_clip<SE>(v[i], rs);
     return tree_sum(t);
   } else {
 #pragma unroll
@@ -185,12 +199,12 @@ __device__ __forceinline__ float2 lane_online(const float (&v)[N], Clip clip) {
     const float m_new = fmaxf(m, mk);
     const RowShift rs = row_shift(m_new == kNegInf ? 0.0f : m_new, clip);
     // two interleaved partials keep few exponentials live at once
-    float p0 = exp_shift_clip<kExpAccurate>(v[k0], rs);
-    float p1 = SUB > 1 ? exp_shift_clip<kExpAccurate>(v[k0 + 1], rs) : 0.0f;
+    float p0 = exp_shift_clip<kSumExp>(v[k0], rs);
+    float p1 = SUB > 1 ? exp_shift_clip<kSumExp>(v[k0 + 1], rs) : 0.0f;
 #pragma unroll
     for (int i = 2; i < SUB; i += 2) {
-      p0 = p0 + exp_shift_clip<kExpAccurate>(v[k0 + i], rs);
-      if (i + 1 < SUB) p1 = p1 + exp_shift_clip<kExpAccurate>(v[k0 + i + 1], rs);
+      p0 = p0 + exp_shift_clip<kSumExp>(v[k0 + i], rs);
+      if (i + 1 < SUB) p1 = p1 + exp_shift_clip<kSumExp>(v[k0 + i + 1], rs);
     }
     const float sk = p0 + p1;
     if (k0 == 0) {
@@ -529,7 +543,11 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y,
     load_strip<V, VEC4>(v, xr, tid, NT, lim);
     const LabelPick pick = pick_label<V, VEC4, MODE>(v, label, cols, 0, lim, tid, NT, tid == 0);
     const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max), clip);
-    const float s = block_sum<NW>(exp_strip<MODE>(v, rs), red_sum);
+    // Log outputs of 32 values per lane keep the accurate exponential: with
+    // the cheap one the compiler keeps more terms in flight, which needs
+    // more than the 64 VGPRs of two workgroups per CU.
+    constexpr int SE = (MODE == kLogOut && V >= 8) ? kExpAccurate : kSumExp;
+    const float s = block_sum<NW>(exp_strip<MODE, 4 * V, SE>(v, rs), red_sum);
     finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, pick, tid, NT);
   }
 }
