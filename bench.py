@@ -569,7 +569,8 @@ def summarize_trace(directory: str, w: workloads.Workload, command: str,
         f.write("Per dispatch, grouped by kernel and grid (eager and graph-replayed "
                 "launches together; durations are the profiler's begin-to-end times). "
                 "The last template argument of the softmax kernels is the mode: 0 "
-                "softmax_fwd, 1 no clip, 2 approximate exponential, 3 log-softmax.  A "
+                "softmax_fwd, 1 no clip, 2 approximate exponential, 3 log-softmax, 4 "
+                "negative log-likelihood.  A "
                 "shape seen in separate parts of the run is split into runs: the second "
                 "run of the DAM-shaped k_packed mode 0 is the unfused attention "
                 "reference (softmax_fwd between two hipBLAS products).\n\n")
