@@ -203,7 +203,10 @@ SOFTMAX_API int softmax_log_fwd(const float* x, float* y, int64_t rows, int64_t 
  *
  * Accuracy: |loss - loss*| <= 2e-6 + 2.5e-7 * (|loss*| + ln(cols)), as for
  * softmax_log_fwd.  Ownership, asynchrony, workspace (rows longer than
- * 32768 columns) and error codes follow softmax_fwd_clip.
+ * 32768 columns) and error codes follow softmax_fwd_clip, except that in
+ * the one-pass long-row kernel a row's workgroups do not wait for each
+ * other: the last to finish merges the row's partial pairs, writes the loss
+ * and returns the workspace to its resting state.
  */
 SOFTMAX_API int softmax_nll_fwd(const float* x, const int64_t* labels, float* loss,
                                 int64_t rows, int64_t cols, float clip_lo,

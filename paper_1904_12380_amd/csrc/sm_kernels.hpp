@@ -540,15 +540,37 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y,
     const int64_t label = row_label<MODE>(labels, row);
     const int lim = static_cast<int>(cols);
     float v[4 * V];
-    load_strip<V, VEC4>(v, xr, tid, NT, lim);
-    const LabelPick pick = pick_label<V, VEC4, MODE>(v, label, cols, 0, lim, tid, NT, tid == 0);
-    const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max), clip);
-    // Log outputs of 32 values per lane keep the accurate exponential: with
-    // the cheap one the compiler keeps more terms in flight, which needs
-    // more than the 64 VGPRs of two workgroups per CU.
-    constexpr int SE = (MODE == kLogOut && V >= 8) ? kExpAccurate : kSumExp;
-    const float s = block_sum<NW>(exp_strip<MODE, 4 * V, SE>(v, rs), red_sum);
-    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, pick, tid, NT);
+    if constexpr (MODE == kNllOut && VEC4) {
+      // The loss needs only the row's (max, sum) and one logit.  The sums
+      // are folded in as the loads land, and thread 0 reads the label's
+      // logit itself (one more cache line per row), so no value has to stay
+      // live after its exponential: two workgroups per CU still fit.  (With
+      // 32-bit loads the fold needs more registers than that; those rows
+      // take the reduction below.)
+      // The row's loads go out first; the logit's load waits only for the
+      // label, and is issued by every thread (one cache line per wavefront)
+      // so that no branch makes the compiler wait for all of them.
+      load_strip_flat<V, VEC4>(v, xr, tid, NT, lim);
+      const bool bad = label < 0 || label >= cols;
+      const float xl = xr[bad ? 0 : label];
+      const float2 ms = lane_online(v, clip);
+      const float m = block_max<NW>(ms.x, red_max);
+      const float s =
+          block_sum<NW>(lane_share(ms, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
+      if (tid == 0)
+        y[row] = bad ? __builtin_nanf("") : -log_out(xl, row_shift(m, clip), log_of_sum(s));
+    } else {
+      load_strip<V, VEC4>(v, xr, tid, NT, lim);
+      const LabelPick pick =
+          pick_label<V, VEC4, MODE>(v, label, cols, 0, lim, tid, NT, tid == 0);
+      const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max), clip);
+      // Log outputs of 32 values per lane keep the accurate exponential: with
+      // the cheap one the compiler keeps more terms in flight, which needs
+      // more than the 64 VGPRs of two workgroups per CU.
+      constexpr int SE = (MODE == kLogOut && V >= 8) ? kExpAccurate : kSumExp;
+      const float s = block_sum<NW>(exp_strip<MODE, 4 * V, SE>(v, rs), red_sum);
+      finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, pick, tid, NT);
+    }
   }
 }
 
@@ -667,6 +689,9 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
 // long as G workgroups of the launch fit on the device at once (G <= 64).
 // The wait is also bounded: a workgroup that gives up writes NaN for its
 // chunk instead of stalling the device.
+//
+// NLL outputs (one value per row) take no wait at all: the last workgroup
+// of the row to depart does the merge (below).
 constexpr unsigned long long kSlotEmpty = ~0ull;
 constexpr unsigned kSpinLimit = 1u << 20;
 
@@ -702,7 +727,13 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
   float m;
   float s;
   LabelPick pick{0.0f, false, false};
-  if constexpr (keeps_logits<MODE>()) {
+  if constexpr (MODE == kNllOut) {
+    // The label's logit is read by the merging workgroup below, so the
+    // values die as they are folded in.
+    const float2 ms = lane_online(v, clip);
+    m = block_max<NW>(ms.x, red_max);
+    s = block_sum<NW>(lane_share(ms, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
+  } else if constexpr (keeps_logits<MODE>()) {
     const float2 ms = lane_online(v, clip);
     pick = pick_label<V, VEC4, MODE>(v, label, cols, c0, lim, tid, NT, g == 0 && tid == 0);
     m = block_max<NW>(ms.x, red_max);
@@ -713,6 +744,55 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
   }
   const bool empty_max = (m == kNegInf);
   if (empty_max) s = static_cast<float>(lim);
+
+  if constexpr (MODE == kNllOut) {
+    // One value per row: no workgroup waits.  Each publishes its pair and
+    // then counts itself out on depart[row]; the slot store has completed
+    // before the count (explicit wait), so the workgroup that brings the
+    // count to G sees all G pairs.  That one merges them as below, reads
+    // the label's logit itself, writes the loss and puts the row's slots
+    // and counter back.
+    if (tid < 64) {
+      unsigned long long* pr = part + row * chunks;
+      unsigned old = 0u;
+      if (tid == 0) {
+        unsigned long long val = pack_pair(m, s);
+        if (val == kSlotEmpty) val = pack_pair(__builtin_nanf(""), __builtin_nanf(""));
+        __hip_atomic_store(&part[b], val, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __builtin_amdgcn_s_waitcnt(0);
+        old = __hip_atomic_fetch_add(&depart[row], 1u, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+      }
+      old = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(old)));
+      if (old == static_cast<unsigned>(chunks) - 1u) {
+        const unsigned long long q =
+            (tid < chunks)
+                ? __hip_atomic_load(&pr[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                : 0ull;
+        const float pm =
+            (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q)) : kNegInf;
+        const float ps =
+            (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q >> 32)) : 0.0f;
+        const float mrow = seg_max<64>(pm);
+        const RowShift rs = row_shift(mrow, clip);
+        const float term = (tid < chunks) ? ps * exp_shift_clip<kExpAccurate>(pm, rs) : 0.0f;
+        const float srow = seg_sum<64>(term);
+        const bool bad = label < 0 || label >= cols;
+        const float xl = x[row * cols + (bad ? 0 : label)];
+        const float loss = bad ? __builtin_nanf("") : -log_out(xl, rs, log_of_sum(srow));
+        if (tid == 0) y[row] = loss;
+        // The slot reads have returned (the loss depends on them): put the
+        // row's slots and counter back for the next launch.
+        asm volatile("" : : "v"(loss));
+        __builtin_amdgcn_s_waitcnt(0);
+        if (tid < chunks)
+          __hip_atomic_store(&pr[tid], kSlotEmpty, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (tid == 0)
+          __hip_atomic_store(&depart[row], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    return;
+  }
 
   if (tid == 0) {
     unsigned long long val = pack_pair(m, s);

@@ -122,9 +122,8 @@ def test_labels_out_of_range_and_nonfinite_rows(cols):
 def test_minus_log_softmax_at_label(key):
     """The loss is minus softmax_log_fwd's output at the label: bit for bit
     where both modes take the same row sum, and within the shared bound on
-    the 1024-thread row kernel at 32 values per lane (vocab rows), where the
-    log mode keeps the accurate exponential for registers and the NLL takes
-    the cheap one."""
+    the 1024-thread row kernel (vocab rows), where the NLL folds its sums in
+    as the loads land and the log mode reduces the loaded row."""
     import torch
     x = torch.from_numpy(workloads.generate(key)).to("cuda:0")
     t = torch.from_numpy(workloads.generate_labels(key)).to("cuda:0")
@@ -141,6 +140,33 @@ def test_minus_log_softmax_at_label(key):
             b = (-picked).double().cpu().numpy()
             bound = 2.0 * (2e-6 + 2.5e-7 * (np.abs(a) + math.log(cols)))
             assert np.all(np.abs(a - b) <= bound), (key, lo)
+
+
+@pytest.mark.parametrize("rows,cols", [(3, 100003), (64, 262144), (2, 1048580)])
+def test_long_rows_interleaved_with_other_modes(rows, cols):
+    """Long rows share the library's exchange slots between the modes: the
+    loss's merging workgroup puts them back, so softmax, log-softmax and
+    loss calls in any order on one stream all stay exact."""
+    import torch
+    x = workloads.random_logits(rows, cols, seed=cols + rows, kind="clip_heavy")
+    t = np.random.default_rng(cols).integers(0, cols, size=rows, dtype=np.int64)
+    xt = torch.from_numpy(x).to("cuda:0")
+    tt = torch.from_numpy(t).to("cuda:0")
+    want_nll = oracle.nll_clipped(x, t, -64.0)
+    sample = np.random.default_rng(rows).integers(0, rows, size=min(rows, 2))
+    want_y = oracle.softmax_clipped(x[sample], -64.0)
+    for rep in range(3):
+        loss = sm.softmax_nll_fwd(xt, tt)
+        y = sm.softmax_fwd(xt)
+        loss2 = sm.softmax_nll_fwd(xt, tt)
+        ylog = sm.softmax_log_fwd(xt)
+        torch.cuda.synchronize()
+        assert torch.equal(loss.view(torch.int32), loss2.view(torch.int32)), rep
+        check_nll(x, t, loss.cpu().numpy(), -64.0, f"interleaved {rows}x{cols} rep {rep}")
+        got = y.cpu().numpy()[sample].astype(np.float64)
+        assert np.all(np.abs(got - want_y) <= 4e-6 * want_y), rep
+        picked = ylog.gather(1, tt.view(-1, 1)).view(-1)
+        assert torch.equal(loss.view(torch.int32), (-picked).view(torch.int32)), rep
 
 
 def test_uniform_rows():
