@@ -106,10 +106,12 @@ __global__ __launch_bounds__(256) void k_attention(const float* q, const float* 
     if (q0 >= lq) continue;                       // wave-uniform; no barriers below
     const int nq = lq - q0 < 16 ? lq - q0 : 16;   // valid queries of this wave
     // The wave's 16 query rows of Q and O, and the batch element's K and V.
-    const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + (b * lq + q0) * static_cast<int64_t>(d), nq * d * 4);
+    const __amdgpu_buffer_rsrc_t rq =
+        make_rsrc(q + (b * lq + q0) * static_cast<int64_t>(d), nq * d * 4);
     const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + b * lk * static_cast<int64_t>(d), lk * d * 4);
     const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + b * lk * static_cast<int64_t>(dv), lk * dv * 4);
-    const __amdgpu_buffer_rsrc_t ro = make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
+    const __amdgpu_buffer_rsrc_t ro =
+        make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
 
     // ---- scores S^T = K Q^T for this wave's 16 queries --------------------
     // Lane (j, g) reads query j and key 16 kt + j at columns t0 .. t0+3,
@@ -288,7 +290,9 @@ __global__ __launch_bounds__(256) void k_attention(const float* q, const float* 
 //
 // Each batch element's K and V cross HBM and L2 once, instead of once per
 // wavefront, and the matrix-op operands come from LDS.  Two workgroups fit
-// per CU, so one copies while the other computes.
+// per CU, and one can copy while the other computes; they do not stay out
+// of step, though, and the compute phase (the matrix ops and the VALU work
+// that feeds them) sets the kernel's time.
 constexpr int kAttnLdsBytes = 80 * 1024;
 constexpr int kAttnMaxDQ = 224;  // d up to this keeps Q in registers (14 blocks)
 

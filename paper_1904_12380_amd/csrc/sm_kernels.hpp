@@ -6,9 +6,11 @@
 // subtract, exp, row sum, scale by the reciprocal of the sum) with the clip
 // of the reference functor (Sec. 1.2, Fig. 1) at a bound lo given as a
 // kernel argument (default -64; no clip runs as the floor bound with a
-// clipped value of 0).  The exponential is evaluated as the template argument EM says
-// (accurate, accurate into the denormal range, or the fast approximation).  Unlike the CPU functor, no kernel uses y
-// as scratch: x is read from HBM once (twice for rows over 2^21 columns)
+// clipped value of 0).  The MODE template argument says how the exponential
+// is evaluated (accurate, accurate into the denormal range, or the fast
+// approximation) or what is written instead of y: its logarithm, or one
+// negative log-likelihood per row.  Unlike the CPU functor, no kernel uses
+// y as scratch: x is read from HBM once (twice for rows over 2^21 columns)
 // and y is written once.
 //
 //   k_packed      cols <= 64: a persistent workgroup stages tiles of whole
