@@ -88,8 +88,10 @@ extern "C" {
  * Workspace: rows longer than 32768 columns use a 140 KiB device workspace
  * that the library allocates (hipMalloc, initialised) on the first such call on
  * each (device, stream) and keeps until the process ends, so calls on
- * different streams never share one.  Up to 64 streams per device get their
- * own; past that the least recently used one is reassigned after a
+ * different streams never share one.  (Streams are told apart by handle: a
+ * stream destroyed while its work still runs and a new stream that gets the
+ * same handle count as one.)  Up to 64 streams per device get their own;
+ * past that the least recently used one is reassigned after a
  * hipDeviceSynchronize().  Under stream capture no allocation is made: the
  * capture uses one workspace per device, created by an earlier uncaptured
  * long-row call on that device (otherwise SOFTMAX_ERR_INVALID_ARG), and
