@@ -767,10 +767,24 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
       }
       old = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(old)));
       if (old == static_cast<unsigned>(chunks) - 1u) {
-        const unsigned long long q =
-            (tid < chunks)
-                ? __hip_atomic_load(&pr[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                : 0ull;
+        // Every pair was stored before its count, so none should read empty;
+        // a slot that still does is read again (bounded, as in the exchange
+        // below), so the merge does not rest on when a completed store
+        // becomes visible to other XCDs.
+        unsigned long long q = 0ull;
+        unsigned spins = 0;
+        bool ok = true;
+        while (true) {
+          q = (tid < chunks)
+                  ? __hip_atomic_load(&pr[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                  : 0ull;
+          if (__builtin_amdgcn_ballot_w64(tid < chunks && q == kSlotEmpty) == 0) break;
+          __builtin_amdgcn_s_sleep(2);
+          if (++spins > kSpinLimit) {
+            ok = false;
+            break;
+          }
+        }
         const float pm =
             (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q)) : kNegInf;
         const float ps =
@@ -781,7 +795,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
         const float srow = seg_sum<64>(term);
         const bool bad = label < 0 || label >= cols;
         const float xl = x[row * cols + (bad ? 0 : label)];
-        const float loss = bad ? __builtin_nanf("") : -log_out(xl, rs, log_of_sum(srow));
+        const float loss =
+            (bad || !ok) ? __builtin_nanf("") : -log_out(xl, rs, log_of_sum(srow));
         if (tid == 0) y[row] = loss;
         // The slot reads have returned (the loss depends on them): put the
         // row's slots and counter back for the next launch.
