@@ -15,9 +15,9 @@ and the graph is replayed: W untimed steps, then exactly K steps between two
 synchronisations, timed with HIP events recorded on the stream the kernels
 run on.  The graph removes host launch overhead (about 4 us per call through
 the C ABI plus Python); the same steps launched one by one from Python are
-reported as ``eager``.  All of it runs on a dedicated stream.  The roofline object uses the algorithmic traffic of one call
-(8 bytes per element: one fp32 read of x, one fp32 write of y) divided by the
-average step time.  ``cpu_baseline`` times the float64 oracle on the host,
+reported as ``eager``.  All of it runs on a dedicated stream.  The roofline
+object uses the algorithmic traffic of one call (8 bytes per element: one
+fp32 read of x, one fp32 write of y) divided by the average step time.  ``cpu_baseline`` times the float64 oracle on the host,
 ``cpu_fp32_baseline`` a plain single-thread fp32 C loop.
 
 Counter passes (FETCH_SIZE, WRITE_SIZE, and optionally occupancy) use two
