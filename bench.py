@@ -17,8 +17,9 @@ run on.  The graph removes host launch overhead (about 4 us per call through
 the C ABI plus Python); the same steps launched one by one from Python are
 reported as ``eager``.  All of it runs on a dedicated stream.  The roofline
 object uses the algorithmic traffic of one call (8 bytes per element: one
-fp32 read of x, one fp32 write of y) divided by the average step time.  ``cpu_baseline`` times the float64 oracle on the host,
-``cpu_fp32_baseline`` a plain single-thread fp32 C loop.
+fp32 read of x, one fp32 write of y) divided by the average step time.
+``cpu_baseline`` times the float64 oracle on the host, ``cpu_fp32_baseline``
+a plain single-thread fp32 C loop.
 
 Counter passes (FETCH_SIZE, WRITE_SIZE, and optionally occupancy) use two
 extra modes:
@@ -483,9 +484,11 @@ def summarize_pmc(directory: str, w: workloads.Workload, command: str) -> dict:
         f.write("Commands (from the repository root on the GPU machine):\n\n```\n"
                 f"{command}\n```\n\n")
         f.write("| quantity | softmax kernel | copy kernel (same bytes) |\n|---|---|---|\n")
-        f.write(f"| FETCH_SIZE KiB/dispatch (median) | {doc['softmax_fetch_kib_per_dispatch']:.1f} | "
+        f.write("| FETCH_SIZE KiB/dispatch (median) | "
+                f"{doc['softmax_fetch_kib_per_dispatch']:.1f} | "
                 f"{doc['copy_fetch_kib_per_dispatch']:.1f} |\n")
-        f.write(f"| WRITE_SIZE KiB/dispatch (median) | {doc['softmax_write_kib_per_dispatch']:.1f} | "
+        f.write("| WRITE_SIZE KiB/dispatch (median) | "
+                f"{doc['softmax_write_kib_per_dispatch']:.1f} | "
                 f"{doc['copy_write_kib_per_dispatch']:.1f} |\n\n")
         f.write(f"Copy kernel moves {bytes_each_way:.0f} bytes each way; scale factors "
                 f"fetch {scale_fetch:.4f}, write {scale_write:.4f}.\n\n")

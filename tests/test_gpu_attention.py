@@ -193,4 +193,5 @@ def test_bad_arguments_raise():
     with pytest.raises(sm.SoftmaxError):
         sm.softmax_attention_fwd(q, k, v)              # 65 keys
     with pytest.raises(sm.SoftmaxError):
-        sm.softmax_attention_fwd(q, k[:, :8].contiguous(), v[:, :8].contiguous(), scale=float("nan"))
+        sm.softmax_attention_fwd(q, k[:, :8].contiguous(), v[:, :8].contiguous(),
+                                 scale=float("nan"))

@@ -51,7 +51,8 @@ def check_parity(x: np.ndarray, y: np.ndarray, what: str):
     rel = np.abs(y64[finite] - want[finite]) / want[finite]
     worst = float(rel.max()) if rel.size else 0.0
     if worst > REL_TOL:
-        idx = np.unravel_index(np.argmax(np.where(finite, np.abs(y64 - want) / np.where(finite, want, 1), 0)), y.shape)
+        rel_all = np.where(finite, np.abs(y64 - want) / np.where(finite, want, 1), 0)
+        idx = np.unravel_index(np.argmax(rel_all), y.shape)
         pytest.fail(f"{what}: max rel err {worst:.3e} at {idx}: got {y64[idx]!r}, "
                     f"want {want[idx]!r}, x={x[idx]!r}, rowmax={x[idx[0]].max()!r}")
     rows_ok = np.all(finite, axis=1)
