@@ -292,6 +292,7 @@ def time_attention(sm, torch, key: str, steps: int, warmup: int) -> dict:
     torch.cuda.empty_cache()
     gbps = wa.algorithmic_bytes / (ms * 1e-3) / 1e9
     tflops = wa.flops / (ms * 1e-3) / 1e12
+    traffic, traffic_note = load_traffic(key)
     return {
         "workload": key, "batch": wa.batch, "lq": wa.lq, "lk": wa.lk, "d": wa.d, "dv": wa.dv,
         "ms_per_step": ms, "eager_ms_per_step": eager_ms,
@@ -302,6 +303,8 @@ def time_attention(sm, torch, key: str, steps: int, warmup: int) -> dict:
         "frac_of_fp32_matrix_peak": tflops / FP32_MATRIX_PEAK_TFLOPS,
         "unfused_ms_per_step": unfused_ms, "fused_speedup": unfused_ms / ms,
         "sampled_normwise_err": err, "rotation_sets": nset,
+        "traffic": traffic,
+        **({"traffic_note": traffic_note} if traffic_note else {}),
     }
 
 
