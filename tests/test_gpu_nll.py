@@ -121,9 +121,11 @@ def test_labels_out_of_range_and_nonfinite_rows(cols):
                                  "vocab_512x32768", "longrow_64x262144"])
 def test_minus_log_softmax_at_label(key):
     """The loss is minus softmax_log_fwd's output at the label: bit for bit
-    where both modes take the same row sum, and within the shared bound on
-    the 1024-thread row kernel (vocab rows), where the NLL folds its sums in
-    as the loads land and the log mode reduces the loaded row."""
+    where both modes take the same row sum, and within the shared bound
+    where they do not: on the 1024-thread row kernel (vocab rows), where the
+    NLL folds its sums in as the loads land and the log mode reduces the
+    loaded row, and on long rows, where the NLL's one-pass chunks are twice
+    as wide."""
     import torch
     x = torch.from_numpy(workloads.generate(key)).to("cuda:0")
     t = torch.from_numpy(workloads.generate_labels(key)).to("cuda:0")
@@ -133,7 +135,7 @@ def test_minus_log_softmax_at_label(key):
         ylog = sm.softmax_log_fwd(x, lo)
         picked = ylog.gather(1, t.view(-1, 1)).view(-1)
         torch.cuda.synchronize()
-        if key != "vocab_512x32768":
+        if key not in ("vocab_512x32768", "longrow_64x262144"):
             assert torch.equal(loss.view(torch.int32), (-picked).view(torch.int32)), (key, lo)
         else:
             a = loss.double().cpu().numpy()
@@ -146,7 +148,7 @@ def test_minus_log_softmax_at_label(key):
 def test_long_rows_interleaved_with_other_modes(rows, cols):
     """Long rows share the library's exchange slots between the modes: the
     loss's merging workgroup puts them back, so softmax, log-softmax and
-    loss calls in any order on one stream all stay exact.  70 x 500000
+    loss calls in any order on one stream all stay within their bounds.  70 x 500000
     takes three one-pass launches per call (31 chunks per row, 33 rows per
     launch)."""
     import torch
@@ -168,7 +170,10 @@ def test_long_rows_interleaved_with_other_modes(rows, cols):
         got = y.cpu().numpy()[sample].astype(np.float64)
         assert np.all(np.abs(got - want_y) <= 4e-6 * want_y), rep
         picked = ylog.gather(1, tt.view(-1, 1)).view(-1)
-        assert torch.equal(loss.view(torch.int32), (-picked).view(torch.int32)), rep
+        a = loss.double().cpu().numpy()
+        b = (-picked).double().cpu().numpy()
+        bound = 2.0 * (2e-6 + 2.5e-7 * (np.abs(a) + math.log(cols)))
+        assert np.all(np.abs(a - b) <= bound), rep
 
 
 def test_uniform_rows():
