@@ -729,9 +729,14 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
   float m;
   float s;
   LabelPick pick{0.0f, false, false};
+  // NLL outputs: every workgroup reads the row's label logit right after its
+  // chunk's loads (one cache line per wavefront, after the label itself),
+  // so the one that merges the row below already holds it, and the values
+  // die as they are folded in.
+  const bool bad_label = label < 0 || label >= cols;
+  float xl = 0.0f;
+  if constexpr (MODE == kNllOut) xl = x[row * cols + (bad_label ? 0 : label)];
   if constexpr (MODE == kNllOut) {
-    // The label's logit is read by the merging workgroup below, so the
-    // values die as they are folded in.
     const float2 ms = lane_online(v, clip);
     m = block_max<NW>(ms.x, red_max);
     s = block_sum<NW>(lane_share(ms, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
@@ -751,9 +756,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     // One value per row: no workgroup waits.  Each publishes its pair and
     // then counts itself out on depart[row]; the slot store has completed
     // before the count (explicit wait), so the workgroup that brings the
-    // count to G sees all G pairs.  That one merges them as below, reads
-    // the label's logit itself, writes the loss and puts the row's slots
-    // and counter back.
+    // count to G sees all G pairs.  That one merges them as below, writes
+    // the loss with the label logit it read at the start, and puts the
+    // row's slots and counter back.
     if (tid < 64) {
       unsigned long long* pr = part + row * chunks;
       unsigned old = 0u;
@@ -793,10 +798,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
         const RowShift rs = row_shift(mrow, clip);
         const float term = (tid < chunks) ? ps * exp_shift_clip<kExpAccurate>(pm, rs) : 0.0f;
         const float srow = seg_sum<64>(term);
-        const bool bad = label < 0 || label >= cols;
-        const float xl = x[row * cols + (bad ? 0 : label)];
         const float loss =
-            (bad || !ok) ? __builtin_nanf("") : -log_out(xl, rs, log_of_sum(srow));
+            (bad_label || !ok) ? __builtin_nanf("") : -log_out(xl, rs, log_of_sum(srow));
         if (tid == 0) y[row] = loss;
         // The slot reads have returned (the loss depends on them): put the
         // row's slots and counter back for the next launch.
