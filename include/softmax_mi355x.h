@@ -208,7 +208,9 @@ SOFTMAX_API int softmax_log_fwd(const float* x, float* y, int64_t rows, int64_t 
  * 32768 columns) and error codes follow softmax_fwd_clip, except that in
  * the one-pass long-row kernel a row's workgroups do not wait for each
  * other: the last to finish merges the row's partial pairs, writes the loss
- * and returns the workspace to its resting state.
+ * and returns the workspace to its resting state.  With 128-bit access
+ * those rows are cut into chunks of 32768 columns (1024-thread workgroups)
+ * rather than the 16384 that softmax_plan() reports for softmax_fwd.
  */
 SOFTMAX_API int softmax_nll_fwd(const float* x, const int64_t* labels, float* loss,
                                 int64_t rows, int64_t cols, float clip_lo,
