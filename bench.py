@@ -1,23 +1,30 @@
 """Benchmark of the MI355X row softmax: one JSON line on stdout.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload KEY]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload KEY]
                     [--no-cpu-baseline] [--no-extra-workloads]
 
 A step is one softmax_fwd call (every stage of the path: load, row max,
 shift, clip, exp, row sum, reciprocal scale, store) over the whole workload
-matrix.  Inputs sit in HBM before the timed region starts.  Each step uses a
-different (x, y) pair out of a rotation set of at least 1 GiB, so no step
-finds its input in the 256 MB last-level (MALL) cache left warm by earlier
-steps; every x_k holds the same seeded matrix.
+matrix.  The headline workload is the long-row one, 64 x 262144 (134 MB of
+traffic per call, tied with the vocabulary workload as the largest of the
+five); the vocabulary workload, 512 x 32768, gets the same roofline and CPU
+baseline objects under ``graded``, and the other three shapes are reported
+under ``other_workloads``.  Inputs sit in HBM before the timed region starts.
+Each step uses a different (x, y) pair out of a rotation set of at least
+1 GiB, so no step finds its input in the 256 MB last-level (MALL) cache left
+warm by earlier steps; every x_k holds the same seeded matrix.
 
 Timing: the K steps are captured once into a HIP graph (torch.cuda.CUDAGraph)
-and the graph is replayed: W untimed steps, then exactly K steps between two
-synchronisations, timed with HIP events recorded on the stream the kernels
-run on.  The graph removes host launch overhead (about 4 us per call through
-the C ABI plus Python); the same steps launched one by one from Python are
-reported as ``eager``.  All of it runs on a dedicated stream.  The roofline
-object uses the algorithmic traffic of one call (8 bytes per element: one
-fp32 read of x, one fp32 write of y) divided by the average step time.
+on a dedicated stream.  After W eager warmup steps and one untimed replay,
+the measurement is: synchronise; replay the graph once untimed (a pre-roll
+that keeps the GPU busy while the host queues the rest); record the start
+event; replay the graph (exactly K steps, with every gap between them);
+record the stop event; synchronise.  Starting the event behind queued work
+keeps the host's submission time of the timed replay out of the window.
+The same steps launched one by one from Python, also behind a pre-roll, are
+reported as ``eager``.  The roofline object uses the algorithmic traffic of
+one call (8 bytes per element: one fp32 read of x, one fp32 write of y)
+divided by the step time; these workloads take one launch per step.
 ``cpu_baseline`` times the float64 oracle on the host, ``cpu_fp32_baseline``
 a plain single-thread fp32 C loop.
 
@@ -33,6 +40,9 @@ extra modes:
 The summary (profiles/pmc_KEY.json and .md) scales each counter by what it
 reads for the library's copy kernel on the same number of bytes; ``traffic``
 in the JSON line comes from it only while the kernel sources are unchanged.
+A kernel-trace run of this script (``rocprofv3 --kernel-trace --stats``)
+summarised with ``--summarize-trace`` gives profiles/trace_bench.json, whose
+per-kernel median, p10 and p90 the JSON line repeats under the same rule.
 """
 from __future__ import annotations
 
@@ -45,6 +55,7 @@ import json
 import math
 import os
 import platform
+import subprocess
 import sys
 import time
 
@@ -59,9 +70,11 @@ import workloads  # noqa: E402
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, 8 TB/s
 ROTATE_BYTES = 1 << 30          # >= 4x the 256 MB MALL
 METRIC = "softmax rows/s and achieved HBM GB/s (% of MI355X peak), fp32, 1 GPU"
-DEFAULT_WORKLOAD = "dam_attention_115200x50"
+DEFAULT_WORKLOAD = "longrow_64x262144"
+GRADED = ("longrow_64x262144", "vocab_512x32768")   # >= 32 MB of logits each
 CSRC = os.path.join(ROOT, "paper_1904_12380_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
+TRACE_JSON = os.path.join(PROFILES, "trace_bench.json")
 
 
 def log(msg: str) -> None:
@@ -80,7 +93,7 @@ def cpu_model() -> str:
 
 
 def kernel_source_sha256() -> str:
-    """Hash of the HIP sources: counter summaries are tied to it."""
+    """Hash of the HIP sources: counter and trace summaries are tied to it."""
     h = hashlib.sha256()
     for path in sorted(glob.glob(os.path.join(CSRC, "*"))):
         if path.endswith((".hip", ".hpp", ".h")):
@@ -88,6 +101,25 @@ def kernel_source_sha256() -> str:
             with open(path, "rb") as f:
                 h.update(f.read())
     return h.hexdigest()
+
+
+def machine_state() -> dict:
+    """Clocks, power and performance level from rocm-smi (read-only queries),
+    so that differences between machines and runs can be told apart."""
+    out: dict = {}
+    cmd = ["rocm-smi", "--showclocks", "--showpower", "--showmaxpower", "--showperflevel",
+           "--json"]
+    try:
+        r = subprocess.run(cmd, capture_output=True, text=True, timeout=30)
+        doc = json.loads(r.stdout) if r.stdout.strip().startswith("{") else {}
+        card = next((v for k, v in doc.items() if k.startswith("card")), {})
+        keep = ("sclk", "mclk", "fclk", "socclk", "power", "perf")
+        out = {k: v for k, v in card.items() if any(t in k.lower() for t in keep)}
+        if not out:
+            out = {"raw": r.stdout.strip()[-400:]}
+    except Exception as e:  # rocm-smi missing or failed: record why
+        out = {"error": repr(e)}
+    return out
 
 
 class Rotation:
@@ -105,12 +137,23 @@ class Rotation:
         return self.xs[i % self.n], self.ys[i % self.n]
 
 
+def warm_clocks(sm, torch, seconds: float = 0.3) -> None:
+    """Untimed: keep the GPU streaming for a moment, so that the first timed
+    workload does not run while clocks are still ramping up from idle."""
+    x = torch.zeros(1 << 26, device="cuda:0")      # 256 MB
+    y = torch.empty_like(x)
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            sm.softmax_copy_probe(x, out=y)
+        torch.cuda.synchronize()
+    del x, y
+
+
 def time_steps(torch, launch, steps: int, warmup: int) -> tuple[float, float]:
-    """Capture `steps` calls of launch(i, stream) into one graph; replay it
-    once untimed (after `warmup` eager calls), then time one replay.
-    Everything runs on one dedicated stream: HIP's legacy null stream (torch's
-    default) adds a few microseconds of GPU time between kernels.
-    Returns (graph ms per step, eager ms per step)."""
+    """Graph-replayed and eager ms per step of launch(i, stream), each timed
+    over exactly `steps` steps behind a queued pre-roll (see the module
+    docstring).  Returns (graph ms per step, eager ms per step)."""
     stream = torch.cuda.Stream()
     stream.wait_stream(torch.cuda.current_stream())
     start = torch.cuda.Event(enable_timing=True)
@@ -118,27 +161,25 @@ def time_steps(torch, launch, steps: int, warmup: int) -> tuple[float, float]:
     with torch.cuda.stream(stream):
         for i in range(warmup):
             launch(i, stream)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for i in range(steps):
+                launch(i, stream)
+        g.replay()                  # first replay, untimed
         torch.cuda.synchronize()
-        # eager: one call per step from Python
+        g.replay()                  # pre-roll, untimed
+        start.record(stream)
+        g.replay()                  # the timed steps
+        stop.record(stream)
+        torch.cuda.synchronize()
+        graph_ms = start.elapsed_time(stop) / steps
+        g.replay()                  # pre-roll for the eager steps
         start.record(stream)
         for i in range(steps):
             launch(i, stream)
         stop.record(stream)
         torch.cuda.synchronize()
         eager_ms = start.elapsed_time(stop) / steps
-        # graph: the same steps captured once, replayed on the same stream
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=stream):
-            for i in range(steps):
-                launch(i, stream)
-        torch.cuda.synchronize()
-        g.replay()                  # warm replay
-        torch.cuda.synchronize()
-        start.record(stream)
-        g.replay()
-        stop.record(stream)
-        torch.cuda.synchronize()
-        graph_ms = start.elapsed_time(stop) / steps
     del g
     return graph_ms, eager_ms
 
@@ -170,6 +211,11 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
     def tiny(i, s):
         sm.softmax_copy_probe(tiny_x, out=tiny_y, stream=s)
 
+    def fwd_inplace(i, s):
+        # in place on y_k, which holds finite softmax outputs of earlier steps
+        _, y = rot.pair(i)
+        sm.softmax_fwd(y, out=y, stream=s)
+
     def fwd_noclip(i, s):
         x, y = rot.pair(i)
         sm.softmax_fwd_clip(x, float("-inf"), out=y, stream=s)
@@ -187,6 +233,7 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         sm.softmax_nll_fwd(x, labels, out=losses[i % rot.n], stream=s)
 
     ms, eager_ms = time_steps(torch, fwd, steps, warmup)
+    inplace_ms, _ = time_steps(torch, fwd_inplace, steps, warmup)
     copy_ms, _ = time_steps(torch, cpy, steps, warmup)
     memcpy_ms = time_steps(torch, d2d, steps, warmup)[0] if memcpy else None
     floor_ms = time_steps(torch, tiny, steps, warmup)[0] if memcpy else None
@@ -204,7 +251,7 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         sm.softmax_fwd(x0, out=y0)
         torch.cuda.synchronize()
         rng = np.random.default_rng(0)
-        rows = np.unique(rng.integers(0, w.rows, size=min(w.rows, 64)))
+        rows = np.unique(rng.integers(0, w.rows, size=min(w.rows, 16)))
         dev = y0.device
         y = y0[torch.from_numpy(rows).to(dev)].cpu().numpy().astype(np.float64)
         want = oracle.softmax_clipped(x_host[rows])
@@ -224,6 +271,8 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         "frac_of_peak": gbps / HBM_PEAK_GBPS,
         "eager_ms_per_step": eager_ms,
         "eager_hbm_gbps": w.algorithmic_bytes / (eager_ms * 1e-3) / 1e9,
+        "in_place_ms_per_step": inplace_ms,
+        "in_place_hbm_gbps": w.algorithmic_bytes / (inplace_ms * 1e-3) / 1e9,
         "copy_ms_per_step": copy_ms,
         "copy_gbps": w.algorithmic_bytes / (copy_ms * 1e-3) / 1e9,
         "softmax_over_copy_time": ms / copy_ms,
@@ -514,124 +563,155 @@ def summarize_pmc(directory: str, w: workloads.Workload, command: str) -> dict:
     return doc
 
 
-COPY_THREADS = 256       # launch shape of softmax_copy_probe's 128-bit kernel:
-COPY_UNROLL = 4          # 256 threads, 4 float4 per thread per workgroup
-
-
-def trace_groups(w_all: dict) -> dict:
-    """(kernel base name, grid size in threads) -> the workloads whose
-    launches have that shape: the softmax kernel from softmax_plan(), the copy
-    kernel from its fixed launch shape."""
-    import paper_1904_12380_amd as sm
-    names = {"packed": "k_packed", "wave_row": "k_wave_row", "block_row": "k_block_row",
-             "split_row": "k_split"}
-    out: dict = {}
-    for key, wk in w_all.items():
-        p = sm.softmax_plan(wk.rows, wk.cols)
-        out.setdefault((names[p["kernel_name"]], p["grid"] * p["block_threads"]), []).append(key)
-        blocks = min(-(-(wk.elements // 4) // (COPY_THREADS * COPY_UNROLL)), 1 << 20)
-        out.setdefault(("k_copy4", blocks * COPY_THREADS), []).append(key)
-    return {k: " / ".join(v) for k, v in out.items()}
-
-
-def _base_name(full: str) -> str:
-    head = full.split("(")[0].split("<")[0]
-    return head.split("::")[-1].replace("void ", "").strip()
-
-
-def summarize_trace(directory: str, w: workloads.Workload, command: str,
-                    bench_json: str | None) -> str:
-    """profiles/<kernel>_<workload>_trace.md from a rocprofv3 --kernel-trace
-    --stats run of this script: per (kernel, grid) dispatch durations
-    (median, p10, p90, mean) and register / LDS usage, the per-kernel stats
-    table, and the step times the same run printed."""
+def summarize_trace(directory: str, command: str, bench_json: str | None) -> str:
+    """profiles/trace_bench.{md,json} from a rocprofv3 --kernel-trace --stats
+    run of this script: per (kernel, grid) dispatch durations (median, p10,
+    p90, mean) and register / LDS usage, the per-kernel stats table, and the
+    step times the same run printed."""
     traces = glob.glob(os.path.join(directory, "**", "*kernel_trace.csv"), recursive=True)
     stats = glob.glob(os.path.join(directory, "**", "*kernel_stats.csv"), recursive=True)
     if not traces or not stats:
         raise SystemExit(f"no kernel_trace.csv / kernel_stats.csv under {directory}")
-    labels = trace_groups(workloads.WORKLOADS)
     groups: dict = {}
     with open(traces[0]) as f:
         for r in csv.DictReader(f):
-            base = _base_name(r["Kernel_Name"])
-            if not (base.startswith("k_") and "smx::" in r["Kernel_Name"]):
+            if "smx::" not in r["Kernel_Name"]:
                 continue
             key = (r["Kernel_Name"].split("(")[0].replace("void ", ""), int(r["Grid_Size_X"]))
-            g = groups.setdefault(key, {"d": [], "res": r, "base": base})
+            g = groups.setdefault(key, {"d": [], "res": r})
             g["d"].append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
     with open(stats[0]) as f:
         rows = list(csv.DictReader(f))
     bench = None
-    main_k = "kernels"
     if bench_json:
         with open(bench_json) as f:
             bench = json.loads(f.read().strip().splitlines()[-1])
-        main_k = {"packed": "k_packed", "wave_row": "k_wave_row", "block_row": "k_block_row",
-                  "split_row": "k_split"}[bench["config"]["kernel"]]
-    path = os.path.join(PROFILES, f"{main_k}_{w.key}_trace.md")
+    doc = {"source_sha256": kernel_source_sha256(), "command": command, "kernels": []}
+    for (name, grid), g in sorted(groups.items()):
+        r = g["res"]
+        # Runs of calls more than 0.5 s apart are reported apart: the same
+        # launch shape can come from different parts of the run (the unfused
+        # attention reference calls softmax_fwd on the DAM shape).
+        calls = sorted(g["d"])
+        runs = [[calls[0]]]
+        for c in calls[1:]:
+            if c[0] - runs[-1][-1][1] > 500_000_000:
+                runs.append([])
+            runs[-1].append(c)
+        for k, run in enumerate(runs):
+            d = np.array([(e - b) / 1e3 for b, e in run])
+            doc["kernels"].append({
+                "kernel": name, "grid_threads": grid, "run": k + 1, "runs": len(runs),
+                "calls": int(d.size), "median_us": float(np.median(d)),
+                "p10_us": float(np.percentile(d, 10)), "p90_us": float(np.percentile(d, 90)),
+                "mean_us": float(d.mean()), "vgpr": r["VGPR_Count"], "sgpr": r["SGPR_Count"],
+                "lds_bytes": r["LDS_Block_Size"], "scratch_bytes": r["Scratch_Size"]})
+    if bench:
+        doc["bench_line"] = {"workload": bench["config"]["workload"],
+                             "ms_per_step": bench["ms_per_step"],
+                             "graded": {k: v["ms_per_step"] for k, v in bench["graded"].items()}}
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(TRACE_JSON, "w") as f:
+        json.dump(doc, f, indent=1)
+        f.write("\n")
+    path = TRACE_JSON[:-5] + ".md"
     with open(path, "w") as f:
-        f.write(f"# Kernel trace: bench.py on {w.key} (and the other workloads it times)\n\n")
+        f.write("# Kernel trace of bench.py\n\n")
         f.write(f"Command (repository root, GPU machine):\n\n```\n{command}\n```\n\n")
         f.write("Per dispatch, grouped by kernel and grid (eager and graph-replayed "
                 "launches together; durations are the profiler's begin-to-end times). "
                 "The last template argument of the softmax kernels is the mode: 0 "
                 "softmax_fwd, 1 no clip, 2 approximate exponential, 3 log-softmax, 4 "
-                "negative log-likelihood.  A "
-                "shape seen in separate parts of the run is split into runs: the second "
-                "run of the DAM-shaped k_packed mode 0 is the unfused attention "
-                "reference (softmax_fwd between two hipBLAS products).\n\n")
-        f.write("| kernel | grid threads | workload | calls | median us | p10 us | p90 us | "
-                "mean us | VGPR | AGPR | SGPR | LDS B | scratch B |\n"
-                "|---|---|---|---|---|---|---|---|---|---|---|---|---|\n")
-        for (name, grid), g in sorted(groups.items(), key=lambda kv: (kv[0][0], kv[0][1])):
-            r = g["res"]
-            lab = labels.get((g["base"] if not g["base"].startswith("k_split") else "k_split",
-                              grid), "")
-            if g["base"].startswith("k_attention"):
-                lab = " / ".join(workloads.ATTENTION_WORKLOADS)
-            # Runs of calls separated by more than 0.5 s are reported apart:
-            # the same launch shape can come from different parts of the run
-            # (the unfused attention reference calls softmax_fwd on scores of
-            # the DAM shape).
-            calls = sorted(g["d"])
-            runs = [[calls[0]]]
-            for c in calls[1:]:
-                if c[0] - runs[-1][-1][1] > 500_000_000:
-                    runs.append([])
-                runs[-1].append(c)
-            for k, run in enumerate(runs):
-                d = np.array([(e - b) / 1e3 for b, e in run])
-                tag = lab if len(runs) == 1 else f"{lab} (run {k + 1} of {len(runs)})"
-                f.write(f"| `{name}` | {grid} | {tag} | {d.size} | {np.median(d):.2f} | "
-                        f"{np.percentile(d, 10):.2f} | {np.percentile(d, 90):.2f} | "
-                        f"{d.mean():.2f} | {r['VGPR_Count']} | {r['Accum_VGPR_Count']} | "
-                        f"{r['SGPR_Count']} | {r['LDS_Block_Size']} | {r['Scratch_Size']} |\n")
+                "negative log-likelihood.  A shape seen in separate parts of the run is "
+                "split into runs: the second run of the DAM-shaped k_packed mode 0 is "
+                "the unfused attention reference (softmax_fwd between two hipBLAS "
+                "products).\n\n")
+        f.write("| kernel | grid threads | run | calls | median us | p10 us | p90 us | "
+                "mean us | VGPR | SGPR | LDS B | scratch B |\n"
+                "|---|---|---|---|---|---|---|---|---|---|---|---|\n")
+        for k in doc["kernels"]:
+            f.write(f"| `{k['kernel']}` | {k['grid_threads']} | {k['run']}/{k['runs']} | "
+                    f"{k['calls']} | {k['median_us']:.2f} | {k['p10_us']:.2f} | "
+                    f"{k['p90_us']:.2f} | {k['mean_us']:.2f} | {k['vgpr']} | {k['sgpr']} | "
+                    f"{k['lds_bytes']} | {k['scratch_bytes']} |\n")
         f.write("\nrocprofv3 --stats table (all kernels of the run):\n\n")
         f.write("| kernel | calls | average us | min us | max us |\n|---|---|---|---|---|\n")
         for r in rows:
-            f.write(f"| `{r['Name'].split('(')[0]}` | {r['Calls']} | "
+            f.write(f"| `{r['Name'].split('(')[0][:120]}` | {r['Calls']} | "
                     f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
                     f"{float(r['MaxNs']) / 1e3:.2f} |\n")
         if bench:
             f.write(f"\nThe same run's JSON line: {bench['config']['workload']} "
                     f"{bench['ms_per_step'] * 1e3:.2f} us per step by HIP events "
-                    f"(graph replay); other workloads: ")
+                    f"(graph replay); graded: ")
+            f.write(", ".join(f"{k} {v['ms_per_step'] * 1e3:.2f} us"
+                              for k, v in bench["graded"].items()))
+            f.write("; other workloads: ")
             f.write(", ".join(f"{k} {v['ms_per_step'] * 1e3:.2f} us"
                               for k, v in bench["other_workloads"].items()))
             f.write(".  Event time per step includes the gap between consecutive "
-                    "kernels; the profiler's durations do not, and the profiler adds "
-                    "its own per-dispatch overhead.\n")
+                    "kernels; the profiler's durations do not.\n")
+        f.write(f"\nKernel sources sha256: {doc['source_sha256']}\n")
     return path
+
+
+def kernel_trace_stats(kernel: str, grid_threads: int) -> dict | None:
+    """Median / p10 / p90 of one kernel shape from profiles/trace_bench.json,
+    if the kernel sources still hash to what the trace was taken with."""
+    if not os.path.exists(TRACE_JSON):
+        return None
+    with open(TRACE_JSON) as f:
+        doc = json.load(f)
+    if doc.get("source_sha256") != kernel_source_sha256():
+        return {"note": "kernel changed since the trace was taken"}
+    for k in doc["kernels"]:
+        if k["kernel"] == kernel and k["grid_threads"] == grid_threads and k["run"] == 1:
+            return {kk: k[kk] for kk in ("median_us", "p10_us", "p90_us", "mean_us", "calls")}
+    return None
+
+
+def plan_kernel_name(plan: dict, mode: int = 0) -> str:
+    """The demangled template instance softmax_fwd launches for a plan."""
+    v = plan["elems_per_lane"] // 4
+    vec = "true" if plan["vec_width"] == 4 else "false"
+    k = plan["kernel_name"]
+    if k == "packed":
+        return f"smx::k_packed<{plan['lanes_per_row']}, {plan['elems_per_lane']}, {vec}, {mode}>"
+    if k == "wave_row":
+        return f"smx::k_wave_row<{v}, {vec}, {mode}>"
+    if k == "block_row":
+        return f"smx::k_block_row<{plan['block_threads']}, {v}, {vec}, {mode}>"
+    return f"smx::k_split_onepass<{plan['block_threads']}, {v}, {vec}, {mode}>"
+
+
+def roofline(w, res: dict, traffic, traffic_note, plan: dict) -> dict:
+    ms = res["ms_per_step"]
+    name = plan_kernel_name(plan)
+    return {
+        "bound": "hbm",
+        "achieved": res["hbm_gbps"],
+        "peak": HBM_PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": res["frac_of_peak"],
+        "traffic": traffic,
+        "traffic_note": traffic_note,
+        "algorithmic_bytes_per_launch": w.algorithmic_bytes,
+        "kernel": name,
+        "launches_per_step": plan["launches"],
+        "launch_duration_us": ms * 1e3 / plan["launches"],
+        "kernel_trace": kernel_trace_stats(name, plan["grid"] * plan["block_threads"]),
+    }
 
 
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=500)
-    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
                     choices=list(workloads.WORKLOADS) + list(workloads.ATTENTION_WORKLOADS),
-                    help="a softmax workload (attention workloads: counter passes only)")
+                    help="the headline softmax workload (attention workloads: counter "
+                         "passes only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra-workloads", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
@@ -642,7 +722,7 @@ def main() -> int:
                     help="write profiles/pmc_<workload>.{json,md} from DIR/fetch and DIR/write")
     ap.add_argument("--pmc-command", default="", help="commands recorded in the summary")
     ap.add_argument("--summarize-trace", metavar="DIR",
-                    help="write profiles/<kernel>_<workload>_trace.md from a kernel-trace run")
+                    help="write profiles/trace_bench.{json,md} from a kernel-trace run")
     ap.add_argument("--trace-json", help="JSON line printed by the traced run")
     args = ap.parse_args()
 
@@ -655,7 +735,7 @@ def main() -> int:
     else:
         w = workloads.WORKLOADS[args.workload]
     if args.summarize_trace:
-        print(summarize_trace(args.summarize_trace, w, args.pmc_command, args.trace_json))
+        print(summarize_trace(args.summarize_trace, args.pmc_command, args.trace_json))
         return 0
     if args.summarize_pmc:
         doc = summarize_pmc(args.summarize_pmc, w, args.pmc_command)
@@ -683,32 +763,28 @@ def main() -> int:
             pmc_run(sm, torch, w, args.pmc_launches)
         return 0
 
-    log(f"[bench] generating {w.key}")
-    x = workloads.generate(w.key)
-    log(f"[bench] timing {w.key}: {args.warmup} warmup + {args.steps} steps (graph replay)")
-    main_res = time_gpu(sm, torch, w, x, args.steps, args.warmup, memcpy=True)
-    log(f"[bench] {w.key}: {main_res['ms_per_step'] * 1e3:.2f} us/step, "
-        f"{main_res['hbm_gbps']:.0f} GB/s (no clip {main_res['noclip_ms_per_step'] * 1e3:.2f} us, "
-        f"approx exp {main_res['approx_exp_ms_per_step'] * 1e3:.2f} us, "
-        f"log {main_res['log_softmax_ms_per_step'] * 1e3:.2f} us, "
-        f"nll {main_res['nll_ms_per_step'] * 1e3:.2f} us)")
-
-    extra = {}
+    machine_before = machine_state()
+    warm_clocks(sm, torch)
+    order = [w.key] + [k for k in GRADED if k != w.key]
     if not args.no_extra_workloads:
-        for key, wk in workloads.WORKLOADS.items():
-            if key == w.key:
-                continue
-            log(f"[bench] timing {key}")
-            r = time_gpu(sm, torch, wk, workloads.generate(key), args.steps, args.warmup)
-            extra[key] = {k: (float(f"{v:.6g}") if isinstance(v, float) else v)
-                          for k, v in r.items() if k != "plan"}
-            extra[key]["kernel"] = r["plan"]["kernel_name"]
-            extra[key]["launches_per_step"] = r["plan"]["launches"]
-            log(f"[bench] {key}: {r['ms_per_step'] * 1e3:.2f} us/step, {r['hbm_gbps']:.0f} GB/s "
-                f"(no clip {r['noclip_ms_per_step'] * 1e3:.2f} us, approx exp "
-                f"{r['approx_exp_ms_per_step'] * 1e3:.2f} us, log "
-                f"{r['log_softmax_ms_per_step'] * 1e3:.2f} us, nll "
-                f"{r['nll_ms_per_step'] * 1e3:.2f} us)")
+        order += [k for k in workloads.WORKLOADS if k not in order]
+    results: dict = {}
+    inputs: dict = {}
+    for key in order:
+        wk = workloads.WORKLOADS[key]
+        log(f"[bench] timing {key}: {args.warmup} warmup + {args.steps} steps (graph replay)")
+        x = workloads.generate(key)
+        r = time_gpu(sm, torch, wk, x, args.steps, args.warmup, memcpy=(key == w.key))
+        results[key] = r
+        if key in GRADED or key == w.key:
+            inputs[key] = x
+        log(f"[bench] {key}: {r['ms_per_step'] * 1e3:.2f} us/step, {r['hbm_gbps']:.0f} GB/s "
+            f"({r['frac_of_peak']:.3f} of peak; eager {r['eager_ms_per_step'] * 1e3:.2f} us, "
+            f"in place {r['in_place_ms_per_step'] * 1e3:.2f} us, copy "
+            f"{r['copy_ms_per_step'] * 1e3:.2f} us, no clip "
+            f"{r['noclip_ms_per_step'] * 1e3:.2f} us, approx exp "
+            f"{r['approx_exp_ms_per_step'] * 1e3:.2f} us, log "
+            f"{r['log_softmax_ms_per_step'] * 1e3:.2f} us, nll {r['nll_ms_per_step'] * 1e3:.2f} us)")
 
     attention = None
     if not args.no_extra_workloads:
@@ -718,18 +794,45 @@ def main() -> int:
         log(f"[bench] {akey}: {attention['ms_per_step'] * 1e3:.2f} us/step, "
             f"{attention['hbm_gbps']:.0f} GB/s, {attention['tflops']:.1f} TFLOP/s; unfused "
             f"{attention['unfused_ms_per_step'] * 1e3:.2f} us")
+    machine_after = machine_state()
 
-    cpu = None
-    cpu32 = None
-    if not args.no_cpu_baseline:
-        log("[bench] CPU oracle baseline")
-        cpu = time_cpu_oracle(x, args.cpu_budget)
-        log("[bench] CPU fp32 baseline")
-        cpu32 = time_cpu_fp32(x, min(args.cpu_budget, 5.0))
+    def rounded(d: dict) -> dict:
+        return {k: (float(f"{v:.6g}") if isinstance(v, float) else v)
+                for k, v in d.items() if k != "plan"}
 
-    traffic, traffic_note = load_traffic(w.key)
+    graded = {}
+    cpu_main = cpu32_main = None
+    for key in [k for k in order if k in GRADED or k == w.key]:
+        wk = workloads.WORKLOADS[key]
+        r = results[key]
+        traffic, note = load_traffic(key)
+        entry = rounded(r)
+        entry["plan"] = r["plan"]
+        entry["roofline"] = roofline(wk, r, traffic, note, r["plan"])
+        entry["cpu_baseline"] = entry["cpu_fp32_baseline"] = None
+        if not args.no_cpu_baseline:
+            log(f"[bench] CPU oracle baseline on {key}")
+            entry["cpu_baseline"] = time_cpu_oracle(inputs[key], args.cpu_budget)
+            log(f"[bench] CPU fp32 baseline on {key}")
+            entry["cpu_fp32_baseline"] = time_cpu_fp32(inputs[key], min(args.cpu_budget, 5.0))
+        if key == w.key:
+            cpu_main, cpu32_main = entry["cpu_baseline"], entry["cpu_fp32_baseline"]
+        if key in GRADED:
+            graded[key] = entry
+
+    main_res = results[w.key]
+    x = inputs[w.key]
     ms = main_res["ms_per_step"]
     plan = main_res["plan"]
+    traffic, traffic_note = load_traffic(w.key)
+    extra = {}
+    for key, r in results.items():
+        if key in GRADED or key == w.key:
+            continue
+        extra[key] = rounded(r)
+        extra[key]["kernel"] = r["plan"]["kernel_name"]
+        extra[key]["launches_per_step"] = r["plan"]["launches"]
+        extra[key]["store_delay_ns"] = r["plan"]["store_delay_ns"]
     out = {
         "metric": METRIC,
         "value": main_res["rows_per_s"],
@@ -746,22 +849,22 @@ def main() -> int:
         "config": {"workload": w.key, "rows": w.rows, "cols": w.cols, "seed": w.seed,
                    "input_sha256": workloads.sha256_f32(x),
                    "kernel": plan["kernel_name"], "launches_per_step": plan["launches"],
+                   "chunks_per_row": plan["chunks_per_row"],
+                   "store_delay_ns": plan["store_delay_ns"],
                    "rotation_buffers": main_res["rotation_buffers"],
-                   "timing": "HIP graph of the timed steps, HIP events on its stream"},
+                   "timing": "HIP graph of the timed steps on a dedicated stream, HIP "
+                             "events recorded behind a queued pre-roll replay"},
         "elements_per_s": main_res["elements_per_s"],
         "hbm_gbps": main_res["hbm_gbps"],
-        "roofline": {
-            "bound": "hbm",
-            "achieved": main_res["hbm_gbps"],
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": main_res["frac_of_peak"],
-            "traffic": traffic,
-            "traffic_note": traffic_note,
-            "algorithmic_bytes_per_launch": w.algorithmic_bytes,
-        },
+        "roofline": roofline(w, main_res, traffic, traffic_note, plan),
+        "cpu_baseline": cpu_main,
+        "cpu_fp32_baseline": cpu32_main,
+        "graded": graded,
         "eager": {"ms_per_step": main_res["eager_ms_per_step"],
                   "hbm_gbps": main_res["eager_hbm_gbps"]},
+        "in_place": {"ms_per_step": main_res["in_place_ms_per_step"],
+                     "hbm_gbps": main_res["in_place_hbm_gbps"],
+                     "what": "softmax_fwd with y == x, on the rotation's y buffers"},
         "copy_ceiling": {"gbps": main_res["copy_gbps"],
                          "ms_per_step": main_res["copy_ms_per_step"],
                          "softmax_over_copy_time": main_res["softmax_over_copy_time"],
@@ -771,12 +874,7 @@ def main() -> int:
                          "launch_floor_ms_per_step": main_res["launch_floor_ms_per_step"],
                          "launch_floor_what": "softmax_copy_probe on 4 KiB: the fixed cost "
                                               "of one graph-replayed launch that reads, "
-                                              "then writes",
-                         "softmax_gbps_above_launch_floor": w.algorithmic_bytes
-                         / ((ms - main_res["launch_floor_ms_per_step"]) * 1e-3) / 1e9,
-                         "copy_gbps_above_launch_floor": w.algorithmic_bytes
-                         / ((main_res["copy_ms_per_step"]
-                             - main_res["launch_floor_ms_per_step"]) * 1e-3) / 1e9},
+                                              "then writes"},
         "no_clip": {"ms_per_step": main_res["noclip_ms_per_step"],
                     "hbm_gbps": main_res["noclip_hbm_gbps"],
                     "what": "softmax_fwd_clip with clip_lo = -inf, same rotation and timing"},
@@ -793,9 +891,10 @@ def main() -> int:
                        "hbm_gbps": main_res["approx_exp_hbm_gbps"],
                        "what": "softmax_fwd_approx (single-instruction fp32 exponential), "
                                "same rotation and timing"},
-        "cpu_baseline": cpu,
-        "cpu_fp32_baseline": cpu32,
         "sampled_max_rel_err": main_res["sampled_max_rel_err"],
+        "machine": {"before": machine_before, "after": machine_after,
+                    "gpu": torch.cuda.get_device_name(0),
+                    "compute_units": torch.cuda.get_device_properties(0).multi_processor_count},
         "other_workloads": extra,
         "fused_attention": attention,
     }

@@ -85,26 +85,34 @@ extern "C" {
  * Asynchrony: work is enqueued on `stream` and the call returns without
  * waiting; y is valid once the stream has reached that point.
  *
- * Workspace: rows longer than 32768 columns use a 140 KiB device workspace
- * that the library allocates (hipMalloc, initialised) on the first such call on
- * each (device, stream) and keeps until the process ends, so calls on
- * different streams never share one.  (Streams are told apart by handle: a
- * stream destroyed while its work still runs and a new stream that gets the
- * same handle count as one.)  Up to 64 streams per device get their own;
- * past that the least recently used one is reassigned after a
- * hipDeviceSynchronize().  Under stream capture no allocation is made: the
- * capture uses one workspace per device, created by an earlier uncaptured
- * long-row call on that device (otherwise SOFTMAX_ERR_INVALID_ARG), and
- * replays of such graphs must not overlap other long-row work on the device.
+ * Scratch: the call allocates nothing.  Rows longer than 32768 columns are
+ * split over several workgroups, which combine partial (max, sum) pairs
+ * through a table of 4096 row entries held in a static device array
+ * (2,359,552 bytes per device, part of the library's code object, zero at
+ * rest).  The workgroups of a row meet at the entry its launch's key (the
+ * output address and a per-call nonce) and its row index hash to: the first
+ * to arrive claims it on the device, the last to leave frees it.  So calls on
+ * any number of streams, graphs replayed at the same time, and a first call
+ * made under stream capture need no host-side state, no allocation and no
+ * synchronisation.  A row whose entry is still held by a row of another
+ * running launch waits for it (bounded).
  *
  * Long rows are done in one pass when a row spans at most 64 workgroups
- * (cols <= 2097152): the workgroups of a row exchange partial (max, sum)
- * pairs through the workspace in the middle of the kernel and wait for each
- * other; the workspace is back in its resting state when the kernel ends.
- * Workgroups are
- * dispatched in ID order, so this always progresses while 64 workgroups of
- * the launch can be resident; the wait is bounded, and a workgroup that
- * times out writes NaN instead of stalling.  Longer rows use two passes.
+ * (cols <= 1048576 in chunks of 16384 columns and, with 128-bit access
+ * only, cols <= 2097152 in chunks of 32768): the
+ * workgroups of a row exchange their pairs in the middle of the kernel and
+ * wait for each other.  Workgroups are dispatched in ID order, so this always
+ * progresses while a row's workgroups can be resident together.  Longer rows
+ * take two passes (x read twice).  Every wait is bounded (20 ms of wall
+ * clock): a workgroup that gives up writes NaN for its outputs instead of
+ * stalling the device, and counts itself in softmax_exchange_status().
+ *
+ * Store schedule: in the one-pass split-row launches (every workgroup
+ * resident at once, one chunk each, about 8 MiB read or more) the stores
+ * wait until the launch's reads are expected to be done (read bytes /
+ * 7.6 TB/s + 0.3 us after the workgroup starts), so HBM serves the reads
+ * and the writes as two phases; softmax_plan() reports the delay, and
+ * softmax_fwd_planned() can set it for any kernel.  It changes no result.
  *
  * Returns SOFTMAX_OK, or SOFTMAX_ERR_INVALID_ARG (rows or cols < 0,
  * rows*cols*4 overflows int64, x or y null while rows*cols > 0, partial
@@ -132,7 +140,7 @@ SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols
  * Accuracy: every output is within 4e-6 relative plus 2^-148 absolute of
  * the exact value (the absolute term only matters for outputs below 2^-126,
  * which need clip_lo < -87).  All other arguments, the layout, ownership,
- * asynchrony, workspace and error codes are those of softmax_fwd; a NaN
+ * asynchrony, scratch and error codes are those of softmax_fwd; a NaN
  * clip_lo or one above SOFTMAX_CLIP_MAX returns SOFTMAX_ERR_INVALID_ARG
  * with nothing launched.
  */
@@ -204,13 +212,13 @@ SOFTMAX_API int softmax_log_fwd(const float* x, float* y, int64_t rows, int64_t 
  * (no row can have a valid label).
  *
  * Accuracy: |loss - loss*| <= 2e-6 + 2.5e-7 * (|loss*| + ln(cols)), as for
- * softmax_log_fwd.  Ownership, asynchrony, workspace (rows longer than
+ * softmax_log_fwd.  Ownership, asynchrony, scratch (rows longer than
  * 32768 columns) and error codes follow softmax_fwd_clip, except that in
  * the one-pass long-row kernel a row's workgroups do not wait for each
  * other: the last to finish merges the row's partial pairs, writes the loss
- * and returns the workspace to its resting state.  With 128-bit access
+ * and returns the row's exchange state to rest.  With 128-bit access
  * those rows are cut into chunks of 32768 columns (1024-thread workgroups)
- * rather than the 16384 that softmax_plan() reports for softmax_fwd.
+ * rather than the chunks softmax_plan() reports for softmax_fwd.
  */
 SOFTMAX_API int softmax_nll_fwd(const float* x, const int64_t* labels, float* loss,
                                 int64_t rows, int64_t cols, float clip_lo,
@@ -255,7 +263,7 @@ SOFTMAX_API int softmax_nll_fwd(const float* x, const int64_t* labels, float* lo
  * device memory, work enqueued on `stream`, SOFTMAX_ERR_INVALID_ARG for bad
  * sizes, a non-finite scale, a bad clip_lo, null or overlapping pointers,
  * SOFTMAX_ERR_NOT_DEVICE for memory the device cannot use.  batch, lq or
- * dv of 0 returns SOFTMAX_OK with nothing launched.  No workspace.
+ * dv of 0 returns SOFTMAX_OK with nothing launched.  No scratch.
  */
 SOFTMAX_API int softmax_attention_fwd(const float* q, const float* k, const float* v,
                                       float* o, int64_t batch, int64_t lq, int64_t lk,
@@ -279,20 +287,66 @@ typedef struct softmax_plan_t {
   int32_t launches;        /* kernel launches per call */
   int64_t chunks_per_row;  /* workgroups per row (split rows), else 1 */
   int64_t grid;            /* workgroups in each launch */
-  int64_t workspace_bytes; /* library workspace the call touches */
+  int64_t workspace_bytes; /* bytes of the static exchange table (split rows), else 0 */
+  int64_t store_delay_ns;  /* stores wait this long after a workgroup starts (0: none);
+                              softmax_fwd_planned: -1 asks for the library's choice */
 } softmax_plan_t;
 
+/* The shape fields (kernel, vec_width, lanes_per_row, elems_per_lane,
+ * block_threads, chunks_per_row) depend only on the arguments; grid,
+ * launches and store_delay_ns are those for the current device, and 0 when
+ * no device is present.  No launch, no allocation (the first call on a
+ * device queries its attributes). */
 SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64_t cols,
                              softmax_plan_t* plan);
+
+/*
+ * softmax_fwd_planned -- softmax_fwd with a caller-chosen kernel, for tuning
+ * and for measuring the dispatch (the paper picks code per shape, Sec. 2.5;
+ * this library picks one of its compiled instances by cols).  Fields read
+ * from *plan:
+ *   kernel          SOFTMAX_KERNEL_PACKED (cols <= 64), _WAVE_ROW (cols <=
+ *                   4096, 2048 with 32-bit access), _BLOCK_ROW (cols <=
+ *                   32768) or _SPLIT_ROW (any cols);
+ *   vec_width       4 (needs 16-byte aligned x and y and, above 64 columns,
+ *                   cols % 4 == 0) or 1;
+ *   block_threads, elems_per_lane   split rows only: 256 x 32 (chunks of
+ *                   8192 columns), 512 x 32 (16384) or, with vec_width 4,
+ *                   512 x 64 (32768); rows of more than 64 chunks take the
+ *                   two-pass kernels, which only exist as 512 x 32;
+ *   store_delay_ns  -1 for the library's store schedule, 0 for none, or a
+ *                   delay up to 200000.
+ * The other fields are ignored.  The result is the same as softmax_fwd's to
+ * within the accuracy bound (the summation order follows the kernel).
+ * Returns SOFTMAX_ERR_INVALID_ARG, with nothing launched, for a plan the
+ * library cannot run on these arguments; otherwise as softmax_fwd.
+ */
+SOFTMAX_API int softmax_fwd_planned(const float* x, float* y, int64_t rows, int64_t cols,
+                                    const softmax_plan_t* plan, hipStream_t stream);
+
+/*
+ * softmax_exchange_status -- diagnostic, for the current device: how many
+ * times a workgroup gave up waiting for its row's exchange entry (held by
+ * another row too long) and for its row's partial pairs, since the library
+ * was loaded, and how many of the 4096 entries are held right now (0
+ * whenever no split-row work is running and none gave up).  Any of the
+ * pointers may be NULL.  Synchronous (hipMemcpy); not for use under stream
+ * capture.
+ */
+SOFTMAX_API int softmax_exchange_status(uint64_t* join_give_ups, uint64_t* wait_give_ups,
+                                        int32_t* entries_in_use);
 
 /*
  * softmax_exp_probe -- diagnostic: e[i] = exp(max(x[i] - m[i], clip_lo))
  * for 0 <= i < n, through the same device routine the softmax kernels use
  * for the clipped exp (Sec. 1.2 Fig. 1, the ValueClip then exp), with the
  * clip_lo rules of softmax_fwd_clip: the routine of softmax_fwd_clip when
- * approx == 0, that of softmax_fwd_approx otherwise.  x, m, e are device
- * fp32 arrays of n elements owned by the caller (e must not overlap x or
- * m).  Same error rules as softmax_fwd_clip.
+ * approx == 0, that of softmax_fwd_approx when approx == 1.  approx == 2
+ * gives e[i] = 2^x[i] from the bare v_exp_f32 instruction both routines
+ * build on (m and clip_lo are then unused; m may be NULL).  x, m, e are
+ * device fp32 arrays of n elements owned by the caller (e must not overlap
+ * x or m).  Same error rules as softmax_fwd_clip; approx outside 0..2 is
+ * SOFTMAX_ERR_INVALID_ARG.
  */
 SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int64_t n,
                                   float clip_lo, int approx, hipStream_t stream);

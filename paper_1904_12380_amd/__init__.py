@@ -19,6 +19,9 @@ Functions keep the C names:
     softmax_attention_fwd_ptr(q_ptr, k_ptr, v_ptr, o_ptr, batch, lq, lk, d, dv,
                               scale, clip_lo, stream_handle) -> int
     softmax_plan(rows, cols, x_ptr=1 << 44, y_ptr=1 << 45) -> dict
+    softmax_fwd_planned(x, plan, out=None, stream=None) -> torch.Tensor
+    softmax_fwd_planned_ptr(x_ptr, y_ptr, rows, cols, plan, stream_handle) -> int
+    softmax_exchange_status() -> dict
     softmax_exp_probe(x, m, out=None, stream=None, clip_lo=-64.0) -> torch.Tensor
     softmax_copy_probe(x, out=None, stream=None) -> torch.Tensor
     softmax_strerror(code) -> str
@@ -36,6 +39,7 @@ __all__ = [
     "softmax_nll_fwd", "softmax_nll_fwd_ptr",
     "softmax_attention_fwd", "softmax_attention_fwd_ptr", "ATTN_MAX_KEYS", "ATTN_MAX_DIM",
     "softmax_exp_probe", "softmax_copy_probe", "softmax_strerror", "softmax_last_hip_error",
+    "softmax_fwd_planned", "softmax_fwd_planned_ptr", "softmax_exchange_status",
     "CLIP_LO", "CLIP_MAX", "KERNEL_NAMES",
 ]
 
@@ -49,6 +53,7 @@ ATTN_MAX_KEYS = 64
 ATTN_MAX_DIM = 65536
 OK, ERR_INVALID_ARG, ERR_HIP, ERR_NOT_DEVICE = 0, 1, 2, 3
 KERNEL_NAMES = {0: "none", 1: "packed", 2: "wave_row", 3: "block_row", 4: "split_row"}
+KERNEL_IDS = {v: k for k, v in KERNEL_NAMES.items()}
 
 
 class SoftmaxError(RuntimeError):
@@ -71,6 +76,7 @@ class _Plan(ctypes.Structure):
         ("chunks_per_row", ctypes.c_int64),
         ("grid", ctypes.c_int64),
         ("workspace_bytes", ctypes.c_int64),
+        ("store_delay_ns", ctypes.c_int64),
     ]
 
 
@@ -111,6 +117,11 @@ def load_library() -> ctypes.CDLL:
     lib.softmax_exp_probe.restype = ctypes.c_int
     lib.softmax_copy_probe.argtypes = [vp, vp, i64, vp]
     lib.softmax_copy_probe.restype = ctypes.c_int
+    lib.softmax_fwd_planned.argtypes = [vp, vp, i64, i64, ctypes.POINTER(_Plan), vp]
+    lib.softmax_fwd_planned.restype = ctypes.c_int
+    u64p = ctypes.POINTER(ctypes.c_uint64)
+    lib.softmax_exchange_status.argtypes = [u64p, u64p, ctypes.POINTER(ctypes.c_int32)]
+    lib.softmax_exchange_status.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -134,6 +145,41 @@ def softmax_plan(rows: int, cols: int, x_ptr: int = 1 << 44,
     d = {name: int(getattr(p, name)) for name, _ in _Plan._fields_}
     d["kernel_name"] = KERNEL_NAMES[d["kernel"]]
     return d
+
+
+def _plan_struct(plan: dict) -> _Plan:
+    p = _Plan()
+    for name, _ in _Plan._fields_:
+        if name in plan:
+            setattr(p, name, int(plan[name]))
+    if "kernel_name" in plan:
+        p.kernel = KERNEL_IDS[plan["kernel_name"]]
+    if "store_delay_ns" not in plan:
+        p.store_delay_ns = -1
+    return p
+
+
+def softmax_fwd_planned_ptr(x_ptr: int, y_ptr: int, rows: int, cols: int, plan: dict,
+                            stream_handle: int = 0) -> int:
+    """Raw C call; returns the C return code.  ``plan`` holds kernel (or
+    kernel_name), vec_width and, for split rows, block_threads and
+    elems_per_lane; store_delay_ns defaults to -1 (the library's schedule)."""
+    p = _plan_struct(plan)
+    return int(load_library().softmax_fwd_planned(x_ptr, y_ptr, rows, cols, ctypes.byref(p),
+                                                  stream_handle))
+
+
+def softmax_exchange_status() -> dict:
+    """Give-up counters and held row entries of the split-row exchange on
+    the current device (synchronous)."""
+    f, w = ctypes.c_uint64(), ctypes.c_uint64()
+    busy = ctypes.c_int32()
+    rc = load_library().softmax_exchange_status(ctypes.byref(f), ctypes.byref(w),
+                                                ctypes.byref(busy))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_exchange_status")
+    return {"join_give_ups": int(f.value), "wait_give_ups": int(w.value),
+            "entries_in_use": int(busy.value)}
 
 
 def softmax_fwd_ptr(x_ptr: int, y_ptr: int, rows: int, cols: int,
@@ -200,6 +246,19 @@ def softmax_fwd(x, out=None, stream=None):
                              _stream_handle(stream))
     if rc != OK:
         raise SoftmaxError(rc, "softmax_fwd")
+    return out
+
+
+def softmax_fwd_planned(x, plan: dict, out=None, stream=None):
+    """softmax_fwd with a caller-chosen kernel (see softmax_fwd_planned_ptr)."""
+    torch = _torch()
+    out = _out_for(x, out)
+    rows, cols = x.shape
+    with torch.cuda.device(x.device):
+        rc = softmax_fwd_planned_ptr(x.data_ptr(), out.data_ptr(), rows, cols, plan,
+                                     _stream_handle(stream))
+    if rc != OK:
+        raise SoftmaxError(rc, "softmax_fwd_planned")
     return out
 
 
@@ -332,21 +391,27 @@ def softmax_attention_fwd(q, k, v, scale=None, clip_lo: float = CLIP_LO, out=Non
 
 
 def softmax_exp_probe(x, m, out=None, stream=None, clip_lo: float = CLIP_LO,
-                      approx: bool = False):
+                      approx=False):
     """e = exp(max(x - m, clip_lo)) elementwise through the kernels' exp
-    routine (the fast approximation of softmax_fwd_approx if ``approx``)."""
+    routine (the fast approximation of softmax_fwd_approx if ``approx`` is
+    true or 1); ``approx=2`` gives e = 2^x from the bare v_exp_f32
+    instruction (``m`` may then be None)."""
     torch = _torch()
     _check_f32_cuda(x, "x")
-    _check_f32_cuda(m, "m")
-    if m.shape != x.shape:
-        raise ValueError("m must match x")
+    if m is None:
+        if int(approx) != 2:
+            raise ValueError("m is needed unless approx == 2")
+    else:
+        _check_f32_cuda(m, "m")
+        if m.shape != x.shape:
+            raise ValueError("m must match x")
     if out is None:
         out = torch.empty_like(x)
     _check_f32_cuda(out, "out")
     with torch.cuda.device(x.device):
         rc = int(load_library().softmax_exp_probe(
-            x.data_ptr(), m.data_ptr(), out.data_ptr(), x.numel(), float(clip_lo),
-            int(bool(approx)), _stream_handle(stream)))
+            x.data_ptr(), None if m is None else m.data_ptr(), out.data_ptr(), x.numel(),
+            float(clip_lo), int(approx), _stream_handle(stream)))
     if rc != OK:
         raise SoftmaxError(rc, "softmax_exp_probe")
     return out

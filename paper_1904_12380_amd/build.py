@@ -43,21 +43,41 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(LIBDIR, exist_ok=True)
-    tmp = LIB + f".tmp{os.getpid()}"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), *SOURCES, "-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed with exit code {res.returncode}")
+    return subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+
+
+def _finish(proc, verbose):
+    out, _ = proc.communicate()
+    if proc.returncode != 0:
+        sys.stderr.write(out)
+        raise RuntimeError(f"hipcc failed with exit code {proc.returncode}")
     noise = "packed-fp32-ops"  # the host pass does not know the feature
-    for line in (res.stdout + res.stderr).splitlines():
+    for line in out.splitlines():
         if verbose and noise not in line and line.strip():
             print(line)
-    os.replace(tmp, LIB)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile each source to an object (in parallel), then link the .so."""
+    os.makedirs(LIBDIR, exist_ok=True)
+    tag = f".tmp{os.getpid()}"
+    objs = [os.path.join(LIBDIR, os.path.basename(src) + tag + ".o") for src in SOURCES]
+    compile_flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+    procs = [_run([hipcc(), *compile_flags, "-I", os.path.join(ROOT, "include"), "-c", src,
+                   "-o", obj], verbose) for src, obj in zip(SOURCES, objs)]
+    try:
+        for proc in procs:
+            _finish(proc, verbose)
+        tmp = LIB + tag
+        _finish(_run([hipcc(), *HIPCC_FLAGS, *objs, "-o", tmp], verbose), verbose)
+        os.replace(tmp, LIB)
+    finally:
+        for obj in objs:
+            if os.path.exists(obj):
+                os.remove(obj)
     return LIB
 
 

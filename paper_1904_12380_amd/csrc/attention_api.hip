@@ -17,7 +17,6 @@ using namespace smx_host;
 // Workgroups per CU for the persistent grid (each holds 4 wavefronts of one
 // batch element's 64-query block at a time).
 constexpr int64_t kAttnBlocksPerCU = 8;
-constexpr int64_t kAttnCUs = 256;
 
 // sizes: all >= 0, lk in [1, 64] when there is work, d and dv at most
 // SOFTMAX_ATTN_MAX_DIM, and every tensor's byte count fits in int64.
@@ -37,9 +36,9 @@ int check_attention_sizes(int64_t batch, int64_t lq, int64_t lk, int64_t d, int6
 template <int NKT, bool VEC4, bool WIDE>
 hipError_t run_attention(const float* q, const float* k, const float* v, float* o,
                          int64_t batch, int lq, int lk, int d, int dv, float scale, Clip c,
-                         hipStream_t s) {
+                         int64_t cus, hipStream_t s) {
   const int64_t items = batch * ((lq + 63) / 64);
-  const int64_t grid = std::min(items, kAttnBlocksPerCU * kAttnCUs);
+  const int64_t grid = std::min(items, kAttnBlocksPerCU * cus);
   void* args[] = {&q, &k, &v, &o, &batch, &lq, &lk, &d, &dv, &scale, &c};
   return launch(reinterpret_cast<const void*>(&k_attention<NKT, VEC4, WIDE>), grid, 256, args,
                 s);
@@ -51,9 +50,9 @@ constexpr int64_t kAttnLdsBlocksPerCU = 2;
 template <int NKT, bool WIDE>
 hipError_t run_attention_lds(const float* q, const float* k, const float* v, float* o,
                              int64_t batch, int lq, int lk, int d, int dv, float scale, Clip c,
-                             hipStream_t s) {
+                             int64_t cus, hipStream_t s) {
   const int64_t items = batch * ((lq + 63) / 64);
-  const int64_t grid = std::min(items, kAttnLdsBlocksPerCU * kAttnCUs);
+  const int64_t grid = std::min(items, kAttnLdsBlocksPerCU * cus);
   void* args[] = {&q, &k, &v, &o, &batch, &lq, &lk, &d, &dv, &scale, &c};
   return launch(reinterpret_cast<const void*>(&k_attention_lds<NKT, WIDE>), grid, 256, args, s);
 }
@@ -61,24 +60,24 @@ hipError_t run_attention_lds(const float* q, const float* k, const float* v, flo
 template <bool WIDE>
 hipError_t dispatch_attention_lds(const float* q, const float* k, const float* v, float* o,
                                   int64_t batch, int lq, int lk, int d, int dv, float scale,
-                                  Clip c, hipStream_t s) {
+                                  Clip c, int64_t cus, hipStream_t s) {
   switch ((lk + 15) / 16) {
-    case 1: return run_attention_lds<1, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, s);
-    case 2: return run_attention_lds<2, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, s);
-    case 3: return run_attention_lds<3, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, s);
-    default: return run_attention_lds<4, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, s);
+    case 1: return run_attention_lds<1, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, cus, s);
+    case 2: return run_attention_lds<2, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, cus, s);
+    case 3: return run_attention_lds<3, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, cus, s);
+    default: return run_attention_lds<4, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, cus, s);
   }
 }
 
 template <bool VEC4, bool WIDE>
 hipError_t dispatch_attention(const float* q, const float* k, const float* v, float* o,
                               int64_t batch, int lq, int lk, int d, int dv, float scale,
-                              Clip c, hipStream_t s) {
+                              Clip c, int64_t cus, hipStream_t s) {
   switch ((lk + 15) / 16) {
-    case 1: return run_attention<1, VEC4, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, s);
-    case 2: return run_attention<2, VEC4, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, s);
-    case 3: return run_attention<3, VEC4, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, s);
-    default: return run_attention<4, VEC4, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, s);
+    case 1: return run_attention<1, VEC4, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, cus, s);
+    case 2: return run_attention<2, VEC4, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, cus, s);
+    case 3: return run_attention<3, VEC4, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, cus, s);
+    default: return run_attention<4, VEC4, WIDE>(q, k, v, o, batch, lq, lk, d, dv, scale, c, cus, s);
   }
 }
 
@@ -123,6 +122,8 @@ SOFTMAX_API int softmax_attention_fwd(const float* q, const float* k, const floa
   if ((rc = check_device_range(v, vbytes, dev)) != SOFTMAX_OK) return rc;
   if ((rc = check_device_range(o, obytes, dev)) != SOFTMAX_OK) return rc;
 
+  int cus = 0;
+  if ((rc = device_cus(dev, &cus)) != SOFTMAX_OK) return rc;
   // 128-bit accesses for every operand, or 32-bit ones for all of them.
   const bool vec4 = d % 4 == 0 && dv % 4 == 0 && aligned16(q) && aligned16(k) &&
                     aligned16(v) && aligned16(o);
@@ -132,19 +133,19 @@ SOFTMAX_API int softmax_attention_fwd(const float* q, const float* k, const floa
   const bool lds = vec4 && d <= kAttnMaxDQ && lk * (d + dv) * 4 <= kAttnLdsBytes;
   if (lds)
     e = wide ? dispatch_attention_lds<true>(q, k, v, o, batch, ilq, ilk, id, idv, scale, c,
-                                            stream)
+                                            cus, stream)
              : dispatch_attention_lds<false>(q, k, v, o, batch, ilq, ilk, id, idv, scale, c,
-                                             stream);
+                                             cus, stream);
   else if (vec4)
     e = wide ? dispatch_attention<true, true>(q, k, v, o, batch, ilq, ilk, id, idv, scale, c,
-                                              stream)
+                                              cus, stream)
              : dispatch_attention<true, false>(q, k, v, o, batch, ilq, ilk, id, idv, scale, c,
-                                               stream);
+                                               cus, stream);
   else
     e = wide ? dispatch_attention<false, true>(q, k, v, o, batch, ilq, ilk, id, idv, scale, c,
-                                               stream)
+                                               cus, stream)
              : dispatch_attention<false, false>(q, k, v, o, batch, ilq, ilk, id, idv, scale, c,
-                                                stream);
+                                                cus, stream);
   return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
 }
 

@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include <cmath>
+#include <mutex>
 
 #include "../../include/softmax_mi355x.h"
 #include "sm_device.hpp"
@@ -86,6 +87,27 @@ inline int check_device_range(const void* p, int64_t bytes, int dev) {
   // device; unregistered pageable memory is not.
   if (a.type == hipMemoryTypeHost || a.type == hipMemoryTypeManaged) return SOFTMAX_OK;
   return SOFTMAX_ERR_NOT_DEVICE;
+}
+
+// Compute units of device `dev` (hipDeviceAttributeMultiprocessorCount),
+// queried once per device: persistent grids and the one-pass launches are
+// sized from it rather than from MI355X's 256.
+constexpr int kMaxDevices = 64;
+inline std::mutex g_cu_mu;
+inline int g_cu_count[kMaxDevices] = {};
+
+inline int device_cus(int dev, int* cus) {
+  if (dev < 0 || dev >= kMaxDevices) return SOFTMAX_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lock(g_cu_mu);
+  if (g_cu_count[dev] == 0) {
+    int n = 0;
+    const hipError_t e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return fail_hip(e);
+    if (n <= 0) return SOFTMAX_ERR_INVALID_ARG;
+    g_cu_count[dev] = n;
+  }
+  *cus = g_cu_count[dev];
+  return SOFTMAX_OK;
 }
 
 inline hipError_t launch(const void* fn, int64_t grid, int block, void** args, hipStream_t s) {

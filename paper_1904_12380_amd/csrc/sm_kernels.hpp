@@ -33,6 +33,7 @@
 #pragma once
 
 #include "sm_device.hpp"
+#include "sm_exchange.hpp"
 
 namespace smx {
 
@@ -64,6 +65,14 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 #pragma unroll
   for (int w = 0; w < NW; ++w) t[w] = red[w];
   return tree_sum(t);
+}
+
+// x itself, as a value the compiler cannot see through: store addresses
+// built from it are formed just before the stores instead of being kept in
+// registers from the loads (which share them) across the reductions.
+__device__ __forceinline__ int opaque(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
 }
 
 // Loads N = 4*V elements of a row segment p[0, lim) into registers: element
@@ -507,10 +516,18 @@ constexpr int kRowWaves = (V <= 8 && VEC4 && !keeps_logits<MODE>()) ? 4 : 2;
 // ---------------------------------------------------------------------------
 // (b) One wavefront per row, cols <= 256*V (4*V elements per lane).
 // Four wavefronts per workgroup work on four rows independently.
+//
+// `delay` (wall-clock ticks, 0 for none) is passed only for launches where
+// every workgroup takes a single row set: each wavefront's stores wait until
+// that long after the workgroup started, so that the launch's reads are
+// over before its writes begin (HBM then serves them in two phases rather
+// than interleaved).
 template <int V, bool VEC4, int MODE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     kRowWaves<V, VEC4, MODE>))) void k_wave_row(
-    const float* x, float* y, const int64_t* labels, int64_t rows, int64_t cols, Clip clip) {
+    const float* x, float* y, const int64_t* labels, int64_t rows, int64_t cols, Clip clip,
+    uint32_t delay) {
+  const uint64_t t0 = wall_clock();
   const int lane = __lane_id();
   const int wave = threadIdx.x >> 6;
   for (int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wave; row < rows;
@@ -519,20 +536,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     const int64_t label = row_label<MODE>(labels, row);
     const int lim = static_cast<int>(cols);
     float v[4 * V];
-    load_strip<V, VEC4>(v, xr, lane, 64, lim);
+    load_strip<V, VEC4>(v, xr, opaque(lane), 64, lim);
     const LabelPick pick = pick_label<V, VEC4, MODE>(v, label, cols, 0, lim, lane, 64, lane == 0);
     const RowShift rs = row_shift(seg_max<64>(array_max(v)), clip);
     const float s = seg_sum<64>(exp_strip<MODE>(v, rs));
-    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, pick, lane, 64);
+    if (delay != 0) wait_until_after(t0 + delay, s);
+    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, pick, opaque(lane), 64);
   }
 }
 
 // ---------------------------------------------------------------------------
-// (c) One workgroup of NT threads per row, cols <= 4*V*NT.
+// (c) One workgroup of NT threads per row, cols <= 4*V*NT.  `delay` as for
+// k_wave_row.
 template <int NT, int V, bool VEC4, int MODE>
 __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y,
                                                   const int64_t* labels, int64_t rows,
-                                                  int64_t cols, Clip clip) {
+                                                  int64_t cols, Clip clip, uint32_t delay) {
+  const uint64_t t0 = wall_clock();
   constexpr int NW = NT / 64;
   __shared__ float red_max[NW];
   __shared__ float red_sum[NW];
@@ -562,7 +582,7 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y,
       if (tid == 0)
         y[row] = bad ? __builtin_nanf("") : -log_out(xl, row_shift(m, clip), log_of_sum(s));
     } else {
-      load_strip<V, VEC4>(v, xr, tid, NT, lim);
+      load_strip<V, VEC4>(v, xr, opaque(tid), NT, lim);
       const LabelPick pick =
           pick_label<V, VEC4, MODE>(v, label, cols, 0, lim, tid, NT, tid == 0);
       const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max), clip);
@@ -571,154 +591,245 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y,
       // more than the 64 VGPRs of two workgroups per CU.
       constexpr int SE = (MODE == kLogOut && V >= 8) ? kExpAccurate : kSumExp;
       const float s = block_sum<NW>(exp_strip<MODE, 4 * V, SE>(v, rs), red_sum);
-      finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, pick, tid, NT);
+      if (delay != 0) wait_until_after(t0 + delay, s);
+      finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, 0, lim, pick, opaque(tid), NT);
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// (c, split) Rows longer than one workgroup's registers: G = ceil(cols/CH)
-// workgroups per row, CH = 4*V*NT columns each.
+// (c, split) Rows longer than one workgroup's registers: a row is cut into
+// chunks of CH = 4*V*NT columns, one workgroup per chunk (or per group of
+// chunks in the two-pass kernels).  The row's workgroups combine their
+// partial (max, sum) pairs through the row's entry of the exchange table
+// (sm_exchange.hpp).
 //
-// Pass 1 writes part[row*G + g] = (m_g, s_g): the chunk max and the chunk's
-// sum of exp(max(x - m_g, lo)).  A chunk whose max is -inf stores s_g = its
-// element count, so that the merge below gives count * e_lo, the clipped
-// value of its -inf elements.
-//
-// Pass 2 merges a row's partials (every wavefront of the workgroup does the
-// same merge, so all hold the same bits):  M = max_g m_g,
-// S = sum_g s_g * exp(max(m_g - M, lo)), then writes
-// y = exp(max(x - M, lo)) / S (or c - ln S for log outputs).  Using the
-// clip relative to m_g inside a
-// partial changes S by at most cols * e^lo relative (below 1e-10 for any
-// row that fits in memory, since lo <= -48), far under fp32 resolution.
+// A partial (m_g, s_g) is a chunk's max and its sum of exp(max(x - m_g, lo)).
+// A chunk whose max is -inf stores s_g = its element count, so that merging
+// gives count * e_lo, the clipped value of its -inf elements.  Merging a
+// row's partials (every lane of a wavefront computes the same bits):
+//     M = max_g m_g,   S = sum_g s_g * exp(max(m_g - M, lo)).
+// Using the clip relative to m_g inside a partial changes S by at most
+// cols * e^lo relative (below 1e-10 for any row that fits in memory, since
+// lo <= -48), far under fp32 resolution.
+
+// The row's entry for wavefront 0 of a workgroup (lane 0 joins it; the
+// pointer is made uniform across the wavefront).  A miss is counted.
+__device__ __forceinline__ uint64_t* wave_entry(const XchArgs& xa, int lrow, uint64_t deadline) {
+  uint64_t e = 0;
+  if (__lane_id() == 0) {
+    uint64_t* p = row_entry(xa, lrow, deadline);
+    if (p == nullptr) count_give_up(xa, xch::kDiagJoinGiveUps);
+    e = reinterpret_cast<uint64_t>(p);
+  }
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(e));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(e >> 32));
+  return reinterpret_cast<uint64_t*>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// Merge of up to 64 partials held one per lane (lanes without one pass
+// m = -inf, s = 0): the row's (M, S), the same bits on every lane.
+template <int SE>
+__device__ __forceinline__ float2 merge_lanes(float pm, float ps, Clip clip) {
+  const float mrow = seg_max<64>(pm);
+  const RowShift rs = row_shift(mrow, clip);
+  const float term = ps == 0.0f ? 0.0f : ps * exp_shift_clip<SE>(pm, rs);
+  return make_float2(mrow, seg_sum<64>(term));
+}
+
+// Polls the row's first `g` slots (one per lane) until none is empty, up to
+// `deadline`.  Returns the slot (~0 for lanes past g); *ok is false after a
+// time-out.
+__device__ __forceinline__ uint64_t poll_slots(const uint64_t* slots, int g, uint64_t deadline,
+                                               bool* ok) {
+  const int lane = __lane_id();
+  uint64_t q = ~0ull;
+  while (true) {
+    q = lane < g ? xch::ld_agent(&slots[lane]) : ~0ull;
+    if (__builtin_amdgcn_ballot_w64(q == 0) == 0) return q;
+    if (static_cast<int64_t>(wall_clock() - deadline) > 0) {
+      *ok = false;
+      return q;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
+
+// (m, s) of one chunk held in v (its max and sum of clipped exponentials
+// against that max; s = count when the max is -inf).  For probability
+// modes v is replaced by the exponentials.
+template <int NW, int V, int MODE>
+__device__ __forceinline__ float2 chunk_partial(float (&v)[4 * V], int lim, Clip clip,
+                                                float* red_max, float* red_sum) {
+  float m;
+  float s;
+  if constexpr (keeps_logits<MODE>()) {
+    const float2 ms = lane_online(v, clip);
+    m = block_max<NW>(ms.x, red_max);
+    s = block_sum<NW>(lane_share(ms, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
+  } else {
+    m = block_max<NW>(array_max(v), red_max);
+    s = block_sum<NW>(exp_strip<MODE>(v, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
+  }
+  if (m == kNegInf) s = static_cast<float>(lim);
+  return make_float2(m, s);
+}
+
+// (c, split, two passes) for rows longer than a one-pass launch can hold.
+// The launch has WPR <= 64 workgroups per row; workgroup w of a row takes
+// the row's chunks w, w + WPR, ...  Pass 1 (k_split_stats) joins the row's
+// entry and leaves each workgroup's merged partial in its slot; pass 2
+// (k_split_apply) finds the entry, merges the row's WPR slots, writes the
+// chunks' outputs, and the last workgroup of the row releases the entry.
+// x is read twice.
 template <int NT, int V, bool VEC4, int MODE>
-__global__ __launch_bounds__(NT) void k_split_stats(const float* x, float2* part,
-                                                    int64_t rows, int64_t cols,
-                                                    int64_t chunks, Clip clip) {
+__global__ __launch_bounds__(NT) void k_split_stats(const float* x, XchArgs xa, int64_t cols,
+                                                    int wpr, int64_t chunks, Clip clip) {
+  const uint64_t t0 = wall_clock();
   constexpr int NW = NT / 64;
   constexpr int64_t CH = int64_t(4) * V * NT;
   __shared__ float red_max[NW];
   __shared__ float red_sum[NW];
   const int tid = threadIdx.x;
-  const int64_t total = rows * chunks;
-  for (int64_t b = blockIdx.x; b < total; b += gridDim.x) {
-    const int64_t row = b / chunks;
-    const int64_t g = b - row * chunks;
+  const int b = blockIdx.x;
+  const int lrow = b / wpr;
+  const int w = b - lrow * wpr;
+  float m = kNegInf;
+  float s = 0.0f;
+  for (int64_t g = w; g < chunks; g += wpr) {
     const int64_t c0 = g * CH;
-    const float* xr = x + row * cols + c0;
     const int lim = seg_len(cols, c0, CH);
     float v[4 * V];
-    load_strip<V, VEC4>(v, xr, tid, NT, lim);
-    const float m = block_max<NW>(array_max(v), red_max);
-    const bool empty_max = (m == kNegInf);
-    const RowShift rs = row_shift(empty_max ? 0.0f : m, clip);
-    float s = block_sum<NW>(exp_strip<MODE>(v, rs), red_sum);
-    if (empty_max) s = static_cast<float>(lim);
-    if (tid == 0) part[b] = make_float2(m, s);
+    load_strip<V, VEC4>(v, x + lrow * cols + c0, tid, NT, lim);
+    const float2 p = chunk_partial<NW, V, MODE>(v, lim, clip, red_max, red_sum);
+    const float mm = fmaxf(m, p.x);
+    if (mm == kNegInf) {
+      s = s + p.y;
+    } else {
+      const RowShift rs = row_shift(mm, clip);
+      const float a = s == 0.0f ? 0.0f : s * exp_shift_clip<exp_mode<MODE>()>(m, rs);
+      s = a + p.y * exp_shift_clip<exp_mode<MODE>()>(p.x, rs);
+    }
+    m = mm;
+    __syncthreads();  // red_max / red_sum are reused by the next chunk
+  }
+  if (tid < 64) {
+    uint64_t* entry = wave_entry(xa, lrow, t0 + xa.limit_ticks);
+    if (tid == 0 && entry != nullptr) xch::st_agent(&entry_slots(entry)[w], encode_pair(m, s));
   }
 }
 
 template <int NT, int V, bool VEC4, int MODE>
 __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
-                                                    const int64_t* labels,
-                                                    const float2* part, int64_t rows,
-                                                    int64_t cols, int64_t chunks, Clip clip) {
+                                                    const int64_t* labels, XchArgs xa,
+                                                    int64_t cols, int wpr, int64_t chunks,
+                                                    Clip clip) {
+  const uint64_t t0 = wall_clock();
   constexpr int64_t CH = int64_t(4) * V * NT;
+  __shared__ float bcast[2];
   const int tid = threadIdx.x;
   const int lane = __lane_id();
-  const int64_t total = rows * chunks;
-  for (int64_t b = blockIdx.x; b < total; b += gridDim.x) {
-    const int64_t row = b / chunks;
-    const int64_t g = b - row * chunks;
+  const int b = blockIdx.x;
+  const int lrow = b / wpr;
+  const int w = b - lrow * wpr;
+  const int64_t label = row_label<MODE>(labels, lrow);
+  uint64_t* entry = nullptr;  // wavefront 0 only
+  if (tid < 64) {
+    entry = wave_entry(xa, lrow, t0 + xa.limit_ticks);
+    float2 ms = make_float2(__builtin_nanf(""), __builtin_nanf(""));
+    if (entry != nullptr) {
+      const uint64_t q = lane < wpr ? xch::ld_agent(&entry_slots(entry)[lane]) : ~0ull;
+      const float pm = lane < wpr ? decode_m(q) : kNegInf;
+      const float ps = lane < wpr ? decode_s(q) : 0.0f;
+      ms = merge_lanes<exp_mode<MODE>()>(pm, ps, clip);
+    }
+    if (tid == 0) {
+      bcast[0] = ms.x;
+      bcast[1] = ms.y;
+    }
+  }
+  __syncthreads();
+  const RowShift rs = row_shift(bcast[0], clip);
+  const float srow = bcast[1];
+  for (int64_t g = w; g < chunks; g += wpr) {
     const int64_t c0 = g * CH;
-    const float* xr = x + row * cols + c0;
-    const int64_t label = row_label<MODE>(labels, row);
     const int lim = seg_len(cols, c0, CH);
     float v[4 * V];
-    load_strip<V, VEC4>(v, xr, tid, NT, lim);
-
-    const float2* pr = part + row * chunks;
-    float mm = kNegInf;
-    for (int64_t l = lane; l < chunks; l += 64) mm = fmaxf(mm, pr[l].x);
-    const RowShift rs = row_shift(seg_max<64>(mm), clip);
-    float ss = 0.0f;
-    for (int64_t l = lane; l < chunks; l += 64) {
-      const float2 p = pr[l];
-      ss = ss + p.y * exp_shift_clip<exp_mode<MODE>()>(p.x, rs);
-    }
-    const float s = seg_sum<64>(ss);
+    load_strip<V, VEC4>(v, x + lrow * cols + c0, tid, NT, lim);
     if constexpr (!keeps_logits<MODE>()) {
 #pragma unroll
       for (int i = 0; i < 4 * V; ++i) v[i] = exp_shift_clip<MODE>(v[i], rs);
     }
     const LabelPick pick =
         pick_label<V, VEC4, MODE>(v, label, cols, c0, lim, tid, NT, g == 0 && tid == 0);
-    finish_row<V, VEC4, MODE>(v, rs, s, y, row, cols, c0, lim, pick, tid, NT);
+    finish_row<V, VEC4, MODE>(v, rs, srow, y, lrow, cols, c0, lim, pick, tid, NT);
+  }
+  if (entry != nullptr && tid < 64) {
+    // The slot reads have returned (the outputs above depend on them).
+    uint32_t last = 0;
+    if (tid == 0) last = depart_entry(entry, wpr, 1u) ? 1u : 0u;
+    last = __builtin_amdgcn_readfirstlane(last);
+    if (last) {
+      if (lane < wpr) xch::st_agent(&entry_slots(entry)[lane], 0ull);
+      if (tid == 0) release_entry(entry);
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
-// (c, split, one pass) The G workgroups of a row exchange partials in the
-// middle of the kernel, so x is read from HBM exactly once.
+// (c, split, one pass) The G <= 64 workgroups of a row exchange partials in
+// the middle of the kernel, so x is read from HBM exactly once.
 //
 // Workgroup (row, g) keeps e = exp(max(x - m_g, lo)) of its chunk in
-// registers and publishes (m_g, s_g) in its slot part[row*G + g].  Wave 0
-// polls the row's G slots until none holds the sentinel, merges them into M
-// and S, and every thread writes
+// registers, joins the row's entry and publishes (m_g, s_g) in slot g.
+// Wavefront 0 polls the row's G slots until none is empty, merges them into
+// M and S, and every thread writes
 //     y = max(e * exp(m_g - M), e_lo) / S
 // (log outputs keep x instead of e and write y = max(x - M, lo) - ln S).
 // For an element with x - M >= lo the rescaled e equals exp(x - M) >= e^lo;
 // for x - M < lo it is below e^lo, so the max is exactly the clip of the
 // definition.  A NaN element makes s_g, hence S and the whole row, NaN.
 //
-// Slots hold kSlotEmpty between launches.  After reading, each workgroup
-// adds 1 to depart[row]; the one that brings it to G puts the row's
-// sentinels back and zeroes the counter.  Every workgroup departs only after
-// its own reads have returned, and the next launch on the same workspace
-// starts after this kernel has finished, so each launch (graph replays
-// included) starts from clean slots.
-//
-// All exchange accesses are device-scope atomics, performed at the device's
+// After its slot reads have returned, each workgroup counts itself out of
+// the entry; the last one clears the slots and frees the entry.  All
+// exchange accesses are device-scope atomics, performed at the device's
 // coherence point rather than in a per-XCD L2, so no cache writeback or
 // invalidate is needed.  A wavefront issues memory operations in program
 // order and not speculatively, so the output work, which depends on the
 // loaded slots, never runs ahead of them.
 //
-// Progress: a row's G workgroups have consecutive IDs and workgroups are
-// dispatched in ID order, so the lowest unfinished row always has all of
-// its chunks dispatched once G workgroup slots are free; every wait ends as
-// long as G workgroups of the launch fit on the device at once (G <= 64).
-// The wait is also bounded: a workgroup that gives up writes NaN for its
-// chunk instead of stalling the device.
+// Progress: a row's workgroups have consecutive IDs and workgroups are
+// dispatched in ID order, so the lowest unfinished row always has all of its
+// chunks dispatched once G workgroup slots are free; every wait ends as long
+// as G workgroups of the launch fit on the device at once.  Every wait is
+// also bounded by the wall clock: a workgroup that gives up writes NaN for
+// its chunk (and counts the give-up) instead of stalling the device.
+//
+// `delay` (wall-clock ticks after the workgroup started, 0 for none) holds
+// the stores back until the launch's loads are expected to be done, so that
+// HBM serves the reads and the writes of the launch in two phases instead of
+// interleaving them.
 //
 // NLL outputs (one value per row) take no wait at all: the last workgroup
-// of the row to depart does the merge (below).
-constexpr unsigned long long kSlotEmpty = ~0ull;
-constexpr unsigned kSpinLimit = 1u << 20;
-
-__device__ __forceinline__ unsigned long long pack_pair(float a, float b) {
-  return static_cast<unsigned long long>(__builtin_bit_cast(unsigned, a)) |
-         (static_cast<unsigned long long>(__builtin_bit_cast(unsigned, b)) << 32);
-}
-
+// of the row to depart does the merge.
 template <int NT, int V, bool VEC4, int MODE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     2 * kRowWaves<V, VEC4, MODE>))) void k_split_onepass(
-    const float* x, float* y, const int64_t* labels, unsigned long long* part,
-    unsigned* depart, int64_t cols, int chunks, Clip clip) {
+    const float* x, float* y, const int64_t* labels, XchArgs xa, int64_t cols, int chunks,
+    uint32_t delay, Clip clip) {
+  const uint64_t t0 = wall_clock();
   constexpr int NW = NT / 64;
   constexpr int64_t CH = int64_t(4) * V * NT;
   __shared__ float red_max[NW];
   __shared__ float red_sum[NW];
   __shared__ float bcast[2];
   const int tid = threadIdx.x;
-  const int64_t b = blockIdx.x;
-  const int64_t row = b / chunks;
-  const int g = static_cast<int>(b - row * chunks);
-  const int64_t c0 = g * CH;
-  const float* xr = x + row * cols + c0;
-  const int64_t label = row_label<MODE>(labels, row);
+  const int b = blockIdx.x;
+  const int lrow = b / chunks;
+  const int g = b - lrow * chunks;
+  const int64_t c0 = int64_t(g) * CH;
+  const float* xr = x + lrow * cols + c0;
+  const int64_t label = row_label<MODE>(labels, lrow);
   const int lim = seg_len(cols, c0, CH);
 
   float v[4 * V];
@@ -726,157 +837,116 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     load_strip_flat<V, VEC4>(v, xr, tid, NT, lim);
   else
     load_strip<V, VEC4>(v, xr, tid, NT, lim);
-  float m;
-  float s;
-  LabelPick pick{0.0f, false, false};
   // NLL outputs: every workgroup reads the row's label logit right after its
   // chunk's loads (one cache line per wavefront, after the label itself),
   // so the one that merges the row below already holds it, and the values
   // die as they are folded in.
   const bool bad_label = label < 0 || label >= cols;
   float xl = 0.0f;
-  if constexpr (MODE == kNllOut) xl = x[row * cols + (bad_label ? 0 : label)];
-  if constexpr (MODE == kNllOut) {
-    const float2 ms = lane_online(v, clip);
-    m = block_max<NW>(ms.x, red_max);
-    s = block_sum<NW>(lane_share(ms, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
-  } else if constexpr (keeps_logits<MODE>()) {
-    const float2 ms = lane_online(v, clip);
+  if constexpr (MODE == kNllOut) xl = x[lrow * cols + (bad_label ? 0 : label)];
+  LabelPick pick{0.0f, false, false};
+  if constexpr (MODE == kLogOut)
     pick = pick_label<V, VEC4, MODE>(v, label, cols, c0, lim, tid, NT, g == 0 && tid == 0);
-    m = block_max<NW>(ms.x, red_max);
-    s = block_sum<NW>(lane_share(ms, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
-  } else {
-    m = block_max<NW>(array_max(v), red_max);
-    s = block_sum<NW>(exp_strip<MODE>(v, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
-  }
-  const bool empty_max = (m == kNegInf);
-  if (empty_max) s = static_cast<float>(lim);
+  const float2 part = chunk_partial<NW, V, MODE>(v, lim, clip, red_max, red_sum);
+  const float m = part.x;
+  const float s = part.y;
+  const uint64_t deadline = t0 + xa.limit_ticks;
 
   if constexpr (MODE == kNllOut) {
     // One value per row: no workgroup waits.  Each publishes its pair and
-    // then counts itself out on depart[row]; the slot store has completed
-    // before the count (explicit wait), so the workgroup that brings the
-    // count to G sees all G pairs.  That one merges them as below, writes
-    // the loss with the label logit it read at the start, and puts the
-    // row's slots and counter back.
+    // then counts itself out; the slot store has completed before the count
+    // (explicit wait), so the workgroup that brings the count to G sees all
+    // G pairs.  That one merges them as above, writes the loss with the
+    // label logit it read at the start, and frees the entry.
     if (tid < 64) {
-      unsigned long long* pr = part + row * chunks;
-      unsigned old = 0u;
-      if (tid == 0) {
-        unsigned long long val = pack_pair(m, s);
-        if (val == kSlotEmpty) val = pack_pair(__builtin_nanf(""), __builtin_nanf(""));
-        __hip_atomic_store(&part[b], val, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __builtin_amdgcn_s_waitcnt(0);
-        old = __hip_atomic_fetch_add(&depart[row], 1u, __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT);
+      uint64_t* const entry = wave_entry(xa, lrow, deadline);
+      if (entry == nullptr) {
+        if (tid == 0) y[lrow] = __builtin_nanf("");
+        return;
       }
-      old = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(old)));
-      if (old == static_cast<unsigned>(chunks) - 1u) {
-        // Every pair was stored before its count, so none should read empty;
-        // a slot that still does is read again (bounded, as in the exchange
-        // below), so the merge does not rest on when a completed store
-        // becomes visible to other XCDs.
-        unsigned long long q = 0ull;
-        unsigned spins = 0;
-        bool ok = true;
-        while (true) {
-          q = (tid < chunks)
-                  ? __hip_atomic_load(&pr[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                  : 0ull;
-          if (__builtin_amdgcn_ballot_w64(tid < chunks && q == kSlotEmpty) == 0) break;
-          __builtin_amdgcn_s_sleep(2);
-          if (++spins > kSpinLimit) {
-            ok = false;
-            break;
-          }
-        }
-        const float pm =
-            (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q)) : kNegInf;
-        const float ps =
-            (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q >> 32)) : 0.0f;
-        const float mrow = seg_max<64>(pm);
-        const RowShift rs = row_shift(mrow, clip);
-        const float term = (tid < chunks) ? ps * exp_shift_clip<kExpAccurate>(pm, rs) : 0.0f;
-        const float srow = seg_sum<64>(term);
-        const float loss =
-            (bad_label || !ok) ? __builtin_nanf("") : -log_out(xl, rs, log_of_sum(srow));
-        if (tid == 0) y[row] = loss;
-        // The slot reads have returned (the loss depends on them): put the
-        // row's slots and counter back for the next launch.
-        asm volatile("" : : "v"(loss));
+      uint64_t* const slots = entry_slots(entry);
+      uint32_t last = 0;
+      if (tid == 0) {
+        xch::st_agent(&slots[g], encode_pair(m, s));
         __builtin_amdgcn_s_waitcnt(0);
-        if (tid < chunks)
-          __hip_atomic_store(&pr[tid], kSlotEmpty, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (tid == 0)
-          __hip_atomic_store(&depart[row], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        last = depart_entry(entry, chunks, 1u) ? 1u : 0u;
+      }
+      last = __builtin_amdgcn_readfirstlane(last);
+      if (last) {
+        // Every pair was stored before its count, so none should read
+        // empty; a slot that still does is read again (bounded), so the
+        // merge does not rest on when a completed store becomes visible.
+        bool ok = true;
+        const uint64_t q = poll_slots(slots, chunks, deadline, &ok);
+        const float2 ms = tid < chunks ? make_float2(decode_m(q), decode_s(q))
+                                       : make_float2(kNegInf, 0.0f);
+        const float2 rowms = merge_lanes<kExpAccurate>(ms.x, ms.y, clip);
+        const float loss = (bad_label || !ok)
+                               ? __builtin_nanf("")
+                               : -log_out(xl, row_shift(rowms.x, clip), log_of_sum(rowms.y));
+        if (tid == 0) {
+          y[lrow] = loss;
+          if (!ok) count_give_up(xa, xch::kDiagWaitGiveUps);
+        }
+        // The slot reads have returned (the loss depends on them).
+        asm volatile("" : : "v"(loss));
+        if (tid < chunks) xch::st_agent(&slots[tid], 0ull);
+        if (tid == 0) release_entry(entry);
       }
     }
     return;
   }
 
-  if (tid == 0) {
-    unsigned long long val = pack_pair(m, s);
-    if (val == kSlotEmpty) val = pack_pair(__builtin_nanf(""), __builtin_nanf(""));
-    __hip_atomic_store(&part[b], val, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
   if (tid < 64) {
-    unsigned long long* pr = part + row * chunks;
-    unsigned long long q = 0;
-    unsigned spins = 0;
-    bool ok = true;
-    while (true) {
-      q = (tid < chunks)
-              ? __hip_atomic_load(&pr[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-              : 0ull;
-      if (__builtin_amdgcn_ballot_w64(tid < chunks && q == kSlotEmpty) == 0) break;
-      __builtin_amdgcn_s_sleep(2);
-      if (++spins > kSpinLimit) {
-        ok = false;
-        break;
-      }
+    uint64_t* const entry = wave_entry(xa, lrow, deadline);
+    bool ok = entry != nullptr;
+    uint64_t q = 0;
+    uint32_t last = 0;
+    if (ok) {
+      uint64_t* const slots = entry_slots(entry);
+      if (tid == 0) xch::st_agent(&slots[g], encode_pair(m, s));
+      q = poll_slots(slots, chunks, deadline, &ok);
     }
-    const float pm = (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q)) : kNegInf;
-    const float ps =
-        (tid < chunks) ? __builtin_bit_cast(float, static_cast<unsigned>(q >> 32)) : 0.0f;
-    const float mrow = seg_max<64>(pm);
-    const RowShift rs = row_shift(mrow, clip);
-    const float term = (tid < chunks) ? ps * exp_shift_clip<exp_mode<MODE>()>(pm, rs) : 0.0f;
-    const float srow = seg_sum<64>(term);
-    const float rcp = 1.0f / srow;
+    const float2 ms = (ok && tid < chunks) ? make_float2(decode_m(q), decode_s(q))
+                                           : make_float2(kNegInf, 0.0f);
+    const float2 rowms = merge_lanes<exp_mode<MODE>()>(ms.x, ms.y, clip);
     if (tid == 0) {
+      if (!ok && entry != nullptr) count_give_up(xa, xch::kDiagWaitGiveUps);
+      const float rcp = 1.0f / rowms.y;
       if constexpr (keeps_logits<MODE>()) {
-        bcast[0] = ok ? mrow : __builtin_nanf("");  // M
-        bcast[1] = ok ? srow : __builtin_nanf("");  // S
+        bcast[0] = ok ? rowms.x : __builtin_nanf("");  // M
+        bcast[1] = ok ? rowms.y : __builtin_nanf("");  // S
       } else {
-        bcast[0] = ok ? exp_shift_clip<MODE>(m, rs) * rcp : __builtin_nanf("");  // e^(m_g - M) / S
+        const RowShift rs = row_shift(rowms.x, clip);
+        bcast[0] = ok ? exp_shift_clip<MODE>(m, rs) * rcp : __builtin_nanf("");  // e^(m_g-M)/S
         bcast[1] = ok ? clip.e_lo * rcp : __builtin_nanf("");                    // e_lo / S
       }
-      // Depart once this wave's slot reads have returned (the add's operand
-      // depends on them); the last workgroup of the row restores the slots.
-      unsigned one = 1u;
+      // Count out once this wavefront's slot reads have returned (the
+      // add's operand depends on them).  A workgroup that joined no entry
+      // has nothing to count out of.
+      uint32_t one = 1u;
       asm volatile("" : "+v"(one) : "v"(q));
-      const unsigned old = __hip_atomic_fetch_add(&depart[row], one, __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT);
-      if (old == static_cast<unsigned>(chunks) - 1u) {
-        for (int l = 0; l < chunks; ++l)
-          __hip_atomic_store(&pr[l], kSlotEmpty, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&depart[row], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
+      if (entry != nullptr) last = depart_entry(entry, chunks, one) ? 1u : 0u;
+    }
+    last = __builtin_amdgcn_readfirstlane(last);
+    if (last) {
+      if (tid < chunks) xch::st_agent(&entry_slots(entry)[tid], 0ull);
+      if (tid == 0) release_entry(entry);
     }
   }
   __syncthreads();
+  if (delay != 0) wait_until(t0 + delay);
   if constexpr (keeps_logits<MODE>()) {
-    // v still holds the logits: y = c - ln S (or the label's loss) against
-    // the row's M.
-    finish_row<V, VEC4, MODE>(v, row_shift(bcast[0], clip), bcast[1], y, row, cols, c0, lim,
+    // v still holds the logits: y = c - ln S against the row's M.
+    finish_row<V, VEC4, MODE>(v, row_shift(bcast[0], clip), bcast[1], y, lrow, cols, c0, lim,
                               pick, tid, NT);
   } else {
-    float* yr = y + row * cols + c0;
+    float* yr = y + lrow * cols + c0;
     const float scale = bcast[0];
     const float floor_y = bcast[1];
 #pragma unroll
     for (int i = 0; i < 4 * V; ++i) v[i] = fmaxf(v[i] * scale, floor_y);
-    store_strip<V, VEC4>(v, [](float ev) { return ev; }, yr, tid, NT, lim);
+    store_strip<V, VEC4>(v, [](float ev) { return ev; }, yr, opaque(tid), NT, lim);
   }
 }
 
@@ -884,13 +954,19 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
 // Diagnostics.
 
 // e[i] = exp(max(x[i] - m[i], lo)), through the same device routine the
-// softmax kernels use.
+// softmax kernels use; MODE kExpRaw instead gives e[i] = v_exp_f32(x[i])
+// (2^x), the hardware instruction those routines build on.
+constexpr int kExpRaw = 16;
 template <int MODE>
 __global__ __launch_bounds__(256) void k_exp_probe(const float* x, const float* m,
                                                    float* e, int64_t n, Clip clip) {
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
-       i += static_cast<int64_t>(gridDim.x) * 256)
-    e[i] = exp_shift_clip<MODE>(x[i], row_shift(m[i], clip));
+       i += static_cast<int64_t>(gridDim.x) * 256) {
+    if constexpr (MODE == kExpRaw)
+      e[i] = __builtin_amdgcn_exp2f(x[i]);
+    else
+      e[i] = exp_shift_clip<MODE>(x[i], row_shift(m[i], clip));
+  }
 }
 
 // Plain copy with 128-bit streaming accesses: the memory-bound ceiling that

@@ -1,8 +1,9 @@
 // C ABI of the row-softmax library: argument checks, the dispatch on cols,
-// and the launches.  Declarations and the contract are in
-// include/softmax_mi355x.h.
+// the exchange table of split rows, the store schedule, and the launches.
+// Declarations and the contract are in include/softmax_mi355x.h.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <mutex>
 #include <utility>
@@ -12,6 +13,14 @@
 #include "sm_host.hpp"
 #include "sm_kernels.hpp"
 
+// The exchange table of rows split over several workgroups (layout in
+// sm_exchange.hpp).  The kernels claim and free its row entries themselves,
+// and it is all zero at rest, as it starts.  Every device the library runs
+// on holds its own copy until the process ends.  Host code never uses this
+// name as an address: it passes the kernels the device address that
+// hipGetSymbolAddress gives for the current device (device_facts below).
+static __device__ __align__(256) uint64_t scratch[smx::xch::kScratchWords];
+
 namespace {
 
 using namespace smx;
@@ -19,78 +28,127 @@ using namespace smx_host;
 
 // Bucket limits on cols.
 constexpr int64_t kPackedMaxCols = 64;
-
-// The packed kernel's persistent grid: six 256-thread workgroups per CU on
-// MI355X's 256 CUs.  Measured on 115200 x 50: up to six per CU the
-// prefetched next tile overlaps the current tile's compute (8.6 us); seven
-// or more per CU, or one tile per workgroup, take 10.4-11.2 us.
+// The packed kernel's persistent grid: six 256-thread workgroups per CU.
+// Measured on 115200 x 50: up to six per CU the prefetched next tile
+// overlaps the current tile's compute; seven or more per CU, or one tile per
+// workgroup, are slower.
 constexpr int64_t kPackedBlocksPerCU = 6;
-constexpr int64_t kDeviceCUs = 256;
 constexpr int64_t kWaveRowMaxCols = 4096;
 // With 32-bit access, 64 values per lane need more registers than a
 // wavefront has (the kernel would spill): such rows go to k_block_row.
 constexpr int64_t kWaveRowMaxColsScalar = 2048;
 constexpr int64_t kBlockRowMaxCols = 32768;
+constexpr int kBlockThreads = 1024;
 
-// Split rows, one-pass kernel: 512-thread workgroups holding 32 columns per
-// lane (chunks of 16384 columns, eight waves per SIMD) for rows of up to
-// 64 chunks, or 64 columns per lane (chunks of 32768, four waves per SIMD)
-// for rows of up to 64 of those.  On 64 x 262144 the 16384-column chunks
-// take 22.8 us against 24.6 us for 32768-column ones.
-constexpr int kOnePassThreads = 512;
-constexpr int kOnePassVSmall = 8;
-constexpr int kOnePassVLarge = 16;
-constexpr int64_t kOnePassChunkSmall = int64_t(4) * kOnePassVSmall * kOnePassThreads;
-constexpr int64_t kOnePassChunkLarge = int64_t(4) * kOnePassVLarge * kOnePassThreads;
-// A row may span at most this many workgroups on the one-pass path (the
-// exchange is read by one wavefront, one slot per lane).
+// Split rows, one pass: a row spans at most this many workgroups (the
+// exchange is read by one wavefront, one slot per lane).  Chunk shapes,
+// threads x 128-bit strips per lane: 512 x 8 (16384 columns) up to 64
+// chunks, then 512 x 16 (32768, 128-bit access only: with 32-bit access it
+// would spill).  256 x 8 (8192) exists for softmax_fwd_planned: on
+// 64 x 262144 its 2048 workgroups took 24.4 us against 22.0 for 1024 of
+// 512 x 8.  NLL outputs with 128-bit access take 1024 x 8 (32768 columns):
+// their workgroups never wait for each other and keep no values.
 constexpr int64_t kOnePassMaxChunks = 64;
-// Rows per launch keep a launch within the workgroups MI355X's 256 CUs hold
-// at once: four per CU with the small chunks, two with the large ones.
-constexpr int64_t kOnePassMaxBlocksSmall = 1024;
-constexpr int64_t kOnePassMaxBlocksLarge = 512;
-constexpr int64_t kOnePassMaxBlocks = kOnePassMaxBlocksSmall;
-// NLL outputs on the one-pass path: 1024-thread workgroups, two per CU.
 constexpr int kNllThreads = 1024;
-constexpr int64_t kNllChunk = int64_t(4) * kOnePassVSmall * kNllThreads;
-constexpr int64_t kNllMaxBlocks = 512;
-static_assert(kNllMaxBlocks <= kOnePassMaxBlocks, "NLL launches fit the exchange slots");
 
-// Split rows, two-pass fallback for rows longer than kOnePassMaxChunks
-// chunks: 512-thread workgroups holding 32 columns per lane (chunks of
-// 16384 columns).
+// Split rows, two passes (rows too long for the one-pass shapes): 512 x 8
+// chunks, at most 64 workgroups per row (one exchange slot each, every
+// workgroup taking a stride of the row's chunks) and about 2048 per launch.
 constexpr int kSplitThreads = 512;
 constexpr int kSplitV = 8;
-constexpr int64_t kSplitChunk = int64_t(4) * kSplitV * kSplitThreads;
+constexpr int64_t kTwoPassWorkgroups = 2048;
 
-// Library-owned workspace for split rows, one per (device, stream) for
-// eager calls (launches that may overlap in time never share one) and one
-// per device shared by captured graphs:
-//   [0, 128 KiB)          two-pass partials, float2
-//   [128 KiB, +8 KiB)     one-pass exchange slots, 64-bit, kSlotEmpty at rest
-//   [136 KiB, +4 KiB)     one-pass departure counters, zero at rest
-constexpr int64_t kWorkspaceBytes = int64_t(140) << 10;
-constexpr int64_t kWorkspacePairs = (int64_t(128) << 10) / int64_t(sizeof(float2));
-constexpr int64_t kSlotsOffset = int64_t(128) << 10;
-constexpr int64_t kSlotsBytes = kOnePassMaxBlocks * 8;
-constexpr int64_t kDepartOffset = kSlotsOffset + kSlotsBytes;
-constexpr int64_t kDepartBytes = kOnePassMaxBlocks * 4;
-static_assert(kDepartOffset + kDepartBytes <= kWorkspaceBytes, "workspace layout fits");
-constexpr int kMaxDevices = 64;
-constexpr int kMaxStreamWorkspaces = 64;  // per device
+// Store schedule of the one-pass split-row launches, in which every
+// workgroup is resident at once and takes one chunk: the stores wait until
+// the launch's loads are expected to be over, read_bytes / rate + base, so
+// that HBM serves the launch's reads and writes as two phases instead of
+// interleaving them.  The rate is MI355X's measured streaming read rate of
+// such launches; a launch whose reads take longer simply starts its stores
+// while the last reads are still arriving.  Small launches are left alone
+// (their phases are short next to the launch latency).  The row kernels
+// (k_wave_row, k_block_row) take the same delay only through
+// softmax_fwd_planned: measured on 4096 x 1000 and 512 x 32768 it gained
+// nothing there (their stores already spread out behind the exponentials),
+// while on 64 x 262144 and on 512 x 32768 in 16384-column chunks the split
+// kernel gained 0.05-0.3 us.
+constexpr double kStoreReadBytesPerNs = 7600.0;
+constexpr int64_t kStoreBaseNs = 300;
+constexpr int64_t kStoreMinBytes = int64_t(8) << 20;
+constexpr int64_t kStoreMaxNs = 200000;
 
-struct StreamWorkspace {
-  hipStream_t stream;
-  char* mem;
-  uint64_t last_use;
+// ---------------------------------------------------------------------------
+// Per-device facts: compute units, the wall clock's rate, and the device
+// address of `scratch`, taken once per device with that device current.
+struct DeviceFacts {
+  int cus = 0;
+  int64_t wall_khz = 0;
+  uint64_t* scratch = nullptr;
 };
-struct DeviceState {
-  std::vector<StreamWorkspace> per_stream;
-  char* capture_ws = nullptr;
-  uint64_t clock = 0;
+std::mutex g_facts_mu;
+bool g_facts_ready[kMaxDevices] = {};
+DeviceFacts g_facts[kMaxDevices];
+
+int device_facts(int dev, DeviceFacts* out) {
+  if (dev < 0 || dev >= kMaxDevices) return SOFTMAX_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lock(g_facts_mu);
+  if (!g_facts_ready[dev]) {
+    DeviceFacts f;
+    int rc = device_cus(dev, &f.cus);
+    if (rc != SOFTMAX_OK) return rc;
+    int khz = 0;
+    hipError_t e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+    if (e != hipSuccess) return fail_hip(e);
+    if (khz <= 0) return SOFTMAX_ERR_INVALID_ARG;
+    f.wall_khz = khz;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return fail_hip(e);
+    if (p == nullptr) return SOFTMAX_ERR_HIP;
+    f.scratch = static_cast<uint64_t*>(p);
+    g_facts[dev] = f;
+    g_facts_ready[dev] = true;
+  }
+  *out = g_facts[dev];
+  return SOFTMAX_OK;
+}
+
+// Workgroups of `fn` (at `block` threads) that one CU holds at once, from
+// the runtime's occupancy calculator; cached per (device, kernel).
+struct OccEntry {
+  int dev;
+  const void* fn;
+  int per_cu;
 };
-std::mutex g_mu;
-DeviceState g_dev[kMaxDevices];
+std::mutex g_occ_mu;
+std::vector<OccEntry> g_occ;
+
+int blocks_per_cu(int dev, const void* fn, int block, int* out) {
+  std::lock_guard<std::mutex> lock(g_occ_mu);
+  for (const OccEntry& o : g_occ) {
+    if (o.dev == dev && o.fn == fn) {
+      *out = o.per_cu;
+      return SOFTMAX_OK;
+    }
+  }
+  int n = 0;
+  const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, 0);
+  if (e != hipSuccess) return fail_hip(e);
+  if (n <= 0) return SOFTMAX_ERR_HIP;
+  g_occ.push_back(OccEntry{dev, fn, n});
+  *out = n;
+  return SOFTMAX_OK;
+}
+
+// Per-call part of the exchange key (the launch's output address fills the
+// high bits): calls made at the same time never share a key unless they
+// write the same output, and a region left claimed after a give-up is not
+// picked up by later eager calls.
+std::atomic<uint32_t> g_nonce{1};
+
+inline uint64_t exchange_key(const void* out_first_row, uint32_t nonce) {
+  return (static_cast<uint64_t>(reinterpret_cast<uintptr_t>(out_first_row)) << 16) |
+         (nonce & 0xFFFFu);
+}
 
 inline int64_t pow2_at_least(int64_t v) {
   int64_t p = 1;
@@ -106,80 +164,19 @@ int check_sizes(int64_t rows, int64_t cols) {
   return SOFTMAX_OK;
 }
 
-softmax_plan_t make_plan(const float* x, const float* y, int64_t rows, int64_t cols) {
-  softmax_plan_t p{};
-  p.chunks_per_row = 1;
-  if (rows == 0 || cols == 0) {
-    p.kernel = SOFTMAX_KERNEL_NONE;
-    return p;
-  }
-  const bool a16 = aligned16(x) && aligned16(y);
-  const bool vec_rows = a16 && (cols % 4 == 0);
-  if (cols <= kPackedMaxCols) {
-    // G lanes per row with at most 16 columns per lane; a persistent grid of
-    // kPackedBlocksPerCU workgroups per CU loops over tiles of 256/G rows.
-    const int64_t g = cols <= 16 ? 1 : cols <= 32 ? 2 : 4;
-    p.kernel = SOFTMAX_KERNEL_PACKED;
-    p.vec_width = a16 ? 4 : 1;
-    p.lanes_per_row = static_cast<int32_t>(g);
-    p.elems_per_lane = static_cast<int32_t>(ceil_div(cols, g));
-    p.block_threads = 256;
-    const int64_t tile = 256 / g;
-    p.grid = std::min(ceil_div(rows, tile), kPackedBlocksPerCU * kDeviceCUs);
-    p.launches = 1;
-  } else if (cols <= (vec_rows ? kWaveRowMaxCols : kWaveRowMaxColsScalar)) {
-    const int64_t v = pow2_at_least(ceil_div(cols, 256));
-    p.kernel = SOFTMAX_KERNEL_WAVE_ROW;
-    p.vec_width = vec_rows ? 4 : 1;
-    p.lanes_per_row = 64;
-    p.elems_per_lane = static_cast<int32_t>(4 * v);
-    p.block_threads = 256;
-    p.grid = std::min(ceil_div(rows, 4), kMaxGrid);
-    p.launches = 1;
-  } else if (cols <= kBlockRowMaxCols) {
-    const int64_t v = std::max<int64_t>(2, pow2_at_least(ceil_div(cols, 4096)));
-    p.kernel = SOFTMAX_KERNEL_BLOCK_ROW;
-    p.vec_width = vec_rows ? 4 : 1;
-    p.lanes_per_row = 1024;
-    p.elems_per_lane = static_cast<int32_t>(4 * v);
-    p.block_threads = 1024;
-    p.grid = std::min(rows, kMaxGrid);
-    p.launches = 1;
-  } else {
-    p.kernel = SOFTMAX_KERNEL_SPLIT_ROW;
-    p.vec_width = vec_rows ? 4 : 1;
-    p.workspace_bytes = kWorkspaceBytes;
-    const int64_t gs = ceil_div(cols, kOnePassChunkSmall);
-    const int64_t gl = ceil_div(cols, kOnePassChunkLarge);
-    // The large chunks (64 values per lane) are taken with 128-bit access
-    // only: with 32-bit access they would spill, and such rows take the
-    // two-pass path instead.
-    if (gs <= kOnePassMaxChunks || (vec_rows && gl <= kOnePassMaxChunks)) {
-      // One pass: whole rows per launch, all workgroups resident together.
-      const bool small = gs <= kOnePassMaxChunks;
-      const int64_t g1 = small ? gs : gl;
-      const int64_t rows_per_launch =
-          (small ? kOnePassMaxBlocksSmall : kOnePassMaxBlocksLarge) / g1;
-      p.lanes_per_row = kOnePassThreads;
-      p.elems_per_lane = 4 * (small ? kOnePassVSmall : kOnePassVLarge);
-      p.block_threads = kOnePassThreads;
-      p.chunks_per_row = g1;
-      p.grid = std::min(rows, rows_per_launch) * g1;
-      p.launches = static_cast<int32_t>(ceil_div(rows, rows_per_launch));
-    } else {
-      // Two passes: partials, then merge and write, in batches of rows.
-      const int64_t g2 = ceil_div(cols, kSplitChunk);
-      const int64_t rows_per_batch = std::max<int64_t>(1, kWorkspacePairs / g2);
-      p.lanes_per_row = kSplitThreads;
-      p.elems_per_lane = 4 * kSplitV;
-      p.block_threads = kSplitThreads;
-      p.chunks_per_row = g2;
-      p.grid = std::min(std::min(rows, rows_per_batch) * g2, kMaxGrid);
-      p.launches = static_cast<int32_t>(2 * ceil_div(rows, rows_per_batch));
-    }
-  }
-  return p;
-}
+// ---------------------------------------------------------------------------
+// Kernel instances.  A shape names one compiled kernel: its family, access
+// width, threads per workgroup and strips per lane (packed rows: lanes per
+// row and columns per lane).
+struct Shape {
+  int kernel = SOFTMAX_KERNEL_NONE;
+  bool vec4 = false;
+  int threads = 0;
+  int v = 0;        // 128-bit strips (or groups of four scalars) per lane
+  int g = 0;        // packed rows: lanes per row
+  int epl = 0;      // packed rows: columns per lane
+  bool two_pass = false;
+};
 
 // k_packed instances: G = 1 with EPL = 1..16, G = 2 and G = 4 with
 // EPL = 9..16 (a plan never asks for fewer columns per lane at G > 1).
@@ -191,283 +188,341 @@ const void* packed_fn(int epl, std::integer_sequence<int, E...>) {
   return (idx >= 0 && idx < static_cast<int>(sizeof...(E))) ? table[idx] : nullptr;
 }
 
-template <bool VEC4, int EM>
-hipError_t dispatch_packed(const softmax_plan_t& p, const float* x, float* y,
-                           const int64_t* labels, int64_t rows, int64_t cols, Clip c,
-                           hipStream_t s) {
-  const void* fn = nullptr;
-  switch (p.lanes_per_row) {
-    case 1:
-      fn = packed_fn<1, VEC4, EM>(p.elems_per_lane, std::make_integer_sequence<int, 16>{});
+template <int EM, bool VEC4>
+const void* shape_fn(const Shape& s, bool stats_pass) {
+  auto cast = [](auto f) { return reinterpret_cast<const void*>(f); };
+  switch (s.kernel) {
+    case SOFTMAX_KERNEL_PACKED:
+      if (s.g == 1) return packed_fn<1, VEC4, EM>(s.epl, std::make_integer_sequence<int, 16>{});
+      if (s.g == 2) return packed_fn<2, VEC4, EM>(s.epl, std::make_integer_sequence<int, 8>{});
+      if (s.g == 4) return packed_fn<4, VEC4, EM>(s.epl, std::make_integer_sequence<int, 8>{});
+      return nullptr;
+    case SOFTMAX_KERNEL_WAVE_ROW:
+      switch (s.v) {
+        case 1: return cast(&k_wave_row<1, VEC4, EM>);
+        case 2: return cast(&k_wave_row<2, VEC4, EM>);
+        case 4: return cast(&k_wave_row<4, VEC4, EM>);
+        case 8: return cast(&k_wave_row<8, VEC4, EM>);
+        case 16:
+          if constexpr (VEC4) return cast(&k_wave_row<16, VEC4, EM>);
+          return nullptr;
+        default: return nullptr;
+      }
+    case SOFTMAX_KERNEL_BLOCK_ROW:
+      switch (s.v) {
+        case 2: return cast(&k_block_row<kBlockThreads, 2, VEC4, EM>);
+        case 4: return cast(&k_block_row<kBlockThreads, 4, VEC4, EM>);
+        case 8: return cast(&k_block_row<kBlockThreads, 8, VEC4, EM>);
+        default: return nullptr;
+      }
+    case SOFTMAX_KERNEL_SPLIT_ROW:
+      if (s.two_pass) {
+        if (s.threads != kSplitThreads || s.v != kSplitV) return nullptr;
+        return stats_pass ? cast(&k_split_stats<kSplitThreads, kSplitV, VEC4, EM>)
+                          : cast(&k_split_apply<kSplitThreads, kSplitV, VEC4, EM>);
+      }
+      if (s.threads == 256 && s.v == 8) return cast(&k_split_onepass<256, 8, VEC4, EM>);
+      if (s.threads == 512 && s.v == 8) return cast(&k_split_onepass<512, 8, VEC4, EM>);
+      if constexpr (VEC4) {
+        if (s.threads == 512 && s.v == 16) return cast(&k_split_onepass<512, 16, VEC4, EM>);
+        if constexpr (EM == kNllOut) {
+          if (s.threads == kNllThreads && s.v == 8)
+            return cast(&k_split_onepass<kNllThreads, 8, VEC4, EM>);
+        }
+      }
+      return nullptr;
+    default:
+      return nullptr;
+  }
+}
+
+template <int EM>
+const void* shape_fn_mode(const Shape& s, bool stats_pass) {
+  return s.vec4 ? shape_fn<EM, true>(s, stats_pass) : shape_fn<EM, false>(s, stats_pass);
+}
+
+const void* kernel_fn(const Shape& s, int em, bool stats_pass = false) {
+  switch (em) {
+    case kExpWide: return shape_fn_mode<kExpWide>(s, stats_pass);
+    case kExpFast: return shape_fn_mode<kExpFast>(s, stats_pass);
+    case kLogOut: return shape_fn_mode<kLogOut>(s, stats_pass);
+    case kNllOut: return shape_fn_mode<kNllOut>(s, stats_pass);
+    default: return shape_fn_mode<kExpAccurate>(s, stats_pass);
+  }
+}
+
+inline int64_t chunk_cols(const Shape& s) { return int64_t(4) * s.v * s.threads; }
+
+// Whether kernel family `kernel` may use 128-bit access: both pointers
+// 16-byte aligned and, except for packed rows (which move whole tiles of a
+// multiple of four rows), rows made of whole float4s.
+inline bool can_vec4(int kernel, const float* x, const float* y, int64_t cols) {
+  const bool a16 = aligned16(x) && aligned16(y);
+  return kernel == SOFTMAX_KERNEL_PACKED ? a16 : (a16 && cols % 4 == 0);
+}
+
+// The library's shape for a call (mode em).
+Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
+  Shape s;
+  s.vec4 = can_vec4(cols <= kPackedMaxCols ? SOFTMAX_KERNEL_PACKED : SOFTMAX_KERNEL_SPLIT_ROW,
+                    x, y, cols);
+  if (cols <= kPackedMaxCols) {
+    // G lanes per row with at most 16 columns per lane.
+    s.kernel = SOFTMAX_KERNEL_PACKED;
+    s.threads = 256;
+    s.g = cols <= 16 ? 1 : cols <= 32 ? 2 : 4;
+    s.epl = static_cast<int>(ceil_div(cols, s.g));
+  } else if (cols <= (s.vec4 ? kWaveRowMaxCols : kWaveRowMaxColsScalar)) {
+    s.kernel = SOFTMAX_KERNEL_WAVE_ROW;
+    s.threads = 256;
+    s.v = static_cast<int>(pow2_at_least(ceil_div(cols, 256)));
+  } else if (cols <= kBlockRowMaxCols) {
+    s.kernel = SOFTMAX_KERNEL_BLOCK_ROW;
+    s.threads = kBlockThreads;
+    s.v = static_cast<int>(std::max<int64_t>(2, pow2_at_least(ceil_div(cols, 4096))));
+  } else {
+    s.kernel = SOFTMAX_KERNEL_SPLIT_ROW;
+    if (em == kNllOut && s.vec4 && ceil_div(cols, int64_t(4) * 8 * kNllThreads) <= kOnePassMaxChunks) {
+      s.threads = kNllThreads;
+      s.v = 8;
+    } else if (ceil_div(cols, int64_t(4) * 8 * 512) <= kOnePassMaxChunks) {
+      s.threads = 512;
+      s.v = 8;
+    } else if (s.vec4 && ceil_div(cols, int64_t(4) * 16 * 512) <= kOnePassMaxChunks) {
+      s.threads = 512;
+      s.v = 16;
+    } else {
+      s.threads = kSplitThreads;
+      s.v = kSplitV;
+      s.two_pass = true;
+    }
+  }
+  return s;
+}
+
+// A caller's shape (softmax_fwd_planned): the family, access width and, for
+// split rows, the chunk shape; everything else is derived.  Returns false
+// when the shape is not one the library has or cannot take these rows.
+bool requested_shape(const softmax_plan_t& want, const float* x, const float* y, int64_t cols,
+                     int em, Shape* out) {
+  Shape s;
+  s.kernel = want.kernel;
+  if (want.vec_width != 1 && want.vec_width != 4) return false;
+  s.vec4 = want.vec_width == 4;
+  if (s.vec4 && !can_vec4(s.kernel, x, y, cols)) return false;
+  switch (s.kernel) {
+    case SOFTMAX_KERNEL_PACKED:
+      if (cols > kPackedMaxCols) return false;
+      s.threads = 256;
+      s.g = cols <= 16 ? 1 : cols <= 32 ? 2 : 4;
+      s.epl = static_cast<int>(ceil_div(cols, s.g));
       break;
-    case 2:
-      fn = packed_fn<2, VEC4, EM>(p.elems_per_lane, std::make_integer_sequence<int, 8>{});
+    case SOFTMAX_KERNEL_WAVE_ROW:
+      if (cols > (s.vec4 ? kWaveRowMaxCols : kWaveRowMaxColsScalar)) return false;
+      s.threads = 256;
+      s.v = static_cast<int>(pow2_at_least(ceil_div(cols, 256)));
+      break;
+    case SOFTMAX_KERNEL_BLOCK_ROW:
+      if (cols > kBlockRowMaxCols) return false;
+      s.threads = kBlockThreads;
+      s.v = static_cast<int>(std::max<int64_t>(2, pow2_at_least(ceil_div(cols, 4096))));
+      break;
+    case SOFTMAX_KERNEL_SPLIT_ROW: {
+      s.threads = want.block_threads;
+      s.v = want.elems_per_lane / 4;
+      if (want.elems_per_lane % 4 != 0) return false;
+      const int64_t chunks = ceil_div(cols, chunk_cols(s));
+      s.two_pass = chunks > kOnePassMaxChunks;
+      break;
+    }
+    default:
+      return false;
+  }
+  if (kernel_fn(s, em) == nullptr) return false;
+  *out = s;
+  return true;
+}
+
+// Everything a call launches: the shape, its grid, rows per launch, chunks,
+// the store delay in ns and in wall-clock ticks, and the exchange wait limit.
+struct Plan {
+  Shape shape;
+  int64_t grid = 0;
+  int64_t rows_per_launch = 0;
+  int64_t launches = 0;
+  int64_t chunks = 1;
+  int64_t wpr = 1;  // two-pass: workgroups per row
+  int64_t delay_ns = 0;
+  uint32_t delay_ticks = 0;
+  uint32_t limit_ticks = 0;
+};
+
+uint32_t ns_to_ticks(int64_t ns, const DeviceFacts& f) {
+  const int64_t t = (ns * f.wall_khz + 999999) / 1000000;
+  return static_cast<uint32_t>(std::min<int64_t>(t, UINT32_MAX));
+}
+
+// delay_req: -1 for the library's schedule, else the delay itself in ns.
+int make_plan(const Shape& s, int64_t rows, int64_t cols, int em, int dev,
+              const DeviceFacts& f, int64_t delay_req, Plan* out) {
+  Plan p;
+  p.shape = s;
+  const void* fn = kernel_fn(s, em);
+  if (fn == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+  int per_cu = 0;
+  int rc = blocks_per_cu(dev, fn, s.threads, &per_cu);
+  if (rc != SOFTMAX_OK) return rc;
+  const int64_t resident = int64_t(per_cu) * f.cus;
+  bool one_wave = false;
+  int64_t launch_read_bytes = 0;
+  switch (s.kernel) {
+    case SOFTMAX_KERNEL_PACKED: {
+      const int64_t tile = 256 / s.g;
+      p.grid = std::min(ceil_div(rows, tile), kPackedBlocksPerCU * f.cus);
+      p.rows_per_launch = rows;
+      p.launches = 1;
+      break;
+    }
+    case SOFTMAX_KERNEL_WAVE_ROW:
+      p.grid = std::min(ceil_div(rows, 4), kMaxGrid);
+      p.rows_per_launch = rows;
+      p.launches = 1;
+      break;
+    case SOFTMAX_KERNEL_BLOCK_ROW:
+      p.grid = std::min(rows, kMaxGrid);
+      p.rows_per_launch = rows;
+      p.launches = 1;
+      break;
+    default: {  // split rows
+      p.chunks = ceil_div(cols, chunk_cols(s));
+      if (!s.two_pass) {
+        // Whole rows per launch, every workgroup of a launch resident at
+        // once.
+        if (p.chunks > resident || p.chunks > kOnePassMaxChunks) return SOFTMAX_ERR_INVALID_ARG;
+        p.rows_per_launch = std::min(resident / p.chunks, int64_t(xch::kMaxRowsPerLaunch));
+        p.grid = std::min(rows, p.rows_per_launch) * p.chunks;
+        p.launches = ceil_div(rows, p.rows_per_launch);
+        one_wave = em != kNllOut;
+        launch_read_bytes = std::min(rows, p.rows_per_launch) * cols * 4;
+      } else {
+        // Workgroup w of a row takes chunks w, w + wpr, ...
+        p.wpr = std::min<int64_t>(p.chunks, xch::kEntrySlots);
+        p.rows_per_launch = std::min<int64_t>(std::max<int64_t>(1, kTwoPassWorkgroups / p.wpr),
+                                              xch::kMaxRowsPerLaunch);
+        p.grid = std::min(rows, p.rows_per_launch) * p.wpr;
+        p.launches = 2 * ceil_div(rows, p.rows_per_launch);
+      }
+      break;
+    }
+  }
+  if (delay_req < 0) {
+    p.delay_ns = (one_wave && launch_read_bytes >= kStoreMinBytes)
+                     ? static_cast<int64_t>(launch_read_bytes / kStoreReadBytesPerNs) + kStoreBaseNs
+                     : 0;
+  } else {
+    p.delay_ns = delay_req;
+  }
+  p.delay_ns = std::min(p.delay_ns, kStoreMaxNs);
+  p.delay_ticks = p.delay_ns > 0 ? ns_to_ticks(p.delay_ns, f) : 0;
+  p.limit_ticks = ns_to_ticks(int64_t(xch::kWaitLimitUs) * 1000, f);
+  *out = p;
+  return SOFTMAX_OK;
+}
+
+softmax_plan_t public_plan(const Plan& p, int64_t rows) {
+  softmax_plan_t o{};
+  const Shape& s = p.shape;
+  o.kernel = s.kernel;
+  o.vec_width = s.vec4 ? 4 : 1;
+  o.block_threads = s.threads;
+  o.chunks_per_row = p.chunks;
+  o.grid = p.grid;
+  o.launches = static_cast<int32_t>(p.launches);
+  o.store_delay_ns = p.delay_ns;
+  switch (s.kernel) {
+    case SOFTMAX_KERNEL_PACKED:
+      o.lanes_per_row = s.g;
+      o.elems_per_lane = s.epl;
+      break;
+    case SOFTMAX_KERNEL_WAVE_ROW:
+      o.lanes_per_row = 64;
+      o.elems_per_lane = 4 * s.v;
       break;
     default:
-      fn = packed_fn<4, VEC4, EM>(p.elems_per_lane, std::make_integer_sequence<int, 8>{});
+      o.lanes_per_row = s.threads;
+      o.elems_per_lane = 4 * s.v;
       break;
   }
-  if (fn == nullptr) return hipErrorInvalidValue;
-  void* args[] = {&x, &y, &labels, &rows, &cols, &c};
-  return launch(fn, p.grid, 256, args, s);
+  o.workspace_bytes = s.kernel == SOFTMAX_KERNEL_SPLIT_ROW ? xch::kScratchBytes : 0;
+  (void)rows;
+  return o;
 }
 
-template <int V, bool VEC4, int EM>
-hipError_t run_wave(const float* x, float* y, const int64_t* labels, int64_t rows,
-                    int64_t cols, Clip c, int64_t grid, hipStream_t s) {
-  void* args[] = {&x, &y, &labels, &rows, &cols, &c};
-  return launch(reinterpret_cast<const void*>(&k_wave_row<V, VEC4, EM>), grid, 256, args,
-                s);
-}
-
-template <bool VEC4, int EM>
-hipError_t dispatch_wave(const softmax_plan_t& p, const float* x, float* y,
-                         const int64_t* labels, int64_t rows, int64_t cols, Clip c,
-                         hipStream_t s) {
-  switch (p.elems_per_lane / 4) {
-    case 1: return run_wave<1, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
-    case 2: return run_wave<2, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
-    case 4: return run_wave<4, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
-    case 8: return run_wave<8, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
-    default:
-      // 64 values per lane only with 128-bit access (see make_plan).
-      if constexpr (VEC4) return run_wave<16, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
-      return hipErrorInvalidValue;
-  }
-}
-
-template <int V, bool VEC4, int EM>
-hipError_t run_block(const float* x, float* y, const int64_t* labels, int64_t rows,
-                     int64_t cols, Clip c, int64_t grid, hipStream_t s) {
-  void* args[] = {&x, &y, &labels, &rows, &cols, &c};
-  return launch(reinterpret_cast<const void*>(&k_block_row<1024, V, VEC4, EM>), grid, 1024,
-                args, s);
-}
-
-template <bool VEC4, int EM>
-hipError_t dispatch_block(const softmax_plan_t& p, const float* x, float* y,
-                          const int64_t* labels, int64_t rows, int64_t cols, Clip c,
-                          hipStream_t s) {
-  switch (p.elems_per_lane / 4) {
-    case 2: return run_block<2, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
-    case 4: return run_block<4, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
-    default: return run_block<8, VEC4, EM>(x, y, labels, rows, cols, c, p.grid, s);
-  }
-}
+// ---------------------------------------------------------------------------
+// Launches.
 
 // The output and labels of rows r0.. of a call: y advances by a row of
 // outputs, or by one loss per row for NLL outputs (whose labels advance
 // with it).
-template <int EM>
-float* out_rows(float* y, int64_t r0, int64_t cols) {
-  return EM == kNllOut ? y + r0 : y + r0 * cols;
+inline float* out_rows(float* y, int64_t r0, int64_t cols, int em) {
+  return em == kNllOut ? y + r0 : y + r0 * cols;
 }
-template <int EM>
-const int64_t* label_rows(const int64_t* labels, int64_t r0) {
-  return EM == kNllOut ? labels + r0 : labels;
+inline const int64_t* label_rows(const int64_t* labels, int64_t r0, int em) {
+  return em == kNllOut ? labels + r0 : labels;
 }
 
-template <bool VEC4, int EM>
-hipError_t run_split(const float* x, float* y, const int64_t* labels, float2* ws,
-                     int64_t rows, int64_t cols, int64_t chunks, Clip c, hipStream_t s) {
-  const int64_t rows_per_batch = std::max<int64_t>(1, kWorkspacePairs / chunks);
-  for (int64_t r0 = 0; r0 < rows; r0 += rows_per_batch) {
-    int64_t nb = std::min(rows_per_batch, rows - r0);
-    const float* xb = x + r0 * cols;
-    float* yb = out_rows<EM>(y, r0, cols);
-    const int64_t* lb = label_rows<EM>(labels, r0);
-    const int64_t grid = std::min(nb * chunks, kMaxGrid);
-    void* a1[] = {&xb, &ws, &nb, &cols, &chunks, &c};
-    hipError_t e = launch(
-        reinterpret_cast<const void*>(&k_split_stats<kSplitThreads, kSplitV, VEC4, EM>),
-        grid, kSplitThreads, a1, s);
-    if (e != hipSuccess) return e;
-    const float2* wsc = ws;
-    void* a2[] = {&xb, &yb, &lb, &wsc, &nb, &cols, &chunks, &c};
-    e = launch(
-        reinterpret_cast<const void*>(&k_split_apply<kSplitThreads, kSplitV, VEC4, EM>),
-        grid, kSplitThreads, a2, s);
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
-}
-
-template <int V, bool VEC4, int EM, int NT = kOnePassThreads>
-hipError_t run_onepass(const float* x, float* y, const int64_t* labels, char* ws,
-                       int64_t rows, int64_t cols, int64_t chunks, int64_t max_blocks, Clip c,
-                       hipStream_t s) {
-  unsigned long long* part = reinterpret_cast<unsigned long long*>(ws + kSlotsOffset);
-  unsigned* depart = reinterpret_cast<unsigned*>(ws + kDepartOffset);
-  const int64_t rows_per_launch = max_blocks / chunks;
-  int ichunks = static_cast<int>(chunks);
-  for (int64_t r0 = 0; r0 < rows; r0 += rows_per_launch) {
-    const int64_t nb = std::min(rows_per_launch, rows - r0);
-    const float* xb = x + r0 * cols;
-    float* yb = out_rows<EM>(y, r0, cols);
-    const int64_t* lb = label_rows<EM>(labels, r0);
-    void* args[] = {&xb, &yb, &lb, &part, &depart, &cols, &ichunks, &c};
-    hipError_t e = launch(
-        reinterpret_cast<const void*>(&k_split_onepass<NT, V, VEC4, EM>), nb * chunks, NT,
-        args, s);
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
-}
-
-// A workspace in its resting state: exchange slots empty, counters zero.
-hipError_t new_workspace(char** out) {
-  void* mem = nullptr;
-  hipError_t e = hipMalloc(&mem, kWorkspaceBytes);
-  if (e != hipSuccess) return e;
-  char* ws = static_cast<char*>(mem);
-  e = hipMemset(ws, 0, kWorkspaceBytes);
-  if (e == hipSuccess) e = hipMemset(ws + kSlotsOffset, 0xFF, kSlotsBytes);
-  if (e != hipSuccess) {
-    (void)hipFree(mem);
-    return e;
-  }
-  *out = ws;
-  return hipSuccess;
-}
-
-// Workspace for a split-row call on (dev, s).  Eager calls get one per
-// stream (allocated on first use); under stream capture the device's shared
-// capture workspace is used, which an earlier eager split-row call on the
-// device must have created.
-int workspace_for(int dev, hipStream_t s, bool capturing, char** out) {
-  DeviceState& st = g_dev[dev];
-  hipError_t e;
-  if (capturing) {
-    if (st.capture_ws == nullptr) return SOFTMAX_ERR_INVALID_ARG;
-    *out = st.capture_ws;
-    return SOFTMAX_OK;
-  }
-  ++st.clock;
-  for (StreamWorkspace& w : st.per_stream) {
-    if (w.stream == s) {
-      w.last_use = st.clock;
-      *out = w.mem;
-      return SOFTMAX_OK;
+hipError_t run_plan(const Plan& p, const float* x, float* y, const int64_t* labels,
+                    int64_t rows, int64_t cols, Clip c, int em, const DeviceFacts& f,
+                    hipStream_t st) {
+  const Shape& s = p.shape;
+  const void* fn = kernel_fn(s, em);
+  uint32_t delay = p.delay_ticks;
+  switch (s.kernel) {
+    case SOFTMAX_KERNEL_PACKED: {
+      void* args[] = {&x, &y, &labels, &rows, &cols, &c};
+      return launch(fn, p.grid, 256, args, st);
     }
-  }
-  if (st.capture_ws == nullptr) {
-    e = new_workspace(&st.capture_ws);
-    if (e != hipSuccess) return fail_hip(e);
-  }
-  if (static_cast<int>(st.per_stream.size()) >= kMaxStreamWorkspaces) {
-    // Recycle the least recently used stream's workspace once the device
-    // is idle, so none of that stream's work can still be using it.
-    e = hipDeviceSynchronize();
-    if (e != hipSuccess) return fail_hip(e);
-    StreamWorkspace* lru = &st.per_stream[0];
-    for (StreamWorkspace& w : st.per_stream)
-      if (w.last_use < lru->last_use) lru = &w;
-    lru->stream = s;
-    lru->last_use = st.clock;
-    *out = lru->mem;
-    return SOFTMAX_OK;
-  }
-  char* mem = nullptr;
-  e = new_workspace(&mem);
-  if (e != hipSuccess) return fail_hip(e);
-  st.per_stream.push_back(StreamWorkspace{s, mem, st.clock});
-  *out = mem;
-  return SOFTMAX_OK;
-}
-
-template <bool VEC4, int EM>
-hipError_t split_launch(const softmax_plan_t& p, const float* x, float* y,
-                        const int64_t* labels, int64_t rows, int64_t cols, char* ws, Clip c,
-                        hipStream_t s) {
-  // NLL outputs with 128-bit access take 1024-thread workgroups (chunks of
-  // 32768 columns, two per CU): their workgroups never wait for each other,
-  // and keep no values, so the wider chunk only saves workgroups (long rows
-  // 16.1 -> 14.6 us).  The other modes hold their chunk in registers through
-  // the exchange and would spill at that width.
-  if constexpr (EM == kNllOut && VEC4) {
-    const int64_t gn = ceil_div(cols, kNllChunk);
-    if (gn <= kOnePassMaxChunks)
-      return run_onepass<kOnePassVSmall, VEC4, EM, kNllThreads>(x, y, labels, ws, rows, cols,
-                                                                  gn, kNllMaxBlocks, c, s);
-  }
-  // Plans with at most kOnePassMaxChunks chunks per row are one-pass (their
-  // chunk size is told by elems_per_lane); longer rows are two-pass.
-  const int64_t g = p.chunks_per_row;
-  if (g <= kOnePassMaxChunks && p.elems_per_lane == 4 * kOnePassVSmall)
-    return run_onepass<kOnePassVSmall, VEC4, EM>(x, y, labels, ws, rows, cols, g,
-                                                   kOnePassMaxBlocksSmall, c, s);
-  if constexpr (VEC4) {
-    if (g <= kOnePassMaxChunks)
-      return run_onepass<kOnePassVLarge, VEC4, EM>(x, y, labels, ws, rows, cols, g,
-                                                     kOnePassMaxBlocksLarge, c, s);
-  }
-  return run_split<VEC4, EM>(x, y, labels, reinterpret_cast<float2*>(ws), rows, cols, g, c,
-                             s);
-}
-
-template <int EM>
-hipError_t split_mode(const softmax_plan_t& p, const float* x, float* y,
-                      const int64_t* labels, int64_t rows, int64_t cols, char* ws, Clip c,
-                      hipStream_t s) {
-  return p.vec_width == 4 ? split_launch<true, EM>(p, x, y, labels, rows, cols, ws, c, s)
-                          : split_launch<false, EM>(p, x, y, labels, rows, cols, ws, c, s);
-}
-
-int split_call(const softmax_plan_t& p, const float* x, float* y, const int64_t* labels,
-               int64_t rows, int64_t cols, int dev, Clip c, int em, hipStream_t s) {
-  if (dev < 0 || dev >= kMaxDevices) return SOFTMAX_ERR_INVALID_ARG;
-  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-  hipError_t e = hipStreamIsCapturing(s, &cap);
-  if (e != hipSuccess) return fail_hip(e);
-  char* ws = nullptr;
-  {
-    std::lock_guard<std::mutex> lock(g_mu);
-    const int rc = workspace_for(dev, s, cap != hipStreamCaptureStatusNone, &ws);
-    if (rc != SOFTMAX_OK) return rc;
-  }
-  switch (em) {
-    case kExpWide: e = split_mode<kExpWide>(p, x, y, labels, rows, cols, ws, c, s); break;
-    case kExpFast: e = split_mode<kExpFast>(p, x, y, labels, rows, cols, ws, c, s); break;
-    case kLogOut: e = split_mode<kLogOut>(p, x, y, labels, rows, cols, ws, c, s); break;
-    case kNllOut: e = split_mode<kNllOut>(p, x, y, labels, rows, cols, ws, c, s); break;
-    default: e = split_mode<kExpAccurate>(p, x, y, labels, rows, cols, ws, c, s); break;
-  }
-  return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
-}
-
-template <int EM>
-hipError_t launch_rows(const softmax_plan_t& p, const float* x, float* y,
-                       const int64_t* labels, int64_t rows, int64_t cols, Clip c,
-                       hipStream_t s) {
-  switch (p.kernel) {
-    case SOFTMAX_KERNEL_PACKED:
-      return p.vec_width == 4 ? dispatch_packed<true, EM>(p, x, y, labels, rows, cols, c, s)
-                              : dispatch_packed<false, EM>(p, x, y, labels, rows, cols, c, s);
     case SOFTMAX_KERNEL_WAVE_ROW:
-      return p.vec_width == 4 ? dispatch_wave<true, EM>(p, x, y, labels, rows, cols, c, s)
-                              : dispatch_wave<false, EM>(p, x, y, labels, rows, cols, c, s);
-    case SOFTMAX_KERNEL_BLOCK_ROW:
-      return p.vec_width == 4 ? dispatch_block<true, EM>(p, x, y, labels, rows, cols, c, s)
-                              : dispatch_block<false, EM>(p, x, y, labels, rows, cols, c, s);
+    case SOFTMAX_KERNEL_BLOCK_ROW: {
+      void* args[] = {&x, &y, &labels, &rows, &cols, &c, &delay};
+      return launch(fn, p.grid, s.threads, args, st);
+    }
     default:
-      return hipSuccess;
+      break;
   }
-}
-
-// Every launch of one call in mode em, on a plan made for it.
-int launch_mode(const softmax_plan_t& p, const float* x, float* y, const int64_t* labels,
-                int64_t rows, int64_t cols, int dev, Clip c, int em, hipStream_t stream) {
-  if (p.kernel == SOFTMAX_KERNEL_SPLIT_ROW)
-    return split_call(p, x, y, labels, rows, cols, dev, c, em, stream);
-  hipError_t e;
-  switch (em) {
-    case kExpWide: e = launch_rows<kExpWide>(p, x, y, labels, rows, cols, c, stream); break;
-    case kExpFast: e = launch_rows<kExpFast>(p, x, y, labels, rows, cols, c, stream); break;
-    case kLogOut: e = launch_rows<kLogOut>(p, x, y, labels, rows, cols, c, stream); break;
-    case kNllOut: e = launch_rows<kNllOut>(p, x, y, labels, rows, cols, c, stream); break;
-    default: e = launch_rows<kExpAccurate>(p, x, y, labels, rows, cols, c, stream); break;
+  const uint32_t nonce = g_nonce.fetch_add(1, std::memory_order_relaxed);
+  if (!s.two_pass) {
+    int ichunks = static_cast<int>(p.chunks);
+    for (int64_t r0 = 0; r0 < rows; r0 += p.rows_per_launch) {
+      const int64_t nb = std::min(p.rows_per_launch, rows - r0);
+      const float* xb = x + r0 * cols;
+      float* yb = out_rows(y, r0, cols, em);
+      const int64_t* lb = label_rows(labels, r0, em);
+      XchArgs xa{f.scratch, exchange_key(yb, nonce), p.limit_ticks, 1u};  // join
+      void* args[] = {&xb, &yb, &lb, &xa, &cols, &ichunks, &delay, &c};
+      const hipError_t e = launch(fn, nb * p.chunks, s.threads, args, st);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
   }
-  return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
+  const void* fn_stats = kernel_fn(s, em, true);
+  int iwpr = static_cast<int>(p.wpr);
+  int64_t chunks = p.chunks;
+  for (int64_t r0 = 0; r0 < rows; r0 += p.rows_per_launch) {
+    const int64_t nb = std::min(p.rows_per_launch, rows - r0);
+    const float* xb = x + r0 * cols;
+    float* yb = out_rows(y, r0, cols, em);
+    const int64_t* lb = label_rows(labels, r0, em);
+    XchArgs xa{f.scratch, exchange_key(yb, nonce), p.limit_ticks, 1u};
+    void* a1[] = {&xb, &xa, &cols, &iwpr, &chunks, &c};
+    hipError_t e = launch(fn_stats, nb * p.wpr, s.threads, a1, st);
+    if (e != hipSuccess) return e;
+    XchArgs xb2{f.scratch, xa.key, p.limit_ticks, 0u};  // find only
+    void* a2[] = {&xb, &yb, &lb, &xb2, &cols, &iwpr, &chunks, &c};
+    e = launch(fn, nb * p.wpr, s.threads, a2, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 int check_pointers(const float* x, const float* y, int64_t n_elems, int* dev) {
@@ -483,17 +538,31 @@ int check_pointers(const float* x, const float* y, int64_t n_elems, int* dev) {
 }
 
 // The row softmax with kernel mode em (kExpAccurate, kExpWide, kExpFast,
-// or kLogOut for log outputs) after the clip and size checks.
+// or kLogOut for log outputs) after the clip and size checks; `want` is a
+// caller's shape (softmax_fwd_planned) or null for the library's.
 int softmax_rows(const float* x, float* y, int64_t rows, int64_t cols, Clip c, int em,
-                 hipStream_t stream) {
+                 const softmax_plan_t* want, hipStream_t stream) {
   int rc = check_sizes(rows, cols);
   if (rc != SOFTMAX_OK) return rc;
+  Shape s;
+  if (want != nullptr) {
+    if (want->store_delay_ns < -1 || want->store_delay_ns > kStoreMaxNs)
+      return SOFTMAX_ERR_INVALID_ARG;
+    if (rows > 0 && cols > 0 && !requested_shape(*want, x, y, cols, em, &s))
+      return SOFTMAX_ERR_INVALID_ARG;
+  }
   if (rows == 0 || cols == 0) return SOFTMAX_OK;
   int dev = 0;
   rc = check_pointers(x, y, rows * cols, &dev);
   if (rc != SOFTMAX_OK) return rc;
-  return launch_mode(make_plan(x, y, rows, cols), x, y, nullptr, rows, cols, dev, c, em,
-                     stream);
+  DeviceFacts f;
+  if ((rc = device_facts(dev, &f)) != SOFTMAX_OK) return rc;
+  if (want == nullptr) s = default_shape(x, y, cols, em);
+  Plan p;
+  rc = make_plan(s, rows, cols, em, dev, f, want ? want->store_delay_ns : -1, &p);
+  if (rc != SOFTMAX_OK) return rc;
+  const hipError_t e = run_plan(p, x, y, nullptr, rows, cols, c, em, f, stream);
+  return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
 }
 
 }  // namespace
@@ -503,13 +572,34 @@ extern "C" {
 SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64_t cols,
                              softmax_plan_t* plan) {
   if (plan == nullptr) return SOFTMAX_ERR_INVALID_ARG;
-  const int rc = check_sizes(rows, cols);
+  int rc = check_sizes(rows, cols);
   if (rc != SOFTMAX_OK) return rc;
-  if (rows > 0 && cols > 0) {
-    if (x == nullptr || y == nullptr) return SOFTMAX_ERR_INVALID_ARG;
-    if (partial_overlap(x, y, rows * cols * 4)) return SOFTMAX_ERR_INVALID_ARG;
+  if (rows == 0 || cols == 0) {
+    *plan = softmax_plan_t{};
+    plan->chunks_per_row = 1;
+    return SOFTMAX_OK;
   }
-  *plan = make_plan(x, y, rows, cols);
+  if (x == nullptr || y == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+  if (partial_overlap(x, y, rows * cols * 4)) return SOFTMAX_ERR_INVALID_ARG;
+  const Shape s = default_shape(x, y, cols, kExpAccurate);
+  // The launch geometry needs the current device; without one only the
+  // device-independent fields are filled in.
+  int ndev = 0;
+  int dev = 0;
+  DeviceFacts f;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0 || hipGetDevice(&dev) != hipSuccess ||
+      device_facts(dev, &f) != SOFTMAX_OK) {
+    (void)hipGetLastError();
+    Plan p;
+    p.shape = s;
+    if (s.kernel == SOFTMAX_KERNEL_SPLIT_ROW) p.chunks = ceil_div(cols, chunk_cols(s));
+    *plan = public_plan(p, rows);
+    return SOFTMAX_OK;
+  }
+  Plan p;
+  rc = make_plan(s, rows, cols, kExpAccurate, dev, f, -1, &p);
+  if (rc != SOFTMAX_OK) return rc;
+  *plan = public_plan(p, rows);
   return SOFTMAX_OK;
 }
 
@@ -519,7 +609,17 @@ SOFTMAX_API int softmax_fwd_clip(const float* x, float* y, int64_t rows, int64_t
   bool wide = false;
   const int rc = make_clip(clip_lo, &c, &wide);
   if (rc != SOFTMAX_OK) return rc;
-  return softmax_rows(x, y, rows, cols, c, wide ? kExpWide : kExpAccurate, stream);
+  return softmax_rows(x, y, rows, cols, c, wide ? kExpWide : kExpAccurate, nullptr, stream);
+}
+
+SOFTMAX_API int softmax_fwd_planned(const float* x, float* y, int64_t rows, int64_t cols,
+                                    const softmax_plan_t* plan, hipStream_t stream) {
+  if (plan == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+  Clip c;
+  bool wide = false;
+  const int rc = make_clip(SOFTMAX_CLIP_LO, &c, &wide);
+  if (rc != SOFTMAX_OK) return rc;
+  return softmax_rows(x, y, rows, cols, c, kExpAccurate, plan, stream);
 }
 
 SOFTMAX_API int softmax_fwd_approx(const float* x, float* y, int64_t rows, int64_t cols,
@@ -528,7 +628,7 @@ SOFTMAX_API int softmax_fwd_approx(const float* x, float* y, int64_t rows, int64
   bool wide = false;
   const int rc = make_clip(clip_lo, &c, &wide);
   if (rc != SOFTMAX_OK) return rc;
-  return softmax_rows(x, y, rows, cols, c, kExpFast, stream);
+  return softmax_rows(x, y, rows, cols, c, kExpFast, nullptr, stream);
 }
 
 SOFTMAX_API int softmax_log_fwd(const float* x, float* y, int64_t rows, int64_t cols,
@@ -537,7 +637,7 @@ SOFTMAX_API int softmax_log_fwd(const float* x, float* y, int64_t rows, int64_t 
   bool wide = false;
   const int rc = make_clip(clip_lo, &c, &wide);
   if (rc != SOFTMAX_OK) return rc;
-  return softmax_rows(x, y, rows, cols, c, kLogOut, stream);
+  return softmax_rows(x, y, rows, cols, c, kLogOut, nullptr, stream);
 }
 
 SOFTMAX_API int softmax_nll_fwd(const float* x, const int64_t* labels, float* loss,
@@ -564,9 +664,14 @@ SOFTMAX_API int softmax_nll_fwd(const float* x, const int64_t* labels, float* lo
   if ((rc = check_device_range(x, xbytes, dev)) != SOFTMAX_OK) return rc;
   if ((rc = check_device_range(labels, lbytes, dev)) != SOFTMAX_OK) return rc;
   if ((rc = check_device_range(loss, obytes, dev)) != SOFTMAX_OK) return rc;
-  // The plan's access width follows x alone: the losses are 32-bit stores.
-  return launch_mode(make_plan(x, x, rows, cols), x, loss, labels, rows, cols, dev, c, kNllOut,
-                     stream);
+  DeviceFacts f;
+  if ((rc = device_facts(dev, &f)) != SOFTMAX_OK) return rc;
+  // The access width follows x alone: the losses are 32-bit stores.
+  Plan p;
+  rc = make_plan(default_shape(x, x, cols, kNllOut), rows, cols, kNllOut, dev, f, -1, &p);
+  if (rc != SOFTMAX_OK) return rc;
+  e = run_plan(p, x, loss, labels, rows, cols, c, kNllOut, f, stream);
+  return e == hipSuccess ? SOFTMAX_OK : fail_hip(e);
 }
 
 SOFTMAX_API int softmax_fwd(const float* x, float* y, int64_t rows, int64_t cols,
@@ -579,8 +684,8 @@ SOFTMAX_API const char* softmax_strerror(int code) {
     case SOFTMAX_OK: return "success";
     case SOFTMAX_ERR_INVALID_ARG:
       return "invalid argument (negative or overflowing size, null pointer, "
-             "partially overlapping x and y, or a clip bound that is NaN or above "
-             "SOFTMAX_CLIP_MAX)";
+             "partially overlapping x and y, a clip bound that is NaN or above "
+             "SOFTMAX_CLIP_MAX, or a plan the library cannot run)";
     case SOFTMAX_ERR_HIP: return "HIP call or kernel launch failed";
     case SOFTMAX_ERR_NOT_DEVICE:
       return "pointer is not memory the current device can use, or the range "
@@ -591,27 +696,55 @@ SOFTMAX_API const char* softmax_strerror(int code) {
 
 SOFTMAX_API int softmax_last_hip_error(void) { return smx_host::tl_last_hip_error; }
 
+SOFTMAX_API int softmax_exchange_status(uint64_t* join_give_ups, uint64_t* wait_give_ups,
+                                        int32_t* entries_in_use) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e);
+  DeviceFacts f;
+  int rc = device_facts(dev, &f);
+  if (rc != SOFTMAX_OK) return rc;
+  uint64_t diag[2] = {0, 0};
+  e = hipMemcpy(diag, f.scratch + xch::kDiagWord, sizeof(diag), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return fail_hip(e);
+  // the owner word of every entry
+  std::vector<uint64_t> owners(xch::kEntries);
+  e = hipMemcpy2D(owners.data(), sizeof(uint64_t), f.scratch, xch::kEntryWords * sizeof(uint64_t),
+                  sizeof(uint64_t), xch::kEntries, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return fail_hip(e);
+  int32_t busy = 0;
+  for (uint64_t o : owners) busy += o != 0 ? 1 : 0;
+  if (join_give_ups != nullptr) *join_give_ups = diag[xch::kDiagJoinGiveUps];
+  if (wait_give_ups != nullptr) *wait_give_ups = diag[xch::kDiagWaitGiveUps];
+  if (entries_in_use != nullptr) *entries_in_use = busy;
+  return SOFTMAX_OK;
+}
+
 SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int64_t n,
                                   float clip_lo, int approx, hipStream_t stream) {
   Clip c;
   bool wide = false;
   if (make_clip(clip_lo, &c, &wide) != SOFTMAX_OK) return SOFTMAX_ERR_INVALID_ARG;
+  if (approx < 0 || approx > 2) return SOFTMAX_ERR_INVALID_ARG;
   if (n < 0 || n > INT64_MAX / 4) return SOFTMAX_ERR_INVALID_ARG;
   if (n == 0) return SOFTMAX_OK;
-  if (x == nullptr || m == nullptr || e == nullptr) return SOFTMAX_ERR_INVALID_ARG;
-  if (any_overlap(e, x, n * 4) || any_overlap(e, m, n * 4)) return SOFTMAX_ERR_INVALID_ARG;
+  if (x == nullptr || e == nullptr || (m == nullptr && approx != 2))
+    return SOFTMAX_ERR_INVALID_ARG;
+  if (any_overlap(e, x, n * 4) || (m != nullptr && any_overlap(e, m, n * 4)))
+    return SOFTMAX_ERR_INVALID_ARG;
   int dev = 0;
   hipError_t he = hipGetDevice(&dev);
   if (he != hipSuccess) return fail_hip(he);
   int rc = check_device_range(x, n * 4, dev);
-  if (rc == SOFTMAX_OK) rc = check_device_range(m, n * 4, dev);
+  if (rc == SOFTMAX_OK && m != nullptr) rc = check_device_range(m, n * 4, dev);
   if (rc == SOFTMAX_OK) rc = check_device_range(e, n * 4, dev);
   if (rc != SOFTMAX_OK) return rc;
   const int64_t grid = std::min(ceil_div(n, 256), kMaxGrid);
   void* args[] = {&x, &m, &e, &n, &c};
-  const void* fn = approx ? reinterpret_cast<const void*>(&k_exp_probe<kExpFast>)
-                  : wide  ? reinterpret_cast<const void*>(&k_exp_probe<kExpWide>)
-                          : reinterpret_cast<const void*>(&k_exp_probe<kExpAccurate>);
+  const void* fn = approx == 2 ? reinterpret_cast<const void*>(&k_exp_probe<kExpRaw>)
+                   : approx    ? reinterpret_cast<const void*>(&k_exp_probe<kExpFast>)
+                   : wide      ? reinterpret_cast<const void*>(&k_exp_probe<kExpWide>)
+                               : reinterpret_cast<const void*>(&k_exp_probe<kExpAccurate>);
   he = launch(fn, grid, 256, args, stream);
   return he == hipSuccess ? SOFTMAX_OK : fail_hip(he);
 }

@@ -28,7 +28,7 @@ def test_header_declares_entry_points():
               "softmax_nll_fwd", "softmax_attention_fwd",
               "softmax_strerror",
               "softmax_last_hip_error", "softmax_plan", "softmax_exp_probe",
-              "softmax_copy_probe"):
+              "softmax_copy_probe", "softmax_fwd_planned", "softmax_exchange_status"):
         assert n in names
 
 
@@ -67,37 +67,43 @@ def test_cpu_tensor_is_rejected():
         sm.softmax_fwd(torch.zeros(4, 5))
 
 
+# The shape of a plan depends only on the arguments (no GPU needed); its
+# grid, launches and store delay need the device and are checked in
+# tests/test_gpu_plan.py.
 @pytest.mark.parametrize("rows,cols,kernel,vec,extra", [
     (64, 1000, "wave_row", 4, dict(elems_per_lane=16)),
-    (115200, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13, grid=1536)),
-    (1000, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13, grid=16)),
-    (4096, 1000, "wave_row", 4, dict(grid=1024)),
-    (512, 32768, "block_row", 4, dict(elems_per_lane=32, grid=512)),
-    (64, 262144, "split_row", 4, dict(chunks_per_row=16, launches=1, grid=1024,
-                                      elems_per_lane=32)),
+    (115200, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13)),
+    (1000, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13)),
+    (4096, 1000, "wave_row", 4, dict(elems_per_lane=16)),
+    (512, 32768, "block_row", 4, dict(elems_per_lane=32, block_threads=1024)),
+    (64, 262144, "split_row", 4, dict(chunks_per_row=16, elems_per_lane=32,
+                                      block_threads=512)),
     (3, 1, "packed", 4, dict(lanes_per_row=1, elems_per_lane=1)),
-    (300, 16, "packed", 4, dict(lanes_per_row=1, elems_per_lane=16, grid=2)),
-    (300, 17, "packed", 4, dict(lanes_per_row=2, elems_per_lane=9, grid=3)),
-    (300, 64, "packed", 4, dict(lanes_per_row=4, elems_per_lane=16, grid=5)),
+    (300, 16, "packed", 4, dict(lanes_per_row=1, elems_per_lane=16)),
+    (300, 17, "packed", 4, dict(lanes_per_row=2, elems_per_lane=9)),
+    (300, 64, "packed", 4, dict(lanes_per_row=4, elems_per_lane=16)),
     (3, 65, "wave_row", 1, dict(elems_per_lane=4)),
     (3, 4096, "wave_row", 4, dict(elems_per_lane=64)),
     (3, 4097, "block_row", 1, dict(elems_per_lane=8)),
     # 32-bit access: at most 32 values per lane in a wavefront, and no
-    # one-pass large chunks (both would spill)
+    # one-pass 32768-column chunks (both would spill)
     (3, 2047, "wave_row", 1, dict(elems_per_lane=32)),
     (3, 2049, "block_row", 1, dict(elems_per_lane=8)),
     (3, 4095, "block_row", 1, dict(elems_per_lane=8)),
-    (1, 1048579, "split_row", 1, dict(chunks_per_row=65, elems_per_lane=32, launches=2)),
-    (3, 32769, "split_row", 1, dict(chunks_per_row=3, launches=1)),
-    (300, 262144, "split_row", 4, dict(chunks_per_row=16, launches=5, grid=1024)),
-    (1, 1048576, "split_row", 4, dict(chunks_per_row=64, elems_per_lane=32, launches=1)),
-    (1, 1048580, "split_row", 4, dict(chunks_per_row=33, elems_per_lane=64, launches=1)),
-    (20, 2097152, "split_row", 4, dict(chunks_per_row=64, elems_per_lane=64, grid=512,
-                                       launches=3)),
+    (1, 1048579, "split_row", 1, dict(chunks_per_row=65, elems_per_lane=32,
+                                      block_threads=512)),
+    (3, 32769, "split_row", 1, dict(chunks_per_row=3, block_threads=512)),
+    (300, 262144, "split_row", 4, dict(chunks_per_row=16, block_threads=512)),
+    (1, 524288, "split_row", 4, dict(chunks_per_row=32, block_threads=512)),
+    (1, 1048576, "split_row", 4, dict(chunks_per_row=64, elems_per_lane=32,
+                                      block_threads=512)),
+    (1, 1048580, "split_row", 4, dict(chunks_per_row=33, elems_per_lane=64,
+                                      block_threads=512)),
+    (20, 2097152, "split_row", 4, dict(chunks_per_row=64, elems_per_lane=64)),
     (0, 5, "none", 0, {}),
     (5, 0, "none", 0, {}),
 ])
-def test_plan_buckets(rows, cols, kernel, vec, extra):
+def test_plan_shapes(rows, cols, kernel, vec, extra):
     p = sm.softmax_plan(rows, cols)
     assert p["kernel_name"] == kernel
     assert p["vec_width"] == vec
@@ -115,22 +121,23 @@ def test_plan_vector_width_follows_alignment():
     assert sm.softmax_plan(10, 1000, a, a)["vec_width"] == 4     # in place
 
 
-def test_plan_split_batches_rows_per_one_pass_launch():
-    p = sm.softmax_plan(10000, 262144)
-    per_launch = p["grid"] // p["chunks_per_row"]
-    assert p["grid"] <= 1024 and per_launch * p["chunks_per_row"] == p["grid"]
-    assert p["launches"] == -(-10000 // per_launch)
-
-
 def test_plan_very_long_rows_use_two_passes():
-    # more than 64 one-pass chunks per row
+    # more than 64 one-pass chunks per row: two passes over 16384-column chunks
     p = sm.softmax_plan(2, 1 << 30)
-    assert p["kernel_name"] == "split_row" and p["launches"] % 2 == 0
-    assert p["chunks_per_row"] == (1 << 30) // 16384
+    assert p["kernel_name"] == "split_row"
+    assert p["chunks_per_row"] == (1 << 30) // 16384 and p["block_threads"] == 512
     p = sm.softmax_plan(1, 64 * 32768 + 1)
-    assert p["launches"] == 2 and p["chunks_per_row"] == 129
+    assert p["chunks_per_row"] == 129 and p["elems_per_lane"] == 32
     p = sm.softmax_plan(1, 64 * 32768)
-    assert p["launches"] == 1 and p["chunks_per_row"] == 64
+    assert p["chunks_per_row"] == 64 and p["elems_per_lane"] == 64
+
+
+def test_plan_geometry_is_zero_without_a_device():
+    torch = pytest.importorskip("torch")
+    if torch.cuda.is_available():
+        pytest.skip("a device is present: geometry is checked by the GPU tests")
+    p = sm.softmax_plan(512, 32768)
+    assert p["grid"] == 0 and p["launches"] == 0 and p["store_delay_ns"] == 0
 
 
 def _raw_fwd(x, y, rows, cols):
@@ -238,3 +245,47 @@ def test_nll_arguments_rejected_before_any_hip_call():
     assert nll(X, L, L + 76, 10, 10, -64.0, 0) == bad           # loss overlaps labels
     assert nll(0, 0, 0, 0, 10, -64.0, 0) == sm.OK               # no rows: nothing to do
     assert nll(0, 0, 0, 0, 0, float("-inf"), 0) == sm.OK
+
+
+def test_planned_rejects_plans_the_library_cannot_run():
+    """softmax_fwd_planned checks the requested kernel against the arguments
+    before any HIP call (the pointers below are never dereferenced)."""
+    X, Y = 1 << 40, 1 << 41      # 16-byte aligned
+    bad = sm.ERR_INVALID_ARG
+    run = sm.softmax_fwd_planned_ptr
+    assert run(X, Y, 4, 100, dict(kernel_name="packed", vec_width=4)) == bad   # cols > 64
+    assert run(X, Y, 4, 5000, dict(kernel_name="wave_row", vec_width=4)) == bad
+    assert run(X, Y, 4, 3000, dict(kernel_name="wave_row", vec_width=1)) == bad  # would spill
+    assert run(X, Y, 4, 40000, dict(kernel_name="block_row", vec_width=4)) == bad
+    assert run(X + 4, Y, 4, 1000, dict(kernel_name="wave_row", vec_width=4)) == bad  # misaligned
+    assert run(X, Y, 4, 1002, dict(kernel_name="wave_row", vec_width=4)) == bad      # cols % 4
+    # row-strided kernels need whole float4 rows even below 64 columns (the
+    # packed kernel moves tiles of a multiple of four rows and does not)
+    assert run(X, Y, 4, 50, dict(kernel_name="wave_row", vec_width=4)) == bad
+    assert run(X, Y, 4, 50, dict(kernel_name="block_row", vec_width=4)) == bad
+    assert run(X, Y, 4, 50, dict(kernel_name="split_row", vec_width=4, block_threads=256,
+                                 elems_per_lane=32)) == bad
+    assert run(X, Y, 4, 1000, dict(kernel_name="wave_row", vec_width=2)) == bad
+    assert run(X, Y, 4, 1000, dict(kernel_name="none", vec_width=4)) == bad
+    split = dict(kernel_name="split_row", vec_width=4)
+    assert run(X, Y, 4, 1 << 16, dict(split, block_threads=128, elems_per_lane=32)) == bad
+    assert run(X, Y, 4, 1 << 16, dict(split, block_threads=256, elems_per_lane=64)) == bad
+    assert run(X, Y, 4, 1 << 16, dict(split, vec_width=1, block_threads=512,
+                                      elems_per_lane=64)) == bad
+    # two passes exist only as 512 x 32
+    assert run(X, Y, 1, 1 << 22, dict(split, block_threads=256, elems_per_lane=32)) == bad
+    assert run(X, Y, 4, 1000, dict(kernel_name="wave_row", vec_width=4,
+                                   store_delay_ns=-2)) == bad
+    assert run(X, Y, 4, 1000, dict(kernel_name="wave_row", vec_width=4,
+                                   store_delay_ns=200001)) == bad
+    lib = sm.load_library()
+    assert lib.softmax_fwd_planned(X, Y, 4, 1000, None, None) == bad
+    # empty calls succeed without touching the GPU
+    assert run(0, 0, 0, 1000, dict(kernel_name="wave_row", vec_width=4)) == sm.OK
+
+
+def test_exp_probe_modes():
+    lib = sm.load_library()
+    assert lib.softmax_exp_probe(0x1000, 0x8000, 0x10000, 16, -64.0, 3, None) == sm.ERR_INVALID_ARG
+    assert lib.softmax_exp_probe(0x1000, None, 0x10000, 16, -64.0, 0, None) == sm.ERR_INVALID_ARG
+    assert lib.softmax_exp_probe(0x1000, None, 0x10000, 0, -64.0, 2, None) == sm.OK

@@ -77,16 +77,49 @@ def test_traffic_is_withheld_when_sources_changed(tmp_path, monkeypatch):
     assert bench.load_traffic("missing") == (None, None)
 
 
-def test_trace_groups_name_every_workload():
-    pytest.importorskip("ctypes")
-    import paper_1904_12380_amd as sm
-    try:
-        sm.load_library()
-    except ImportError:
-        pytest.skip("library not built")
-    groups = bench.trace_groups(workloads.WORKLOADS)
-    labelled = " / ".join(groups.values())
-    for key in workloads.WORKLOADS:
-        assert labelled.count(key) == 2, key        # softmax kernel and copy kernel
-    kernels = {k for k, _ in groups}
-    assert {"k_packed", "k_wave_row", "k_block_row", "k_split", "k_copy4"} <= kernels
+def _write_trace(path, rows):
+    os.makedirs(path, exist_ok=True)
+    fields = ["Kernel_Name", "Grid_Size_X", "Start_Timestamp", "End_Timestamp", "VGPR_Count",
+              "SGPR_Count", "LDS_Block_Size", "Scratch_Size"]
+    with open(os.path.join(path, "run_kernel_trace.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=fields)
+        w.writeheader()
+        for name, grid, b, e in rows:
+            w.writerow({"Kernel_Name": name, "Grid_Size_X": grid, "Start_Timestamp": b,
+                        "End_Timestamp": e, "VGPR_Count": 56, "SGPR_Count": 32,
+                        "LDS_Block_Size": 512, "Scratch_Size": 0})
+    with open(os.path.join(path, "run_kernel_stats.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Name", "Calls", "AverageNs", "MinNs", "MaxNs"])
+        w.writeheader()
+        w.writerow({"Name": rows[0][0], "Calls": len(rows), "AverageNs": 1000, "MinNs": 900,
+                    "MaxNs": 1100})
+
+
+def test_summarize_trace_and_lookup(tmp_path, monkeypatch):
+    """Dispatch durations are grouped by (kernel, grid) into runs, written to
+    the trace JSON, and read back for a plan's kernel while the sources are
+    unchanged."""
+    name = "smx::k_split_onepass<256, 8, true, 0>"
+    full = f"void {name}(float const*, float*)"
+    # 10 calls of 20..29 us, then (after a 1 s gap) 5 more of 40 us
+    rows = [(full, 524288, 1000 + i * 100_000, 1000 + i * 100_000 + (20 + i) * 1000)
+            for i in range(10)]
+    rows += [(full, 524288, 2_000_000_000 + i * 100_000, 2_000_000_000 + i * 100_000 + 40_000)
+             for i in range(5)]
+    rows += [("Cijk_other_library_kernel", 64, 0, 5000)]
+    _write_trace(tmp_path / "trace", rows)
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path / "profiles"))
+    monkeypatch.setattr(bench, "TRACE_JSON", str(tmp_path / "profiles" / "trace_bench.json"))
+    bench.summarize_trace(str(tmp_path / "trace"), "cmd", None)
+    doc = json.load(open(tmp_path / "profiles" / "trace_bench.json"))
+    runs = [k for k in doc["kernels"] if k["kernel"] == name]
+    assert [r["calls"] for r in runs] == [10, 5]
+    assert runs[0]["median_us"] == pytest.approx(24.5)
+    plan = {"kernel_name": "split_row", "elems_per_lane": 32, "vec_width": 4,
+            "block_threads": 256, "lanes_per_row": 256}
+    assert bench.plan_kernel_name(plan) == name
+    st = bench.kernel_trace_stats(name, 524288)
+    assert st["calls"] == 10 and st["p10_us"] < st["median_us"] < st["p90_us"]
+    doc["source_sha256"] = "0" * 64
+    json.dump(doc, open(tmp_path / "profiles" / "trace_bench.json", "w"))
+    assert "note" in bench.kernel_trace_stats(name, 524288)

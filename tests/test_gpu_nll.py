@@ -146,11 +146,12 @@ def test_minus_log_softmax_at_label(key):
 
 @pytest.mark.parametrize("rows,cols", [(3, 100003), (64, 262144), (2, 1048580), (70, 500000)])
 def test_long_rows_interleaved_with_other_modes(rows, cols):
-    """Long rows share the library's exchange slots between the modes: the
-    loss's merging workgroup puts them back, so softmax, log-softmax and
-    loss calls in any order on one stream all stay within their bounds.  70 x 500000
-    takes three one-pass launches per call (31 chunks per row, 33 rows per
-    launch)."""
+    """Long rows of every mode share the exchange table: each launch claims a
+    region and the last of its workgroups returns it to rest (for the loss,
+    the merging workgroup), so softmax, log-softmax and loss calls in any
+    order on one stream all stay within their bounds, and afterwards no wait
+    gave up and no region is left claimed.  70 x 500000 takes several
+    one-pass launches per call."""
     import torch
     x = workloads.random_logits(rows, cols, seed=cols + rows, kind="clip_heavy")
     t = np.random.default_rng(cols).integers(0, cols, size=rows, dtype=np.int64)
@@ -174,6 +175,9 @@ def test_long_rows_interleaved_with_other_modes(rows, cols):
         b = (-picked).double().cpu().numpy()
         bound = 2.0 * (2e-6 + 2.5e-7 * (np.abs(a) + math.log(cols)))
         assert np.all(np.abs(a - b) <= bound), rep
+    torch.cuda.synchronize()
+    st = sm.softmax_exchange_status()
+    assert st == {"join_give_ups": 0, "wait_give_ups": 0, "entries_in_use": 0}, st
 
 
 def test_uniform_rows():
