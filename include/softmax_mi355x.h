@@ -60,7 +60,8 @@ extern "C" {
 #define SOFTMAX_KERNEL_NONE 0      /* rows*cols == 0: nothing is launched */
 #define SOFTMAX_KERNEL_PACKED 1    /* cols <= 64: several rows per wavefront */
 #define SOFTMAX_KERNEL_WAVE_ROW 2  /* cols <= 4096: one wavefront per row */
-#define SOFTMAX_KERNEL_BLOCK_ROW 3 /* cols <= 32768: one workgroup per row */
+#define SOFTMAX_KERNEL_BLOCK_ROW 3 /* cols <= 8192 (log and NLL outputs:
+                                      32768): one workgroup per row */
 #define SOFTMAX_KERNEL_SPLIT_ROW 4 /* longer rows: several workgroups per row */
 
 /*
@@ -85,7 +86,7 @@ extern "C" {
  * Asynchrony: work is enqueued on `stream` and the call returns without
  * waiting; y is valid once the stream has reached that point.
  *
- * Scratch: the call allocates nothing.  Rows longer than 32768 columns are
+ * Scratch: the call allocates nothing.  Rows longer than 8192 columns are
  * split over several workgroups, which combine partial (max, sum) pairs
  * through a table of 4096 row entries held in a static device array
  * (2,359,552 bytes per device, part of the library's code object, zero at
@@ -98,8 +99,9 @@ extern "C" {
  * running launch waits for it (bounded).
  *
  * Long rows are done in one pass when a row spans at most 64 workgroups
- * (cols <= 1048576 in chunks of 16384 columns and, with 128-bit access
- * only, cols <= 2097152 in chunks of 32768): the
+ * (chunks of 8192 columns up to cols = 65536, then chunks of 16384 up to
+ * cols = 1048576 and, with 128-bit access only, chunks of 32768 up to
+ * cols = 2097152): the
  * workgroups of a row exchange their pairs in the middle of the kernel and
  * wait for each other.  Workgroups are dispatched in ID order, so this always
  * progresses while a row's workgroups can be resident together.  Longer rows
@@ -107,8 +109,9 @@ extern "C" {
  * clock): a workgroup that gives up writes NaN for its outputs instead of
  * stalling the device, and counts itself in softmax_exchange_status().
  *
- * Store schedule: in the one-pass split-row launches (every workgroup
- * resident at once, one chunk each, about 8 MiB read or more) the stores
+ * Store schedule: in the one-pass split-row launches with 128-bit access
+ * (every workgroup resident at once, one chunk each, about 8 MiB read or
+ * more) the stores
  * wait until the launch's reads are expected to be done (read bytes /
  * 7.6 TB/s + 0.3 us after the workgroup starts), so HBM serves the reads
  * and the writes as two phases; softmax_plan() reports the delay, and

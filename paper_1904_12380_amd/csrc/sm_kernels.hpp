@@ -236,8 +236,114 @@ __device__ __forceinline__ float2 lane_online(const float (&v)[N], Clip clip) {
 // This lane's share of the row sum against the row max M (rs), from its
 // lane_online result: s * exp(max(m - M, lo)), or s itself for a lane with
 // no finite element.
+template <int EM = kExpAccurate>
 __device__ __forceinline__ float lane_share(float2 ms, RowShift rs) {
-  return ms.x == kNegInf ? ms.y : ms.y * exp_shift_clip<kExpAccurate>(ms.x, rs);
+  return ms.x == kNegInf ? ms.y : ms.y * exp_shift_clip<EM>(ms.x, rs);
+}
+
+// Loads as load_strip, for a segment whose strips are all whole
+// (lim = 4*V*stride): no masks and no control flow, and issued in order
+// (the scheduling barriers keep the compiler from reordering them), so each
+// use of a value waits only for the loads up to its own.
+template <int V, bool VEC4>
+__device__ __forceinline__ void load_strip_whole(float (&v)[4 * V], const float* p,
+                                                 int lane_off, int stride) {
+  if constexpr (VEC4) {
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const f32x4 q = ld_stream(p + 4 * (lane_off + stride * j));
+      __builtin_amdgcn_sched_barrier(0);
+      v[4 * j + 0] = q.x;
+      v[4 * j + 1] = q.y;
+      v[4 * j + 2] = q.z;
+      v[4 * j + 3] = q.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4 * V; ++i) {
+      v[i] = __builtin_nontemporal_load(p + lane_off + stride * i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+// Sub-strip length of the online reduction of the probability modes.
+constexpr int kOnlineSub = 8;
+// Whether a lane's N values take that reduction (two sub-strips at least).
+template <int N>
+constexpr bool online_exp() { return N >= 2 * kOnlineSub; }
+
+// The probability modes' online form of a lane's reduction (lanes holding
+// N >= 16 values, in load order): v is taken in sub-strips of kOnlineSub
+// elements, and each is replaced by its clipped exponentials against the
+// lane's running max as soon as its own loads have returned, so the
+// exponential work overlaps the arrival of the rest of the segment instead
+// of starting after its last load.  mk[k] keeps the running max that
+// sub-strip k was taken against, for the output step (store_online).
+// Returns the lane max m (-inf when every element is) and
+// s = sum exp(max(x - m, lo)) over the lane's elements, with the same
+// rescaling rule as lane_online.
+template <int MODE, int N>
+__device__ __forceinline__ float2 lane_online_exp(float (&v)[N], float (&mk)[N / kOnlineSub],
+                                                  Clip clip) {
+  constexpr int SUB = kOnlineSub;
+  static_assert(N % SUB == 0, "whole sub-strips");
+  float m = kNegInf;
+  float s = 0.0f;
+#pragma unroll
+  for (int k0 = 0; k0 < N; k0 += SUB) {
+    float mx = v[k0];
+#pragma unroll
+    for (int i = 1; i < SUB; ++i) mx = fmaxf(mx, v[k0 + i]);
+    const float m_new = fmaxf(m, mx);
+    const RowShift rs = row_shift(m_new == kNegInf ? 0.0f : m_new, clip);
+    float t[SUB];
+#pragma unroll
+    for (int i = 0; i < SUB; ++i) {
+      v[k0 + i] = exp_shift_clip<MODE>(v[k0 + i], rs);
+      t[i] = v[k0 + i];
+    }
+    const float sk = tree_sum(t);
+    if (k0 == 0) {
+      s = sk;
+    } else {
+      const float f = m == kNegInf ? 1.0f : exp_shift_clip<exp_mode<MODE>()>(m, rs);
+      s = s * f + sk;
+    }
+    m = m_new;
+    mk[k0 / SUB] = m_new;
+    // Finish this sub-strip here: its exponentials are not sunk below the
+    // next sub-strip's max, which waits for that sub-strip's loads.
+    asm volatile("" : "+v"(s), "+v"(m));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  return make_float2(m, s);
+}
+
+// A segment's (m, s) through lane_online_exp, over the workgroup's NW
+// wavefronts: m the segment max, s its sum of exp(max(x - m, lo)) (for
+// m = -inf, the lanes' sums of clipped values).  v holds the lane's
+// exponentials afterwards (see lane_online_exp).
+template <int NW, int V, bool VEC4, int MODE>
+__device__ __forceinline__ float2 segment_online(float (&v)[4 * V],
+                                                 float (&mk)[4 * V / kOnlineSub],
+                                                 const float* p, int lane_off, int stride,
+                                                 int lim, Clip clip, float* red_max,
+                                                 float* red_sum) {
+  // Each branch reduces its own loads: after a join the compiler would wait
+  // for all of them before the first use.
+  float2 ms;
+  if (lim == 4 * V * stride) {
+    load_strip_whole<V, VEC4>(v, p, lane_off, stride);
+    ms = lane_online_exp<MODE>(v, mk, clip);
+  } else {
+    load_strip<V, VEC4>(v, p, opaque(lane_off), stride, lim);
+    ms = lane_online_exp<MODE>(v, mk, clip);
+  }
+  const float m = block_max<NW>(ms.x, red_max);
+  const float s = block_sum<NW>(
+      lane_share<exp_mode<MODE>()>(ms, row_shift(m == kNegInf ? 0.0f : m, clip)), red_sum);
+  return make_float2(m, s);
 }
 
 // Stores out(v[i]) for the columns of the strip that are inside the row.
@@ -278,6 +384,27 @@ __device__ __forceinline__ void store_row(const float (&v)[4 * V], RowShift rs, 
     const float rcp = 1.0f / s;
     store_strip<V, VEC4>(v, [&](float ev) { return ev * rcp; }, p, lane_off, stride, lim);
   }
+}
+
+// Stores the probabilities of a segment left by segment_online: with the
+// row's shift rs (max M) and rcp = 1/S,
+//     y = max(e * exp(max(mk - M, lo)) * rcp, e_lo * rcp)
+// per sub-strip.  For x - M >= lo the rescaled e is exp(x - M) / S; below
+// it, under e^lo / S, so the max gives the clipped value exactly.
+template <int V, bool VEC4, int MODE>
+__device__ __forceinline__ void store_online(float (&v)[4 * V],
+                                             const float (&mk)[4 * V / kOnlineSub], RowShift rs,
+                                             float rcp, float* p, int lane_off, int stride,
+                                             int lim) {
+  constexpr int SUB = kOnlineSub;
+  const float floor_y = rs.e_lo * rcp;
+#pragma unroll
+  for (int k = 0; k < 4 * V / SUB; ++k) {
+    const float sc = exp_shift_clip<exp_mode<MODE>()>(mk[k], rs) * rcp;
+#pragma unroll
+    for (int i = 0; i < SUB; ++i) v[k * SUB + i] = fmaxf(v[k * SUB + i] * sc, floor_y);
+  }
+  store_strip<V, VEC4>(v, [](float ev) { return ev; }, p, lane_off, stride, lim);
 }
 
 // The row's label as a column of the segment [c0, c0 + lim), or -1 when it
@@ -582,6 +709,8 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y,
       if (tid == 0)
         y[row] = bad ? __builtin_nanf("") : -log_out(xl, row_shift(m, clip), log_of_sum(s));
     } else {
+      // (The online reduction of the split kernel measured slower here:
+      // 23.2 us against 22.5 us on 512 rows of 32768.)
       load_strip<V, VEC4>(v, xr, opaque(tid), NT, lim);
       const LabelPick pick =
           pick_label<V, VEC4, MODE>(v, label, cols, 0, lim, tid, NT, tid == 0);
@@ -832,11 +961,18 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
   const int64_t label = row_label<MODE>(labels, lrow);
   const int lim = seg_len(cols, c0, CH);
 
+  constexpr bool ONLINE = !keeps_logits<MODE>() && online_exp<4 * V>();
   float v[4 * V];
-  if constexpr (keeps_logits<MODE>())
+  float mk[ONLINE ? 4 * V / kOnlineSub : 1];
+  float2 part;
+  if constexpr (ONLINE) {
+    part = segment_online<NW, V, VEC4, MODE>(v, mk, xr, tid, NT, lim, clip, red_max, red_sum);
+    if (part.x == kNegInf) part.y = static_cast<float>(lim);
+  } else if constexpr (keeps_logits<MODE>()) {
     load_strip_flat<V, VEC4>(v, xr, tid, NT, lim);
-  else
+  } else {
     load_strip<V, VEC4>(v, xr, tid, NT, lim);
+  }
   // NLL outputs: every workgroup reads the row's label logit right after its
   // chunk's loads (one cache line per wavefront, after the label itself),
   // so the one that merges the row below already holds it, and the values
@@ -847,7 +983,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
   LabelPick pick{0.0f, false, false};
   if constexpr (MODE == kLogOut)
     pick = pick_label<V, VEC4, MODE>(v, label, cols, c0, lim, tid, NT, g == 0 && tid == 0);
-  const float2 part = chunk_partial<NW, V, MODE>(v, lim, clip, red_max, red_sum);
+  if constexpr (!ONLINE) part = chunk_partial<NW, V, MODE>(v, lim, clip, red_max, red_sum);
   const float m = part.x;
   const float s = part.y;
   const uint64_t deadline = t0 + xa.limit_ticks;
@@ -916,6 +1052,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
       if constexpr (keeps_logits<MODE>()) {
         bcast[0] = ok ? rowms.x : __builtin_nanf("");  // M
         bcast[1] = ok ? rowms.y : __builtin_nanf("");  // S
+      } else if constexpr (ONLINE) {
+        bcast[0] = ok ? rowms.x : __builtin_nanf("");  // M
+        bcast[1] = ok ? rcp : __builtin_nanf("");      // 1 / S
       } else {
         const RowShift rs = row_shift(rowms.x, clip);
         bcast[0] = ok ? exp_shift_clip<MODE>(m, rs) * rcp : __builtin_nanf("");  // e^(m_g-M)/S
@@ -940,6 +1079,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     // v still holds the logits: y = c - ln S against the row's M.
     finish_row<V, VEC4, MODE>(v, row_shift(bcast[0], clip), bcast[1], y, lrow, cols, c0, lim,
                               pick, tid, NT);
+  } else if constexpr (ONLINE) {
+    store_online<V, VEC4, MODE>(v, mk, row_shift(bcast[0], clip), bcast[1],
+                                y + lrow * cols + c0, opaque(tid), NT, lim);
   } else {
     float* yr = y + lrow * cols + c0;
     const float scale = bcast[0];

@@ -39,16 +39,28 @@ constexpr int64_t kWaveRowMaxCols = 4096;
 constexpr int64_t kWaveRowMaxColsScalar = 2048;
 constexpr int64_t kBlockRowMaxCols = 32768;
 constexpr int kBlockThreads = 1024;
+// Probability rows longer than this take the one-pass split kernel rather
+// than one workgroup per row (measured with the dispatch sweep,
+// paper_1904_12380_amd/sweep.py): per 64 MiB of logits, 16384 columns ran
+// 21.8 us split against 25.8 us, 32768 columns 21.7 against 22.2, and 8192
+// columns 25.4 against 25.3.  Log and NLL rows keep k_block_row up to
+// kBlockRowMaxCols.
+constexpr int64_t kSplitMinColsProb = 8192;
 
 // Split rows, one pass: a row spans at most this many workgroups (the
 // exchange is read by one wavefront, one slot per lane).  Chunk shapes,
-// threads x 128-bit strips per lane: 512 x 8 (16384 columns) up to 64
-// chunks, then 512 x 16 (32768, 128-bit access only: with 32-bit access it
-// would spill).  256 x 8 (8192) exists for softmax_fwd_planned: on
-// 64 x 262144 its 2048 workgroups took 24.4 us against 22.0 for 1024 of
-// 512 x 8.  NLL outputs with 128-bit access take 1024 x 8 (32768 columns):
-// their workgroups never wait for each other and keep no values.
+// threads x 4-element strips per lane: probability rows take 256 x 8
+// (8192 columns) up to kSmallChunkMaxChunks chunks; then every mode takes
+// 512 x 8 (16384 columns) up to 64 chunks, then 512 x 16 (32768, 128-bit
+// access only: with 32-bit access it would spill).  Measured per 64 MiB:
+// 256 x 8 ran 21.6-21.8 us on rows of 16384 to 65536 columns against
+// 21.8-22.7 for 512 x 8, but 22.5 against 21.7 on 131072 columns and 24.2
+// against 22.0 on 262144 (the row's wait for 16 or 32 partials costs more
+// than the smaller workgroups gain).  NLL outputs with 128-bit access take
+// 1024 x 8 (32768 columns): their workgroups never wait for each other and
+// keep no values.
 constexpr int64_t kOnePassMaxChunks = 64;
+constexpr int64_t kSmallChunkMaxChunks = 8;
 constexpr int kNllThreads = 1024;
 
 // Split rows, two passes (rows too long for the one-pass shapes): 512 x 8
@@ -264,6 +276,7 @@ inline bool can_vec4(int kernel, const float* x, const float* y, int64_t cols) {
 // The library's shape for a call (mode em).
 Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
   Shape s;
+  const bool prob = em != kLogOut && em != kNllOut;
   s.vec4 = can_vec4(cols <= kPackedMaxCols ? SOFTMAX_KERNEL_PACKED : SOFTMAX_KERNEL_SPLIT_ROW,
                     x, y, cols);
   if (cols <= kPackedMaxCols) {
@@ -276,7 +289,7 @@ Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
     s.kernel = SOFTMAX_KERNEL_WAVE_ROW;
     s.threads = 256;
     s.v = static_cast<int>(pow2_at_least(ceil_div(cols, 256)));
-  } else if (cols <= kBlockRowMaxCols) {
+  } else if (cols <= (prob ? kSplitMinColsProb : kBlockRowMaxCols)) {
     s.kernel = SOFTMAX_KERNEL_BLOCK_ROW;
     s.threads = kBlockThreads;
     s.v = static_cast<int>(std::max<int64_t>(2, pow2_at_least(ceil_div(cols, 4096))));
@@ -284,6 +297,9 @@ Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
     s.kernel = SOFTMAX_KERNEL_SPLIT_ROW;
     if (em == kNllOut && s.vec4 && ceil_div(cols, int64_t(4) * 8 * kNllThreads) <= kOnePassMaxChunks) {
       s.threads = kNllThreads;
+      s.v = 8;
+    } else if (prob && ceil_div(cols, int64_t(4) * 8 * 256) <= kSmallChunkMaxChunks) {
+      s.threads = 256;
       s.v = 8;
     } else if (ceil_div(cols, int64_t(4) * 8 * 512) <= kOnePassMaxChunks) {
       s.threads = 512;
@@ -402,7 +418,9 @@ int make_plan(const Shape& s, int64_t rows, int64_t cols, int em, int dev,
         p.rows_per_launch = std::min(resident / p.chunks, int64_t(xch::kMaxRowsPerLaunch));
         p.grid = std::min(rows, p.rows_per_launch) * p.chunks;
         p.launches = ceil_div(rows, p.rows_per_launch);
-        one_wave = em != kNllOut;
+        // The store schedule pays with 128-bit access; with 32-bit access
+        // (rows of 16383 and 32765 columns) it measured 0.1-0.4 us slower.
+        one_wave = em != kNllOut && s.vec4;
         launch_read_bytes = std::min(rows, p.rows_per_launch) * cols * 4;
       } else {
         // Workgroup w of a row takes chunks w, w + wpr, ...

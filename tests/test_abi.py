@@ -75,7 +75,12 @@ def test_cpu_tensor_is_rejected():
     (115200, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13)),
     (1000, 50, "packed", 4, dict(lanes_per_row=4, elems_per_lane=13)),
     (4096, 1000, "wave_row", 4, dict(elems_per_lane=16)),
-    (512, 32768, "block_row", 4, dict(elems_per_lane=32, block_threads=1024)),
+    (512, 32768, "split_row", 4, dict(chunks_per_row=4, elems_per_lane=32,
+                                      block_threads=256)),
+    (3, 8192, "block_row", 4, dict(elems_per_lane=8, block_threads=1024)),
+    (3, 8193, "split_row", 1, dict(chunks_per_row=2, block_threads=256)),
+    (2, 65536, "split_row", 4, dict(chunks_per_row=8, block_threads=256)),
+    (2, 65540, "split_row", 4, dict(chunks_per_row=5, block_threads=512)),
     (64, 262144, "split_row", 4, dict(chunks_per_row=16, elems_per_lane=32,
                                       block_threads=512)),
     (3, 1, "packed", 4, dict(lanes_per_row=1, elems_per_lane=1)),
@@ -92,7 +97,7 @@ def test_cpu_tensor_is_rejected():
     (3, 4095, "block_row", 1, dict(elems_per_lane=8)),
     (1, 1048579, "split_row", 1, dict(chunks_per_row=65, elems_per_lane=32,
                                       block_threads=512)),
-    (3, 32769, "split_row", 1, dict(chunks_per_row=3, block_threads=512)),
+    (3, 32769, "split_row", 1, dict(chunks_per_row=5, block_threads=256)),
     (300, 262144, "split_row", 4, dict(chunks_per_row=16, block_threads=512)),
     (1, 524288, "split_row", 4, dict(chunks_per_row=32, block_threads=512)),
     (1, 1048576, "split_row", 4, dict(chunks_per_row=64, elems_per_lane=32,

@@ -234,7 +234,11 @@ def test_plan_geometry_on_device():
     p = sm.softmax_plan(4096, 1000)
     assert p["kernel_name"] == "wave_row" and p["grid"] == 1024 and p["store_delay_ns"] == 0
     p = sm.softmax_plan(512, 32768)
-    assert p["grid"] == 512 and p["launches"] == 1 and p["store_delay_ns"] == 0
+    assert p["kernel_name"] == "split_row" and p["chunks_per_row"] == 4
+    assert p["grid"] == 2048 and p["launches"] == 1
+    assert 8000 < p["store_delay_ns"] < 10000
+    p = sm.softmax_plan(512, 32767)              # 32-bit access: no store schedule
+    assert p["vec_width"] == 1 and p["store_delay_ns"] == 0
     p = sm.softmax_plan(64, 262144)
     assert p["chunks_per_row"] == 16 and p["launches"] == 1 and p["grid"] == 1024
     assert 8000 < p["store_delay_ns"] < 10000

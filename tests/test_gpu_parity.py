@@ -326,9 +326,9 @@ def test_split_rows_several_one_pass_launches():
 
 @pytest.mark.parametrize("rows,cols", [(3, 1048580), (2, 2097152), (1, 1048576), (5, 524292)])
 def test_split_rows_large_chunks(rows, cols):
-    """Rows past 64 chunks of 8192 columns use 16384-column chunks, and past
-    64 of those 32768-column chunks (with 128-bit access; a ragged 128-bit
-    tail at 1048580)."""
+    """Rows past 64 chunks of 16384 columns use 32768-column chunks (with
+    128-bit access; a ragged 128-bit tail at 1048580); 524292 columns take
+    33 chunks of 16384."""
     log(f"[parity] split rows, large chunks {rows}x{cols}")
     p = sm.softmax_plan(rows, cols)
     assert p["kernel_name"] == "split_row" and p["launches"] == 1
