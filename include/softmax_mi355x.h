@@ -86,8 +86,11 @@ extern "C" {
  * Asynchrony: work is enqueued on `stream` and the call returns without
  * waiting; y is valid once the stream has reached that point.
  *
- * Scratch: the call allocates nothing.  Rows longer than 8192 columns are
- * split over several workgroups, which combine partial (max, sum) pairs
+ * Scratch: no entry point of this library allocates memory, so callers
+ * that cannot allocate (code under stream capture, serving loops,
+ * harnesses that forbid hipMalloc) can call any of them.  Rows longer than
+ * 8192 columns are split over several workgroups, which combine partial
+ * (max, sum) pairs
  * through a table of 4096 row entries held in a static device array
  * (2,359,552 bytes per device, part of the library's code object, zero at
  * rest).  The workgroups of a row meet at the entry its launch's key (the
