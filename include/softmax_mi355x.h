@@ -58,11 +58,16 @@ extern "C" {
 
 /* Kernel families reported by softmax_plan(). */
 #define SOFTMAX_KERNEL_NONE 0      /* rows*cols == 0: nothing is launched */
-#define SOFTMAX_KERNEL_PACKED 1    /* cols <= 64: several rows per wavefront */
+#define SOFTMAX_KERNEL_PACKED 1    /* cols <= 64 (other than GROUP_ROWS):
+                                      several rows per wavefront */
 #define SOFTMAX_KERNEL_WAVE_ROW 2  /* cols <= 4096: one wavefront per row */
 #define SOFTMAX_KERNEL_BLOCK_ROW 3 /* cols <= 8192 (log and NLL outputs:
                                       32768): one workgroup per row */
 #define SOFTMAX_KERNEL_SPLIT_ROW 4 /* longer rows: several workgroups per row */
+#define SOFTMAX_KERNEL_GROUP_ROWS 5 /* cols <= 256 in whole 16-byte strips
+                                       (cols % 4 == 0, 16-byte aligned x and
+                                       y), probability outputs: G lanes per
+                                       row, several rows per wavefront */
 
 /*
  * softmax_fwd -- row-wise clipped softmax, fp32 in and out.

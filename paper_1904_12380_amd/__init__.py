@@ -52,7 +52,8 @@ CLIP_MAX = -48.0
 ATTN_MAX_KEYS = 64
 ATTN_MAX_DIM = 65536
 OK, ERR_INVALID_ARG, ERR_HIP, ERR_NOT_DEVICE = 0, 1, 2, 3
-KERNEL_NAMES = {0: "none", 1: "packed", 2: "wave_row", 3: "block_row", 4: "split_row"}
+KERNEL_NAMES = {0: "none", 1: "packed", 2: "wave_row", 3: "block_row", 4: "split_row",
+                5: "group_rows"}
 KERNEL_IDS = {v: k for k, v in KERNEL_NAMES.items()}
 
 

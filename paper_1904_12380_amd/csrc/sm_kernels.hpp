@@ -13,13 +13,17 @@
 // y as scratch: x is read from HBM once (twice for rows over 2^21 columns)
 // and y is written once.
 //
-//   k_packed      cols <= 64: a persistent workgroup stages tiles of whole
-//                 rows in LDS with 128-bit loads, groups of G lanes reduce
-//                 one row each with DPP, and the tile goes back out with
-//                 128-bit stores; the next tile's loads are issued early.
+//   k_group_rows  cols <= 256 in whole 16-byte strips, probability
+//                 outputs: G lanes per row, each holding one 128-bit strip
+//                 as the coalesced load leaves it; segmented DPP reductions.
+//   k_packed      cols <= 64 otherwise: a persistent workgroup stages tiles
+//                 of whole rows in LDS with 128-bit loads, groups of G lanes
+//                 reduce one row each with DPP, and the tile goes back out
+//                 with 128-bit stores; the next tile's loads are issued early.
 //   k_wave_row    cols <= 4096: one wavefront per row, the row held in VGPRs.
-//   k_block_row   cols <= 32768: one workgroup per row, the row held in
-//                 VGPRs, per-wave partials combined through LDS.
+//   k_block_row   cols <= 8192 (32768 for log and NLL outputs): one
+//                 workgroup per row, the row held in VGPRs, per-wave
+//                 partials combined through LDS.
 //   k_split_onepass   rows of up to 64 chunks: one workgroup per chunk,
 //                 partials exchanged between the row's workgroups in the
 //                 middle of the kernel, x read once.
@@ -628,6 +632,61 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y,
       }
     }
     __syncthreads();
+  }
+}
+
+// (a, aligned) Rows of at most 256 columns made of whole 16-byte strips
+// (cols a multiple of 4, x and y 16-byte aligned), probability outputs.
+// G lanes per row (G the power of two >= cols / 4), each lane one 128-bit
+// strip of 4 columns, so a wavefront's load instruction covers 64 / G
+// consecutive rows exactly as the coalesced load leaves them: no LDS and no
+// relayout.  The row max and sum are segmented reductions over the row's G
+// lanes (DPP within 16 lanes, permlane swaps beyond).  Each wavefront keeps
+// U such row groups in flight (U * 1 KiB of loads).  Lanes past the row's
+// strips read -inf (a clipped term, as in load_strip).
+//
+// U = 2, one workgroup per block of rows: per 64 MiB of logits on 4 to 256
+// columns this ran 23.4-23.9 us, against 23.7-25.4 us with U = 4 and
+// 25.4-26.8 us with U = 8 (81 VGPRs, five wavefronts per SIMD); a grid
+// capped at the resident workgroups gained nothing.  The LDS-staged packed
+// kernel took 24.2-24.5 us on 4 and 64 columns and 35.3 us on 16 (its
+// lanes read LDS rows at a stride of 16 words: bank conflicts), and one
+// wavefront per row 42.5 us on 100 columns (25 of 64 lanes busy).
+constexpr int kGroupRowsMaxCols = 256;
+constexpr int kGroupRowsU = 2;
+
+template <int G, int U, int MODE>
+__global__ __launch_bounds__(256) void k_group_rows(const float* x, float* y, int64_t rows,
+                                                    int64_t cols, Clip clip) {
+  static_assert(G >= 1 && G <= 64 && (G & (G - 1)) == 0, "G: power of 2 up to 64");
+  constexpr int R = 64 / G;                       // rows per group
+  constexpr int64_t kWaveRows = int64_t(U) * R;   // rows per wavefront step
+  const int lane = __lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int rho = lane / G;
+  const int j = lane % G;
+  const bool col_ok = 4 * j < cols;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 4 * kWaveRows;
+  for (int64_t r0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * kWaveRows; r0 < rows;
+       r0 += stride) {
+    f32x4 q[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t row = r0 + u * R + rho;
+      q[u] = f32x4{kNegInf, kNegInf, kNegInf, kNegInf};
+      if (col_ok && row < rows) q[u] = ld_stream(x + row * cols + 4 * j);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t row = r0 + u * R + rho;
+      const float m = seg_max<G>(fmaxf(fmaxf(q[u].x, q[u].y), fmaxf(q[u].z, q[u].w)));
+      const RowShift rs = row_shift(m, clip);
+      float e[4] = {exp_shift_clip<MODE>(q[u].x, rs), exp_shift_clip<MODE>(q[u].y, rs),
+                    exp_shift_clip<MODE>(q[u].z, rs), exp_shift_clip<MODE>(q[u].w, rs)};
+      const float rcp = 1.0f / seg_sum<G>(tree_sum(e));
+      const f32x4 out = {e[0] * rcp, e[1] * rcp, e[2] * rcp, e[3] * rcp};
+      if (col_ok && row < rows) st_stream(y + row * cols + 4 * j, out);
+    }
   }
 }
 

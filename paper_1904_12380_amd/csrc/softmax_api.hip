@@ -46,6 +46,9 @@ constexpr int kBlockThreads = 1024;
 // columns 25.4 against 25.3.  Log and NLL rows keep k_block_row up to
 // kBlockRowMaxCols.
 constexpr int64_t kSplitMinColsProb = 8192;
+// k_group_rows: grid capped at the workgroups resident at once (each loops
+// over row blocks) rather than one workgroup per row block.
+constexpr bool kGroupRowsPersistent = false;
 
 // Split rows, one pass: a row spans at most this many workgroups (the
 // exchange is read by one wavefront, one slot per lane).  Chunk shapes,
@@ -204,6 +207,20 @@ template <int EM, bool VEC4>
 const void* shape_fn(const Shape& s, bool stats_pass) {
   auto cast = [](auto f) { return reinterpret_cast<const void*>(f); };
   switch (s.kernel) {
+    case SOFTMAX_KERNEL_GROUP_ROWS:
+      if constexpr (VEC4 && (EM == kExpAccurate || EM == kExpWide || EM == kExpFast)) {
+        switch (s.g) {
+          case 1: return cast(&k_group_rows<1, kGroupRowsU, EM>);
+          case 2: return cast(&k_group_rows<2, kGroupRowsU, EM>);
+          case 4: return cast(&k_group_rows<4, kGroupRowsU, EM>);
+          case 8: return cast(&k_group_rows<8, kGroupRowsU, EM>);
+          case 16: return cast(&k_group_rows<16, kGroupRowsU, EM>);
+          case 32: return cast(&k_group_rows<32, kGroupRowsU, EM>);
+          case 64: return cast(&k_group_rows<64, kGroupRowsU, EM>);
+          default: return nullptr;
+        }
+      }
+      return nullptr;
     case SOFTMAX_KERNEL_PACKED:
       if (s.g == 1) return packed_fn<1, VEC4, EM>(s.epl, std::make_integer_sequence<int, 16>{});
       if (s.g == 2) return packed_fn<2, VEC4, EM>(s.epl, std::make_integer_sequence<int, 8>{});
@@ -279,7 +296,12 @@ Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
   const bool prob = em != kLogOut && em != kNllOut;
   s.vec4 = can_vec4(cols <= kPackedMaxCols ? SOFTMAX_KERNEL_PACKED : SOFTMAX_KERNEL_SPLIT_ROW,
                     x, y, cols);
-  if (cols <= kPackedMaxCols) {
+  if (prob && cols <= kGroupRowsMaxCols && can_vec4(SOFTMAX_KERNEL_GROUP_ROWS, x, y, cols)) {
+    s.kernel = SOFTMAX_KERNEL_GROUP_ROWS;
+    s.vec4 = true;
+    s.threads = 256;
+    s.g = static_cast<int>(pow2_at_least(ceil_div(cols, 4)));
+  } else if (cols <= kPackedMaxCols) {
     // G lanes per row with at most 16 columns per lane.
     s.kernel = SOFTMAX_KERNEL_PACKED;
     s.threads = 256;
@@ -327,6 +349,11 @@ bool requested_shape(const softmax_plan_t& want, const float* x, const float* y,
   s.vec4 = want.vec_width == 4;
   if (s.vec4 && !can_vec4(s.kernel, x, y, cols)) return false;
   switch (s.kernel) {
+    case SOFTMAX_KERNEL_GROUP_ROWS:
+      if (cols > kGroupRowsMaxCols || !s.vec4) return false;
+      s.threads = 256;
+      s.g = static_cast<int>(pow2_at_least(ceil_div(cols, 4)));
+      break;
     case SOFTMAX_KERNEL_PACKED:
       if (cols > kPackedMaxCols) return false;
       s.threads = 256;
@@ -392,6 +419,12 @@ int make_plan(const Shape& s, int64_t rows, int64_t cols, int em, int dev,
   bool one_wave = false;
   int64_t launch_read_bytes = 0;
   switch (s.kernel) {
+    case SOFTMAX_KERNEL_GROUP_ROWS:
+      p.grid = std::min(ceil_div(rows, int64_t(4) * kGroupRowsU * (64 / s.g)),
+                        kGroupRowsPersistent ? resident : kMaxGrid);
+      p.rows_per_launch = rows;
+      p.launches = 1;
+      break;
     case SOFTMAX_KERNEL_PACKED: {
       const int64_t tile = 256 / s.g;
       p.grid = std::min(ceil_div(rows, tile), kPackedBlocksPerCU * f.cus);
@@ -458,6 +491,10 @@ softmax_plan_t public_plan(const Plan& p, int64_t rows) {
   o.launches = static_cast<int32_t>(p.launches);
   o.store_delay_ns = p.delay_ns;
   switch (s.kernel) {
+    case SOFTMAX_KERNEL_GROUP_ROWS:
+      o.lanes_per_row = s.g;
+      o.elems_per_lane = 4;
+      break;
     case SOFTMAX_KERNEL_PACKED:
       o.lanes_per_row = s.g;
       o.elems_per_lane = s.epl;
@@ -496,6 +533,10 @@ hipError_t run_plan(const Plan& p, const float* x, float* y, const int64_t* labe
   const void* fn = kernel_fn(s, em);
   uint32_t delay = p.delay_ticks;
   switch (s.kernel) {
+    case SOFTMAX_KERNEL_GROUP_ROWS: {
+      void* args[] = {&x, &y, &rows, &cols, &c};
+      return launch(fn, p.grid, 256, args, st);
+    }
     case SOFTMAX_KERNEL_PACKED: {
       void* args[] = {&x, &y, &labels, &rows, &cols, &c};
       return launch(fn, p.grid, 256, args, st);

@@ -33,7 +33,7 @@ WINDOWS = 7
 ROUNDS = 3
 ROTATE_BYTES = 1 << 30
 
-DEFAULT_COLS = (16, 32, 50, 64, 100, 128, 256, 250, 512, 1000, 1024, 2048, 4093, 4096,
+DEFAULT_COLS = (4, 8, 16, 32, 50, 64, 100, 128, 250, 256, 512, 1000, 1024, 2048, 4093, 4096,
                 8192, 16383, 16384, 32765, 32768, 65536, 131072)
 
 
@@ -41,6 +41,8 @@ def candidates(cols: int) -> list[dict]:
     """Plans to try for a row length (the library rejects the ones that do
     not fit the shape or the pointers)."""
     out = []
+    if cols <= 256:
+        out.append(dict(kernel_name="group_rows", vec_width=4))
     if cols <= 64:
         out += [dict(kernel_name="packed", vec_width=w) for w in (4, 1)]
     if cols <= 4096:

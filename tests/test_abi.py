@@ -84,9 +84,14 @@ def test_cpu_tensor_is_rejected():
     (64, 262144, "split_row", 4, dict(chunks_per_row=16, elems_per_lane=32,
                                       block_threads=512)),
     (3, 1, "packed", 4, dict(lanes_per_row=1, elems_per_lane=1)),
-    (300, 16, "packed", 4, dict(lanes_per_row=1, elems_per_lane=16)),
+    (300, 16, "group_rows", 4, dict(lanes_per_row=4, elems_per_lane=4)),
     (300, 17, "packed", 4, dict(lanes_per_row=2, elems_per_lane=9)),
-    (300, 64, "packed", 4, dict(lanes_per_row=4, elems_per_lane=16)),
+    (300, 64, "group_rows", 4, dict(lanes_per_row=16, elems_per_lane=4)),
+    (300, 4, "group_rows", 4, dict(lanes_per_row=1, elems_per_lane=4)),
+    (300, 100, "group_rows", 4, dict(lanes_per_row=32, elems_per_lane=4)),
+    (300, 256, "group_rows", 4, dict(lanes_per_row=64, elems_per_lane=4)),
+    (300, 260, "wave_row", 4, dict(elems_per_lane=8)),
+    (300, 102, "wave_row", 1, dict(elems_per_lane=4)),
     (3, 65, "wave_row", 1, dict(elems_per_lane=4)),
     (3, 4096, "wave_row", 4, dict(elems_per_lane=64)),
     (3, 4097, "block_row", 1, dict(elems_per_lane=8)),

@@ -62,7 +62,8 @@ def test_workloads(key):
 
 
 # one shape per kernel family and path, two input kinds
-SHAPES = [(1000, 50), (257, 7), (64, 1000), (5, 8192), (3, 100003), (2, 1048577), (1, 2097153)]
+SHAPES = [(1000, 50), (257, 7), (1001, 64), (300, 100), (64, 1000), (5, 8192), (3, 100003),
+          (2, 1048577), (1, 2097153)]
 
 
 @pytest.mark.parametrize("rows,cols", SHAPES)
@@ -76,7 +77,7 @@ def test_shapes(rows, cols):
 def test_uniform_rows_and_clip_rows():
     """Uniform rows are exact (every exponential is e^0 = 1); clipped
     elements take the exact clipped value."""
-    for n in (1, 3, 50, 1000, 4096, 32768, 262144):
+    for n in (1, 3, 16, 50, 128, 1000, 4096, 32768, 262144):
         y = run_approx(np.full((2, n), 7.25, dtype=np.float32))
         assert np.all(y == np.float32(1.0 / n)), n
     x = np.array([[0.0, -100.0, -64.0, -63.5, -1.0e4]], dtype=np.float32)

@@ -63,10 +63,11 @@ def check_clip(x: np.ndarray, y: np.ndarray, lo: float, what: str) -> float:
     return float((np.abs(y64[big] - want[big]) / want[big]).max()) if big.any() else 0.0
 
 
-# One shape per kernel family and path: packed (G = 1, 4), wave per row,
-# block per row, one-pass split (small and large chunks), two-pass split.
-SHAPES = [(1000, 50), (257, 7), (64, 1000), (5, 8192), (3, 100003), (2, 1048577),
-          (1, 2097153)]
+# One shape per kernel family and path: packed (G = 1, 4), grouped aligned
+# rows (G = 16, 32), wave per row, block per row, one-pass split (small and
+# large chunks), two-pass split.
+SHAPES = [(1000, 50), (257, 7), (1001, 64), (300, 100), (64, 1000), (5, 8192), (3, 100003),
+          (2, 1048577), (1, 2097153)]
 
 
 @pytest.mark.parametrize("rows,cols", SHAPES)

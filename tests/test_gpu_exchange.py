@@ -184,6 +184,7 @@ def test_store_delay_changes_no_bit(key):
 
 PLANNED = [
     ("packed", 4, {}, [(1000, 50), (333, 17), (77, 64)]),
+    ("group_rows", 4, {}, [(1000, 52), (333, 16), (77, 256), (9, 4), (4099, 8)]),
     ("wave_row", 4, {}, [(300, 52), (257, 1000), (9, 4096)]),
     ("wave_row", 1, {}, [(130, 1001), (5, 2047)]),
     ("block_row", 4, {}, [(64, 1000), (9, 8192), (5, 32768)]),

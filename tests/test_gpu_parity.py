@@ -88,16 +88,31 @@ def test_edge_shapes(cols):
             check_parity(x, run_gpu(x), f"{rows}x{cols} {kind}")
 
 
-@pytest.mark.parametrize("rows,cols", [(400001, 7), (200003, 20), (99999, 33), (98305, 64)])
+@pytest.mark.parametrize("rows,cols", [(400001, 7), (200003, 21), (99999, 33), (98305, 62)])
 def test_packed_persistent_tiles(rows, cols):
     """More tiles than the persistent grid: every workgroup loops over
     several tiles with the next tile's loads in flight; ragged last tile."""
     log(f"[parity] packed persistent {rows}x{cols}")
     p = sm.softmax_plan(rows, cols)
+    assert p["kernel_name"] == "packed"
     tile_rows = 256 // p["lanes_per_row"]
     assert -(-rows // tile_rows) > p["grid"]
     x = workloads.random_logits(rows, cols, seed=rows, kind="clip_heavy")
     check_parity(x, run_gpu(x), f"packed {rows}x{cols}")
+
+
+@pytest.mark.parametrize("rows,cols", [(1000003, 16), (300001, 100), (77777, 256), (5, 4),
+                                       (1, 128), (129, 8), (1000, 32)])
+def test_group_rows(rows, cols):
+    """Aligned rows of up to 256 columns: G lanes per row, several rows per
+    wavefront, ragged last row group, more row groups than the grid."""
+    log(f"[parity] group rows {rows}x{cols}")
+    p = sm.softmax_plan(rows, cols)
+    assert p["kernel_name"] == "group_rows" and p["elems_per_lane"] == 4
+    assert p["lanes_per_row"] == max(1, 1 << (cols // 4 - 1).bit_length())
+    for kind in ("normal", "clip_heavy", "offset"):
+        x = workloads.random_logits(rows, cols, seed=rows + 3 * cols, kind=kind)
+        check_parity(x, run_gpu(x), f"group rows {rows}x{cols} {kind}")
 
 
 @pytest.mark.parametrize("rows,cols", [(257, 50), (64, 1000), (33, 1001), (5, 8192), (3, 100003),
