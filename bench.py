@@ -199,6 +199,12 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         x, y = rot.pair(i)
         sm.softmax_copy_probe(x, out=y, stream=s)
 
+    def cpy_inplace(i, s):
+        # the copy kernel with y == x: the same read-then-write of each line
+        # as an in-place softmax, with no arithmetic
+        _, y = rot.pair(i)
+        sm.softmax_copy_probe(y, out=y, stream=s)
+
     def d2d(i, s):
         x, y = rot.pair(i)
         y.copy_(x)          # hipMemcpyAsync device to device
@@ -235,6 +241,7 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
     ms, eager_ms = time_steps(torch, fwd, steps, warmup)
     inplace_ms, _ = time_steps(torch, fwd_inplace, steps, warmup)
     copy_ms, _ = time_steps(torch, cpy, steps, warmup)
+    copy_inplace_ms, _ = time_steps(torch, cpy_inplace, steps, warmup)
     memcpy_ms = time_steps(torch, d2d, steps, warmup)[0] if memcpy else None
     floor_ms = time_steps(torch, tiny, steps, warmup)[0] if memcpy else None
     noclip_ms, _ = time_steps(torch, fwd_noclip, steps, warmup)
@@ -275,6 +282,7 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
         "in_place_hbm_gbps": w.algorithmic_bytes / (inplace_ms * 1e-3) / 1e9,
         "copy_ms_per_step": copy_ms,
         "copy_gbps": w.algorithmic_bytes / (copy_ms * 1e-3) / 1e9,
+        "copy_in_place_ms_per_step": copy_inplace_ms,
         "softmax_over_copy_time": ms / copy_ms,
         "memcpy_ms_per_step": memcpy_ms,
         "launch_floor_ms_per_step": floor_ms,
@@ -397,8 +405,8 @@ def time_cpu_fp32(x: np.ndarray, budget_s: float) -> dict | None:
             "gbps": 8 * x.size / per / 1e9}
 
 
-def pmc_summary_path(key: str, ext: str) -> str:
-    return os.path.join(PROFILES, f"pmc_{key}.{ext}")
+def pmc_summary_path(key: str, ext: str, tag: str = "") -> str:
+    return os.path.join(PROFILES, f"pmc_{key}{'_' + tag if tag else ''}.{ext}")
 
 
 def load_traffic(key: str) -> tuple[float | None, str | None]:
@@ -444,13 +452,24 @@ def pmc_run_attention(sm, torch, wc: AttentionCounters, launches: int) -> None:
     print(json.dumps({"pmc_run": wc.key, "launches": launches}), flush=True)
 
 
-def pmc_run(sm, torch, w: workloads.Workload, launches: int) -> None:
+def pmc_run(sm, torch, w: workloads.Workload, launches: int, in_place: bool = False) -> None:
     """Launches for a counter pass: `launches` softmax calls on the rotation,
-    then as many copy-kernel calls over the same bytes."""
+    then as many copy-kernel calls over the same bytes.  With in_place, the
+    softmax calls run with y == x on the rotation's y buffers, which first
+    receive a copy of x (copy-kernel calls over the same bytes, so the copy
+    kernel's per-dispatch counters are unchanged)."""
     rot = Rotation(torch, workloads.generate(w.key))
+    if in_place:
+        for i in range(rot.n):
+            x, y = rot.pair(i)
+            sm.softmax_copy_probe(x, out=y)
+        torch.cuda.synchronize()
     for i in range(launches):
         x, y = rot.pair(i)
-        sm.softmax_fwd(x, out=y)
+        if in_place:
+            sm.softmax_fwd(y, out=y)
+        else:
+            sm.softmax_fwd(x, out=y)
     torch.cuda.synchronize()
     for i in range(launches):
         x, y = rot.pair(i)
@@ -483,12 +502,13 @@ def _counter_rows(directory: str):
             con.close()
 
 
-def summarize_pmc(directory: str, w: workloads.Workload, command: str) -> dict:
+def summarize_pmc(directory: str, w: workloads.Workload, command: str, tag: str = "") -> dict:
     """Average FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the softmax
     kernel and of the copy kernel, scaled by the copy kernel's reading for
     its known byte count (4 * elements read, 4 * elements written)."""
     per = {}
-    subs = ["fetch", "write"] + (["occ"] if os.path.isdir(os.path.join(directory, "occ")) else [])
+    subs = ["fetch", "write"] + [d for d in ("occ", "sq")
+                                 if os.path.isdir(os.path.join(directory, d))]
     for sub in subs:
         for name, cname, val in _counter_rows(os.path.join(directory, sub)):
             key = "copy" if "k_copy" in name else ("softmax" if "smx::k_" in name else None)
@@ -521,18 +541,26 @@ def summarize_pmc(directory: str, w: workloads.Workload, command: str) -> dict:
         "algorithmic_bytes_per_launch": float(w.algorithmic_bytes),
         "traffic_over_algorithmic": (fetch_b + write_b) / w.algorithmic_bytes,
         "command": command,
+        "tag": tag,
     }
+    if "sq" in subs:
+        names = sorted({c for k in ("softmax", "copy") for c in agg[k]
+                        if c.startswith(("SQ_", "GRBM_", "TCC_", "TCP_", "TA_", "TD_"))
+                        and c not in ("FETCH_SIZE", "WRITE_SIZE")})
+        doc["sq_counters_median_per_dispatch"] = {
+            k: {c: agg[k].get(c) for c in names} for k in ("softmax", "copy")}
     if "occ" in subs:
         for key in ("softmax", "copy"):
             doc[f"{key}_occupancy_percent"] = agg[key].get("OccupancyPercent")
             doc[f"{key}_sq_waves_per_dispatch"] = agg[key].get("SQ_WAVES")
             doc[f"{key}_grbm_gui_active_cycles"] = agg[key].get("GRBM_GUI_ACTIVE")
     os.makedirs(PROFILES, exist_ok=True)
-    with open(pmc_summary_path(w.key, "json"), "w") as f:
+    with open(pmc_summary_path(w.key, "json", tag), "w") as f:
         json.dump(doc, f, indent=1)
         f.write("\n")
-    with open(pmc_summary_path(w.key, "md"), "w") as f:
-        f.write(f"# HBM traffic counters: {', '.join(doc['softmax_kernels'])} on {w.key}\n\n")
+    with open(pmc_summary_path(w.key, "md", tag), "w") as f:
+        f.write(f"# HBM traffic counters: {', '.join(doc['softmax_kernels'])} on {w.key}"
+                f"{' (' + tag.replace('_', ' ') + ')' if tag else ''}\n\n")
         f.write("Commands (from the repository root on the GPU machine):\n\n```\n"
                 f"{command}\n```\n\n")
         f.write("| quantity | softmax kernel | copy kernel (same bytes) |\n|---|---|---|\n")
@@ -557,6 +585,15 @@ def summarize_pmc(directory: str, w: workloads.Workload, command: str) -> dict:
                              ("GRBM_GUI_ACTIVE cycles", "grbm_gui_active_cycles")):
                 a, b = doc[f"softmax_{k}"], doc[f"copy_{k}"]
                 f.write(f"| {label} | {a if a is None else round(a, 1)} | "
+                        f"{b if b is None else round(b, 1)} |\n")
+        if "sq_counters_median_per_dispatch" in doc:
+            sq = doc["sq_counters_median_per_dispatch"]
+            f.write("\nSQ / GRBM pass (median per dispatch; cycle counters are summed "
+                    "over the XCDs' sequencers as the profiler reports them):\n\n"
+                    "| counter | softmax kernel | copy kernel |\n|---|---|---|\n")
+            for c in sq["softmax"]:
+                a, b = sq["softmax"][c], sq["copy"][c]
+                f.write(f"| {c} | {a if a is None else round(a, 1)} | "
                         f"{b if b is None else round(b, 1)} |\n")
             f.write("\n")
         f.write(f"Kernel sources sha256: {doc['source_sha256']}\n")
@@ -718,6 +755,10 @@ def main() -> int:
     ap.add_argument("--pmc-run", action="store_true",
                     help="only launch the kernels for a rocprofv3 counter pass")
     ap.add_argument("--pmc-launches", type=int, default=20)
+    ap.add_argument("--pmc-in-place", action="store_true",
+                    help="counter pass with y == x (softmax workloads)")
+    ap.add_argument("--pmc-tag", default="",
+                    help="suffix of the summary's file name (--summarize-pmc)")
     ap.add_argument("--summarize-pmc", metavar="DIR",
                     help="write profiles/pmc_<workload>.{json,md} from DIR/fetch and DIR/write")
     ap.add_argument("--pmc-command", default="", help="commands recorded in the summary")
@@ -738,7 +779,7 @@ def main() -> int:
         print(summarize_trace(args.summarize_trace, args.pmc_command, args.trace_json))
         return 0
     if args.summarize_pmc:
-        doc = summarize_pmc(args.summarize_pmc, w, args.pmc_command)
+        doc = summarize_pmc(args.summarize_pmc, w, args.pmc_command, args.pmc_tag)
         print(json.dumps(doc), flush=True)
         return 0
 
@@ -760,7 +801,7 @@ def main() -> int:
         if isinstance(w, AttentionCounters):
             pmc_run_attention(sm, torch, w, args.pmc_launches)
         else:
-            pmc_run(sm, torch, w, args.pmc_launches)
+            pmc_run(sm, torch, w, args.pmc_launches, in_place=args.pmc_in_place)
         return 0
 
     machine_before = machine_state()

@@ -13,7 +13,11 @@
  *
  * Accuracy: every output is within 4e-6 relative of the exact value of the
  * formula above (derivation: the exp argument is carried in extended
- * precision, v_exp_f32 is within 1 ulp, the row sum is a fixed-depth tree).
+ * precision, the row sum is a fixed-depth tree).  Measured by a dense scan
+ * on MI355X against float64: v_exp_f32 (2^t) is within 0.783 ulp over every
+ * fp32 t in [-126, 0], and the library's clipped exponential within
+ * 1.269 ulp over every fp32 x - M in [-64, 0] (stated bound 1.5 ulp; the
+ * scan is tests/test_gpu_exp_scan.py).
  * Outputs are bitwise deterministic for a given input, shape and alignment.
  *
  * Non-finite inputs: a NaN or +inf anywhere in a row, or a row of all -inf,
@@ -366,7 +370,9 @@ SOFTMAX_API int softmax_exp_probe(const float* x, const float* m, float* e, int6
  * softmax_copy_probe -- diagnostic: y[i] = x[i] for 0 <= i < n with 128-bit
  * accesses when both are 16-byte aligned.  The memory-bound ceiling for the
  * same bytes softmax moves (the paper's memcpy comparison, Sec. 2.6).
- * x and y are caller-owned device arrays that must not overlap.
+ * x and y are caller-owned device arrays; y == x (each element read, then
+ * written back, by the same thread: the traffic of an in-place softmax
+ * with no arithmetic) is allowed, any other overlap is rejected.
  */
 SOFTMAX_API int softmax_copy_probe(const float* x, float* y, int64_t n, hipStream_t stream);
 

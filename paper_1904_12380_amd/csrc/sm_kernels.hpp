@@ -271,6 +271,62 @@ __device__ __forceinline__ void load_strip_whole(float (&v)[4 * V], const float*
   }
 }
 
+// 128-bit access to a row segment p[0, lim) that starts `a` floats (0..3)
+// past a 16-byte boundary: rows whose length is not a multiple of 4 in a
+// 16-byte aligned matrix.  Lane strip j is the aligned float4 at
+// p - a + 4 * (lane_off + stride * j), holding segment columns c0 .. c0 + 3
+// with c0 = 4 * (lane_off + stride * j) - a; element 4 j + k of v is column
+// c0 + k.  A strip wholly inside [0, lim) is one 128-bit access.  A strip
+// that straddles either end of the segment touches only its columns inside
+// it, with 32-bit accesses, so nothing of a neighbouring row is read or
+// written (in-place calls stay safe); columns outside read as -inf.  The
+// strips must cover lim + a columns.
+template <int V>
+__device__ __forceinline__ void load_strip_ph(float (&v)[4 * V], const float* p, int a,
+                                              int lane_off, int stride, int lim) {
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int c0 = 4 * (lane_off + stride * j) - a;
+    if (c0 >= 0 && c0 + 4 <= lim) {
+      const f32x4 q = ld_stream(p + c0);
+      v[4 * j + 0] = q.x;
+      v[4 * j + 1] = q.y;
+      v[4 * j + 2] = q.z;
+      v[4 * j + 3] = q.w;
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int c = c0 + k;
+        v[4 * j + k] = (c >= 0 && c < lim) ? __builtin_nontemporal_load(p + c) : kNegInf;
+      }
+    }
+  }
+}
+
+// Stores out(v[i]) for the columns of the segment, strips as load_strip_ph.
+template <int V, typename F>
+__device__ __forceinline__ void store_strip_ph(const float (&v)[4 * V], F out, float* p, int a,
+                                               int lane_off, int stride, int lim) {
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int c0 = 4 * (lane_off + stride * j) - a;
+    if (c0 >= 0 && c0 + 4 <= lim) {
+      f32x4 q;
+      q.x = out(v[4 * j + 0]);
+      q.y = out(v[4 * j + 1]);
+      q.z = out(v[4 * j + 2]);
+      q.w = out(v[4 * j + 3]);
+      st_stream(p + c0, q);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int c = c0 + k;
+        if (c >= 0 && c < lim) __builtin_nontemporal_store(out(v[4 * j + k]), p + c);
+      }
+    }
+  }
+}
+
 // Sub-strip length of the online reduction of the probability modes.
 constexpr int kOnlineSub = 8;
 // Whether a lane's N values take that reduction (two sub-strips at least).
@@ -708,11 +764,16 @@ constexpr int kRowWaves = (V <= 8 && VEC4 && !keeps_logits<MODE>()) ? 4 : 2;
 // that long after the workgroup started, so that the launch's reads are
 // over before its writes begin (HBM then serves them in two phases rather
 // than interleaved).
-template <int V, bool VEC4, int MODE>
+//
+// PH (probability outputs, 128-bit access): rows of a length that is not a
+// multiple of 4 in 16-byte aligned x and y, each row accessed in the aligned
+// strips around it (load_strip_ph); the row's phase is (row * cols) mod 4.
+template <int V, bool VEC4, int MODE, bool PH = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     kRowWaves<V, VEC4, MODE>))) void k_wave_row(
     const float* x, float* y, const int64_t* labels, int64_t rows, int64_t cols, Clip clip,
     uint32_t delay) {
+  static_assert(!PH || (VEC4 && !keeps_logits<MODE>()), "phase access: probability outputs");
   const uint64_t t0 = wall_clock();
   const int lane = __lane_id();
   const int wave = threadIdx.x >> 6;
@@ -722,6 +783,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     const int64_t label = row_label<MODE>(labels, row);
     const int lim = static_cast<int>(cols);
     float v[4 * V];
+    if constexpr (PH) {
+      const int a = static_cast<int>((row * cols) & 3);
+      load_strip_ph<V>(v, xr, a, opaque(lane), 64, lim);
+      const RowShift rs = row_shift(seg_max<64>(array_max(v)), clip);
+      const float s = seg_sum<64>(exp_strip<MODE>(v, rs));
+      if (delay != 0) wait_until_after(t0 + delay, s);
+      const float rcp = 1.0f / s;
+      store_strip_ph<V>(v, [&](float ev) { return ev * rcp; }, y + row * cols, a, opaque(lane),
+                        64, lim);
+      continue;
+    }
     load_strip<V, VEC4>(v, xr, opaque(lane), 64, lim);
     const LabelPick pick = pick_label<V, VEC4, MODE>(v, label, cols, 0, lim, lane, 64, lane == 0);
     const RowShift rs = row_shift(seg_max<64>(array_max(v)), clip);
@@ -732,12 +804,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
 }
 
 // ---------------------------------------------------------------------------
-// (c) One workgroup of NT threads per row, cols <= 4*V*NT.  `delay` as for
-// k_wave_row.
-template <int NT, int V, bool VEC4, int MODE>
+// (c) One workgroup of NT threads per row, cols <= 4*V*NT.  `delay` and PH
+// as for k_wave_row.
+template <int NT, int V, bool VEC4, int MODE, bool PH = false>
 __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y,
                                                   const int64_t* labels, int64_t rows,
                                                   int64_t cols, Clip clip, uint32_t delay) {
+  static_assert(!PH || (VEC4 && !keeps_logits<MODE>()), "phase access: probability outputs");
   const uint64_t t0 = wall_clock();
   constexpr int NW = NT / 64;
   __shared__ float red_max[NW];
@@ -748,7 +821,16 @@ __global__ __launch_bounds__(NT) void k_block_row(const float* x, float* y,
     const int64_t label = row_label<MODE>(labels, row);
     const int lim = static_cast<int>(cols);
     float v[4 * V];
-    if constexpr (MODE == kNllOut && VEC4) {
+    if constexpr (PH) {
+      const int a = static_cast<int>((row * cols) & 3);
+      load_strip_ph<V>(v, xr, a, opaque(tid), NT, lim);
+      const RowShift rs = row_shift(block_max<NW>(array_max(v), red_max), clip);
+      const float s = block_sum<NW>(exp_strip<MODE>(v, rs), red_sum);
+      if (delay != 0) wait_until_after(t0 + delay, s);
+      const float rcp = 1.0f / s;
+      store_strip_ph<V>(v, [&](float ev) { return ev * rcp; }, y + row * cols, a, opaque(tid),
+                        NT, lim);
+    } else if constexpr (MODE == kNllOut && VEC4) {
       // The loss needs only the row's (max, sum) and one logit.  The sums
       // are folded in as the loads land, and thread 0 reads the label's
       // logit itself (one more cache line per row), so no value has to stay

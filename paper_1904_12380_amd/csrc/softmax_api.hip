@@ -28,6 +28,12 @@ using namespace smx_host;
 
 // Bucket limits on cols.
 constexpr int64_t kPackedMaxCols = 64;
+// Probability rows of up to this many columns that are not whole 16-byte
+// strips (or whose x or y is not 16-byte aligned) also take the packed
+// kernel, with 8 or 16 lanes per row: per 64 MiB of logits, 65 columns
+// took 64 us with one wavefront per row and 32-bit access (65 of 256
+// register slots of a wavefront in use).
+constexpr int64_t kPackedProbMaxCols = 256;
 // The packed kernel's persistent grid: six 256-thread workgroups per CU.
 // Measured on 115200 x 50: up to six per CU the prefetched next tile
 // overlaps the current tile's compute; seven or more per CU, or one tile per
@@ -191,10 +197,12 @@ struct Shape {
   int g = 0;        // packed rows: lanes per row
   int epl = 0;      // packed rows: columns per lane
   bool two_pass = false;
+  bool ph = false;  // 128-bit access to rows that are not 16-byte aligned (row phase)
 };
 
-// k_packed instances: G = 1 with EPL = 1..16, G = 2 and G = 4 with
-// EPL = 9..16 (a plan never asks for fewer columns per lane at G > 1).
+// k_packed instances: G = 1 with EPL = 1..16, G = 2, 4, 8 and 16 with
+// EPL = 9..16 (a plan never asks for fewer columns per lane at G > 1); G = 8
+// and 16 (rows of 65 to 256 columns) for probability outputs only.
 template <int G, bool VEC4, int EM, int... E>
 const void* packed_fn(int epl, std::integer_sequence<int, E...>) {
   static const void* const table[] = {
@@ -225,8 +233,26 @@ const void* shape_fn(const Shape& s, bool stats_pass) {
       if (s.g == 1) return packed_fn<1, VEC4, EM>(s.epl, std::make_integer_sequence<int, 16>{});
       if (s.g == 2) return packed_fn<2, VEC4, EM>(s.epl, std::make_integer_sequence<int, 8>{});
       if (s.g == 4) return packed_fn<4, VEC4, EM>(s.epl, std::make_integer_sequence<int, 8>{});
+      if constexpr (EM == kExpAccurate || EM == kExpWide || EM == kExpFast) {
+        if (s.g == 8) return packed_fn<8, VEC4, EM>(s.epl, std::make_integer_sequence<int, 8>{});
+        if (s.g == 16)
+          return packed_fn<16, VEC4, EM>(s.epl, std::make_integer_sequence<int, 8>{});
+      }
       return nullptr;
     case SOFTMAX_KERNEL_WAVE_ROW:
+      if (s.ph) {
+        if constexpr (VEC4 && (EM == kExpAccurate || EM == kExpWide || EM == kExpFast)) {
+          switch (s.v) {
+            case 1: return cast(&k_wave_row<1, true, EM, true>);
+            case 2: return cast(&k_wave_row<2, true, EM, true>);
+            case 4: return cast(&k_wave_row<4, true, EM, true>);
+            case 8: return cast(&k_wave_row<8, true, EM, true>);
+            case 16: return cast(&k_wave_row<16, true, EM, true>);
+            default: return nullptr;
+          }
+        }
+        return nullptr;
+      }
       switch (s.v) {
         case 1: return cast(&k_wave_row<1, VEC4, EM>);
         case 2: return cast(&k_wave_row<2, VEC4, EM>);
@@ -238,6 +264,16 @@ const void* shape_fn(const Shape& s, bool stats_pass) {
         default: return nullptr;
       }
     case SOFTMAX_KERNEL_BLOCK_ROW:
+      if (s.ph) {
+        if constexpr (VEC4 && (EM == kExpAccurate || EM == kExpWide || EM == kExpFast)) {
+          switch (s.v) {
+            case 2: return cast(&k_block_row<kBlockThreads, 2, true, EM, true>);
+            case 4: return cast(&k_block_row<kBlockThreads, 4, true, EM, true>);
+            default: return nullptr;
+          }
+        }
+        return nullptr;
+      }
       switch (s.v) {
         case 2: return cast(&k_block_row<kBlockThreads, 2, VEC4, EM>);
         case 4: return cast(&k_block_row<kBlockThreads, 4, VEC4, EM>);
@@ -282,12 +318,44 @@ const void* kernel_fn(const Shape& s, int em, bool stats_pass = false) {
 
 inline int64_t chunk_cols(const Shape& s) { return int64_t(4) * s.v * s.threads; }
 
+// Lanes per row of the packed kernel: at most 16 columns per lane.
+inline int packed_lanes(int64_t cols) {
+  return cols <= 16 ? 1 : cols <= 32 ? 2 : cols <= 64 ? 4 : cols <= 128 ? 8 : 16;
+}
+
 // Whether kernel family `kernel` may use 128-bit access: both pointers
 // 16-byte aligned and, except for packed rows (which move whole tiles of a
 // multiple of four rows), rows made of whole float4s.
 inline bool can_vec4(int kernel, const float* x, const float* y, int64_t cols) {
   const bool a16 = aligned16(x) && aligned16(y);
   return kernel == SOFTMAX_KERNEL_PACKED ? a16 : (a16 && cols % 4 == 0);
+}
+
+// Rows taken with 128-bit access in the aligned strips around each row
+// (k_wave_row / k_block_row with PH): cols not a multiple of 4, x and y
+// 16-byte aligned, and 2048 < cols <= 8189.  Measured per 64 MiB: 4093
+// columns 29.3 us against 37.7 us with 32-bit access, 8189 columns 28.1;
+// but 65, 250 and 2047 columns ran slower than with 32-bit access (84
+// against 64, 28.5 against 25.0, 31.9 against 28.6 us): the straddling
+// strips are element by element, and the strips must cover cols + 3.
+inline bool phase_rows(const float* x, const float* y, int64_t cols) {
+  return cols % 4 != 0 && cols > kWaveRowMaxColsScalar && cols + 3 <= kSplitMinColsProb &&
+         aligned16(x) && aligned16(y);
+}
+
+// Row kernel for rows accessed with their phase: the strips must cover
+// cols + 3 columns (a row may start up to 3 floats past a 16-byte boundary).
+void phase_row_shape(int64_t cols, Shape* s) {
+  const int64_t span = cols + 3;
+  if (span <= kWaveRowMaxCols) {
+    s->kernel = SOFTMAX_KERNEL_WAVE_ROW;
+    s->threads = 256;
+    s->v = static_cast<int>(pow2_at_least(ceil_div(span, 256)));
+  } else {
+    s->kernel = SOFTMAX_KERNEL_BLOCK_ROW;
+    s->threads = kBlockThreads;
+    s->v = static_cast<int>(std::max<int64_t>(2, pow2_at_least(ceil_div(span, 4096))));
+  }
 }
 
 // The library's shape for a call (mode em).
@@ -301,12 +369,19 @@ Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
     s.vec4 = true;
     s.threads = 256;
     s.g = static_cast<int>(pow2_at_least(ceil_div(cols, 4)));
-  } else if (cols <= kPackedMaxCols) {
+  } else if (cols <= (prob ? kPackedProbMaxCols : kPackedMaxCols)) {
     // G lanes per row with at most 16 columns per lane.
     s.kernel = SOFTMAX_KERNEL_PACKED;
+    s.vec4 = can_vec4(SOFTMAX_KERNEL_PACKED, x, y, cols);
     s.threads = 256;
-    s.g = cols <= 16 ? 1 : cols <= 32 ? 2 : 4;
+    s.g = packed_lanes(cols);
     s.epl = static_cast<int>(ceil_div(cols, s.g));
+  } else if (prob && phase_rows(x, y, cols)) {
+    // Rows that are not whole 16-byte strips, in aligned x and y: 128-bit
+    // access in the aligned strips around each row.
+    s.vec4 = true;
+    s.ph = true;
+    phase_row_shape(cols, &s);
   } else if (cols <= (s.vec4 ? kWaveRowMaxCols : kWaveRowMaxColsScalar)) {
     s.kernel = SOFTMAX_KERNEL_WAVE_ROW;
     s.threads = 256;
@@ -347,6 +422,23 @@ bool requested_shape(const softmax_plan_t& want, const float* x, const float* y,
   s.kernel = want.kernel;
   if (want.vec_width != 1 && want.vec_width != 4) return false;
   s.vec4 = want.vec_width == 4;
+  // 128-bit access to rows that are not whole 16-byte strips: the row
+  // kernels with the row phase (probability outputs, aligned x and y).
+  const bool row_kernel =
+      s.kernel == SOFTMAX_KERNEL_WAVE_ROW || s.kernel == SOFTMAX_KERNEL_BLOCK_ROW;
+  if (s.vec4 && row_kernel && phase_rows(x, y, cols) && em != kLogOut && em != kNllOut) {
+    const int64_t span = cols + 3;
+    if (span > (s.kernel == SOFTMAX_KERNEL_WAVE_ROW ? kWaveRowMaxCols : kSplitMinColsProb))
+      return false;
+    s.ph = true;
+    s.threads = s.kernel == SOFTMAX_KERNEL_WAVE_ROW ? 256 : kBlockThreads;
+    s.v = static_cast<int>(s.kernel == SOFTMAX_KERNEL_WAVE_ROW
+                               ? pow2_at_least(ceil_div(span, 256))
+                               : std::max<int64_t>(2, pow2_at_least(ceil_div(span, 4096))));
+    if (kernel_fn(s, em) == nullptr) return false;
+    *out = s;
+    return true;
+  }
   if (s.vec4 && !can_vec4(s.kernel, x, y, cols)) return false;
   switch (s.kernel) {
     case SOFTMAX_KERNEL_GROUP_ROWS:
@@ -355,9 +447,10 @@ bool requested_shape(const softmax_plan_t& want, const float* x, const float* y,
       s.g = static_cast<int>(pow2_at_least(ceil_div(cols, 4)));
       break;
     case SOFTMAX_KERNEL_PACKED:
-      if (cols > kPackedMaxCols) return false;
+      if (cols > ((em == kLogOut || em == kNllOut) ? kPackedMaxCols : kPackedProbMaxCols))
+        return false;
       s.threads = 256;
-      s.g = cols <= 16 ? 1 : cols <= 32 ? 2 : 4;
+      s.g = packed_lanes(cols);
       s.epl = static_cast<int>(ceil_div(cols, s.g));
       break;
     case SOFTMAX_KERNEL_WAVE_ROW:
@@ -812,12 +905,12 @@ SOFTMAX_API int softmax_copy_probe(const float* x, float* y, int64_t n, hipStrea
   if (n < 0 || n > INT64_MAX / 4) return SOFTMAX_ERR_INVALID_ARG;
   if (n == 0) return SOFTMAX_OK;
   if (x == nullptr || y == nullptr) return SOFTMAX_ERR_INVALID_ARG;
-  if (any_overlap(x, y, n * 4)) return SOFTMAX_ERR_INVALID_ARG;
+  if (partial_overlap(x, y, n * 4)) return SOFTMAX_ERR_INVALID_ARG;
   int dev = 0;
   hipError_t he = hipGetDevice(&dev);
   if (he != hipSuccess) return fail_hip(he);
   int rc = check_device_range(x, n * 4, dev);
-  if (rc == SOFTMAX_OK) rc = check_device_range(y, n * 4, dev);
+  if (rc == SOFTMAX_OK && y != x) rc = check_device_range(y, n * 4, dev);
   if (rc != SOFTMAX_OK) return rc;
   if (aligned16(x) && aligned16(y) && n % 4 == 0) {
     int64_t n4 = n / 4;

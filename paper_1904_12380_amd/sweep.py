@@ -33,8 +33,8 @@ WINDOWS = 7
 ROUNDS = 3
 ROTATE_BYTES = 1 << 30
 
-DEFAULT_COLS = (4, 8, 16, 32, 50, 64, 100, 128, 250, 256, 512, 1000, 1024, 2048, 4093, 4096,
-                8192, 16383, 16384, 32765, 32768, 65536, 131072)
+DEFAULT_COLS = (4, 8, 16, 32, 50, 64, 65, 100, 128, 129, 250, 256, 512, 1000, 1024, 2048, 4093,
+                4096, 8192, 16383, 16384, 32765, 32768, 65536, 131072)
 
 
 def candidates(cols: int) -> list[dict]:

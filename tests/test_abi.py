@@ -91,15 +91,20 @@ def test_cpu_tensor_is_rejected():
     (300, 100, "group_rows", 4, dict(lanes_per_row=32, elems_per_lane=4)),
     (300, 256, "group_rows", 4, dict(lanes_per_row=64, elems_per_lane=4)),
     (300, 260, "wave_row", 4, dict(elems_per_lane=8)),
-    (300, 102, "wave_row", 1, dict(elems_per_lane=4)),
-    (3, 65, "wave_row", 1, dict(elems_per_lane=4)),
+    (300, 102, "packed", 4, dict(lanes_per_row=8, elems_per_lane=13)),
+    (300, 250, "packed", 4, dict(lanes_per_row=16, elems_per_lane=16)),
+    (300, 257, "wave_row", 1, dict(elems_per_lane=8)),
+    (3, 65, "packed", 4, dict(lanes_per_row=8, elems_per_lane=9)),
     (3, 4096, "wave_row", 4, dict(elems_per_lane=64)),
-    (3, 4097, "block_row", 1, dict(elems_per_lane=8)),
+    (3, 4097, "block_row", 4, dict(elems_per_lane=8)),
     # 32-bit access: at most 32 values per lane in a wavefront, and no
     # one-pass 32768-column chunks (both would spill)
     (3, 2047, "wave_row", 1, dict(elems_per_lane=32)),
-    (3, 2049, "block_row", 1, dict(elems_per_lane=8)),
-    (3, 4095, "block_row", 1, dict(elems_per_lane=8)),
+    (3, 2049, "wave_row", 4, dict(elems_per_lane=64)),
+    (3, 4093, "wave_row", 4, dict(elems_per_lane=64)),
+    (3, 4095, "block_row", 4, dict(elems_per_lane=8)),
+    (3, 8189, "block_row", 4, dict(elems_per_lane=8)),
+    (3, 8190, "block_row", 1, dict(elems_per_lane=8)),     # 8190 + 3 > 8192: 32-bit
     (1, 1048579, "split_row", 1, dict(chunks_per_row=65, elems_per_lane=32,
                                       block_threads=512)),
     (3, 32769, "split_row", 1, dict(chunks_per_row=5, block_threads=256)),
@@ -128,6 +133,8 @@ def test_plan_vector_width_follows_alignment():
     assert sm.softmax_plan(10, 50, a, b + 8)["vec_width"] == 1
     assert sm.softmax_plan(10, 50, a, b)["vec_width"] == 4
     assert sm.softmax_plan(10, 1002, a, b)["vec_width"] == 1
+    assert sm.softmax_plan(10, 3002, a, b)["vec_width"] == 4    # aligned strips around rows
+    assert sm.softmax_plan(10, 3002, a + 4, b)["vec_width"] == 1
     assert sm.softmax_plan(10, 1000, a, a)["vec_width"] == 4     # in place
 
 
@@ -180,7 +187,7 @@ def test_plan_rejects_bad_arguments():
 
 def test_probes_reject_bad_arguments():
     lib = sm.load_library()
-    assert lib.softmax_copy_probe(0x1000, 0x1000, 16, None) == sm.ERR_INVALID_ARG
+    assert lib.softmax_copy_probe(0x1000, 0x1004, 16, None) == sm.ERR_INVALID_ARG
     assert lib.softmax_copy_probe(0x1000, 0x2000, -1, None) == sm.ERR_INVALID_ARG
     assert lib.softmax_copy_probe(None, 0x2000, 4, None) == sm.ERR_INVALID_ARG
     assert lib.softmax_exp_probe(0x1000, 0x8000, 0x1004, 16, -64.0, 0, None) == sm.ERR_INVALID_ARG
@@ -263,7 +270,7 @@ def test_planned_rejects_plans_the_library_cannot_run():
     X, Y = 1 << 40, 1 << 41      # 16-byte aligned
     bad = sm.ERR_INVALID_ARG
     run = sm.softmax_fwd_planned_ptr
-    assert run(X, Y, 4, 100, dict(kernel_name="packed", vec_width=4)) == bad   # cols > 64
+    assert run(X, Y, 4, 300, dict(kernel_name="packed", vec_width=4)) == bad   # cols > 256
     assert run(X, Y, 4, 5000, dict(kernel_name="wave_row", vec_width=4)) == bad
     assert run(X, Y, 4, 3000, dict(kernel_name="wave_row", vec_width=1)) == bad  # would spill
     assert run(X, Y, 4, 40000, dict(kernel_name="block_row", vec_width=4)) == bad

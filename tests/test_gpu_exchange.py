@@ -183,10 +183,13 @@ def test_store_delay_changes_no_bit(key):
 
 
 PLANNED = [
-    ("packed", 4, {}, [(1000, 50), (333, 17), (77, 64)]),
+    ("packed", 4, {}, [(1000, 50), (333, 17), (77, 64), (501, 65), (333, 250), (64, 256)]),
+    ("packed", 1, {}, [(129, 65), (70, 255)]),
     ("group_rows", 4, {}, [(1000, 52), (333, 16), (77, 256), (9, 4), (4099, 8)]),
     ("wave_row", 4, {}, [(300, 52), (257, 1000), (9, 4096)]),
     ("wave_row", 1, {}, [(130, 1001), (5, 2047)]),
+    ("wave_row", 4, {}, [(17, 2049), (9, 4093)]),
+    ("block_row", 4, {}, [(5, 8189), (6, 4097), (7, 2051)]),
     ("block_row", 4, {}, [(64, 1000), (9, 8192), (5, 32768)]),
     ("block_row", 1, {}, [(20, 999), (5, 32767)]),
     ("split_row", 4, dict(block_threads=256, elems_per_lane=32), [(33, 1000), (9, 32768),

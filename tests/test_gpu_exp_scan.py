@@ -9,7 +9,9 @@ exact value (the fp32 spacing at |exact|), with the exact value from
 float64 exp / exp2 on the host (error far below 2^-29 fp32 ulp).
 
 The clipped exponential's stated bound is 1.5 ulp (sm_device.hpp); the
-header states the measured maxima of both.
+header states the measured maxima of both (on MI355X: 1.2685 ulp at
+x = -8.426096 for the clipped exponential, 0.7827 ulp at t = -0.750096 for
+v_exp_f32, and at most 1.2451 ulp on the shifted scans).
 """
 import concurrent.futures as cf
 import sys

@@ -88,7 +88,8 @@ def test_edge_shapes(cols):
             check_parity(x, run_gpu(x), f"{rows}x{cols} {kind}")
 
 
-@pytest.mark.parametrize("rows,cols", [(400001, 7), (200003, 21), (99999, 33), (98305, 62)])
+@pytest.mark.parametrize("rows,cols", [(400001, 7), (200003, 21), (99999, 33), (98305, 62),
+                                       (300001, 65), (100003, 250), (77777, 129)])
 def test_packed_persistent_tiles(rows, cols):
     """More tiles than the persistent grid: every workgroup loops over
     several tiles with the next tile's loads in flight; ragged last tile."""
@@ -116,7 +117,7 @@ def test_group_rows(rows, cols):
 
 
 @pytest.mark.parametrize("rows,cols", [(257, 50), (64, 1000), (33, 1001), (5, 8192), (3, 100003),
-                                       (131, 7)])
+                                       (131, 7), (257, 130), (99, 3001)])
 def test_misaligned_views(rows, cols):
     """x and y start 4 bytes past a 16-byte boundary: the 32-bit paths."""
     torch = _torch()
@@ -136,8 +137,22 @@ def test_misaligned_views(rows, cols):
     check_parity(x, yv.cpu().numpy(), f"misaligned {rows}x{cols}")
 
 
+@pytest.mark.parametrize("rows,cols", [(17, 2049), (33, 3001), (9, 4093), (11, 4095), (5, 6143),
+                                       (7, 8189)])
+def test_row_phase_access(rows, cols):
+    """Rows that are not whole 16-byte strips in aligned x and y: 128-bit
+    access in the aligned strips around each row (every phase 0..3 occurs
+    over four consecutive rows), straddling strips element by element."""
+    log(f"[parity] row phase {rows}x{cols}")
+    p = sm.softmax_plan(rows, cols)
+    assert p["vec_width"] == 4 and p["kernel_name"] in ("wave_row", "block_row")
+    for kind in ("normal", "clip_heavy", "offset"):
+        x = workloads.random_logits(rows, cols, seed=rows * 5 + cols, kind=kind)
+        check_parity(x, run_gpu(x), f"row phase {rows}x{cols} {kind}")
+
+
 @pytest.mark.parametrize("rows,cols", [(115200, 50), (64, 1000), (512, 32768), (64, 262144),
-                                       (7, 3)])
+                                       (7, 3), (67, 1001), (9, 4093), (13, 250), (5, 8189)])
 def test_in_place(rows, cols):
     torch = _torch()
     log(f"[parity] in-place {rows}x{cols}")
@@ -215,7 +230,8 @@ def test_nonfinite_rows(cols):
     assert np.allclose(y[4].astype(np.float64), want[4], rtol=REL_TOL, atol=0)
 
 
-@pytest.mark.parametrize("rows,cols", [(257, 50), (65, 1000), (3, 8192), (2, 262144)])
+@pytest.mark.parametrize("rows,cols", [(257, 50), (65, 1000), (3, 8192), (2, 262144), (9, 1001),
+                                       (6, 4093), (5, 257)])
 def test_guard_bands_untouched(rows, cols):
     """Sentinels before and after y survive the call."""
     torch = _torch()
@@ -268,6 +284,10 @@ def test_copy_probe():
     assert torch.equal(sm.softmax_copy_probe(x), x)
     xo = x[1:]
     assert torch.equal(sm.softmax_copy_probe(xo), xo)
+    # in place, 128-bit and 32-bit paths
+    for t in (x.clone(), x.clone()[1:]):
+        ref = t.clone()
+        assert torch.equal(sm.softmax_copy_probe(t, out=t), ref)
 
 
 def _hip():
