@@ -16,7 +16,11 @@ warm by earlier steps; every x_k holds the same seeded matrix.
 
 Timing: the K steps are captured once into a HIP graph (torch.cuda.CUDAGraph)
 on a dedicated stream.  After W eager warmup steps and one untimed replay,
-the measurement is: synchronise; replay the graph once untimed (a pre-roll
+the graph is replayed, untimed, until at least SETTLE_S seconds of GPU work
+have run (the GPU's clocks drop while the host prepares each workload, and
+take tens of milliseconds to come back up; a window timed right after the
+preparation measured up to 10% slower).  Then the measurement is:
+synchronise; replay the graph once untimed (a pre-roll
 that keeps the GPU busy while the host queues the rest); record the start
 event; replay the graph (exactly K steps, with every gap between them);
 record the stop event; synchronise.  Starting the event behind queued work
@@ -150,10 +154,14 @@ def warm_clocks(sm, torch, seconds: float = 0.3) -> None:
     del x, y
 
 
+SETTLE_S = 0.05
+
+
 def time_steps(torch, launch, steps: int, warmup: int) -> tuple[float, float]:
     """Graph-replayed and eager ms per step of launch(i, stream), each timed
-    over exactly `steps` steps behind a queued pre-roll (see the module
-    docstring).  Returns (graph ms per step, eager ms per step)."""
+    over exactly `steps` steps behind a queued pre-roll, after untimed
+    replays that let the clocks settle (see the module docstring).  Returns
+    (graph ms per step, eager ms per step)."""
     stream = torch.cuda.Stream()
     stream.wait_stream(torch.cuda.current_stream())
     start = torch.cuda.Event(enable_timing=True)
@@ -167,6 +175,11 @@ def time_steps(torch, launch, steps: int, warmup: int) -> tuple[float, float]:
                 launch(i, stream)
         g.replay()                  # first replay, untimed
         torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < SETTLE_S:   # clocks settle, untimed
+            for _ in range(4):
+                g.replay()
+            torch.cuda.synchronize()
         g.replay()                  # pre-roll, untimed
         start.record(stream)
         g.replay()                  # the timed steps
