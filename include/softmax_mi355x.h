@@ -102,13 +102,17 @@ extern "C" {
  * (max, sum) pairs
  * through a table of 4096 row entries held in a static device array
  * (2,359,552 bytes per device, part of the library's code object, zero at
- * rest).  The workgroups of a row meet at the entry its launch's key (the
- * output address and a per-call nonce) and its row index hash to: the first
- * to arrive claims it on the device, the last to leave frees it.  So calls on
- * any number of streams, graphs replayed at the same time, and a first call
- * made under stream capture need no host-side state, no allocation and no
- * synchronisation.  A row whose entry is still held by a row of another
- * running launch waits for it (bounded).
+ * rest).  Each launch takes as many consecutive entries as it has rows,
+ * from a per-device cursor on the host (launch bases advance mod 4096); the
+ * workgroups of a row meet at its entry: the first to arrive claims it on
+ * the device, the last to leave frees it.  So calls on any number of
+ * streams, graphs replayed at the same time, and a first call made under
+ * stream capture need no allocation and no synchronisation, and launches
+ * in flight together use disjoint entries as long as they hold fewer than
+ * 4096 split rows between them.  Beyond that (or when one graph is
+ * replayed on two streams at once) a row whose entry is still held waits
+ * for it; the wait is bounded, and a row that gives up is written as NaN
+ * and counted (softmax_exchange_status).
  *
  * Long rows are done in one pass when a row spans at most 64 workgroups
  * (chunks of 8192 columns up to cols = 65536, then chunks of 16384 up to

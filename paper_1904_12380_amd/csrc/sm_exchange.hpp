@@ -3,18 +3,27 @@
 //
 // The exchange lives in a fixed table of row entries in a static device
 // array (the library allocates no memory).  The workgroups of one row meet
-// at one entry: entry (H + row) mod kEntries, where H hashes the launch's
-// key (the output address of the launch's first row, mixed with a per-call
-// nonce), so the rows of a launch take consecutive entries.  The first
-// workgroup of the row to arrive claims the entry with a compare-and-swap
-// of its owner word from 0 to the row's tag (a hash of the key and the
-// row); the others find the tag there and join.  Each publishes a partial
-// pair in its slot, and the last to leave puts the entry back to rest
-// (slots, counter and owner zero).  Rows of concurrent launches that hash
-// onto an entry in use wait for it.  So calls on any number of streams,
-// graphs replayed at the same time, and a first call made under stream
-// capture all work without host-side state, and every atomic is shared only
-// by the workgroups of one row.
+// at one entry: entry (base + row) mod kEntries, where the host gives every
+// launch a base from a per-device cursor that advances by the launch's row
+// count, so the rows of a launch take consecutive entries and launches in
+// flight together take disjoint ones while they hold fewer than kEntries
+// rows between them.  The first workgroup of the row to arrive claims the
+// entry with a compare-and-swap of its owner word from 0 to the row's tag
+// (a hash of the launch's key and the row; the key mixes the output
+// address with a per-call nonce); the others find the tag there and join.
+// Each publishes a partial pair in its slot, and the last to leave puts the
+// entry back to rest (slots, counter and owner zero).  A row whose entry is
+// still held (by a launch kEntries rows of split-row work earlier, or by a
+// second replay of the same graph) waits for it.  So calls on any number
+// of streams, graphs replayed at the same time, and a first call made under
+// stream capture all work without host-side synchronisation, and every
+// atomic is shared only by the workgroups of one row.
+//
+// Rows that waited for an entry held by another launch could deadlock: the
+// waiting workgroups hold compute-unit slots that the holder's remaining
+// workgroups need.  Disjoint bases keep concurrent launches from ever
+// waiting on each other; the bounded wait turns what is left into a NaN
+// row (counted) rather than a hang.
 //
 // Every wait is bounded by the wall clock.  A workgroup that gives up
 // counts itself in a give-up counter (readable from the host), writes NaN
@@ -96,6 +105,8 @@ struct XchArgs {
   uint64_t key;
   uint32_t limit_ticks;
   uint32_t join;
+  uint32_t base;  // entry of the launch's row 0 (mod kEntries)
+  uint32_t unused;
 };
 
 // Entry of row `lrow` of the launch, joined (or, with a.join == 0, found)
@@ -103,7 +114,7 @@ struct XchArgs {
 __device__ __forceinline__ uint64_t* row_entry(const XchArgs& a, int lrow, uint64_t deadline) {
   using namespace xch;
   const uint64_t h = mix64(a.key);
-  const int e = static_cast<int>((h + static_cast<uint64_t>(lrow)) & (kEntries - 1));
+  const int e = static_cast<int>((a.base + static_cast<uint32_t>(lrow)) & (kEntries - 1));
   uint64_t tag = mix64(h ^ (static_cast<uint64_t>(lrow) * 0x9E3779B97F4A7C15ull));
   if (tag == 0) tag = 1;
   uint64_t* entry = a.scratch + int64_t(e) * kEntryWords;

@@ -303,6 +303,29 @@ __device__ __forceinline__ void load_strip_ph(float (&v)[4 * V], const float* p,
   }
 }
 
+// The loads of load_strip_ph with fewer registers, for the split kernels:
+// every strip that holds a column of the segment is one 128-bit load, and
+// columns outside [0, lim) are replaced by -inf after the load.  A
+// straddling strip therefore also reads up to 3 floats of the neighbouring
+// row, or, at the end of the matrix, up to 12 bytes past it inside the same
+// 16-byte block, which lies in the same memory page as the row's last
+// column; those values are never used.  (Stores stay element by element in
+// straddling strips: store_strip_ph.)
+template <int V>
+__device__ __forceinline__ void load_strip_ph_wide(float (&v)[4 * V], const float* p, int a,
+                                                   int lane_off, int stride, int lim) {
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int c0 = 4 * (lane_off + stride * j) - a;
+    f32x4 q = f32x4{kNegInf, kNegInf, kNegInf, kNegInf};
+    if (c0 < lim) q = ld_stream(p + c0);
+    v[4 * j + 0] = (c0 + 0 >= 0 && c0 + 0 < lim) ? q.x : kNegInf;
+    v[4 * j + 1] = (c0 + 1 >= 0 && c0 + 1 < lim) ? q.y : kNegInf;
+    v[4 * j + 2] = (c0 + 2 >= 0 && c0 + 2 < lim) ? q.z : kNegInf;
+    v[4 * j + 3] = (c0 + 3 >= 0 && c0 + 3 < lim) ? q.w : kNegInf;
+  }
+}
+
 // Stores out(v[i]) for the columns of the segment, strips as load_strip_ph.
 template <int V, typename F>
 __device__ __forceinline__ void store_strip_ph(const float (&v)[4 * V], F out, float* p, int a,
@@ -384,17 +407,22 @@ __device__ __forceinline__ float2 lane_online_exp(float (&v)[N], float (&mk)[N /
 // wavefronts: m the segment max, s its sum of exp(max(x - m, lo)) (for
 // m = -inf, the lanes' sums of clipped values).  v holds the lane's
 // exponentials afterwards (see lane_online_exp).
-template <int NW, int V, bool VEC4, int MODE>
+// With PH the segment starts `a` floats past a 16-byte boundary
+// (load_strip_ph); a = 0 and a whole segment take the aligned loads.
+template <int NW, int V, bool VEC4, int MODE, bool PH = false>
 __device__ __forceinline__ float2 segment_online(float (&v)[4 * V],
                                                  float (&mk)[4 * V / kOnlineSub],
                                                  const float* p, int lane_off, int stride,
                                                  int lim, Clip clip, float* red_max,
-                                                 float* red_sum) {
+                                                 float* red_sum, int a = 0) {
   // Each branch reduces its own loads: after a join the compiler would wait
   // for all of them before the first use.
   float2 ms;
-  if (lim == 4 * V * stride) {
+  if (lim == 4 * V * stride && a == 0) {
     load_strip_whole<V, VEC4>(v, p, lane_off, stride);
+    ms = lane_online_exp<MODE>(v, mk, clip);
+  } else if constexpr (PH) {
+    load_strip_ph_wide<V>(v, p, a, opaque(lane_off), stride, lim);
     ms = lane_online_exp<MODE>(v, mk, clip);
   } else {
     load_strip<V, VEC4>(v, p, opaque(lane_off), stride, lim);
@@ -451,11 +479,13 @@ __device__ __forceinline__ void store_row(const float (&v)[4 * V], RowShift rs, 
 //     y = max(e * exp(max(mk - M, lo)) * rcp, e_lo * rcp)
 // per sub-strip.  For x - M >= lo the rescaled e is exp(x - M) / S; below
 // it, under e^lo / S, so the max gives the clipped value exactly.
-template <int V, bool VEC4, int MODE>
+// With PH the segment starts `a` floats past a 16-byte boundary, as in
+// segment_online.
+template <int V, bool VEC4, int MODE, bool PH = false>
 __device__ __forceinline__ void store_online(float (&v)[4 * V],
                                              const float (&mk)[4 * V / kOnlineSub], RowShift rs,
                                              float rcp, float* p, int lane_off, int stride,
-                                             int lim) {
+                                             int lim, int a = 0) {
   constexpr int SUB = kOnlineSub;
   const float floor_y = rs.e_lo * rcp;
 #pragma unroll
@@ -464,7 +494,10 @@ __device__ __forceinline__ void store_online(float (&v)[4 * V],
 #pragma unroll
     for (int i = 0; i < SUB; ++i) v[k * SUB + i] = fmaxf(v[k * SUB + i] * sc, floor_y);
   }
-  store_strip<V, VEC4>(v, [](float ev) { return ev; }, p, lane_off, stride, lim);
+  if constexpr (PH)
+    store_strip_ph<V>(v, [](float ev) { return ev; }, p, a, lane_off, stride, lim);
+  else
+    store_strip<V, VEC4>(v, [](float ev) { return ev; }, p, lane_off, stride, lim);
 }
 
 // The row's label as a column of the segment [c0, c0 + lim), or -1 when it
@@ -1082,11 +1115,20 @@ __global__ __launch_bounds__(NT) void k_split_apply(const float* x, float* y,
 //
 // NLL outputs (one value per row) take no wait at all: the last workgroup
 // of the row to depart does the merge.
-template <int NT, int V, bool VEC4, int MODE>
+//
+// PH (probability outputs): rows whose length is not a multiple of 4, in
+// 16-byte aligned x and y.  Chunk g then covers the row's columns
+// [g*CH - a, (g+1)*CH - a) (clamped to the row), a = the row's phase, so
+// every chunk but the first starts on a 16-byte boundary and only the row's
+// two end strips straddle (load_strip_ph).  The launch has
+// ceil((cols + 3) / CH) chunks per row; a row whose phase leaves its last
+// chunk empty publishes an empty pair from it (count 0).
+template <int NT, int V, bool VEC4, int MODE, bool PH = false>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     2 * kRowWaves<V, VEC4, MODE>))) void k_split_onepass(
     const float* x, float* y, const int64_t* labels, XchArgs xa, int64_t cols, int chunks,
     uint32_t delay, Clip clip) {
+  static_assert(!PH || (VEC4 && !keeps_logits<MODE>()), "phase access: probability outputs");
   const uint64_t t0 = wall_clock();
   constexpr int NW = NT / 64;
   constexpr int64_t CH = int64_t(4) * V * NT;
@@ -1097,17 +1139,29 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
   const int b = blockIdx.x;
   const int lrow = b / chunks;
   const int g = b - lrow * chunks;
-  const int64_t c0 = int64_t(g) * CH;
+  int64_t c0 = int64_t(g) * CH;
+  int lim = seg_len(cols, c0, CH);
+  int a = 0;  // phase of this chunk's first column (PH: the first chunk only)
+  if constexpr (PH) {
+    const int ra =
+        static_cast<int>((reinterpret_cast<uintptr_t>(x + lrow * cols) >> 2) & 3);
+    const int64_t s0 = int64_t(g) * CH - ra;
+    const int64_t e0 = s0 + CH < cols ? s0 + CH : cols;
+    c0 = s0 < 0 ? 0 : s0;
+    lim = e0 > c0 ? static_cast<int>(e0 - c0) : 0;
+    a = g == 0 ? ra : 0;
+  }
   const float* xr = x + lrow * cols + c0;
   const int64_t label = row_label<MODE>(labels, lrow);
-  const int lim = seg_len(cols, c0, CH);
 
   constexpr bool ONLINE = !keeps_logits<MODE>() && online_exp<4 * V>();
+  static_assert(!PH || ONLINE, "phase access: the online reduction");
   float v[4 * V];
   float mk[ONLINE ? 4 * V / kOnlineSub : 1];
   float2 part;
   if constexpr (ONLINE) {
-    part = segment_online<NW, V, VEC4, MODE>(v, mk, xr, tid, NT, lim, clip, red_max, red_sum);
+    part = segment_online<NW, V, VEC4, MODE, PH>(v, mk, xr, tid, NT, lim, clip, red_max,
+                                                 red_sum, a);
     if (part.x == kNegInf) part.y = static_cast<float>(lim);
   } else if constexpr (keeps_logits<MODE>()) {
     load_strip_flat<V, VEC4>(v, xr, tid, NT, lim);
@@ -1221,8 +1275,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     finish_row<V, VEC4, MODE>(v, row_shift(bcast[0], clip), bcast[1], y, lrow, cols, c0, lim,
                               pick, tid, NT);
   } else if constexpr (ONLINE) {
-    store_online<V, VEC4, MODE>(v, mk, row_shift(bcast[0], clip), bcast[1],
-                                y + lrow * cols + c0, opaque(tid), NT, lim);
+    store_online<V, VEC4, MODE, PH>(v, mk, row_shift(bcast[0], clip), bcast[1],
+                                    y + lrow * cols + c0, opaque(tid), NT, lim, a);
   } else {
     float* yr = y + lrow * cols + c0;
     const float scale = bcast[0];

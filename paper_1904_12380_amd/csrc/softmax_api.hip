@@ -101,6 +101,7 @@ constexpr int64_t kStoreMaxNs = 200000;
 // Per-device facts: compute units, the wall clock's rate, and the device
 // address of `scratch`, taken once per device with that device current.
 struct DeviceFacts {
+  int dev = 0;
   int cus = 0;
   int64_t wall_khz = 0;
   uint64_t* scratch = nullptr;
@@ -114,6 +115,7 @@ int device_facts(int dev, DeviceFacts* out) {
   std::lock_guard<std::mutex> lock(g_facts_mu);
   if (!g_facts_ready[dev]) {
     DeviceFacts f;
+    f.dev = dev;
     int rc = device_cus(dev, &f.cus);
     if (rc != SOFTMAX_OK) return rc;
     int khz = 0;
@@ -162,9 +164,20 @@ int blocks_per_cu(int dev, const void* fn, int block, int* out) {
 
 // Per-call part of the exchange key (the launch's output address fills the
 // high bits): calls made at the same time never share a key unless they
-// write the same output, and a region left claimed after a give-up is not
-// picked up by later eager calls.
+// write the same output, and an entry left claimed after a give-up is not
+// picked up by later calls.
 std::atomic<uint32_t> g_nonce{1};
+
+// Per device: the exchange entry the next split-row launch starts at.
+// Every launch takes as many consecutive entries as it has rows (mod
+// xch::kEntries), so launches in flight together never meet at an entry
+// while they hold fewer than xch::kEntries rows between them.
+std::atomic<uint32_t> g_entry_cursor[kMaxDevices];
+
+inline uint32_t entry_base(const DeviceFacts& f, int64_t rows_in_launch) {
+  return g_entry_cursor[f.dev].fetch_add(static_cast<uint32_t>(rows_in_launch),
+                                        std::memory_order_relaxed);
+}
 
 inline uint64_t exchange_key(const void* out_first_row, uint32_t nonce) {
   return (static_cast<uint64_t>(reinterpret_cast<uintptr_t>(out_first_row)) << 16) |
@@ -286,6 +299,13 @@ const void* shape_fn(const Shape& s, bool stats_pass) {
         return stats_pass ? cast(&k_split_stats<kSplitThreads, kSplitV, VEC4, EM>)
                           : cast(&k_split_apply<kSplitThreads, kSplitV, VEC4, EM>);
       }
+      if (s.ph) {
+        if constexpr (VEC4 && (EM == kExpAccurate || EM == kExpWide || EM == kExpFast)) {
+          if (s.threads == 256 && s.v == 8) return cast(&k_split_onepass<256, 8, true, EM, true>);
+          if (s.threads == 512 && s.v == 8) return cast(&k_split_onepass<512, 8, true, EM, true>);
+        }
+        return nullptr;
+      }
       if (s.threads == 256 && s.v == 8) return cast(&k_split_onepass<256, 8, VEC4, EM>);
       if (s.threads == 512 && s.v == 8) return cast(&k_split_onepass<512, 8, VEC4, EM>);
       if constexpr (VEC4) {
@@ -318,6 +338,13 @@ const void* kernel_fn(const Shape& s, int em, bool stats_pass = false) {
 
 inline int64_t chunk_cols(const Shape& s) { return int64_t(4) * s.v * s.threads; }
 
+// Chunks per row of a split shape: with the row phase (s.ph) the chunks
+// must cover cols + 3 columns (a row may start up to 3 floats past a
+// 16-byte boundary, and every chunk but the first is aligned).
+inline int64_t row_chunks(const Shape& s, int64_t cols) {
+  return ceil_div(cols + (s.ph ? 3 : 0), chunk_cols(s));
+}
+
 // Lanes per row of the packed kernel: at most 16 columns per lane.
 inline int packed_lanes(int64_t cols) {
   return cols <= 16 ? 1 : cols <= 32 ? 2 : cols <= 64 ? 4 : cols <= 128 ? 8 : 16;
@@ -341,6 +368,27 @@ inline bool can_vec4(int kernel, const float* x, const float* y, int64_t cols) {
 inline bool phase_rows(const float* x, const float* y, int64_t cols) {
   return cols % 4 != 0 && cols > kWaveRowMaxColsScalar && cols + 3 <= kSplitMinColsProb &&
          aligned16(x) && aligned16(y);
+}
+
+// Split rows taken with the row phase (k_split_onepass with PH): threads
+// per workgroup (8192-column chunks while a row needs at most 8, else
+// 16384), and whether a row qualifies: cols not a multiple of 4, x and y
+// 16-byte aligned, longer than the row kernels' phase range, one pass, and
+// the phase adds no chunk (the chunks cover cols + 3 columns; where that
+// takes one more chunk than cols, the extra, nearly empty workgroups per
+// row cost more than 128-bit access gains: 16383 columns ran 33.5 us with
+// the phase and 28.2 us with 32-bit access, 131071 columns 33.2 against
+// 28.6).  Measured per 64 MiB: 32765 and 65533 columns ran 23.9 us with the
+// phase against about 28.3 with 32-bit access.
+inline int split_phase_threads(int64_t cols) {
+  return ceil_div(cols + 3, int64_t(4) * 8 * 256) <= kSmallChunkMaxChunks ? 256 : 512;
+}
+inline bool split_phase_rows(const float* x, const float* y, int64_t cols) {
+  if (cols % 4 == 0 || cols + 3 <= kSplitMinColsProb || !aligned16(x) || !aligned16(y))
+    return false;
+  const int64_t ch = int64_t(4) * 8 * split_phase_threads(cols);
+  return ceil_div(cols + 3, ch) == ceil_div(cols, ch) &&
+         ceil_div(cols + 3, ch) <= kOnePassMaxChunks;
 }
 
 // Row kernel for rows accessed with their phase: the strips must cover
@@ -382,6 +430,14 @@ Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
     s.vec4 = true;
     s.ph = true;
     phase_row_shape(cols, &s);
+  } else if (prob && split_phase_rows(x, y, cols)) {
+    // Long rows that are not whole 16-byte strips, in aligned x and y: the
+    // one-pass split kernel with the row phase.
+    s.kernel = SOFTMAX_KERNEL_SPLIT_ROW;
+    s.vec4 = true;
+    s.ph = true;
+    s.v = 8;
+    s.threads = split_phase_threads(cols);
   } else if (cols <= (s.vec4 ? kWaveRowMaxCols : kWaveRowMaxColsScalar)) {
     s.kernel = SOFTMAX_KERNEL_WAVE_ROW;
     s.threads = 256;
@@ -426,6 +482,18 @@ bool requested_shape(const softmax_plan_t& want, const float* x, const float* y,
   // kernels with the row phase (probability outputs, aligned x and y).
   const bool row_kernel =
       s.kernel == SOFTMAX_KERNEL_WAVE_ROW || s.kernel == SOFTMAX_KERNEL_BLOCK_ROW;
+  // The same for split rows (one pass, 8192- or 16384-column chunks).
+  if (s.vec4 && s.kernel == SOFTMAX_KERNEL_SPLIT_ROW && split_phase_rows(x, y, cols) &&
+      em != kLogOut && em != kNllOut) {
+    s.ph = true;
+    s.threads = want.block_threads;
+    s.v = want.elems_per_lane / 4;
+    if (want.elems_per_lane % 4 != 0 || s.v != 8) return false;
+    if (row_chunks(s, cols) > kOnePassMaxChunks) return false;
+    if (kernel_fn(s, em) == nullptr) return false;
+    *out = s;
+    return true;
+  }
   if (s.vec4 && row_kernel && phase_rows(x, y, cols) && em != kLogOut && em != kNllOut) {
     const int64_t span = cols + 3;
     if (span > (s.kernel == SOFTMAX_KERNEL_WAVE_ROW ? kWaveRowMaxCols : kSplitMinColsProb))
@@ -467,7 +535,7 @@ bool requested_shape(const softmax_plan_t& want, const float* x, const float* y,
       s.threads = want.block_threads;
       s.v = want.elems_per_lane / 4;
       if (want.elems_per_lane % 4 != 0) return false;
-      const int64_t chunks = ceil_div(cols, chunk_cols(s));
+      const int64_t chunks = row_chunks(s, cols);
       s.two_pass = chunks > kOnePassMaxChunks;
       break;
     }
@@ -536,7 +604,7 @@ int make_plan(const Shape& s, int64_t rows, int64_t cols, int em, int dev,
       p.launches = 1;
       break;
     default: {  // split rows
-      p.chunks = ceil_div(cols, chunk_cols(s));
+      p.chunks = row_chunks(s, cols);
       if (!s.two_pass) {
         // Whole rows per launch, every workgroup of a launch resident at
         // once.
@@ -650,7 +718,8 @@ hipError_t run_plan(const Plan& p, const float* x, float* y, const int64_t* labe
       const float* xb = x + r0 * cols;
       float* yb = out_rows(y, r0, cols, em);
       const int64_t* lb = label_rows(labels, r0, em);
-      XchArgs xa{f.scratch, exchange_key(yb, nonce), p.limit_ticks, 1u};  // join
+      XchArgs xa{f.scratch, exchange_key(yb, nonce), p.limit_ticks, 1u,  // join
+                 entry_base(f, nb), 0u};
       void* args[] = {&xb, &yb, &lb, &xa, &cols, &ichunks, &delay, &c};
       const hipError_t e = launch(fn, nb * p.chunks, s.threads, args, st);
       if (e != hipSuccess) return e;
@@ -665,11 +734,11 @@ hipError_t run_plan(const Plan& p, const float* x, float* y, const int64_t* labe
     const float* xb = x + r0 * cols;
     float* yb = out_rows(y, r0, cols, em);
     const int64_t* lb = label_rows(labels, r0, em);
-    XchArgs xa{f.scratch, exchange_key(yb, nonce), p.limit_ticks, 1u};
+    XchArgs xa{f.scratch, exchange_key(yb, nonce), p.limit_ticks, 1u, entry_base(f, nb), 0u};
     void* a1[] = {&xb, &xa, &cols, &iwpr, &chunks, &c};
     hipError_t e = launch(fn_stats, nb * p.wpr, s.threads, a1, st);
     if (e != hipSuccess) return e;
-    XchArgs xb2{f.scratch, xa.key, p.limit_ticks, 0u};  // find only
+    XchArgs xb2{f.scratch, xa.key, p.limit_ticks, 0u, xa.base, 0u};  // find only
     void* a2[] = {&xb, &yb, &lb, &xb2, &cols, &iwpr, &chunks, &c};
     e = launch(fn, nb * p.wpr, s.threads, a2, st);
     if (e != hipSuccess) return e;
@@ -744,7 +813,7 @@ SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64
     (void)hipGetLastError();
     Plan p;
     p.shape = s;
-    if (s.kernel == SOFTMAX_KERNEL_SPLIT_ROW) p.chunks = ceil_div(cols, chunk_cols(s));
+    if (s.kernel == SOFTMAX_KERNEL_SPLIT_ROW) p.chunks = row_chunks(s, cols);
     *plan = public_plan(p, rows);
     return SOFTMAX_OK;
   }

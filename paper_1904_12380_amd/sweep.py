@@ -43,7 +43,7 @@ def candidates(cols: int) -> list[dict]:
     out = []
     if cols <= 256:
         out.append(dict(kernel_name="group_rows", vec_width=4))
-    if cols <= 64:
+    if cols <= 256:
         out += [dict(kernel_name="packed", vec_width=w) for w in (4, 1)]
     if cols <= 4096:
         out += [dict(kernel_name="wave_row", vec_width=w) for w in (4, 1)]

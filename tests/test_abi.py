@@ -78,7 +78,7 @@ def test_cpu_tensor_is_rejected():
     (512, 32768, "split_row", 4, dict(chunks_per_row=4, elems_per_lane=32,
                                       block_threads=256)),
     (3, 8192, "block_row", 4, dict(elems_per_lane=8, block_threads=1024)),
-    (3, 8193, "split_row", 1, dict(chunks_per_row=2, block_threads=256)),
+    (3, 8193, "split_row", 4, dict(chunks_per_row=2, block_threads=256)),   # row phase
     (2, 65536, "split_row", 4, dict(chunks_per_row=8, block_threads=256)),
     (2, 65540, "split_row", 4, dict(chunks_per_row=5, block_threads=512)),
     (64, 262144, "split_row", 4, dict(chunks_per_row=16, elems_per_lane=32,
@@ -104,10 +104,15 @@ def test_cpu_tensor_is_rejected():
     (3, 4093, "wave_row", 4, dict(elems_per_lane=64)),
     (3, 4095, "block_row", 4, dict(elems_per_lane=8)),
     (3, 8189, "block_row", 4, dict(elems_per_lane=8)),
-    (3, 8190, "block_row", 1, dict(elems_per_lane=8)),     # 8190 + 3 > 8192: 32-bit
+    (3, 8190, "block_row", 1, dict(elems_per_lane=8)),     # the phase would add a chunk
     (1, 1048579, "split_row", 1, dict(chunks_per_row=65, elems_per_lane=32,
                                       block_threads=512)),
-    (3, 32769, "split_row", 1, dict(chunks_per_row=5, block_threads=256)),
+    (3, 32769, "split_row", 4, dict(chunks_per_row=5, block_threads=256)),
+    (3, 65533, "split_row", 4, dict(chunks_per_row=8, block_threads=256)),   # (cols + 3) / 8192
+    (3, 65535, "split_row", 1, dict(chunks_per_row=8, block_threads=256)),  # would add a chunk
+    (3, 16381, "split_row", 4, dict(chunks_per_row=2, block_threads=256)),
+    (3, 1048573, "split_row", 4, dict(chunks_per_row=64, block_threads=512)),
+    (3, 1048575, "split_row", 1, dict(chunks_per_row=64, block_threads=512)),  # 65 with the phase
     (300, 262144, "split_row", 4, dict(chunks_per_row=16, block_threads=512)),
     (1, 524288, "split_row", 4, dict(chunks_per_row=32, block_threads=512)),
     (1, 1048576, "split_row", 4, dict(chunks_per_row=64, elems_per_lane=32,

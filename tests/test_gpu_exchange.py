@@ -197,6 +197,9 @@ PLANNED = [
     ("split_row", 4, dict(block_threads=512, elems_per_lane=32), [(17, 40000), (3, 1048576)]),
     ("split_row", 4, dict(block_threads=512, elems_per_lane=64), [(6, 65536), (2, 2097152)]),
     ("split_row", 1, dict(block_threads=256, elems_per_lane=32), [(11, 8193), (3, 100003)]),
+    ("split_row", 4, dict(block_threads=256, elems_per_lane=32), [(11, 8193), (3, 100003),
+                                                                  (5, 65533)]),
+    ("split_row", 4, dict(block_threads=512, elems_per_lane=32), [(3, 100003), (2, 1048573)]),
     ("split_row", 1, dict(block_threads=512, elems_per_lane=32), [(3, 1048577)]),
 ]
 
@@ -241,8 +244,12 @@ def test_plan_geometry_on_device():
     assert p["kernel_name"] == "split_row" and p["chunks_per_row"] == 4
     assert p["grid"] == 2048 and p["launches"] == 1
     assert 8000 < p["store_delay_ns"] < 10000
-    p = sm.softmax_plan(512, 32767)              # 32-bit access: no store schedule
+    p = sm.softmax_plan(512, 32765)              # row phase: 128-bit, scheduled stores
+    assert p["vec_width"] == 4 and p["chunks_per_row"] == 4 and p["store_delay_ns"] > 0
+    p = sm.softmax_plan(512, 32765, (1 << 44) + 4, 1 << 45)   # 32-bit access: no schedule
     assert p["vec_width"] == 1 and p["store_delay_ns"] == 0
+    p = sm.softmax_plan(512, 32767)              # the phase would add a chunk: 32-bit
+    assert p["vec_width"] == 1 and p["chunks_per_row"] == 4
     p = sm.softmax_plan(64, 262144)
     assert p["chunks_per_row"] == 16 and p["launches"] == 1 and p["grid"] == 1024
     assert 8000 < p["store_delay_ns"] < 10000

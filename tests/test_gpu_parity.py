@@ -138,21 +138,23 @@ def test_misaligned_views(rows, cols):
 
 
 @pytest.mark.parametrize("rows,cols", [(17, 2049), (33, 3001), (9, 4093), (11, 4095), (5, 6143),
-                                       (7, 8189)])
+                                       (7, 8189), (9, 16381), (5, 32765), (6, 65533), (3, 100003),
+                                       (2, 262147)])
 def test_row_phase_access(rows, cols):
     """Rows that are not whole 16-byte strips in aligned x and y: 128-bit
     access in the aligned strips around each row (every phase 0..3 occurs
     over four consecutive rows), straddling strips element by element."""
     log(f"[parity] row phase {rows}x{cols}")
     p = sm.softmax_plan(rows, cols)
-    assert p["vec_width"] == 4 and p["kernel_name"] in ("wave_row", "block_row")
+    assert p["vec_width"] == 4 and p["kernel_name"] in ("wave_row", "block_row", "split_row")
     for kind in ("normal", "clip_heavy", "offset"):
         x = workloads.random_logits(rows, cols, seed=rows * 5 + cols, kind=kind)
         check_parity(x, run_gpu(x), f"row phase {rows}x{cols} {kind}")
 
 
 @pytest.mark.parametrize("rows,cols", [(115200, 50), (64, 1000), (512, 32768), (64, 262144),
-                                       (7, 3), (67, 1001), (9, 4093), (13, 250), (5, 8189)])
+                                       (7, 3), (67, 1001), (9, 4093), (13, 250), (5, 8189),
+                                       (7, 32767), (3, 100003)])
 def test_in_place(rows, cols):
     torch = _torch()
     log(f"[parity] in-place {rows}x{cols}")
@@ -231,7 +233,7 @@ def test_nonfinite_rows(cols):
 
 
 @pytest.mark.parametrize("rows,cols", [(257, 50), (65, 1000), (3, 8192), (2, 262144), (9, 1001),
-                                       (6, 4093), (5, 257)])
+                                       (6, 4093), (5, 257), (3, 100003), (4, 16385)])
 def test_guard_bands_untouched(rows, cols):
     """Sentinels before and after y survive the call."""
     torch = _torch()
