@@ -62,12 +62,18 @@ extern "C" {
 
 /* Kernel families reported by softmax_plan(). */
 #define SOFTMAX_KERNEL_NONE 0      /* rows*cols == 0: nothing is launched */
-#define SOFTMAX_KERNEL_PACKED 1    /* cols <= 64 (other than GROUP_ROWS):
+#define SOFTMAX_KERNEL_PACKED 1    /* cols <= 256 not taken by GROUP_ROWS
+                                      (log and NLL outputs: cols <= 64):
                                       several rows per wavefront */
-#define SOFTMAX_KERNEL_WAVE_ROW 2  /* cols <= 4096: one wavefront per row */
+#define SOFTMAX_KERNEL_WAVE_ROW 2  /* cols <= 4096: one wavefront per row
+                                      (rows that are not whole 16-byte
+                                      strips: 128-bit access in the aligned
+                                      strips around the row above 2048) */
 #define SOFTMAX_KERNEL_BLOCK_ROW 3 /* cols <= 8192 (log and NLL outputs:
                                       32768): one workgroup per row */
-#define SOFTMAX_KERNEL_SPLIT_ROW 4 /* longer rows: several workgroups per row */
+#define SOFTMAX_KERNEL_SPLIT_ROW 4 /* longer rows: several workgroups per row
+                                      (chunks aligned to the row's phase for
+                                      rows that are not whole strips) */
 #define SOFTMAX_KERNEL_GROUP_ROWS 5 /* cols <= 256 in whole 16-byte strips
                                        (cols % 4 == 0, 16-byte aligned x and
                                        y), probability outputs: G lanes per
@@ -324,11 +330,15 @@ SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64
  * and for measuring the dispatch (the paper picks code per shape, Sec. 2.5;
  * this library picks one of its compiled instances by cols).  Fields read
  * from *plan:
- *   kernel          SOFTMAX_KERNEL_PACKED (cols <= 64), _WAVE_ROW (cols <=
+ *   kernel          SOFTMAX_KERNEL_GROUP_ROWS (cols <= 256, cols % 4 == 0,
+ *                   vec_width 4), _PACKED (cols <= 256), _WAVE_ROW (cols <=
  *                   4096, 2048 with 32-bit access), _BLOCK_ROW (cols <=
  *                   32768) or _SPLIT_ROW (any cols);
- *   vec_width       4 (needs 16-byte aligned x and y and, above 64 columns,
- *                   cols % 4 == 0) or 1;
+ *   vec_width       4 (needs 16-byte aligned x and y and, above 256
+ *                   columns, cols % 4 == 0, except the row-phase shapes
+ *                   the library itself picks for rows that are not whole
+ *                   strips: wave or block rows of 2049 to 8189 columns,
+ *                   split rows whose phase adds no chunk) or 1;
  *   block_threads, elems_per_lane   split rows only: 256 x 32 (chunks of
  *                   8192 columns), 512 x 32 (16384) or, with vec_width 4,
  *                   512 x 64 (32768); rows of more than 64 chunks take the
