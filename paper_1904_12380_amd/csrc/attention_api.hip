@@ -57,6 +57,27 @@ hipError_t run_attention_lds(const float* q, const float* k, const float* v, flo
   return launch(reinterpret_cast<const void*>(&k_attention_lds<NKT, WIDE>), grid, 256, args, s);
 }
 
+// The DAM tile (d = dv = 200, 49 or 50 keys) with d known at compile time,
+// on the ping-pong schedule: one workgroup of 8 wavefronts per CU, 160 KiB
+// of LDS (two buffers of K_b, V_b and a zero row).
+constexpr int kAttnDamDim = 200;
+
+bool dam_tile(int lk, int d, int dv) {
+  return d == kAttnDamDim && dv == kAttnDamDim && lk > 48 &&
+         (lk * (d + dv) + dv + 16) * 4 <= kAttnLdsBytes;
+}
+
+template <bool WIDE>
+hipError_t run_attention_dam(const float* q, const float* k, const float* v, float* o,
+                             int64_t batch, int lq, int lk, int d, int dv, float scale, Clip c,
+                             int64_t cus, hipStream_t s) {
+  const int64_t items = batch * ((lq + 63) / 64);
+  const int64_t grid = std::min(items, cus);
+  void* args[] = {&q, &k, &v, &o, &batch, &lq, &lk, &d, &dv, &scale, &c};
+  return launch(reinterpret_cast<const void*>(&k_attention_pp<4, WIDE, kAttnDamDim>), grid, 512,
+                args, s);
+}
+
 template <bool WIDE>
 hipError_t dispatch_attention_lds(const float* q, const float* k, const float* v, float* o,
                                   int64_t batch, int lq, int lk, int d, int dv, float scale,
@@ -131,7 +152,11 @@ SOFTMAX_API int softmax_attention_fwd(const float* q, const float* k, const floa
   const int id = static_cast<int>(d), idv = static_cast<int>(dv);
   // K_b and V_b staged in LDS when they fit and every access is 128-bit.
   const bool lds = vec4 && d <= kAttnMaxDQ && lk * (d + dv) * 4 <= kAttnLdsBytes;
-  if (lds)
+  if (lds && dam_tile(ilk, id, idv))
+    e = wide ? run_attention_dam<true>(q, k, v, o, batch, ilq, ilk, id, idv, scale, c, cus, stream)
+             : run_attention_dam<false>(q, k, v, o, batch, ilq, ilk, id, idv, scale, c, cus,
+                                        stream);
+  else if (lds)
     e = wide ? dispatch_attention_lds<true>(q, k, v, o, batch, ilq, ilk, id, idv, scale, c,
                                             cus, stream)
              : dispatch_attention_lds<false>(q, k, v, o, batch, ilq, ilk, id, idv, scale, c,

@@ -277,8 +277,8 @@ __global__ __launch_bounds__(256) void k_attention(const float* q, const float* 
 // ---------------------------------------------------------------------------
 // The same computation with K_b and V_b staged in LDS, for problems whose
 // lk * (d + dv) floats fit in kAttnLdsBytes and whose rows allow 128-bit
-// access (d % 4 == dv % 4 == 0, 16-byte aligned operands).  A workgroup of
-// 4 wavefronts takes one batch element (and one block of 64 queries):
+// access (d % 4 == dv % 4 == 0, 16-byte aligned operands).  Four wavefronts
+// take one batch element (and one block of 64 queries):
 //
 //   1. the 4 wavefronts copy K_b and V_b, which are contiguous, into LDS
 //      with LDS-DMA loads (global_load_lds_dwordx4: 1 KiB per wavefront
@@ -289,232 +289,353 @@ __global__ __launch_bounds__(256) void k_attention(const float* q, const float* 
 //   3. a barrier ends the item before the next one overwrites the LDS.
 //
 // Each batch element's K and V cross HBM and L2 once, instead of once per
-// wavefront, and the matrix-op operands come from LDS.  Two workgroups fit
-// per CU, and one can copy while the other computes; they do not stay out
-// of step, though, and the compute phase (the matrix ops and the VALU work
-// that feeds them) sets the kernel's time.
-constexpr int kAttnLdsBytes = 80 * 1024;
-constexpr int kAttnMaxDQ = 224;  // d up to this keeps Q in registers (14 blocks)
+// wavefront, and the matrix-op operands come from LDS.  Two schedules:
+//
+//   * k_attention_lds: two workgroups of 4 wavefronts per CU, each with its
+//     own 80 KiB of LDS, one item after another (copy, wait, compute).  The
+//     two do not stay out of step, so copies and matrix ops overlap only
+//     in part.
+//   * k_attention_pp: one workgroup of 8 wavefronts per CU in two teams that
+//     take turns: one computes an item while the other copies the next.
+//     Used with d = dv = DC known at compile time (the DAM tile, DC = 200),
+//     where the masks and branches of the d loops fold away and the matrix
+//     ops issue back to back; with d at run time one wavefront per SIMD
+//     computes too slowly for this schedule.
+constexpr int kAttnLdsBytes = 80 * 1024;  // one batch element's K_b and V_b
+constexpr int kAttnMaxDQ = 224;           // d up to this keeps Q in registers
+constexpr int kAttnQB = kAttnMaxDQ / 16;  // 16-wide blocks of d in registers
 
-template <int NKT, bool WIDE>
+typedef __attribute__((address_space(3))) char attn_lds_char;
+
+// K_b and V_b (contiguous) into LDS at lk_s and lv_s with LDS-DMA loads,
+// spread over 4 wavefronts wt = 0..3: each instruction writes its 64 lanes'
+// 16 bytes to consecutive LDS bytes from the (uniform) destination.  Whole
+// 1 KiB chunks need no lane mask; in a partial last chunk the lanes past the
+// end are off.
+__device__ __forceinline__ void attn_copy_kv(float* lk_s, float* lv_s, const float* kb,
+                                             const float* vb, int kbytes, int vbytes, int wt,
+                                             int lane) {
+  attn_lds_char* dk = (attn_lds_char*)lk_s;
+  attn_lds_char* dvs = (attn_lds_char*)lv_s;
+  const char* gk = reinterpret_cast<const char*>(kb);
+  const char* gv = reinterpret_cast<const char*>(vb);
+  int c = 1024 * wt;
+  for (; c + 1024 <= kbytes; c += 4096)
+    __builtin_amdgcn_global_load_lds(gk + c + 16 * lane, dk + c, 16, 0, 0);
+  if (c < kbytes && c + 16 * lane < kbytes)
+    __builtin_amdgcn_global_load_lds(gk + c + 16 * lane, dk + c, 16, 0, 0);
+  c = 1024 * wt;
+  for (; c + 1024 <= vbytes; c += 4096)
+    __builtin_amdgcn_global_load_lds(gv + c + 16 * lane, dvs + c, 16, 0, 0);
+  if (c < vbytes && c + 16 * lane < vbytes)
+    __builtin_amdgcn_global_load_lds(gv + c + 16 * lane, dvs + c, 16, 0, 0);
+}
+
+// A wavefront's nq <= 16 query rows q0 .. of batch element b into
+// registers: block blk of lane (j, g) holds Q[q0 + j][16 blk + 4 g .. + 3].
+// Rows past nq and columns past d read as zero (buffer range check and the
+// offset mask).
+template <int DC>
+__device__ __forceinline__ void attn_load_q(f32x4m (&qf)[kAttnQB], const float* q, int64_t b,
+                                            int q0, int nq, int lq, int d, int j, int g) {
+  const __amdgpu_buffer_rsrc_t rq =
+      make_rsrc(q + (b * lq + q0) * static_cast<int64_t>(d), nq * d * 4);
+  const int qoff = (j * d + 4 * g) * 4;
+  const int nblk = (d + 15) >> 4;
+#pragma unroll
+  for (int blk = 0; blk < kAttnQB; ++blk) {
+    // With d known at compile time a block wholly inside d needs no mask.
+    const bool in_d = (DC != 0 && 16 * blk + 16 <= d) || 16 * blk + 4 * g < d;
+    qf[blk] = buf_load4<true>(rq, qoff + 64 * blk, (blk < nblk) & in_d);
+  }
+}
+
+// Scores, clipped softmax and O = P V for one wavefront's nq <= 16 queries
+// q0 .. of batch element b, with K_b at lk_s and V_b at lv_s in LDS and the
+// query rows in qf.  With DC != 0 (d = dv = DC), a zero row of dv + 16
+// floats follows V_b, and padding keys read their values from it.
+template <int NKT, bool WIDE, int DC>
+__device__ __forceinline__ void attn_compute(const float* lk_s, const float* lv_s,
+                                             const f32x4m (&qf)[kAttnQB], float* o, int64_t b,
+                                             int q0, int nq, int lq, int lk, int d, int dv,
+                                             float scale, Clip clip, int j, int g) {
+  constexpr bool ZR = DC != 0;
+  constexpr int QB = kAttnQB;
+  const int nblk = (d + 15) >> 4;
+
+  // ---- scores S^T = K Q^T, K from LDS ---------------------------------------
+  f32x4m acc[NKT];
+#pragma unroll
+  for (int kt = 0; kt < NKT; ++kt) acc[kt] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+  // Keys past lk read row 0: their scores are garbage (even NaN) but the
+  // softmax below masks them.  Columns t past d would read the next row, and
+  // 0 * NaN is NaN, so those operands are zeroed.
+  int krow[NKT];
+#pragma unroll
+  for (int kt = 0; kt < NKT; ++kt) {
+    const int key = 16 * kt + j;
+    krow[kt] = ((kt < NKT - 1 || key < lk) ? key : 0) * d + 4 * g;
+  }
+  // The next block's K operands are read while this block's matrix ops run;
+  // the d mask is applied at use, so no wait comes early.
+  f32x4m kc[NKT], kn[NKT];
+  if (nblk > 0) {
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) kc[kt] = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt]);
+  }
+#pragma unroll
+  for (int blk = 0; blk < QB; ++blk) {
+    if (blk < nblk) {  // uniform
+      if (blk + 1 < nblk) {
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+          kn[kt] = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt] + 16 * (blk + 1));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      const bool t_ok = (DC != 0 && 16 * blk + 16 <= d) || 16 * blk + 4 * g < d;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+          acc[kt] = mfma16x16x4(t_ok ? kc[kt][s] : 0.0f, qf[blk][s], acc[kt]);
+      }
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) kc[kt] = kn[kt];
+    }
+  }
+
+  // ---- clipped softmax over the keys of query j -----------------------------
+  float e[4 * NKT];
+  float m = -__builtin_inff();
+#pragma unroll
+  for (int kt = 0; kt < NKT; ++kt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
+      const float sv = acc[kt][r] * scale;
+      e[4 * kt + r] = sv;
+      m = key_ok ? fmaxf(m, sv) : m;
+    }
+  }
+  m = fmaxf(m, row16_partner(m));
+  m = fmaxf(m, half32_partner(m));
+  const RowShift rs = row_shift(m, clip);
+#pragma unroll
+  for (int kt = 0; kt < NKT; ++kt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
+      const float ev = exp_shift_clip<WIDE ? kExpWide : kExpAccurate>(e[4 * kt + r], rs);
+      e[4 * kt + r] = key_ok ? ev : 0.0f;
+    }
+  }
+  float sum = tree_sum(e);
+  sum = sum + row16_partner(sum);
+  sum = sum + half32_partner(sum);
+  const float rcp = 1.0f / sum;
+#pragma unroll
+  for (int i = 0; i < 4 * NKT; ++i) e[i] = e[i] * rcp;
+
+  // ---- O = P V, V from LDS --------------------------------------------------
+  // Contraction step i = 4 kt + r: key 16 kt + 4 g + r.  Keys past lk (only
+  // in the last key tile) have weight 0; their value operand is the zero row
+  // (ZR), else row 0 zeroed at use, since a stale value could be NaN.
+  auto v_ok = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + 4 * g + (i & 3) < lk; };
+  auto vrow = [&](int i) {
+    return ZR ? (v_ok(i) ? (16 * (i >> 2) + 4 * g + (i & 3)) * dv : lk * dv)
+              : (v_ok(i) ? 16 * (i >> 2) + 4 * g + (i & 3) : 0) * dv;
+  };
+  // A step whose smallest key (lane group 0) is past lk has zero weight in
+  // every lane: its matrix ops are skipped (a uniform branch; for DAM's 50
+  // keys, 2 of the 16 steps).
+  auto step_live = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + (i & 3) < lk; };
+  const __amdgpu_buffer_rsrc_t ro =
+      make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
+  const int orow = 4 * g * dv * 4;
+  const int nfull = dv >> 6;
+  // Each 64-column block in four quarters of NKT contraction steps: the next
+  // quarter's V rows (the next block's first, after the last) are read while
+  // this quarter's matrix ops run; the key mask is applied at use.
+  f32x4m vq[2][NKT];
+  if (nfull > 0) {
+#pragma unroll
+    for (int i = 0; i < NKT; ++i)
+      vq[0][i] = *reinterpret_cast<const f32x4m*>(lv_s + vrow(i) + 4 * j);
+  }
+  for (int cb = 0; cb < nfull; ++cb) {
+    const int c = 64 * cb + 4 * j;
+    f32x4m oacc[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) oacc[u] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int qi = 0; qi < 4; ++qi) {
+      if (qi < 3) {
+#pragma unroll
+        for (int i = 0; i < NKT; ++i)
+          vq[(qi + 1) & 1][i] =
+              *reinterpret_cast<const f32x4m*>(lv_s + vrow((qi + 1) * NKT + i) + c);
+      } else if (cb + 1 < nfull) {
+#pragma unroll
+        for (int i = 0; i < NKT; ++i)
+          vq[0][i] = *reinterpret_cast<const f32x4m*>(lv_s + vrow(i) + c + 64);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < NKT; ++i) {
+        const int st = qi * NKT + i;
+        if (step_live(st)) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            oacc[u] = mfma16x16x4(e[st], (ZR || v_ok(st)) ? vq[qi & 1][i][u] : 0.0f, oacc[u]);
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const f32x4m ov = {oacc[0][r], oacc[1][r], oacc[2][r], oacc[3][r]};
+      __builtin_amdgcn_raw_buffer_store_b128(
+          __builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, ov), ro,
+          orow + (r * dv + c) * 4, 0, 0);
+    }
+  }
+  // The remaining columns, one 16-column tile at a time: lane j takes column
+  // c0 + j.  A column past dv only feeds its own (unstored) output column, so
+  // with the zero row its loads need no mask (they stay inside V_b and the
+  // zero row); without it they are masked.
+  for (int c0 = 64 * nfull; c0 < dv; c0 += 16) {
+    const int c = c0 + j;
+    const bool c_ok = c < dv;
+    f32x4m oa = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int i = 0; i < 4 * NKT; ++i) {
+      if (step_live(i)) {
+        const float x = lv_s[vrow(i) + ((ZR || c_ok) ? c : 0)];
+        oa = mfma16x16x4(e[i], (ZR || (v_ok(i) & c_ok)) ? x : 0.0f, oa);
+      }
+    }
+    // Plain stores here: a 32-bit buffer store of an accumulator element
+    // was compiled to store element 0 for every r by this toolchain.
+    float* orow_p = o + (b * lq + q0 + 4 * g) * static_cast<int64_t>(dv) + c;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      if ((q0 + 4 * g + r < lq) & c_ok)
+        __builtin_nontemporal_store(oa[r], orow_p + static_cast<int64_t>(r) * dv);
+    }
+  }
+}
+
+// Two workgroups of 4 wavefronts per CU, each with its own 80 KiB of LDS:
+// copy K_b and V_b, load Q, wait, compute, one item after another.  With
+// DC != 0 the zero row after V_b is cleared once; no copy writes there.
+template <int NKT, bool WIDE, int DC = 0>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_attention_lds(
     const float* q, const float* k, const float* v, float* o, int64_t batch, int lq, int lk,
-    int d, int dv, float scale, Clip clip) {
+    int d_in, int dv_in, float scale, Clip clip) {
+  const int d = DC ? DC : d_in;
+  const int dv = DC ? DC : dv_in;
   __shared__ __attribute__((aligned(16))) float lds[kAttnLdsBytes / 4];
-  float* lk_s = lds;                       // K_b: lk x d
-  float* lv_s = lds + lk * d;              // V_b: lk x dv (16-byte aligned: d % 4 == 0)
+  float* lk_s = lds;           // K_b: lk x d
+  float* lv_s = lds + lk * d;  // V_b: lk x dv (16-byte aligned: d % 4 == 0)
   const int lane = __lane_id();
   const int j = lane & 15;
   const int g = lane >> 4;
   const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int qblocks = (lq + 63) >> 6;
   const int64_t items = batch * qblocks;
-  const int kbytes = lk * d * 4;
-  const int vbytes = lk * dv * 4;
-
+  if constexpr (DC != 0) {
+    for (int i = threadIdx.x; i < dv + 16; i += 256) lv_s[lk * dv + i] = 0.0f;
+  }
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
     const int64_t b = item / qblocks;
     const int q0 = static_cast<int>(item - b * qblocks) * 64 + 16 * w;
-
-    // ---- 1. K_b and V_b into LDS; Q rows into registers --------------------
+    const bool active = q0 < lq;  // wave-uniform
+    const int nq = active ? (lq - q0 < 16 ? lq - q0 : 16) : 0;
     // The other workgroup on this CU is usually running its matrix ops on
     // the same SIMDs; a higher wave priority gets these copies and loads
-    // issued first, so the memory work starts early (97.4 -> 95.6 us on the
-    // DAM shape together with the unmasked loop below; raising the priority
-    // of the matrix-op loops instead made it 104.4).
+    // issued first, so the memory work starts early (97.7 -> 95.6 us on the
+    // DAM shape; raising the priority of the matrix-op loops instead made
+    // it 104.4).
     __builtin_amdgcn_s_setprio(2);
-    {
-      // Each instruction writes its 64 lanes' 16 bytes to consecutive LDS
-      // bytes from the (uniform) destination.  Whole 1 KiB chunks need no
-      // lane mask; in a partial last chunk the lanes past the end are off.
-      typedef __attribute__((address_space(3))) char lds_char;
-      lds_char* dk = (lds_char*)lk_s;
-      lds_char* dvs = (lds_char*)lv_s;
-      const char* gk = reinterpret_cast<const char*>(k + b * lk * static_cast<int64_t>(d));
-      const char* gv = reinterpret_cast<const char*>(v + b * lk * static_cast<int64_t>(dv));
-      int c = 1024 * w;
-      for (; c + 1024 <= kbytes; c += 4096)
-        __builtin_amdgcn_global_load_lds(gk + c + 16 * lane, dk + c, 16, 0, 0);
-      if (c < kbytes && c + 16 * lane < kbytes)
-        __builtin_amdgcn_global_load_lds(gk + c + 16 * lane, dk + c, 16, 0, 0);
-      c = 1024 * w;
-      for (; c + 1024 <= vbytes; c += 4096)
-        __builtin_amdgcn_global_load_lds(gv + c + 16 * lane, dvs + c, 16, 0, 0);
-      if (c < vbytes && c + 16 * lane < vbytes)
-        __builtin_amdgcn_global_load_lds(gv + c + 16 * lane, dvs + c, 16, 0, 0);
-    }
-    const bool active = q0 < lq;                 // wave-uniform
-    const int nq = active ? (lq - q0 < 16 ? lq - q0 : 16) : 0;
-    constexpr int QB = kAttnMaxDQ / 16;          // d blocks held in registers
-    f32x4m qf[QB];
-    const int nblk = (d + 15) >> 4;
-    if (active) {
-      const __amdgpu_buffer_rsrc_t rq =
-          make_rsrc(q + (b * lq + q0) * static_cast<int64_t>(d), nq * d * 4);
-      const int qoff = (j * d + 4 * g) * 4;
-#pragma unroll
-      for (int blk = 0; blk < QB; ++blk)
-        qf[blk] = buf_load4<true>(rq, qoff + 64 * blk, (blk < nblk) & (16 * blk + 4 * g < d));
-    }
+    attn_copy_kv(lk_s, lv_s, k + b * lk * static_cast<int64_t>(d),
+                 v + b * lk * static_cast<int64_t>(dv), lk * d * 4, lk * dv * 4, w, lane);
+    f32x4m qf[kAttnQB];
+    if (active) attn_load_q<DC>(qf, q, b, q0, nq, lq, d, j, g);
     __builtin_amdgcn_s_setprio(0);
-    __builtin_amdgcn_s_waitcnt(0);               // this wave's copies and loads
-    __syncthreads();                             // everyone's copies
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies and loads
+    __syncthreads();                // everyone's copies
+    if (active)
+      attn_compute<NKT, WIDE, DC>(lk_s, lv_s, qf, o, b, q0, nq, lq, lk, d, dv, scale, clip, j, g);
+    __syncthreads();  // LDS is free for the next item
+  }
+}
 
-    if (active) {
-      // ---- 2a. scores S^T = K Q^T, K from LDS -------------------------------
-      f32x4m acc[NKT];
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt) acc[kt] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
-      // Keys past lk read row 0: their scores are garbage (even NaN) but
-      // the softmax below masks them.  Columns t past d would read the next
-      // row, and 0 * NaN is NaN, so those operands are zeroed.
-      int krow[NKT];
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt) {
-        const int key = 16 * kt + j;
-        krow[kt] = ((kt < NKT - 1 || key < lk) ? key : 0) * d + 4 * g;
-      }
-      // The next block's K operands are read while this block's matrix ops
-      // run; the d mask is applied at use, so no wait comes early.
-      f32x4m kc[NKT], kn[NKT];
-      if (nblk > 0) {
-#pragma unroll
-        for (int kt = 0; kt < NKT; ++kt)
-          kc[kt] = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt]);
-      }
-#pragma unroll
-      for (int blk = 0; blk < QB; ++blk) {
-        if (blk < nblk) {                        // uniform
-          if (blk + 1 < nblk) {
-#pragma unroll
-            for (int kt = 0; kt < NKT; ++kt)
-              kn[kt] = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt] + 16 * (blk + 1));
-          }
-          __builtin_amdgcn_sched_barrier(0);
-          const bool t_ok = 16 * blk + 4 * g < d;
-#pragma unroll
-          for (int s = 0; s < 4; ++s) {
-#pragma unroll
-            for (int kt = 0; kt < NKT; ++kt)
-              acc[kt] = mfma16x16x4(t_ok ? kc[kt][s] : 0.0f, qf[blk][s], acc[kt]);
-          }
-#pragma unroll
-          for (int kt = 0; kt < NKT; ++kt) kc[kt] = kn[kt];
-        }
-      }
-
-      // ---- 2b. clipped softmax over the keys of query j ---------------------
-      float e[4 * NKT];
-      float m = -__builtin_inff();
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
-          const float sv = acc[kt][r] * scale;
-          e[4 * kt + r] = sv;
-          m = key_ok ? fmaxf(m, sv) : m;
-        }
-      }
-      m = fmaxf(m, row16_partner(m));
-      m = fmaxf(m, half32_partner(m));
-      const RowShift rs = row_shift(m, clip);
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
-          const float ev = exp_shift_clip<WIDE ? kExpWide : kExpAccurate>(e[4 * kt + r], rs);
-          e[4 * kt + r] = key_ok ? ev : 0.0f;
-        }
-      }
-      float sum = tree_sum(e);
-      sum = sum + row16_partner(sum);
-      sum = sum + half32_partner(sum);
-      const float rcp = 1.0f / sum;
-#pragma unroll
-      for (int i = 0; i < 4 * NKT; ++i) e[i] = e[i] * rcp;
-
-      // ---- 2c. O = P V, V from LDS ------------------------------------------
-      // Contraction step i = 4 kt + r: key 16 kt + 4 g + r.  Keys past lk
-      // (only in the last key tile) read row 0 and are zeroed: their weight
-      // is 0, but a stale value could be NaN.
-      auto v_ok = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + 4 * g + (i & 3) < lk; };
-      auto vrow = [&](int i) { return (v_ok(i) ? 16 * (i >> 2) + 4 * g + (i & 3) : 0) * dv; };
-      // A step whose smallest key (lane group 0) is past lk has zero weight
-      // in every lane: its matrix ops are skipped (a uniform branch; for
-      // DAM's 50 keys, 2 of the 16 steps).
-      auto step_live = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + (i & 3) < lk; };
-      const __amdgpu_buffer_rsrc_t ro =
-          make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
-      const int orow = 4 * g * dv * 4;
-      const int nfull = dv >> 6;
-      // Each 64-column block in four quarters of NKT contraction steps: the
-      // next quarter's V rows (the next block's first, after the last) are
-      // read while this quarter's matrix ops run; the key mask is applied
-      // at use.
-      f32x4m vq[2][NKT];
-      if (nfull > 0) {
-#pragma unroll
-        for (int i = 0; i < NKT; ++i)
-          vq[0][i] = *reinterpret_cast<const f32x4m*>(lv_s + vrow(i) + 4 * j);
-      }
-      for (int cb = 0; cb < nfull; ++cb) {
-        const int c = 64 * cb + 4 * j;
-        f32x4m oacc[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) oacc[u] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int qi = 0; qi < 4; ++qi) {
-          if (qi < 3) {
-#pragma unroll
-            for (int i = 0; i < NKT; ++i)
-              vq[(qi + 1) & 1][i] =
-                  *reinterpret_cast<const f32x4m*>(lv_s + vrow((qi + 1) * NKT + i) + c);
-          } else if (cb + 1 < nfull) {
-#pragma unroll
-            for (int i = 0; i < NKT; ++i)
-              vq[0][i] = *reinterpret_cast<const f32x4m*>(lv_s + vrow(i) + c + 64);
-          }
-          __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-          for (int i = 0; i < NKT; ++i) {
-            const int st = qi * NKT + i;
-            if (step_live(st)) {
-#pragma unroll
-              for (int u = 0; u < 4; ++u)
-                oacc[u] = mfma16x16x4(e[st], v_ok(st) ? vq[qi & 1][i][u] : 0.0f, oacc[u]);
-            }
-          }
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const f32x4m ov = {oacc[0][r], oacc[1][r], oacc[2][r], oacc[3][r]};
-          __builtin_amdgcn_raw_buffer_store_b128(
-              __builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, ov), ro,
-              orow + (r * dv + c) * 4, 0, 0);
-        }
-      }
-      for (int c0 = 64 * nfull; c0 < dv; c0 += 16) {
-        const int c = c0 + j;
-        const bool c_ok = c < dv;
-        f32x4m oa = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int i = 0; i < 4 * NKT; ++i) {
-          if (step_live(i)) {
-            const float x = lv_s[vrow(i) + (c_ok ? c : 0)];
-            oa = mfma16x16x4(e[i], (v_ok(i) & c_ok) ? x : 0.0f, oa);
-          }
-        }
-        float* orow_p = o + (b * lq + q0 + 4 * g) * static_cast<int64_t>(dv) + c;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          if ((q0 + 4 * g + r < lq) & c_ok)
-            __builtin_nontemporal_store(oa[r], orow_p + static_cast<int64_t>(r) * dv);
-        }
-      }
+// One workgroup of 8 wavefronts per CU in two teams of 4, with two 80 KiB
+// LDS buffers.  The workgroup's items n = 0, 1, ... go to team n % 2 and
+// buffer n % 2.  In phase n, team n % 2 computes item n while the other
+// team copies item n + 1 (K, V into LDS, Q into its registers) and waits
+// for it; a workgroup barrier ends the phase.  So each CU always has one
+// item's copies in flight beside another's matrix ops, one wavefront of
+// each team per SIMD.  Every wavefront passes the same barriers: one after
+// the first copy, one per phase.  The team that copies has raised priority
+// while it issues, as in k_attention_lds.
+template <int NKT, bool WIDE, int DC = 0>
+__global__ __launch_bounds__(512) void k_attention_pp(
+    const float* q, const float* k, const float* v, float* o, int64_t batch, int lq, int lk,
+    int d_in, int dv_in, float scale, Clip clip) {
+  const int d = DC ? DC : d_in;
+  const int dv = DC ? DC : dv_in;
+  constexpr int kBuf = kAttnLdsBytes / 4;  // floats per buffer
+  __shared__ __attribute__((aligned(16))) float lds[2 * kBuf];
+  const int lane = __lane_id();
+  const int j = lane & 15;
+  const int g = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int team = w >> 2;
+  const int wt = w & 3;
+  const int qblocks = (lq + 63) >> 6;
+  const int64_t items = batch * qblocks;
+  // Items of this workgroup: blockIdx.x + n gridDim.x (at least one).
+  const int64_t n_items = (items - 1 - blockIdx.x) / gridDim.x + 1;
+  if constexpr (DC != 0) {
+    for (int i = threadIdx.x; i < dv + 16; i += 512) {
+      lds[lk * (d + dv) + i] = 0.0f;
+      lds[kBuf + lk * (d + dv) + i] = 0.0f;
     }
-    __syncthreads();                             // LDS is free for the next item
+  }
+  f32x4m qf[kAttnQB];
+  auto where = [&](int64_t n, int64_t& b, int& q0, int& nq) {
+    const int64_t item = blockIdx.x + n * gridDim.x;
+    b = item / qblocks;
+    q0 = static_cast<int>(item - b * qblocks) * 64 + 16 * wt;
+    nq = q0 < lq ? (lq - q0 < 16 ? lq - q0 : 16) : 0;
+  };
+  auto stage = [&](int64_t n) {
+    int64_t b;
+    int q0, nq;
+    where(n, b, q0, nq);
+    float* base = lds + (n & 1) * kBuf;
+    __builtin_amdgcn_s_setprio(2);
+    attn_copy_kv(base, base + lk * d, k + b * lk * static_cast<int64_t>(d),
+                 v + b * lk * static_cast<int64_t>(dv), lk * d * 4, lk * dv * 4, wt, lane);
+    if (nq > 0) attn_load_q<DC>(qf, q, b, q0, nq, lq, d, j, g);
+    __builtin_amdgcn_s_setprio(0);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies and loads
+  };
+  if (team == 0) stage(0);
+  __syncthreads();
+  for (int64_t n = 0; n < n_items; ++n) {
+    if (team == (n & 1)) {
+      int64_t b;
+      int q0, nq;
+      where(n, b, q0, nq);
+      const float* base = lds + (n & 1) * kBuf;
+      if (nq > 0)
+        attn_compute<NKT, WIDE, DC>(base, base + lk * d, qf, o, b, q0, nq, lq, lk, d, dv, scale,
+                                    clip, j, g);
+    } else if (n + 1 < n_items) {
+      stage(n + 1);
+    }
+    __syncthreads();  // item n + 1 is in LDS; buffer n % 2 is free
   }
 }
 

@@ -94,7 +94,12 @@ def test_dam_workload():
 SHAPES = [(3, 50, 50, 200, 200), (2, 64, 64, 64, 64), (4, 16, 16, 16, 16), (5, 65, 17, 33, 7),
           (7, 3, 5, 8, 250), (2, 100, 64, 128, 16), (1, 1, 64, 1, 1), (1, 1, 1, 1, 1),
           (9, 48, 32, 20, 3), (2, 130, 49, 12, 70), (3, 7, 33, 300, 5),
-          (2, 40, 52, 64, 64), (3, 17, 35, 24, 40), (2, 33, 4, 16, 8)]
+          (2, 40, 52, 64, 64), (3, 17, 35, 24, 40), (2, 33, 4, 16, 8),
+          # the DAM tile with d = dv = 200 known at compile time (ping-pong
+          # schedule): 49 and 50 keys, one query, query blocks past 64, and
+          # more items than CUs (workgroups of 1, 2 and 3 items)
+          (5, 50, 49, 200, 200), (2, 1, 50, 200, 200), (3, 130, 50, 200, 200),
+          (4, 64, 49, 200, 200), (600, 50, 50, 200, 200), (300, 100, 49, 200, 200)]
 
 
 @pytest.mark.parametrize("b,lq,lk,d,dv", SHAPES)
@@ -160,6 +165,23 @@ def test_nonfinite_inputs():
     assert np.array_equal(np.isnan(got), np.isnan(want))
     assert np.array_equal(np.isinf(got), np.isinf(want))
     assert np.all(np.isnan(got[0, 3]))
+
+
+def test_nonfinite_inputs_dam_tile():
+    """The same on the DAM tile (50 keys, d = dv = 200): padding keys read a
+    zero row, and an inf in the first columns of a key row must not reach
+    the previous key's score through the masked last block of d."""
+    q, k, v = workloads.random_qkv(3, 50, 50, 200, 200, seed=31)
+    q[0, 7, 199] = np.nan
+    k[1, 12, 3] = np.inf
+    v[2, 49, 150] = -np.inf
+    got = run_attn(q, k, v, float(np.float32(1.0 / np.sqrt(200))))
+    want = oracle.attention_clipped(q, k, v, float(np.float32(1.0 / np.sqrt(200))))
+    assert np.array_equal(np.isnan(got), np.isnan(want))
+    assert np.array_equal(np.isinf(got), np.isinf(want))
+    fin = np.isfinite(want)
+    assert np.all(np.abs(got[fin] - want[fin]) <= 1e-4 * np.abs(want[fin]).max())
+    assert np.all(np.isnan(got[0, 7]))
 
 
 def test_deterministic_and_graph_replay():
