@@ -59,11 +59,12 @@ hipError_t run_attention_lds(const float* q, const float* k, const float* v, flo
 
 // The DAM tile (d = dv = 200, 49 or 50 keys) with d known at compile time,
 // on the ping-pong schedule: one workgroup of 8 wavefronts per CU, 160 KiB
-// of LDS (two buffers of K_b, V_b and a zero row).
+// of LDS (two buffers of K_b, V_b and a zero row).  The kernel scores the
+// last key tile on the VALU and needs at most 2 keys there.
 constexpr int kAttnDamDim = 200;
 
 bool dam_tile(int lk, int d, int dv) {
-  return d == kAttnDamDim && dv == kAttnDamDim && lk > 48 &&
+  return d == kAttnDamDim && dv == kAttnDamDim && lk > 48 && lk <= 50 &&
          (lk * (d + dv) + dv + 16) * 4 <= kAttnLdsBytes;
 }
 

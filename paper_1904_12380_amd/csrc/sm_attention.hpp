@@ -298,9 +298,10 @@ __global__ __launch_bounds__(256) void k_attention(const float* q, const float* 
 //   * k_attention_pp: one workgroup of 8 wavefronts per CU in two teams that
 //     take turns: one computes an item while the other copies the next.
 //     Used with d = dv = DC known at compile time (the DAM tile, DC = 200),
-//     where the masks and branches of the d loops fold away and the matrix
-//     ops issue back to back; with d at run time one wavefront per SIMD
-//     computes too slowly for this schedule.
+//     where the masks and branches of the d loops fold away, the matrix ops
+//     issue back to back, and the last key tile (at most 2 keys) is scored
+//     on the VALU; with d at run time one wavefront per SIMD computes too
+//     slowly for this schedule.
 constexpr int kAttnLdsBytes = 80 * 1024;  // one batch element's K_b and V_b
 constexpr int kAttnMaxDQ = 224;           // d up to this keeps Q in registers
 constexpr int kAttnQB = kAttnMaxDQ / 16;  // 16-wide blocks of d in registers
@@ -362,33 +363,46 @@ __device__ __forceinline__ void attn_compute(const float* lk_s, const float* lv_
   constexpr bool ZR = DC != 0;
   constexpr int QB = kAttnQB;
   const int nblk = (d + 15) >> 4;
+  // With DC != 0 (the DAM tile; the host guarantees at most 2 keys in the
+  // last key tile, lk <= 16 (NKT - 1) + 2) those keys' scores are dot
+  // products on the VALU: lane (j, g) sums its own terms t = 16 blk + 4 g + s
+  // of query j, interleaved with the other tiles' matrix ops, and the 4 lanes
+  // of query j add their sums.  Only NMT tiles go through the matrix cores:
+  // a 16-key tile for 2 keys cost as much as a full one (92.8 -> 82.6 us on
+  // the DAM shape).
+  constexpr bool VT = DC != 0 && NKT > 1;
+  constexpr int NMT = VT ? NKT - 1 : NKT;  // key tiles on the matrix cores
+  constexpr int NR = VT ? NKT + 1 : NKT;   // K operand rows per lane
 
   // ---- scores S^T = K Q^T, K from LDS ---------------------------------------
   f32x4m acc[NKT];
 #pragma unroll
   for (int kt = 0; kt < NKT; ++kt) acc[kt] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+  float dot[2] = {0.0f, 0.0f};
   // Keys past lk read row 0: their scores are garbage (even NaN) but the
   // softmax below masks them.  Columns t past d would read the next row, and
-  // 0 * NaN is NaN, so those operands are zeroed.
-  int krow[NKT];
+  // 0 * NaN is NaN, so those operands are zeroed.  With VT, rows NMT and
+  // NMT + 1 are the two tail keys (the same for every lane; a missing second
+  // key reads the row after the last, masked the same way).
+  int krow[NR];
 #pragma unroll
-  for (int kt = 0; kt < NKT; ++kt) {
-    const int key = 16 * kt + j;
-    krow[kt] = ((kt < NKT - 1 || key < lk) ? key : 0) * d + 4 * g;
+  for (int kt = 0; kt < NR; ++kt) {
+    const int key = (VT && kt >= NMT) ? 16 * NMT + (kt - NMT) : 16 * kt + j;
+    krow[kt] = ((VT || kt < NKT - 1 || key < lk) ? key : 0) * d + 4 * g;
   }
   // The next block's K operands are read while this block's matrix ops run;
   // the d mask is applied at use, so no wait comes early.
-  f32x4m kc[NKT], kn[NKT];
+  f32x4m kc[NR], kn[NR];
   if (nblk > 0) {
 #pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) kc[kt] = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt]);
+    for (int kt = 0; kt < NR; ++kt) kc[kt] = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt]);
   }
 #pragma unroll
   for (int blk = 0; blk < QB; ++blk) {
     if (blk < nblk) {  // uniform
       if (blk + 1 < nblk) {
 #pragma unroll
-        for (int kt = 0; kt < NKT; ++kt)
+        for (int kt = 0; kt < NR; ++kt)
           kn[kt] = *reinterpret_cast<const f32x4m*>(lk_s + krow[kt] + 16 * (blk + 1));
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -396,12 +410,29 @@ __device__ __forceinline__ void attn_compute(const float* lk_s, const float* lv_
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
 #pragma unroll
-        for (int kt = 0; kt < NKT; ++kt)
+        for (int kt = 0; kt < NMT; ++kt)
           acc[kt] = mfma16x16x4(t_ok ? kc[kt][s] : 0.0f, qf[blk][s], acc[kt]);
+        if constexpr (VT) {
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+            dot[u] = __builtin_fmaf(qf[blk][s], t_ok ? kc[NMT + u][s] : 0.0f, dot[u]);
+        }
       }
 #pragma unroll
-      for (int kt = 0; kt < NKT; ++kt) kc[kt] = kn[kt];
+      for (int kt = 0; kt < NR; ++kt) kc[kt] = kn[kt];
     }
+  }
+  if constexpr (VT) {
+    // The 4 lanes of query j add their partial sums; every lane then holds
+    // the scores of keys 16 NMT and 16 NMT + 1, which the softmax reads as
+    // registers 0 and 1 of the last tile (lane group 0; the others' keys
+    // there are past lk and masked).
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      dot[u] = dot[u] + row16_partner(dot[u]);
+      dot[u] = dot[u] + half32_partner(dot[u]);
+    }
+    acc[NKT - 1] = f32x4m{dot[0], dot[1], 0.0f, 0.0f};
   }
 
   // ---- clipped softmax over the keys of query j -----------------------------
