@@ -442,7 +442,7 @@ __device__ __forceinline__ void attn_compute(const float* lk_s, const float* lv_
   for (int kt = 0; kt < NKT; ++kt) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
+      const bool key_ok = kt < NKT - 1 || (!(VT && r >= 2) && 16 * kt + 4 * g + r < lk);
       const float sv = acc[kt][r] * scale;
       e[4 * kt + r] = sv;
       m = key_ok ? fmaxf(m, sv) : m;
@@ -455,7 +455,9 @@ __device__ __forceinline__ void attn_compute(const float* lk_s, const float* lv_
   for (int kt = 0; kt < NKT; ++kt) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
+      // With VT, registers 2 and 3 of the last tile hold no key (lk <= 16 NMT
+      // + 2): their exponentials are not computed.
+      const bool key_ok = kt < NKT - 1 || (!(VT && r >= 2) && 16 * kt + 4 * g + r < lk);
       const float ev = exp_shift_clip<WIDE ? kExpWide : kExpAccurate>(e[4 * kt + r], rs);
       e[4 * kt + r] = key_ok ? ev : 0.0f;
     }
