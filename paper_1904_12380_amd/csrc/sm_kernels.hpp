@@ -736,8 +736,13 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y,
 //
 // U = 2, one workgroup per block of rows: per 64 MiB of logits on 4 to 256
 // columns this ran 23.4-23.9 us, against 23.7-25.4 us with U = 4 and
-// 25.4-26.8 us with U = 8 (81 VGPRs, five wavefronts per SIMD); a grid
-// capped at the resident workgroups gained nothing.  The LDS-staged packed
+// 25.4-26.8 us with U = 8 (81 VGPRs, five wavefronts per SIMD).  A
+// workgroup may loop over several row blocks (grid stride), loading the
+// next block before it reduces the current one; the host caps the grid at
+// the resident workgroups only when one workgroup per block would take at
+// most two rounds of them (22 MiB on 4 to 256 columns: 8.9-9.4 us against
+// 10.0-10.3 us with a second, mostly empty round; at 64 and 128 MiB the
+// capped grid was 3-15% slower than one workgroup per block).  The LDS-staged packed
 // kernel took 24.2-24.5 us on 4 and 64 columns and 35.3 us on 16 (its
 // lanes read LDS rows at a stride of 16 words: bank conflicts), and one
 // wavefront per row 42.5 us on 100 columns (25 of 64 lanes busy).
@@ -756,15 +761,21 @@ __global__ __launch_bounds__(256) void k_group_rows(const float* x, float* y, in
   const int j = lane % G;
   const bool col_ok = 4 * j < cols;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * 4 * kWaveRows;
-  for (int64_t r0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * kWaveRows; r0 < rows;
-       r0 += stride) {
-    f32x4 q[U];
+  auto load = [&](f32x4 (&q)[U], int64_t r0) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t row = r0 + u * R + rho;
       q[u] = f32x4{kNegInf, kNegInf, kNegInf, kNegInf};
       if (col_ok && row < rows) q[u] = ld_stream(x + row * cols + 4 * j);
     }
+  };
+  int64_t r0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * kWaveRows;
+  f32x4 q[U];
+  load(q, r0);
+  for (; r0 < rows; r0 += stride) {
+    // The next step's loads are issued before this step's rows are reduced.
+    f32x4 qn[U];
+    load(qn, r0 + stride);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t row = r0 + u * R + rho;
@@ -776,6 +787,8 @@ __global__ __launch_bounds__(256) void k_group_rows(const float* x, float* y, in
       const f32x4 out = {e[0] * rcp, e[1] * rcp, e[2] * rcp, e[3] * rcp};
       if (col_ok && row < rows) st_stream(y + row * cols + 4 * j, out);
     }
+#pragma unroll
+    for (int u = 0; u < U; ++u) q[u] = qn[u];
   }
 }
 

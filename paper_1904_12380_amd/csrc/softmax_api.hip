@@ -52,9 +52,13 @@ constexpr int kBlockThreads = 1024;
 // columns 25.4 against 25.3.  Log and NLL rows keep k_block_row up to
 // kBlockRowMaxCols.
 constexpr int64_t kSplitMinColsProb = 8192;
-// k_group_rows: grid capped at the workgroups resident at once (each loops
-// over row blocks) rather than one workgroup per row block.
-constexpr bool kGroupRowsPersistent = false;
+// k_group_rows: when one workgroup per row block would take more than one
+// but at most this many rounds of the resident workgroups, the grid is
+// capped at the resident ones (each loops over row blocks, loading the next
+// block before reducing the current one): a last round that leaves most of
+// the chip idle costs more than the loop.  Above it, one workgroup per row
+// block keeps more loads in flight.
+constexpr int64_t kGroupRowsPersistentRounds = 2;
 
 // Split rows, one pass: a row spans at most this many workgroups (the
 // exchange is read by one wavefront, one slot per lane).  Chunk shapes,
@@ -581,8 +585,9 @@ int make_plan(const Shape& s, int64_t rows, int64_t cols, int em, int dev,
   int64_t launch_read_bytes = 0;
   switch (s.kernel) {
     case SOFTMAX_KERNEL_GROUP_ROWS:
-      p.grid = std::min(ceil_div(rows, int64_t(4) * kGroupRowsU * (64 / s.g)),
-                        kGroupRowsPersistent ? resident : kMaxGrid);
+      p.grid = ceil_div(rows, int64_t(4) * kGroupRowsU * (64 / s.g));
+      if (p.grid <= kGroupRowsPersistentRounds * resident) p.grid = std::min(p.grid, resident);
+      p.grid = std::min(p.grid, kMaxGrid);
       p.rows_per_launch = rows;
       p.launches = 1;
       break;
