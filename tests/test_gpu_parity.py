@@ -116,6 +116,31 @@ def test_group_rows(rows, cols):
         check_parity(x, run_gpu(x), f"group rows {rows}x{cols} {kind}")
 
 
+@pytest.mark.parametrize("cols", [4, 16, 100, 256])
+def test_group_rows_looping_grid(cols):
+    """Launches that one workgroup per row block would spread over one to two
+    rounds of the resident workgroups: the grid is capped at the resident
+    ones, each loops over row blocks with the next block's loads in flight,
+    and the last block is ragged.  The row count is chosen from the plan, so
+    the test does not assume the device's occupancy."""
+    g = max(1, 1 << (cols // 4 - 1).bit_length())
+    per_wg = 4 * 2 * (64 // g)          # 4 wavefronts x 2 row groups x 64/G rows
+    chosen = None
+    for resident in (1024, 2048, 4096):
+        rows = per_wg * (3 * resident // 2) + 7
+        p = sm.softmax_plan(rows, cols)
+        needed = -(-rows // per_wg)
+        if p["kernel_name"] == "group_rows" and p["grid"] < needed:
+            chosen = (rows, p, needed)
+            break
+    assert chosen is not None, "no row count took the capped grid"
+    rows, p, needed = chosen
+    assert needed <= 2 * p["grid"]
+    log(f"[parity] group rows looping {rows}x{cols}, grid {p['grid']} of {needed} blocks")
+    x = workloads.random_logits(rows, cols, seed=rows + cols, kind="clip_heavy")
+    check_parity(x, run_gpu(x), f"group rows looping {rows}x{cols}")
+
+
 @pytest.mark.parametrize("rows,cols", [(257, 50), (64, 1000), (33, 1001), (5, 8192), (3, 100003),
                                        (131, 7), (257, 130), (99, 3001)])
 def test_misaligned_views(rows, cols):
