@@ -276,44 +276,18 @@ __device__ __forceinline__ void load_strip_whole(float (&v)[4 * V], const float*
 // 16-byte aligned matrix.  Lane strip j is the aligned float4 at
 // p - a + 4 * (lane_off + stride * j), holding segment columns c0 .. c0 + 3
 // with c0 = 4 * (lane_off + stride * j) - a; element 4 j + k of v is column
-// c0 + k.  A strip wholly inside [0, lim) is one 128-bit access.  A strip
-// that straddles either end of the segment touches only its columns inside
-// it, with 32-bit accesses, so nothing of a neighbouring row is read or
-// written (in-place calls stay safe); columns outside read as -inf.  The
-// strips must cover lim + a columns.
+// c0 + k.  The strips must cover lim + a columns.  Every strip that holds a
+// column of the segment is one 128-bit load, and columns outside [0, lim)
+// are replaced by -inf after the load.  A straddling strip therefore also
+// reads up to 3 floats of the neighbouring row, or, at the end of the
+// matrix, up to 12 bytes past it inside the same 16-byte block, which lies
+// in the same memory page as the row's last column; those values are never
+// used.  (Element-wise loads in the straddling strips measured 1.5-10%
+// slower on rows of 2049 to 8189 columns, from the extra instructions and
+// divergence, and cost the split kernels 5-13 spilled VGPRs.)
 template <int V>
 __device__ __forceinline__ void load_strip_ph(float (&v)[4 * V], const float* p, int a,
                                               int lane_off, int stride, int lim) {
-#pragma unroll
-  for (int j = 0; j < V; ++j) {
-    const int c0 = 4 * (lane_off + stride * j) - a;
-    if (c0 >= 0 && c0 + 4 <= lim) {
-      const f32x4 q = ld_stream(p + c0);
-      v[4 * j + 0] = q.x;
-      v[4 * j + 1] = q.y;
-      v[4 * j + 2] = q.z;
-      v[4 * j + 3] = q.w;
-    } else {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int c = c0 + k;
-        v[4 * j + k] = (c >= 0 && c < lim) ? __builtin_nontemporal_load(p + c) : kNegInf;
-      }
-    }
-  }
-}
-
-// The loads of load_strip_ph with fewer registers, for the split kernels:
-// every strip that holds a column of the segment is one 128-bit load, and
-// columns outside [0, lim) are replaced by -inf after the load.  A
-// straddling strip therefore also reads up to 3 floats of the neighbouring
-// row, or, at the end of the matrix, up to 12 bytes past it inside the same
-// 16-byte block, which lies in the same memory page as the row's last
-// column; those values are never used.  (Stores stay element by element in
-// straddling strips: store_strip_ph.)
-template <int V>
-__device__ __forceinline__ void load_strip_ph_wide(float (&v)[4 * V], const float* p, int a,
-                                                   int lane_off, int stride, int lim) {
 #pragma unroll
   for (int j = 0; j < V; ++j) {
     const int c0 = 4 * (lane_off + stride * j) - a;
@@ -327,6 +301,10 @@ __device__ __forceinline__ void load_strip_ph_wide(float (&v)[4 * V], const floa
 }
 
 // Stores out(v[i]) for the columns of the segment, strips as load_strip_ph.
+// A strip wholly inside [0, lim) is one 128-bit store; a strip that
+// straddles either end of the segment writes only its columns inside it,
+// with 32-bit stores, so nothing of a neighbouring row is written (in-place
+// calls and other rows' outputs stay intact).
 template <int V, typename F>
 __device__ __forceinline__ void store_strip_ph(const float (&v)[4 * V], F out, float* p, int a,
                                                int lane_off, int stride, int lim) {
@@ -422,7 +400,7 @@ __device__ __forceinline__ float2 segment_online(float (&v)[4 * V],
     load_strip_whole<V, VEC4>(v, p, lane_off, stride);
     ms = lane_online_exp<MODE>(v, mk, clip);
   } else if constexpr (PH) {
-    load_strip_ph_wide<V>(v, p, a, opaque(lane_off), stride, lim);
+    load_strip_ph<V>(v, p, a, opaque(lane_off), stride, lim);
     ms = lane_online_exp<MODE>(v, mk, clip);
   } else {
     load_strip<V, VEC4>(v, p, opaque(lane_off), stride, lim);
