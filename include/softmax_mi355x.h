@@ -77,7 +77,16 @@ extern "C" {
 #define SOFTMAX_KERNEL_GROUP_ROWS 5 /* cols <= 256 in whole 16-byte strips
                                        (cols % 4 == 0, 16-byte aligned x and
                                        y), probability outputs: G lanes per
-                                       row, several rows per wavefront */
+                                       row (G the power of two >= cols / 4),
+                                       several rows per wavefront.  Past
+                                       about one round of the device's
+                                       resident workgroups, rows that fill
+                                       less than 3/4 of the G lanes take
+                                       PACKED instead, and so do rows of
+                                       more than 64 columns, or that fill
+                                       their lanes in part, while the grid
+                                       takes one to 2.5 rounds (the choice
+                                       depends on rows and the device) */
 
 /*
  * softmax_fwd -- row-wise clipped softmax, fp32 in and out.
@@ -320,10 +329,12 @@ typedef struct softmax_plan_t {
 } softmax_plan_t;
 
 /* The shape fields (kernel, vec_width, lanes_per_row, elems_per_lane,
- * block_threads, chunks_per_row) depend only on the arguments; grid,
- * launches and store_delay_ns are those for the current device, and 0 when
- * no device is present.  No launch, no allocation (the first call on a
- * device queries its attributes). */
+ * block_threads, chunks_per_row) depend only on the arguments, except that
+ * rows of at most 256 columns choose between GROUP_ROWS and PACKED by the
+ * device's resident workgroups too; grid, launches and store_delay_ns are
+ * those for the current device, and 0 when no device is present (then the
+ * kernel is the choice made from the arguments alone).  No launch, no
+ * allocation (the first call on a device queries its attributes). */
 SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64_t cols,
                              softmax_plan_t* plan);
 

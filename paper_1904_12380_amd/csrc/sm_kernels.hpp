@@ -712,20 +712,24 @@ __global__ __launch_bounds__(256) void k_packed(const float* x, float* y,
 // U such row groups in flight (U * 1 KiB of loads).  Lanes past the row's
 // strips read -inf (a clipped term, as in load_strip).
 //
-// U = 2, one workgroup per block of rows: per 64 MiB of logits on 4 to 256
-// columns this ran 23.4-23.9 us, against 23.7-25.4 us with U = 4 and
-// 25.4-26.8 us with U = 8 (81 VGPRs, five wavefronts per SIMD).  A
-// workgroup may loop over several row blocks (grid stride), loading the
-// next block before it reduces the current one; the host caps the grid at
-// the resident workgroups only when one workgroup per block would take at
-// most two rounds of them (22 MiB on 4 to 256 columns: 8.9-9.4 us against
-// 10.0-10.3 us with a second, mostly empty round; at 64 and 128 MiB the
-// capped grid was 3-15% slower than one workgroup per block).  The LDS-staged packed
-// kernel took 24.2-24.5 us on 4 and 64 columns and 35.3 us on 16 (its
-// lanes read LDS rows at a stride of 16 words: bank conflicts), and one
-// wavefront per row 42.5 us on 100 columns (25 of 64 lanes busy).
+// U is 1 or 2, chosen per call by the host.  U = 2, one workgroup per
+// block of rows: per 64 MiB of logits on 4 to 256 columns this ran
+// 23.4-23.9 us, against 23.7-25.4 us with U = 4 and 25.4-26.8 us with U = 8
+// (81 VGPRs, five wavefronts per SIMD).  U = 1 pays when the launch is small
+// enough that U = 2 would leave resident workgroup slots empty: at 2 to
+// 8 MiB on 16 to 256 columns it ran 3-12% faster than U = 2, and at 64 MiB
+// up to 9% slower.  A workgroup may loop over several row blocks (grid
+// stride), loading the next block before it reduces the current one; the
+// host caps the grid at the resident workgroups only when one workgroup per
+// block would take more than one and at most two rounds of them (22 MiB on
+// 4 to 256 columns: 8.9-9.4 us against 10.0-10.3 us with a second, mostly
+// empty round; at 64 and 128 MiB the capped grid was 3-15% slower than one
+// workgroup per block).  The LDS-staged packed kernel took 24.2-24.5 us on
+// 4 and 64 columns and 35.3 us on 16 (its lanes read LDS rows at a stride
+// of 16 words: bank conflicts), and one wavefront per row 42.5 us on 100
+// columns (25 of 64 lanes busy).  Rows that leave many of their G lanes
+// idle go to the packed kernel instead (host dispatch).
 constexpr int kGroupRowsMaxCols = 256;
-constexpr int kGroupRowsU = 2;
 
 template <int G, int U, int MODE>
 __global__ __launch_bounds__(256) void k_group_rows(const float* x, float* y, int64_t rows,

@@ -59,6 +59,34 @@ constexpr int64_t kSplitMinColsProb = 8192;
 // the chip idle costs more than the loop.  Above it, one workgroup per row
 // block keeps more loads in flight.
 constexpr int64_t kGroupRowsPersistentRounds = 2;
+// Rows of at most 256 columns in whole strips: the grouped-rows kernel or
+// the LDS-staged packed kernel (library_shape), by the rounds of resident
+// workgroups one grouped-rows workgroup per row block would take and by the
+// fill, the share of a row's G lanes that hold a strip.  Measured on 4 to
+// 256 columns at 2 to 64 MiB:
+//  * at most kGroupRowsOneStep rounds at U = 1 (a small launch): grouped
+//    rows with U = 1 at any fill; at 2 to 8 MiB U = 1 ran 3-12% faster than
+//    U = 2, and at 3 MiB 3-21% faster than the packed kernel on rows of
+//    fill 0.52-0.69;
+//  * beyond that, fill below 3/4 (36-44, 68-92 and 132-188 columns): the
+//    packed kernel, faster by up to 35% at every size from 8 MiB on, except
+//    on some rows at 40 MiB and above, where it was up to 4% slower;
+//  * fill below 1, or G >= 32 (rows of more than 64 columns), at more than
+//    one and at most kGroupRowsPackedRounds = 2.5 rounds at U = 2: the
+//    packed kernel, level to 18% faster on rows of fill 3/4 to 1 (12 to
+//    244 columns) at 1.0-2.5 rounds, and on 128 and 256 columns from 1%
+//    slower to 6% faster; from about 2.75 rounds (40 and 48 MiB) it ranged
+//    from 5% faster to 8% slower, and at 4-5 rounds (64 MiB) it was 1-6%
+//    slower.
+//    Full rows of at most 64 columns keep grouped rows (at 22 MiB 17-44%
+//    faster than packed, whose LDS tiles of 16 and 32 columns take bank
+//    conflicts).
+constexpr int64_t kGroupRowsMinFillNum = 3;
+constexpr int64_t kGroupRowsMinFillDen = 4;
+constexpr int64_t kGroupRowsPackedRoundsNum = 5;  // kGroupRowsPackedRounds = 2.5
+constexpr int64_t kGroupRowsPackedRoundsDen = 2;
+constexpr int64_t kGroupRowsOneStepNum = 13;  // kGroupRowsOneStep = 1.3 rounds
+constexpr int64_t kGroupRowsOneStepDen = 10;
 
 // Split rows, one pass: a row spans at most this many workgroups (the
 // exchange is read by one wavefront, one slot per lane).  Chunk shapes,
@@ -228,22 +256,31 @@ const void* packed_fn(int epl, std::integer_sequence<int, E...>) {
   return (idx >= 0 && idx < static_cast<int>(sizeof...(E))) ? table[idx] : nullptr;
 }
 
+// k_group_rows instances: G = 1, 2, ..., 64 lanes per row, U = 1 or 2 row
+// groups per wavefront step.
+template <int U, int EM>
+const void* group_rows_fn(int g) {
+  auto cast = [](auto f) { return reinterpret_cast<const void*>(f); };
+  switch (g) {
+    case 1: return cast(&k_group_rows<1, U, EM>);
+    case 2: return cast(&k_group_rows<2, U, EM>);
+    case 4: return cast(&k_group_rows<4, U, EM>);
+    case 8: return cast(&k_group_rows<8, U, EM>);
+    case 16: return cast(&k_group_rows<16, U, EM>);
+    case 32: return cast(&k_group_rows<32, U, EM>);
+    case 64: return cast(&k_group_rows<64, U, EM>);
+    default: return nullptr;
+  }
+}
+
 template <int EM, bool VEC4>
 const void* shape_fn(const Shape& s, bool stats_pass) {
   auto cast = [](auto f) { return reinterpret_cast<const void*>(f); };
   switch (s.kernel) {
     case SOFTMAX_KERNEL_GROUP_ROWS:
       if constexpr (VEC4 && (EM == kExpAccurate || EM == kExpWide || EM == kExpFast)) {
-        switch (s.g) {
-          case 1: return cast(&k_group_rows<1, kGroupRowsU, EM>);
-          case 2: return cast(&k_group_rows<2, kGroupRowsU, EM>);
-          case 4: return cast(&k_group_rows<4, kGroupRowsU, EM>);
-          case 8: return cast(&k_group_rows<8, kGroupRowsU, EM>);
-          case 16: return cast(&k_group_rows<16, kGroupRowsU, EM>);
-          case 32: return cast(&k_group_rows<32, kGroupRowsU, EM>);
-          case 64: return cast(&k_group_rows<64, kGroupRowsU, EM>);
-          default: return nullptr;
-        }
+        if (s.v == 1) return group_rows_fn<1, EM>(s.g);
+        if (s.v == 2) return group_rows_fn<2, EM>(s.g);
       }
       return nullptr;
     case SOFTMAX_KERNEL_PACKED:
@@ -354,6 +391,12 @@ inline int packed_lanes(int64_t cols) {
   return cols <= 16 ? 1 : cols <= 32 ? 2 : cols <= 64 ? 4 : cols <= 128 ? 8 : 16;
 }
 
+// Lanes per row of the grouped-rows kernel: one 16-byte strip per lane, a
+// power of two.
+inline int group_rows_lanes(int64_t cols) {
+  return static_cast<int>(pow2_at_least(ceil_div(cols, 4)));
+}
+
 // Whether kernel family `kernel` may use 128-bit access: both pointers
 // 16-byte aligned and, except for packed rows (which move whole tiles of a
 // multiple of four rows), rows made of whole float4s.
@@ -410,7 +453,8 @@ void phase_row_shape(int64_t cols, Shape* s) {
   }
 }
 
-// The library's shape for a call (mode em).
+// The library's shape for a call (mode em) from the arguments alone;
+// library_shape refines it for short rows by the row count and the device.
 Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
   Shape s;
   const bool prob = em != kLogOut && em != kNllOut;
@@ -420,7 +464,8 @@ Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
     s.kernel = SOFTMAX_KERNEL_GROUP_ROWS;
     s.vec4 = true;
     s.threads = 256;
-    s.g = static_cast<int>(pow2_at_least(ceil_div(cols, 4)));
+    s.g = group_rows_lanes(cols);
+    s.v = 2;
   } else if (cols <= (prob ? kPackedProbMaxCols : kPackedMaxCols)) {
     // G lanes per row with at most 16 columns per lane.
     s.kernel = SOFTMAX_KERNEL_PACKED;
@@ -516,7 +561,8 @@ bool requested_shape(const softmax_plan_t& want, const float* x, const float* y,
     case SOFTMAX_KERNEL_GROUP_ROWS:
       if (cols > kGroupRowsMaxCols || !s.vec4) return false;
       s.threads = 256;
-      s.g = static_cast<int>(pow2_at_least(ceil_div(cols, 4)));
+      s.g = group_rows_lanes(cols);
+      s.v = 2;
       break;
     case SOFTMAX_KERNEL_PACKED:
       if (cols > ((em == kLogOut || em == kNllOut) ? kPackedMaxCols : kPackedProbMaxCols))
@@ -570,12 +616,77 @@ uint32_t ns_to_ticks(int64_t ns, const DeviceFacts& f) {
   return static_cast<uint32_t>(std::min<int64_t>(t, UINT32_MAX));
 }
 
+// Rows per k_group_rows workgroup and step: four wavefronts, each U row
+// groups of 64 / G rows.
+inline int64_t group_rows_block(const Shape& s) { return int64_t(4) * s.v * (64 / s.g); }
+
+// Resident workgroups of the kernel for shape s on device dev.
+int resident_workgroups(const Shape& s, int em, int dev, const DeviceFacts& f, int64_t* out) {
+  const void* fn = kernel_fn(s, em);
+  if (fn == nullptr) return SOFTMAX_ERR_INVALID_ARG;
+  int per_cu = 0;
+  const int rc = blocks_per_cu(dev, fn, s.threads, &per_cu);
+  *out = int64_t(per_cu) * f.cus;
+  return rc;
+}
+
+// Row groups per wavefront step (s->v) of a grouped-rows shape: 1 when one
+// workgroup per row block at U = 1 takes at most kGroupRowsOneStep rounds
+// of the resident workgroups, else 2.
+int group_rows_steps(int64_t rows, int em, int dev, const DeviceFacts& f, Shape* s) {
+  Shape one = *s;
+  one.v = 1;
+  int64_t resident = 0;
+  const int rc = resident_workgroups(one, em, dev, f, &resident);
+  if (rc != SOFTMAX_OK) return rc;
+  s->v = ceil_div(rows, group_rows_block(one)) * kGroupRowsOneStepDen <=
+                 resident * kGroupRowsOneStepNum
+             ? 1
+             : 2;
+  return SOFTMAX_OK;
+}
+
+// The library's shape once rows and the device are known: rows of at most
+// 256 columns in whole strips take the grouped-rows kernel or the packed
+// kernel by the rules measured above (kGroupRowsMinFill, kGroupRowsOneStep
+// and kGroupRowsPackedRounds).
+int library_shape(const float* x, const float* y, int64_t rows, int64_t cols, int em, int dev,
+                  const DeviceFacts& f, Shape* out) {
+  Shape s = default_shape(x, y, cols, em);
+  if (s.kernel == SOFTMAX_KERNEL_GROUP_ROWS) {
+    Shape steps = s;
+    int rc = group_rows_steps(rows, em, dev, f, &steps);  // steps.v == 1: a small launch
+    int64_t resident = 0;                                // at U = 2
+    if (rc == SOFTMAX_OK) rc = resident_workgroups(s, em, dev, f, &resident);
+    if (rc != SOFTMAX_OK) return rc;
+    const int64_t strips = ceil_div(cols, 4);
+    const int64_t blocks = ceil_div(rows, group_rows_block(s));
+    const bool sparse = strips * kGroupRowsMinFillDen < s.g * kGroupRowsMinFillNum;
+    const bool mid = (strips < s.g || s.g >= 32) && blocks > resident &&
+                     blocks * kGroupRowsPackedRoundsDen <= kGroupRowsPackedRoundsNum * resident;
+    if (steps.v == 2 && (sparse || mid)) {
+      s.kernel = SOFTMAX_KERNEL_PACKED;
+      s.vec4 = can_vec4(SOFTMAX_KERNEL_PACKED, x, y, cols);
+      s.threads = 256;
+      s.v = 0;
+      s.g = packed_lanes(cols);
+      s.epl = static_cast<int>(ceil_div(cols, s.g));
+    }
+  }
+  *out = s;
+  return SOFTMAX_OK;
+}
+
 // delay_req: -1 for the library's schedule, else the delay itself in ns.
 int make_plan(const Shape& s, int64_t rows, int64_t cols, int em, int dev,
               const DeviceFacts& f, int64_t delay_req, Plan* out) {
   Plan p;
   p.shape = s;
-  const void* fn = kernel_fn(s, em);
+  if (s.kernel == SOFTMAX_KERNEL_GROUP_ROWS) {
+    const int rc = group_rows_steps(rows, em, dev, f, &p.shape);
+    if (rc != SOFTMAX_OK) return rc;
+  }
+  const void* fn = kernel_fn(p.shape, em);
   if (fn == nullptr) return SOFTMAX_ERR_INVALID_ARG;
   int per_cu = 0;
   int rc = blocks_per_cu(dev, fn, s.threads, &per_cu);
@@ -585,7 +696,7 @@ int make_plan(const Shape& s, int64_t rows, int64_t cols, int em, int dev,
   int64_t launch_read_bytes = 0;
   switch (s.kernel) {
     case SOFTMAX_KERNEL_GROUP_ROWS:
-      p.grid = ceil_div(rows, int64_t(4) * kGroupRowsU * (64 / s.g));
+      p.grid = ceil_div(rows, group_rows_block(p.shape));
       if (p.grid <= kGroupRowsPersistentRounds * resident) p.grid = std::min(p.grid, resident);
       p.grid = std::min(p.grid, kMaxGrid);
       p.rows_per_launch = rows;
@@ -783,7 +894,8 @@ int softmax_rows(const float* x, float* y, int64_t rows, int64_t cols, Clip c, i
   if (rc != SOFTMAX_OK) return rc;
   DeviceFacts f;
   if ((rc = device_facts(dev, &f)) != SOFTMAX_OK) return rc;
-  if (want == nullptr) s = default_shape(x, y, cols, em);
+  if (want == nullptr && (rc = library_shape(x, y, rows, cols, em, dev, f, &s)) != SOFTMAX_OK)
+    return rc;
   Plan p;
   rc = make_plan(s, rows, cols, em, dev, f, want ? want->store_delay_ns : -1, &p);
   if (rc != SOFTMAX_OK) return rc;
@@ -807,7 +919,6 @@ SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64
   }
   if (x == nullptr || y == nullptr) return SOFTMAX_ERR_INVALID_ARG;
   if (partial_overlap(x, y, rows * cols * 4)) return SOFTMAX_ERR_INVALID_ARG;
-  const Shape s = default_shape(x, y, cols, kExpAccurate);
   // The launch geometry needs the current device; without one only the
   // device-independent fields are filled in.
   int ndev = 0;
@@ -816,12 +927,16 @@ SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64
   if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0 || hipGetDevice(&dev) != hipSuccess ||
       device_facts(dev, &f) != SOFTMAX_OK) {
     (void)hipGetLastError();
+    const Shape s = default_shape(x, y, cols, kExpAccurate);
     Plan p;
     p.shape = s;
     if (s.kernel == SOFTMAX_KERNEL_SPLIT_ROW) p.chunks = row_chunks(s, cols);
     *plan = public_plan(p, rows);
     return SOFTMAX_OK;
   }
+  Shape s;
+  rc = library_shape(x, y, rows, cols, kExpAccurate, dev, f, &s);
+  if (rc != SOFTMAX_OK) return rc;
   Plan p;
   rc = make_plan(s, rows, cols, kExpAccurate, dev, f, -1, &p);
   if (rc != SOFTMAX_OK) return rc;

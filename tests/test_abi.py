@@ -90,6 +90,8 @@ def test_cpu_tensor_is_rejected():
     (300, 4, "group_rows", 4, dict(lanes_per_row=1, elems_per_lane=4)),
     (300, 100, "group_rows", 4, dict(lanes_per_row=32, elems_per_lane=4)),
     (300, 256, "group_rows", 4, dict(lanes_per_row=64, elems_per_lane=4)),
+    (300, 36, "group_rows", 4, dict(lanes_per_row=16, elems_per_lane=4)),
+    (300, 188, "group_rows", 4, dict(lanes_per_row=64, elems_per_lane=4)),
     (300, 260, "wave_row", 4, dict(elems_per_lane=8)),
     (300, 102, "packed", 4, dict(lanes_per_row=8, elems_per_lane=13)),
     (300, 250, "packed", 4, dict(lanes_per_row=16, elems_per_lane=16)),

@@ -116,21 +116,24 @@ def test_group_rows(rows, cols):
         check_parity(x, run_gpu(x), f"group rows {rows}x{cols} {kind}")
 
 
-@pytest.mark.parametrize("cols", [4, 16, 100, 256])
-def test_group_rows_looping_grid(cols):
+@pytest.mark.parametrize("cols,steps,rounds", [(4, 2, 1.5), (16, 2, 1.5), (32, 2, 1.5), (64, 2, 1.5),
+                                               (128, 1, 1.125), (256, 1, 1.125), (16, 1, 1.125)])
+def test_group_rows_looping_grid(cols, steps, rounds):
     """Launches that one workgroup per row block would spread over one to two
     rounds of the resident workgroups: the grid is capped at the resident
     ones, each loops over row blocks with the next block's loads in flight,
-    and the last block is ragged.  The row count is chosen from the plan, so
-    the test does not assume the device's occupancy."""
+    and the last block is ragged.  steps = 2 row groups per wavefront step
+    (1.5 rounds of blocks), steps = 1 (1.125 rounds at one row group per
+    step, which the library runs with one).  The row count is chosen from
+    the plan, so the test does not assume the device's occupancy."""
     g = max(1, 1 << (cols // 4 - 1).bit_length())
-    per_wg = 4 * 2 * (64 // g)          # 4 wavefronts x 2 row groups x 64/G rows
+    per_wg = 4 * steps * (64 // g)      # 4 wavefronts x steps row groups x 64/G rows
     chosen = None
     for resident in (1024, 2048, 4096):
-        rows = per_wg * (3 * resident // 2) + 7
+        rows = per_wg * int(rounds * resident) + 7
         p = sm.softmax_plan(rows, cols)
         needed = -(-rows // per_wg)
-        if p["kernel_name"] == "group_rows" and p["grid"] < needed:
+        if p["kernel_name"] == "group_rows" and p["grid"] == resident and resident < needed:
             chosen = (rows, p, needed)
             break
     assert chosen is not None, "no row count took the capped grid"
@@ -139,6 +142,35 @@ def test_group_rows_looping_grid(cols):
     log(f"[parity] group rows looping {rows}x{cols}, grid {p['grid']} of {needed} blocks")
     x = workloads.random_logits(rows, cols, seed=rows + cols, kind="clip_heavy")
     check_parity(x, run_gpu(x), f"group rows looping {rows}x{cols}")
+
+
+@pytest.mark.parametrize("cols,mid,large", [(36, "packed", "packed"), (100, "packed", "group_rows"),
+                                             (128, "packed", "group_rows"),
+                                             (244, "packed", "group_rows"),
+                                             (64, "group_rows", "group_rows")])
+def test_short_row_dispatch(cols, mid, large):
+    """Whole-strip rows of at most 256 columns: grouped rows for a small
+    launch whatever the fill; past it, the packed kernel for rows that fill
+    less than 3/4 of their lanes, and for rows of more than 64 columns or
+    filling their lanes in part while the grouped-rows grid takes one to
+    2.5 rounds of the resident workgroups.  The resident count is found
+    from the plans, not assumed; the mid-size launch is checked for parity."""
+    g = 1 << (cols // 4 - 1).bit_length()
+    per_wg = 4 * 2 * (64 // g)          # rows per workgroup at two row groups per step
+    found = None
+    for resident in (1024, 2048, 4096):
+        kinds = [sm.softmax_plan(per_wg * int(f * resident), cols)["kernel_name"]
+                 for f in (0.3, 2, 6)]
+        if kinds == ["group_rows", mid, large]:
+            found = resident
+            break
+    assert found is not None, "no resident count explains the plans"
+    rows = per_wg * 2 * found + 5
+    p = sm.softmax_plan(rows, cols)
+    assert p["kernel_name"] == mid
+    log(f"[parity] short-row dispatch {rows}x{cols} on {mid}")
+    x = workloads.random_logits(rows, cols, seed=rows, kind="clip_heavy")
+    check_parity(x, run_gpu(x), f"short-row dispatch {rows}x{cols}")
 
 
 @pytest.mark.parametrize("rows,cols", [(257, 50), (64, 1000), (33, 1001), (5, 8192), (3, 100003),
