@@ -289,7 +289,8 @@ SOFTMAX_API int softmax_nll_fwd(const float* x, const int64_t* labels, float* lo
  * on the matrix cores in fp32 (v_mfma_f32_16x16x4f32) and the softmax runs
  * on their accumulators.  On the DAM tile (d = dv = 200, 49 or 50 keys) the
  * scores of the last one or two keys are fp32 fma dot products on the
- * vector ALUs instead.  Accuracy: each score carries the rounding of a
+ * vector ALUs instead, and the value product takes the unnormalised
+ * exponentials (O is scaled by 1 / sum at the end).  Accuracy: each score carries the rounding of a
  * d-term fp32 dot product, delta_i = (d+2)*2^-24 * max_k |scale| sum_t
  * |Q_it K_kt| for query i, so each weight is within a relative
  * 2*delta_i + 4e-6 of the exact weight, and each output within

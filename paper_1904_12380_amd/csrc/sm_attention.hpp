@@ -308,28 +308,45 @@ constexpr int kAttnQB = kAttnMaxDQ / 16;  // 16-wide blocks of d in registers
 
 typedef __attribute__((address_space(3))) char attn_lds_char;
 
-// K_b and V_b (contiguous) into LDS at lk_s and lv_s with LDS-DMA loads,
+// `bytes` bytes from global memory at src into LDS at dst with LDS-DMA loads,
 // spread over 4 wavefronts wt = 0..3: each instruction writes its 64 lanes'
 // 16 bytes to consecutive LDS bytes from the (uniform) destination.  Whole
 // 1 KiB chunks need no lane mask; in a partial last chunk the lanes past the
-// end are off.
+// end are off.  attn_copy_ops is the number of instructions wavefront wt
+// issues.
+__device__ __forceinline__ void attn_copy_lds(float* dst, const float* src, int bytes, int wt,
+                                              int lane) {
+  attn_lds_char* dl = (attn_lds_char*)dst;
+  const char* gs = reinterpret_cast<const char*>(src);
+  int c = 1024 * wt;
+  for (; c + 1024 <= bytes; c += 4096)
+    __builtin_amdgcn_global_load_lds(gs + c + 16 * lane, dl + c, 16, 0, 0);
+  if (c < bytes && c + 16 * lane < bytes)
+    __builtin_amdgcn_global_load_lds(gs + c + 16 * lane, dl + c, 16, 0, 0);
+}
+
+__device__ __forceinline__ int attn_copy_ops(int bytes, int wt) {
+  const int full = bytes >= 1024 * (wt + 1) ? (bytes - 1024 * (wt + 1)) / 4096 + 1 : 0;
+  return full + (1024 * wt + 4096 * full < bytes ? 1 : 0);
+}
+
+// K_b and V_b into LDS at lk_s and lv_s (attn_copy_lds, K_b first).
 __device__ __forceinline__ void attn_copy_kv(float* lk_s, float* lv_s, const float* kb,
                                              const float* vb, int kbytes, int vbytes, int wt,
                                              int lane) {
-  attn_lds_char* dk = (attn_lds_char*)lk_s;
-  attn_lds_char* dvs = (attn_lds_char*)lv_s;
-  const char* gk = reinterpret_cast<const char*>(kb);
-  const char* gv = reinterpret_cast<const char*>(vb);
-  int c = 1024 * wt;
-  for (; c + 1024 <= kbytes; c += 4096)
-    __builtin_amdgcn_global_load_lds(gk + c + 16 * lane, dk + c, 16, 0, 0);
-  if (c < kbytes && c + 16 * lane < kbytes)
-    __builtin_amdgcn_global_load_lds(gk + c + 16 * lane, dk + c, 16, 0, 0);
-  c = 1024 * wt;
-  for (; c + 1024 <= vbytes; c += 4096)
-    __builtin_amdgcn_global_load_lds(gv + c + 16 * lane, dvs + c, 16, 0, 0);
-  if (c < vbytes && c + 16 * lane < vbytes)
-    __builtin_amdgcn_global_load_lds(gv + c + 16 * lane, dvs + c, 16, 0, 0);
+  attn_copy_lds(lk_s, kb, kbytes, wt, lane);
+  attn_copy_lds(lv_s, vb, vbytes, wt, lane);
+}
+
+// A workgroup barrier that leaves this wavefront's LDS-DMA copies in flight:
+// its own LDS accesses complete (lgkmcnt), then s_barrier.  __syncthreads()
+// would wait for the copies too (its fence covers them).  The empty asm
+// statements keep the compiler from moving memory accesses across it.
+__device__ __forceinline__ void attn_barrier_in_flight() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0); vmcnt and expcnt not waited
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // A wavefront's nq <= 16 query rows q0 .. of batch element b into
@@ -351,16 +368,229 @@ __device__ __forceinline__ void attn_load_q(f32x4m (&qf)[kAttnQB], const float* 
   }
 }
 
+// The value product for d = dv = DC known at compile time, with the
+// weights' exponentials taken inside it: sc holds the scaled scores of the
+// wavefront's 16 queries (lane (j, g): query j, keys 16 kt + 4 g + r at
+// 4 kt + r), rs the row shift of query j.  Contraction step i = 4 kt + r
+// multiplies key 16 kt + 4 g + r's unnormalised weight into all dv columns
+// (one 16x16x4 matrix op per 16 columns), and the next step's exponential
+// is independent of this step's matrix ops, so its VALU work issues beside
+// them instead of before the whole product.  O is scaled by 1 / sum when it
+// is stored: the sum of query 4 g + r's weights comes from lane 4 g + r.
+// Keys past lk have weight 0 and read the zero row after V_b.
+template <int NKT, bool WIDE, int DC, bool VT>
+__device__ __forceinline__ void attn_pv_stream(const float (&sc)[4 * NKT], const RowShift& rs,
+                                               const float* lv_s, float* o, int64_t b, int q0,
+                                               int nq, int lq, int lk, int j, int g) {
+  constexpr int dv = DC;
+  constexpr int NS = 4 * NKT;                  // contraction steps
+  constexpr int NF = DC / 64;                  // 64-column blocks: 4 ops of 16 columns
+  constexpr int NT = (DC - 64 * NF + 15) / 16; // 16-column tiles after them
+  auto key_ok = [&](int i) {
+    const int kt = i >> 2, r = i & 3;
+    return kt < NKT - 1 || (!(VT && r >= 2) && 16 * kt + 4 * g + r < lk);
+  };
+  // A step whose smallest key (lane group 0) is past lk has zero weight in
+  // every lane: its matrix ops are skipped (uniform).
+  auto step_live = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + (i & 3) < lk; };
+  auto vrow = [&](int i) {
+    const int key = 16 * (i >> 2) + 4 * g + (i & 3);
+    return ((i >> 2) < NKT - 1 || key < lk ? key : lk) * dv;
+  };
+  auto weight = [&](int i) {
+    return key_ok(i) ? exp_shift_clip<WIDE ? kExpWide : kExpAccurate>(sc[i], rs) : 0.0f;
+  };
+  f32x4m oacc[NF][4];
+  f32x4m ot[NT > 0 ? NT : 1];
+#pragma unroll
+  for (int cb = 0; cb < NF; ++cb)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) oacc[cb][u] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int t = 0; t < NT; ++t) ot[t] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+  // Value operands of a step: lane j reads columns 64 cb + 4 j .. + 3 of
+  // each block and column 64 NF + 16 t + j of each tile (inside V_b and the
+  // zero row for every lane, so no mask).
+  f32x4m va[2][NF > 0 ? NF : 1];
+  float vt[2][NT > 0 ? NT : 1];
+  auto load_v = [&](int i, int slot) {
+    const float* row = lv_s + vrow(i);
+#pragma unroll
+    for (int cb = 0; cb < NF; ++cb)
+      va[slot][cb] = *reinterpret_cast<const f32x4m*>(row + 64 * cb + 4 * j);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) vt[slot][t] = row[64 * NF + 16 * t + j];
+  };
+  load_v(0, 0);
+  float w_next = weight(0);
+  float psum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    const float w = w_next;
+    if (i + 1 < NS) {
+      load_v(i + 1, (i + 1) & 1);
+      w_next = weight(i + 1);
+    }
+    if (step_live(i)) {
+      psum += w;
+#pragma unroll
+      for (int cb = 0; cb < NF; ++cb)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) oacc[cb][u] = mfma16x16x4(w, va[i & 1][cb][u], oacc[cb][u]);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) ot[t] = mfma16x16x4(w, vt[i & 1][t], ot[t]);
+    }
+  }
+  float sum = psum + row16_partner(psum);
+  sum = sum + half32_partner(sum);
+  const float rcp = 1.0f / sum;
+  float rq[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) rq[r] = __shfl(rcp, 4 * g + r);
+  const __amdgpu_buffer_rsrc_t ro =
+      make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
+  const int orow = 4 * g * dv * 4;
+#pragma unroll
+  for (int cb = 0; cb < NF; ++cb) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const f32x4m ov = {oacc[cb][0][r] * rq[r], oacc[cb][1][r] * rq[r], oacc[cb][2][r] * rq[r],
+                         oacc[cb][3][r] * rq[r]};
+      __builtin_amdgcn_raw_buffer_store_b128(
+          __builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, ov), ro,
+          orow + (r * dv + 64 * cb + 4 * j) * 4, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int c = 64 * NF + 16 * t + j;
+    float* orow_p = o + (b * lq + q0 + 4 * g) * static_cast<int64_t>(dv) + c;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      if ((q0 + 4 * g + r < lq) & (c < dv))
+        __builtin_nontemporal_store(ot[t][r] * rq[r], orow_p + static_cast<int64_t>(r) * dv);
+    }
+  }
+}
+
+// The weights and the value product for d at run time (DC = 0): e holds
+// the scaled scores as in attn_pv_stream and becomes the normalised weights
+// before the product.
+template <int NKT, bool WIDE>
+__device__ __forceinline__ void attn_pv_rows(float (&e)[4 * NKT], const RowShift& rs,
+                                             const float* lv_s, float* o, int64_t b, int q0,
+                                             int nq, int lq, int lk, int dv, int j, int g) {
+#pragma unroll
+  for (int kt = 0; kt < NKT; ++kt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const bool key_ok = kt < NKT - 1 || 16 * kt + 4 * g + r < lk;
+      const float ev = exp_shift_clip<WIDE ? kExpWide : kExpAccurate>(e[4 * kt + r], rs);
+      e[4 * kt + r] = key_ok ? ev : 0.0f;
+    }
+  }
+  float sum = tree_sum(e);
+  sum = sum + row16_partner(sum);
+  sum = sum + half32_partner(sum);
+  const float rcp = 1.0f / sum;
+#pragma unroll
+  for (int i = 0; i < 4 * NKT; ++i) e[i] = e[i] * rcp;
+
+  // ---- O = P V, V from LDS --------------------------------------------------
+  // Contraction step i = 4 kt + r: key 16 kt + 4 g + r.  Keys past lk (only
+  // in the last key tile) have weight 0; their value operand is row 0 zeroed
+  // at use, since a stale value could be NaN.
+  auto v_ok = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + 4 * g + (i & 3) < lk; };
+  auto vrow = [&](int i) { return (v_ok(i) ? 16 * (i >> 2) + 4 * g + (i & 3) : 0) * dv; };
+  // A step whose smallest key (lane group 0) is past lk has zero weight in
+  // every lane: its matrix ops are skipped (a uniform branch; for DAM's 50
+  // keys, 2 of the 16 steps).
+  auto step_live = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + (i & 3) < lk; };
+  const __amdgpu_buffer_rsrc_t ro =
+      make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
+  const int orow = 4 * g * dv * 4;
+  const int nfull = dv >> 6;
+  // Each 64-column block in four quarters of NKT contraction steps: the next
+  // quarter's V rows (the next block's first, after the last) are read while
+  // this quarter's matrix ops run; the key mask is applied at use.
+  f32x4m vq[2][NKT];
+  if (nfull > 0) {
+#pragma unroll
+    for (int i = 0; i < NKT; ++i)
+      vq[0][i] = *reinterpret_cast<const f32x4m*>(lv_s + vrow(i) + 4 * j);
+  }
+  for (int cb = 0; cb < nfull; ++cb) {
+    const int c = 64 * cb + 4 * j;
+    f32x4m oacc[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) oacc[u] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int qi = 0; qi < 4; ++qi) {
+      if (qi < 3) {
+#pragma unroll
+        for (int i = 0; i < NKT; ++i)
+          vq[(qi + 1) & 1][i] =
+              *reinterpret_cast<const f32x4m*>(lv_s + vrow((qi + 1) * NKT + i) + c);
+      } else if (cb + 1 < nfull) {
+#pragma unroll
+        for (int i = 0; i < NKT; ++i)
+          vq[0][i] = *reinterpret_cast<const f32x4m*>(lv_s + vrow(i) + c + 64);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < NKT; ++i) {
+        const int st = qi * NKT + i;
+        if (step_live(st)) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            oacc[u] = mfma16x16x4(e[st], v_ok(st) ? vq[qi & 1][i][u] : 0.0f, oacc[u]);
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const f32x4m ov = {oacc[0][r], oacc[1][r], oacc[2][r], oacc[3][r]};
+      __builtin_amdgcn_raw_buffer_store_b128(
+          __builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, ov), ro,
+          orow + (r * dv + c) * 4, 0, 0);
+    }
+  }
+  // The remaining columns, one 16-column tile at a time: lane j takes column
+  // c0 + j; a column past dv reads a masked operand.
+  for (int c0 = 64 * nfull; c0 < dv; c0 += 16) {
+    const int c = c0 + j;
+    const bool c_ok = c < dv;
+    f32x4m oa = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int i = 0; i < 4 * NKT; ++i) {
+      if (step_live(i)) {
+        const float x = lv_s[vrow(i) + (c_ok ? c : 0)];
+        oa = mfma16x16x4(e[i], (v_ok(i) & c_ok) ? x : 0.0f, oa);
+      }
+    }
+    // Plain stores here: a 32-bit buffer store of an accumulator element
+    // was compiled to store element 0 for every r by this toolchain.
+    float* orow_p = o + (b * lq + q0 + 4 * g) * static_cast<int64_t>(dv) + c;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      if ((q0 + 4 * g + r < lq) & c_ok)
+        __builtin_nontemporal_store(oa[r], orow_p + static_cast<int64_t>(r) * dv);
+    }
+  }
+}
+
 // Scores, clipped softmax and O = P V for one wavefront's nq <= 16 queries
 // q0 .. of batch element b, with K_b at lk_s and V_b at lv_s in LDS and the
 // query rows in qf.  With DC != 0 (d = dv = DC), a zero row of dv + 16
-// floats follows V_b, and padding keys read their values from it.
-template <int NKT, bool WIDE, int DC>
+// floats follows V_b, and padding keys read their values from it
+// (attn_pv_stream).  With MID_SYNC the wavefront takes one workgroup barrier
+// between the softmax and the value product (V_b still in flight when the
+// scores start).
+template <int NKT, bool WIDE, int DC, bool MID_SYNC = false>
 __device__ __forceinline__ void attn_compute(const float* lk_s, const float* lv_s,
                                              const f32x4m (&qf)[kAttnQB], float* o, int64_t b,
                                              int q0, int nq, int lq, int lk, int d, int dv,
                                              float scale, Clip clip, int j, int g) {
-  constexpr bool ZR = DC != 0;
   constexpr int QB = kAttnQB;
   const int nblk = (d + 15) >> 4;
   // With DC != 0 (the DAM tile; the host guarantees at most 2 keys in the
@@ -451,109 +681,12 @@ __device__ __forceinline__ void attn_compute(const float* lk_s, const float* lv_
   m = fmaxf(m, row16_partner(m));
   m = fmaxf(m, half32_partner(m));
   const RowShift rs = row_shift(m, clip);
-#pragma unroll
-  for (int kt = 0; kt < NKT; ++kt) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      // With VT, registers 2 and 3 of the last tile hold no key (lk <= 16 NMT
-      // + 2): their exponentials are not computed.
-      const bool key_ok = kt < NKT - 1 || (!(VT && r >= 2) && 16 * kt + 4 * g + r < lk);
-      const float ev = exp_shift_clip<WIDE ? kExpWide : kExpAccurate>(e[4 * kt + r], rs);
-      e[4 * kt + r] = key_ok ? ev : 0.0f;
-    }
-  }
-  float sum = tree_sum(e);
-  sum = sum + row16_partner(sum);
-  sum = sum + half32_partner(sum);
-  const float rcp = 1.0f / sum;
-#pragma unroll
-  for (int i = 0; i < 4 * NKT; ++i) e[i] = e[i] * rcp;
-
-  // ---- O = P V, V from LDS --------------------------------------------------
-  // Contraction step i = 4 kt + r: key 16 kt + 4 g + r.  Keys past lk (only
-  // in the last key tile) have weight 0; their value operand is the zero row
-  // (ZR), else row 0 zeroed at use, since a stale value could be NaN.
-  auto v_ok = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + 4 * g + (i & 3) < lk; };
-  auto vrow = [&](int i) {
-    return ZR ? (v_ok(i) ? (16 * (i >> 2) + 4 * g + (i & 3)) * dv : lk * dv)
-              : (v_ok(i) ? 16 * (i >> 2) + 4 * g + (i & 3) : 0) * dv;
-  };
-  // A step whose smallest key (lane group 0) is past lk has zero weight in
-  // every lane: its matrix ops are skipped (a uniform branch; for DAM's 50
-  // keys, 2 of the 16 steps).
-  auto step_live = [&](int i) { return (i >> 2) < NKT - 1 || 16 * (i >> 2) + (i & 3) < lk; };
-  const __amdgpu_buffer_rsrc_t ro =
-      make_rsrc(o + (b * lq + q0) * static_cast<int64_t>(dv), nq * dv * 4);
-  const int orow = 4 * g * dv * 4;
-  const int nfull = dv >> 6;
-  // Each 64-column block in four quarters of NKT contraction steps: the next
-  // quarter's V rows (the next block's first, after the last) are read while
-  // this quarter's matrix ops run; the key mask is applied at use.
-  f32x4m vq[2][NKT];
-  if (nfull > 0) {
-#pragma unroll
-    for (int i = 0; i < NKT; ++i)
-      vq[0][i] = *reinterpret_cast<const f32x4m*>(lv_s + vrow(i) + 4 * j);
-  }
-  for (int cb = 0; cb < nfull; ++cb) {
-    const int c = 64 * cb + 4 * j;
-    f32x4m oacc[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) oacc[u] = f32x4m{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int qi = 0; qi < 4; ++qi) {
-      if (qi < 3) {
-#pragma unroll
-        for (int i = 0; i < NKT; ++i)
-          vq[(qi + 1) & 1][i] =
-              *reinterpret_cast<const f32x4m*>(lv_s + vrow((qi + 1) * NKT + i) + c);
-      } else if (cb + 1 < nfull) {
-#pragma unroll
-        for (int i = 0; i < NKT; ++i)
-          vq[0][i] = *reinterpret_cast<const f32x4m*>(lv_s + vrow(i) + c + 64);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < NKT; ++i) {
-        const int st = qi * NKT + i;
-        if (step_live(st)) {
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-            oacc[u] = mfma16x16x4(e[st], (ZR || v_ok(st)) ? vq[qi & 1][i][u] : 0.0f, oacc[u]);
-        }
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const f32x4m ov = {oacc[0][r], oacc[1][r], oacc[2][r], oacc[3][r]};
-      __builtin_amdgcn_raw_buffer_store_b128(
-          __builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, ov), ro,
-          orow + (r * dv + c) * 4, 0, 0);
-    }
-  }
-  // The remaining columns, one 16-column tile at a time: lane j takes column
-  // c0 + j.  A column past dv only feeds its own (unstored) output column, so
-  // with the zero row its loads need no mask (they stay inside V_b and the
-  // zero row); without it they are masked.
-  for (int c0 = 64 * nfull; c0 < dv; c0 += 16) {
-    const int c = c0 + j;
-    const bool c_ok = c < dv;
-    f32x4m oa = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int i = 0; i < 4 * NKT; ++i) {
-      if (step_live(i)) {
-        const float x = lv_s[vrow(i) + ((ZR || c_ok) ? c : 0)];
-        oa = mfma16x16x4(e[i], (ZR || (v_ok(i) & c_ok)) ? x : 0.0f, oa);
-      }
-    }
-    // Plain stores here: a 32-bit buffer store of an accumulator element
-    // was compiled to store element 0 for every r by this toolchain.
-    float* orow_p = o + (b * lq + q0 + 4 * g) * static_cast<int64_t>(dv) + c;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      if ((q0 + 4 * g + r < lq) & c_ok)
-        __builtin_nontemporal_store(oa[r], orow_p + static_cast<int64_t>(r) * dv);
-    }
+  if constexpr (DC != 0) {
+    if constexpr (MID_SYNC) __syncthreads();
+    attn_pv_stream<NKT, WIDE, DC, VT>(e, rs, lv_s, o, b, q0, nq, lq, lk, j, g);
+  } else {
+    static_assert(!MID_SYNC, "the mid-item barrier is for the compile-time tile");
+    attn_pv_rows<NKT, WIDE>(e, rs, lv_s, o, b, q0, nq, lq, lk, dv, j, g);
   }
 }
 
@@ -642,7 +775,7 @@ __global__ __launch_bounds__(512) void k_attention_pp(
     q0 = static_cast<int>(item - b * qblocks) * 64 + 16 * wt;
     nq = q0 < lq ? (lq - q0 < 16 ? lq - q0 : 16) : 0;
   };
-  auto stage = [&](int64_t n) {
+  auto stage_issue = [&](int64_t n) {
     int64_t b;
     int q0, nq;
     where(n, b, q0, nq);
@@ -652,11 +785,54 @@ __global__ __launch_bounds__(512) void k_attention_pp(
                  v + b * lk * static_cast<int64_t>(dv), lk * d * 4, lk * dv * 4, wt, lane);
     if (nq > 0) attn_load_q<DC>(qf, q, b, q0, nq, lq, d, j, g);
     __builtin_amdgcn_s_setprio(0);
+  };
+  auto stage = [&](int64_t n) {
+    stage_issue(n);
     __builtin_amdgcn_s_waitcnt(0);  // this wave's copies and loads
   };
-  if (team == 0) stage(0);
-  __syncthreads();
-  for (int64_t n = 0; n < n_items; ++n) {
+  // The first item has no compute to hide its copy behind.  Team 0 copies
+  // K_0 and its query rows and starts the scores as soon as they land; then
+  // team 1 copies V_0 and item 1, and V_0 lands during the score product.
+  // Barriers: (A) K_0 is in LDS, (B) V_0 is in LDS (team 0 takes it between
+  // its softmax and its value product), (C) item 1 is in LDS.  Team 1's
+  // barriers A and B leave its copies in flight.  A wavefront's copies land
+  // in the order it issued them, so waiting until at most kAttnLaterOps of
+  // them are outstanding covers V_0 whenever item 1 issued at least that
+  // many after it.
+  {
+    constexpr int kAttnLaterOps = 16;
+    int64_t b;
+    int q0, nq;
+    where(0, b, q0, nq);
+    if (team == 0) {
+      __builtin_amdgcn_s_setprio(2);
+      attn_copy_lds(lds, k + b * lk * static_cast<int64_t>(d), lk * d * 4, wt, lane);
+      if (nq > 0) attn_load_q<DC>(qf, q, b, q0, nq, lq, d, j, g);
+      __builtin_amdgcn_s_setprio(0);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();  // (A)
+      if (nq > 0)
+        attn_compute<NKT, WIDE, DC, true>(lds, lds + lk * d, qf, o, b, q0, nq, lq, lk, d, dv,
+                                          scale, clip, j, g);  // takes (B)
+      else
+        __syncthreads();  // (B)
+    } else {
+      attn_barrier_in_flight();  // (A)
+      __builtin_amdgcn_s_setprio(2);
+      attn_copy_lds(lds + lk * d, v + b * lk * static_cast<int64_t>(dv), lk * dv * 4, wt, lane);
+      __builtin_amdgcn_s_setprio(0);
+      const bool more = n_items > 1;
+      if (more) stage_issue(1);
+      if (more && attn_copy_ops(lk * d * 4, wt) + attn_copy_ops(lk * dv * 4, wt) >= kAttnLaterOps)
+        __builtin_amdgcn_s_waitcnt(0x0f70 | (kAttnLaterOps & 15) | ((kAttnLaterOps >> 4) << 14));
+      else
+        __builtin_amdgcn_s_waitcnt(0);
+      attn_barrier_in_flight();  // (B)
+      __builtin_amdgcn_s_waitcnt(0);
+    }
+    __syncthreads();  // (C)
+  }
+  for (int64_t n = 1; n < n_items; ++n) {
     if (team == (n & 1)) {
       int64_t b;
       int q0, nq;
