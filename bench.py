@@ -317,6 +317,11 @@ def time_gpu(sm, torch, w: workloads.Workload, x_host: np.ndarray, steps: int, w
 FP32_MATRIX_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix-core peak
 
 
+# The kernel softmax_attention_fwd runs on the DAM tile (d = dv = 200, 49 or
+# 50 keys, 128-bit operands).
+ATTENTION_KERNEL = "smx::k_attention_pp<4, false, 200>"
+
+
 def time_attention(sm, torch, key: str, steps: int, warmup: int) -> dict:
     """The fused attention on the DAM Q, K, V: graph-replayed steps over a
     rotation of at least 1 GiB of (Q, K, V, O) sets, plus the same problem
@@ -375,6 +380,8 @@ def time_attention(sm, torch, key: str, steps: int, warmup: int) -> dict:
         "sampled_normwise_err": err, "rotation_sets": nset,
         "traffic": traffic,
         **({"traffic_note": traffic_note} if traffic_note else {}),
+        "kernel": ATTENTION_KERNEL,
+        "kernel_trace": kernel_trace_stats(ATTENTION_KERNEL, None),
     }
 
 
@@ -705,9 +712,10 @@ def summarize_trace(directory: str, command: str, bench_json: str | None) -> str
     return path
 
 
-def kernel_trace_stats(kernel: str, grid_threads: int) -> dict | None:
-    """Median / p10 / p90 of one kernel shape from profiles/trace_bench.json,
-    if the kernel sources still hash to what the trace was taken with."""
+def kernel_trace_stats(kernel: str, grid_threads: int | None) -> dict | None:
+    """Median / p10 / p90 of one kernel shape (any grid when grid_threads is
+    None) from profiles/trace_bench.json, if the kernel sources still hash to
+    what the trace was taken with."""
     if not os.path.exists(TRACE_JSON):
         return None
     with open(TRACE_JSON) as f:
@@ -715,28 +723,35 @@ def kernel_trace_stats(kernel: str, grid_threads: int) -> dict | None:
     if doc.get("source_sha256") != kernel_source_sha256():
         return {"note": "kernel changed since the trace was taken"}
     for k in doc["kernels"]:
-        if k["kernel"] == kernel and k["grid_threads"] == grid_threads and k["run"] == 1:
+        if (k["kernel"] == kernel and grid_threads in (None, k["grid_threads"])
+                and k["run"] == 1):
             return {kk: k[kk] for kk in ("median_us", "p10_us", "p90_us", "mean_us", "calls")}
     return None
 
 
-def plan_kernel_name(plan: dict, mode: int = 0) -> str:
-    """The demangled template instance softmax_fwd launches for a plan."""
+def plan_kernel_name(plan: dict, cols: int, mode: int = 0) -> str:
+    """The demangled template instance softmax_fwd launches for a plan on
+    rows of `cols` columns (the row kernels' last argument says whether the
+    rows are taken with their phase: 128-bit access to rows that are not
+    whole 16-byte strips)."""
     v = plan["elems_per_lane"] // 4
     vec = "true" if plan["vec_width"] == 4 else "false"
+    ph = "true" if plan["vec_width"] == 4 and cols % 4 != 0 else "false"
     k = plan["kernel_name"]
     if k == "packed":
         return f"smx::k_packed<{plan['lanes_per_row']}, {plan['elems_per_lane']}, {vec}, {mode}>"
+    if k == "group_rows":  # the row groups per step (1 or 2) are not in the plan
+        return "smx::k_group_rows"
     if k == "wave_row":
-        return f"smx::k_wave_row<{v}, {vec}, {mode}>"
+        return f"smx::k_wave_row<{v}, {vec}, {mode}, {ph}>"
     if k == "block_row":
-        return f"smx::k_block_row<{plan['block_threads']}, {v}, {vec}, {mode}>"
-    return f"smx::k_split_onepass<{plan['block_threads']}, {v}, {vec}, {mode}>"
+        return f"smx::k_block_row<{plan['block_threads']}, {v}, {vec}, {mode}, {ph}>"
+    return f"smx::k_split_onepass<{plan['block_threads']}, {v}, {vec}, {mode}, {ph}>"
 
 
 def roofline(w, res: dict, traffic, traffic_note, plan: dict) -> dict:
     ms = res["ms_per_step"]
-    name = plan_kernel_name(plan)
+    name = plan_kernel_name(plan, w.cols)
     return {
         "bound": "hbm",
         "achieved": res["hbm_gbps"],

@@ -99,7 +99,8 @@ def test_summarize_trace_and_lookup(tmp_path, monkeypatch):
     """Dispatch durations are grouped by (kernel, grid) into runs, written to
     the trace JSON, and read back for a plan's kernel while the sources are
     unchanged."""
-    name = "smx::k_split_onepass<256, 8, true, 0>"
+    # as the profiler prints it: every row kernel ends with its row-phase flag
+    name = "smx::k_split_onepass<256, 8, true, 0, false>"
     full = f"void {name}(float const*, float*)"
     # 10 calls of 20..29 us, then (after a 1 s gap) 5 more of 40 us
     rows = [(full, 524288, 1000 + i * 100_000, 1000 + i * 100_000 + (20 + i) * 1000)
@@ -117,7 +118,15 @@ def test_summarize_trace_and_lookup(tmp_path, monkeypatch):
     assert runs[0]["median_us"] == pytest.approx(24.5)
     plan = {"kernel_name": "split_row", "elems_per_lane": 32, "vec_width": 4,
             "block_threads": 256, "lanes_per_row": 256}
-    assert bench.plan_kernel_name(plan) == name
+    assert bench.plan_kernel_name(plan, 32768) == name
+    assert bench.plan_kernel_name(plan, 32765) == "smx::k_split_onepass<256, 8, true, 0, true>"
+    assert bench.plan_kernel_name(dict(plan, vec_width=1), 32765).endswith("false, 0, false>")
+    wave = {"kernel_name": "wave_row", "elems_per_lane": 16, "vec_width": 4,
+            "block_threads": 256, "lanes_per_row": 64}
+    assert bench.plan_kernel_name(wave, 1000) == "smx::k_wave_row<4, true, 0, false>"
+    packed = {"kernel_name": "packed", "elems_per_lane": 13, "vec_width": 4,
+              "block_threads": 256, "lanes_per_row": 4}
+    assert bench.plan_kernel_name(packed, 50) == "smx::k_packed<4, 13, true, 0>"
     st = bench.kernel_trace_stats(name, 524288)
     assert st["calls"] == 10 and st["p10_us"] < st["median_us"] < st["p90_us"]
     doc["source_sha256"] = "0" * 64
