@@ -19,7 +19,8 @@ on a dedicated stream.  After W eager warmup steps and one untimed replay,
 the graph is replayed, untimed, until at least SETTLE_S seconds of GPU work
 have run (the GPU's clocks drop while the host prepares each workload, and
 take tens of milliseconds to come back up; a window timed right after the
-preparation measured up to 10% slower).  Then the measurement is:
+preparation measured up to 10% slower), FIRST_SETTLE_S for the first
+workload of the process, which starts from an idle GPU.  Then the measurement is:
 synchronise; replay the graph once untimed (a pre-roll
 that keeps the GPU busy while the host queues the rest); record the start
 event; replay the graph (exactly K steps, with every gap between them);
@@ -155,6 +156,12 @@ def warm_clocks(sm, torch, seconds: float = 0.3) -> None:
 
 
 SETTLE_S = 0.05
+# The first timed workload of the process starts from an idle GPU (sclk
+# about 170 MHz before the run): it settles longer.  With 0.05 s a session
+# measured the headline's graph window at 22.7 us per step against 21.9-22.1
+# for the same kernel in the modes timed right after it.
+FIRST_SETTLE_S = 0.5
+_settled = False
 
 
 def time_steps(torch, launch, steps: int, warmup: int) -> tuple[float, float]:
@@ -175,8 +182,11 @@ def time_steps(torch, launch, steps: int, warmup: int) -> tuple[float, float]:
                 launch(i, stream)
         g.replay()                  # first replay, untimed
         torch.cuda.synchronize()
+        global _settled
+        settle_s = SETTLE_S if _settled else FIRST_SETTLE_S
+        _settled = True
         t0 = time.perf_counter()
-        while time.perf_counter() - t0 < SETTLE_S:   # clocks settle, untimed
+        while time.perf_counter() - t0 < settle_s:   # clocks settle, untimed
             for _ in range(4):
                 g.replay()
             torch.cuda.synchronize()

@@ -69,8 +69,8 @@ extern "C" {
                                       (rows that are not whole 16-byte
                                       strips: 128-bit access in the aligned
                                       strips around the row above 2048) */
-#define SOFTMAX_KERNEL_BLOCK_ROW 3 /* cols <= 8192 (log and NLL outputs:
-                                      32768): one workgroup per row */
+#define SOFTMAX_KERNEL_BLOCK_ROW 3 /* cols <= 16380 (NLL outputs: 32768):
+                                      one workgroup per row */
 #define SOFTMAX_KERNEL_SPLIT_ROW 4 /* longer rows: several workgroups per row
                                       (chunks aligned to the row's phase for
                                       rows that are not whole strips) */
@@ -113,7 +113,8 @@ extern "C" {
  * Scratch: no entry point of this library allocates memory, so callers
  * that cannot allocate (code under stream capture, serving loops,
  * harnesses that forbid hipMalloc) can call any of them.  Rows longer than
- * 8192 columns are split over several workgroups, which combine partial
+ * 16380 columns (NLL outputs: 32768) are split over several workgroups,
+ * which combine partial
  * (max, sum) pairs
  * through a table of 4096 row entries held in a static device array
  * (2,359,552 bytes per device, part of the library's code object, zero at

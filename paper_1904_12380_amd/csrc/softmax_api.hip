@@ -45,13 +45,21 @@ constexpr int64_t kWaveRowMaxCols = 4096;
 constexpr int64_t kWaveRowMaxColsScalar = 2048;
 constexpr int64_t kBlockRowMaxCols = 32768;
 constexpr int kBlockThreads = 1024;
-// Probability rows longer than this take the one-pass split kernel rather
-// than one workgroup per row (measured with the dispatch sweep,
-// paper_1904_12380_amd/sweep.py): per 64 MiB of logits, 16384 columns ran
-// 21.8 us split against 25.8 us, 32768 columns 21.7 against 22.2, and 8192
-// columns 25.4 against 25.3.  Log and NLL rows keep k_block_row up to
+// Probability and log rows longer than this take the one-pass split kernel
+// rather than one workgroup per row (measured with the dispatch sweep,
+// paper_1904_12380_amd/sweep.py).  Per 64 MiB of logits, 16384 columns ran
+// 21.8 us split against 25.8 us and 32768 columns 21.7 against 22.2.  Rows
+// of 8193 to 16380 columns make two chunks, the second partly empty, and
+// more rows than one launch of resident workgroups takes (1024 rows), so the
+// last launch is ragged.  There one workgroup per row was 11-28% faster at
+// 64 MiB, 10-35% at 128 MiB and 16-33% at 4 and 16 MiB.  At 16380 columns
+// the split kernel was 7% faster at 64 MiB and level at 128 MiB.  Log rows
+// of 16384 to 32768 columns ran 22.3-22.5 us split against 24.2-26.7 us in
+// one workgroup.  Rows of 16381 to 16383 columns that are not whole strips
+// keep the split kernel (16383: 28.0 us split with 32-bit access against
+// 30.6 in one workgroup).  NLL rows keep k_block_row up to
 // kBlockRowMaxCols.
-constexpr int64_t kSplitMinColsProb = 8192;
+constexpr int64_t kSplitMinColsProb = 16380;
 // k_group_rows: when one workgroup per row block would take more than one
 // but at most this many rounds of the resident workgroups, the grid is
 // capped at the resident ones (each loops over row blocks, loading the next
@@ -90,7 +98,7 @@ constexpr int64_t kGroupRowsOneStepDen = 10;
 
 // Split rows, one pass: a row spans at most this many workgroups (the
 // exchange is read by one wavefront, one slot per lane).  Chunk shapes,
-// threads x 4-element strips per lane: probability rows take 256 x 8
+// threads x 4-element strips per lane: probability and log rows take 256 x 8
 // (8192 columns) up to kSmallChunkMaxChunks chunks; then every mode takes
 // 512 x 8 (16384 columns) up to 64 chunks, then 512 x 16 (32768, 128-bit
 // access only: with 32-bit access it would spill).  Measured per 64 MiB:
@@ -407,7 +415,7 @@ inline bool can_vec4(int kernel, const float* x, const float* y, int64_t cols) {
 
 // Rows taken with 128-bit access in the aligned strips around each row
 // (k_wave_row / k_block_row with PH): cols not a multiple of 4, x and y
-// 16-byte aligned, and 2048 < cols <= 8189.  Measured per 64 MiB: 4093
+// 16-byte aligned, and 2048 < cols <= 16377.  Measured per 64 MiB: 4093
 // columns 29.3 us against 37.7 us with 32-bit access, 8189 columns 28.1;
 // but 65, 250 and 2047 columns ran slower than with 32-bit access (84
 // against 64, 28.5 against 25.0, 31.9 against 28.6 us): the straddling
@@ -420,8 +428,9 @@ inline bool phase_rows(const float* x, const float* y, int64_t cols) {
 // Split rows taken with the row phase (k_split_onepass with PH): threads
 // per workgroup (8192-column chunks while a row needs at most 8, else
 // 16384), and whether a row qualifies: cols not a multiple of 4, x and y
-// 16-byte aligned, longer than the row kernels' phase range, one pass, and
-// the phase adds no chunk (the chunks cover cols + 3 columns; where that
+// 16-byte aligned, more than one 8192-column chunk, one pass, and the phase
+// adds no chunk (the library takes it only past phase_rows' range; a
+// caller's plan may ask for it from 8190 columns) (the chunks cover cols + 3 columns; where that
 // takes one more chunk than cols, the extra, nearly empty workgroups per
 // row cost more than 128-bit access gains: 16383 columns ran 33.5 us with
 // the phase and 28.2 us with 32-bit access, 131071 columns 33.2 against
@@ -431,8 +440,7 @@ inline int split_phase_threads(int64_t cols) {
   return ceil_div(cols + 3, int64_t(4) * 8 * 256) <= kSmallChunkMaxChunks ? 256 : 512;
 }
 inline bool split_phase_rows(const float* x, const float* y, int64_t cols) {
-  if (cols % 4 == 0 || cols + 3 <= kSplitMinColsProb || !aligned16(x) || !aligned16(y))
-    return false;
+  if (cols % 4 == 0 || cols + 3 <= 8192 || !aligned16(x) || !aligned16(y)) return false;
   const int64_t ch = int64_t(4) * 8 * split_phase_threads(cols);
   return ceil_div(cols + 3, ch) == ceil_div(cols, ch) &&
          ceil_div(cols + 3, ch) <= kOnePassMaxChunks;
@@ -491,7 +499,7 @@ Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
     s.kernel = SOFTMAX_KERNEL_WAVE_ROW;
     s.threads = 256;
     s.v = static_cast<int>(pow2_at_least(ceil_div(cols, 256)));
-  } else if (cols <= (prob ? kSplitMinColsProb : kBlockRowMaxCols)) {
+  } else if (cols <= (em != kNllOut ? kSplitMinColsProb : kBlockRowMaxCols)) {
     s.kernel = SOFTMAX_KERNEL_BLOCK_ROW;
     s.threads = kBlockThreads;
     s.v = static_cast<int>(std::max<int64_t>(2, pow2_at_least(ceil_div(cols, 4096))));
@@ -500,7 +508,7 @@ Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
     if (em == kNllOut && s.vec4 && ceil_div(cols, int64_t(4) * 8 * kNllThreads) <= kOnePassMaxChunks) {
       s.threads = kNllThreads;
       s.v = 8;
-    } else if (prob && ceil_div(cols, int64_t(4) * 8 * 256) <= kSmallChunkMaxChunks) {
+    } else if (em != kNllOut && ceil_div(cols, int64_t(4) * 8 * 256) <= kSmallChunkMaxChunks) {
       s.threads = 256;
       s.v = 8;
     } else if (ceil_div(cols, int64_t(4) * 8 * 512) <= kOnePassMaxChunks) {

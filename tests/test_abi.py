@@ -78,7 +78,12 @@ def test_cpu_tensor_is_rejected():
     (512, 32768, "split_row", 4, dict(chunks_per_row=4, elems_per_lane=32,
                                       block_threads=256)),
     (3, 8192, "block_row", 4, dict(elems_per_lane=8, block_threads=1024)),
-    (3, 8193, "split_row", 4, dict(chunks_per_row=2, block_threads=256)),   # row phase
+    (3, 8193, "block_row", 4, dict(elems_per_lane=16, block_threads=1024)),  # row phase
+    (3, 12287, "block_row", 4, dict(elems_per_lane=16)),   # row phase
+    (3, 16380, "block_row", 4, dict(elems_per_lane=16)),   # two ragged chunks split
+    (3, 16377, "block_row", 4, dict(elems_per_lane=16)),   # row phase, 16380-column span
+    (3, 16378, "split_row", 4, dict(chunks_per_row=2, block_threads=256)),   # row phase
+    (3, 16383, "split_row", 1, dict(chunks_per_row=2, block_threads=256)),  # phase adds a chunk
     (2, 65536, "split_row", 4, dict(chunks_per_row=8, block_threads=256)),
     (2, 65540, "split_row", 4, dict(chunks_per_row=5, block_threads=512)),
     (64, 262144, "split_row", 4, dict(chunks_per_row=16, elems_per_lane=32,
@@ -106,7 +111,7 @@ def test_cpu_tensor_is_rejected():
     (3, 4093, "wave_row", 4, dict(elems_per_lane=64)),
     (3, 4095, "block_row", 4, dict(elems_per_lane=8)),
     (3, 8189, "block_row", 4, dict(elems_per_lane=8)),
-    (3, 8190, "block_row", 1, dict(elems_per_lane=8)),     # the phase would add a chunk
+    (3, 8190, "block_row", 4, dict(elems_per_lane=16)),    # row phase, 8193-column span
     (1, 1048579, "split_row", 1, dict(chunks_per_row=65, elems_per_lane=32,
                                       block_threads=512)),
     (3, 32769, "split_row", 4, dict(chunks_per_row=5, block_threads=256)),
