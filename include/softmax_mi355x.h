@@ -326,7 +326,9 @@ typedef struct softmax_plan_t {
   int64_t chunks_per_row;  /* workgroups per row (split rows), else 1 */
   int64_t grid;            /* workgroups in each launch */
   int64_t workspace_bytes; /* bytes of the static exchange table (split rows), else 0 */
-  int64_t store_delay_ns;  /* stores wait this long after a workgroup starts (0: none);
+  int64_t store_delay_ns;  /* stores wait this long after a workgroup starts (0: none),
+                              in the first launch; the library's schedule gives a
+                              shorter last launch a delay for its own reads;
                               softmax_fwd_planned: -1 asks for the library's choice */
 } softmax_plan_t;
 
@@ -359,7 +361,7 @@ SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64
  *                   512 x 64 (32768); rows of more than 64 chunks take the
  *                   two-pass kernels, which only exist as 512 x 32;
  *   store_delay_ns  -1 for the library's store schedule, 0 for none, or a
- *                   delay up to 200000.
+ *                   delay up to 200000 (then the same for every launch).
  * The other fields are ignored.  The result is the same as softmax_fwd's to
  * within the accuracy bound (the summation order follows the kernel).
  * Returns SOFTMAX_ERR_INVALID_ARG, with nothing launched, for a plan the

@@ -110,6 +110,35 @@ constexpr int64_t kGroupRowsOneStepDen = 10;
 // keep no values.
 constexpr int64_t kOnePassMaxChunks = 64;
 constexpr int64_t kSmallChunkMaxChunks = 8;
+// Probability rows past kSmallChunkMaxChunks 8192-column chunks take
+// 8192-column chunks anyway (library_shape) when
+//  * that needs fewer launches (each launch holds the rows whose workgroups
+//    are resident at once): 300000 columns x 55 rows made 53 + 2 rows in
+//    16384-column chunks and one launch in 8192-column ones, 24.8 against
+//    29.7 us;
+//  * or the 16384-column grid would hold fewer than 5/8 of a workgroup per
+//    CU and a row at most 40 8192-column chunks: at 8 MiB (114-140
+//    workgroups) on 100000-300000 columns 8.3-8.9 against 8.9-9.3 us, but
+//    524288 columns (64 chunks) 10.0 against 9.8;
+//  * or that grid would hold fewer than 2 per CU, a row at most 32 chunks,
+//    and 16384-column chunks would pad the row by at least 1/32 more: at
+//    16 MiB (247-287 workgroups) 100000 and 200000 columns ran 10.9 and
+//    10.7 against 11.8 and 12.0 us, while 131072, 262144 and 300000 columns
+//    (no or 2.7% more padding) ran 1-7% faster in 16384-column chunks;
+//  * or that grid would hold fewer than 3 per CU and 16384-column chunks
+//    would pad the row by at least 1/16 more: at 32 MiB 100000 columns (581
+//    workgroups, 8.2% more padding) 14.3 against 15.0 us, while 200000
+//    columns (4.1%) ran 0.9% faster in 16384-column chunks.
+// Where the 16384-column grid fills the chip (64 MiB), only fewer launches
+// changed the choice.
+constexpr int64_t kSplitSparseNum = 5;  // workgroups per CU, 5/8
+constexpr int64_t kSplitSparseDen = 8;
+constexpr int64_t kSplitSparseMaxChunks = 40;
+constexpr int64_t kSplitThinPerCU = 2;
+constexpr int64_t kSplitThinMaxChunks = 32;
+constexpr int64_t kSplitThinPadDen = 32;  // extra padding of at least cols / 32
+constexpr int64_t kSplitWidePerCU = 3;
+constexpr int64_t kSplitWidePadDen = 16;  // extra padding of at least cols / 16
 constexpr int kNllThreads = 1024;
 
 // Split rows, two passes (rows too long for the one-pass shapes): 512 x 8
@@ -614,14 +643,21 @@ struct Plan {
   int64_t launches = 0;
   int64_t chunks = 1;
   int64_t wpr = 1;  // two-pass: workgroups per row
-  int64_t delay_ns = 0;
+  int64_t delay_ns = 0;       // the first launch's
   uint32_t delay_ticks = 0;
+  bool delay_per_launch = false;  // the library's schedule: each launch by its own reads
   uint32_t limit_ticks = 0;
 };
 
 uint32_t ns_to_ticks(int64_t ns, const DeviceFacts& f) {
   const int64_t t = (ns * f.wall_khz + 999999) / 1000000;
   return static_cast<uint32_t>(std::min<int64_t>(t, UINT32_MAX));
+}
+
+// The library's store delay for a launch that reads `bytes` (0: none).
+int64_t store_delay_ns(int64_t bytes) {
+  if (bytes < kStoreMinBytes) return 0;
+  return std::min(static_cast<int64_t>(bytes / kStoreReadBytesPerNs) + kStoreBaseNs, kStoreMaxNs);
 }
 
 // Rows per k_group_rows workgroup and step: four wavefronts, each U row
@@ -657,7 +693,8 @@ int group_rows_steps(int64_t rows, int em, int dev, const DeviceFacts& f, Shape*
 // The library's shape once rows and the device are known: rows of at most
 // 256 columns in whole strips take the grouped-rows kernel or the packed
 // kernel by the rules measured above (kGroupRowsMinFill, kGroupRowsOneStep
-// and kGroupRowsPackedRounds).
+// and kGroupRowsPackedRounds); long probability rows choose their chunk
+// size by launches and fill (kSplitFillMinPerCU).
 int library_shape(const float* x, const float* y, int64_t rows, int64_t cols, int em, int dev,
                   const DeviceFacts& f, Shape* out) {
   Shape s = default_shape(x, y, cols, em);
@@ -679,6 +716,35 @@ int library_shape(const float* x, const float* y, int64_t rows, int64_t cols, in
       s.v = 0;
       s.g = packed_lanes(cols);
       s.epl = static_cast<int>(ceil_div(cols, s.g));
+    }
+  } else if (s.kernel == SOFTMAX_KERNEL_SPLIT_ROW && !s.two_pass && s.threads == 512 &&
+             s.v == 8 && em != kLogOut && em != kNllOut) {
+    // Probability rows in 16384-column chunks: 8192-column chunks instead
+    // by launches and grid fill (kSplitSparseNum, kSplitThinPerCU).
+    Shape small = s;
+    small.threads = 256;
+    const int64_t c512 = row_chunks(s, cols);
+    const int64_t c256 = row_chunks(small, cols);
+    if (c256 <= kOnePassMaxChunks) {
+      int64_t r512 = 0;
+      int64_t r256 = 0;
+      int rc = resident_workgroups(s, em, dev, f, &r512);
+      if (rc == SOFTMAX_OK) rc = resident_workgroups(small, em, dev, f, &r256);
+      if (rc != SOFTMAX_OK) return rc;
+      const int64_t per512 = std::min(r512 / c512, int64_t(xch::kMaxRowsPerLaunch));
+      const int64_t per256 = std::min(r256 / c256, int64_t(xch::kMaxRowsPerLaunch));
+      if (per512 > 0 && per256 > 0) {
+        const int64_t grid512 = std::min(rows, per512) * c512;
+        const int64_t pad_more = c512 * chunk_cols(s) - c256 * chunk_cols(small);
+        const bool fewer_launches = ceil_div(rows, per256) < ceil_div(rows, per512);
+        const bool sparse = grid512 * kSplitSparseDen < kSplitSparseNum * f.cus &&
+                            c256 <= kSplitSparseMaxChunks;
+        const bool thin = grid512 < kSplitThinPerCU * f.cus && c256 <= kSplitThinMaxChunks &&
+                          pad_more * kSplitThinPadDen >= cols;
+        const bool padded = grid512 < kSplitWidePerCU * f.cus && c256 <= kSplitThinMaxChunks &&
+                            pad_more * kSplitWidePadDen >= cols;
+        if (fewer_launches || sparse || thin || padded) s = small;
+      }
     }
   }
   *out = s;
@@ -752,9 +818,8 @@ int make_plan(const Shape& s, int64_t rows, int64_t cols, int em, int dev,
     }
   }
   if (delay_req < 0) {
-    p.delay_ns = (one_wave && launch_read_bytes >= kStoreMinBytes)
-                     ? static_cast<int64_t>(launch_read_bytes / kStoreReadBytesPerNs) + kStoreBaseNs
-                     : 0;
+    p.delay_ns = one_wave ? store_delay_ns(launch_read_bytes) : 0;
+    p.delay_per_launch = one_wave;
   } else {
     p.delay_ns = delay_req;
   }
@@ -842,6 +907,13 @@ hipError_t run_plan(const Plan& p, const float* x, float* y, const int64_t* labe
       const float* xb = x + r0 * cols;
       float* yb = out_rows(y, r0, cols, em);
       const int64_t* lb = label_rows(labels, r0, em);
+      // A short last launch waits only as long as its own reads take: with
+      // the first launch's delay, 10 rows of 40000 columns after 409 waited
+      // 8.9 us before storing.
+      if (p.delay_per_launch) {
+        const int64_t ns = store_delay_ns(nb * cols * 4);
+        delay = ns > 0 ? ns_to_ticks(ns, f) : 0;
+      }
       XchArgs xa{f.scratch, exchange_key(yb, nonce), p.limit_ticks, 1u,  // join
                  entry_base(f, nb), 0u};
       void* args[] = {&xb, &yb, &lb, &xa, &cols, &ichunks, &delay, &c};
