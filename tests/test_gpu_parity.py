@@ -418,6 +418,29 @@ def test_split_rows_several_one_pass_launches():
     assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
 
 
+@pytest.mark.parametrize("rows,cols", [(55, 300000), (20, 200000), (419, 40000), (6, 300001)])
+def test_split_rows_chunk_by_row_count(rows, cols):
+    """Long rows whose chunk size the library picks by row count (8192-column
+    chunks where 16384-column ones would take more launches or leave the
+    chip thin), and a call whose last one-pass launch is short (its store
+    delay follows its own reads).  The plan is read back, not assumed: the
+    geometry must be consistent and the output must match the oracle."""
+    log(f"[parity] split rows, chunk by row count {rows}x{cols}")
+    p = sm.softmax_plan(rows, cols)
+    assert p["kernel_name"] == "split_row" and p["block_threads"] in (256, 512)
+    chunk = p["block_threads"] * p["elems_per_lane"]
+    assert p["chunks_per_row"] == -(-(cols + (3 if cols % 4 else 0)) // chunk) or \
+        p["chunks_per_row"] == -(-cols // chunk)
+    assert p["grid"] % p["chunks_per_row"] == 0
+    per_launch = p["grid"] // p["chunks_per_row"]
+    assert p["launches"] == -(-rows // per_launch)
+    x = workloads.random_logits(rows, cols, seed=rows + cols, kind="offset")
+    y1 = run_gpu(x)
+    check_parity(x, y1, f"{rows}x{cols}")
+    y2 = run_gpu(x)
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
 @pytest.mark.parametrize("rows,cols", [(3, 1048580), (2, 2097152), (1, 1048576), (5, 524292)])
 def test_split_rows_large_chunks(rows, cols):
     """Rows past 64 chunks of 16384 columns use 32768-column chunks (with
