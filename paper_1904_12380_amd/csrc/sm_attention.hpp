@@ -312,8 +312,7 @@ typedef __attribute__((address_space(3))) char attn_lds_char;
 // spread over 4 wavefronts wt = 0..3: each instruction writes its 64 lanes'
 // 16 bytes to consecutive LDS bytes from the (uniform) destination.  Whole
 // 1 KiB chunks need no lane mask; in a partial last chunk the lanes past the
-// end are off.  attn_copy_ops is the number of instructions wavefront wt
-// issues.
+// end are off.
 __device__ __forceinline__ void attn_copy_lds(float* dst, const float* src, int bytes, int wt,
                                               int lane) {
   attn_lds_char* dl = (attn_lds_char*)dst;
@@ -325,28 +324,12 @@ __device__ __forceinline__ void attn_copy_lds(float* dst, const float* src, int 
     __builtin_amdgcn_global_load_lds(gs + c + 16 * lane, dl + c, 16, 0, 0);
 }
 
-__device__ __forceinline__ int attn_copy_ops(int bytes, int wt) {
-  const int full = bytes >= 1024 * (wt + 1) ? (bytes - 1024 * (wt + 1)) / 4096 + 1 : 0;
-  return full + (1024 * wt + 4096 * full < bytes ? 1 : 0);
-}
-
 // K_b and V_b into LDS at lk_s and lv_s (attn_copy_lds, K_b first).
 __device__ __forceinline__ void attn_copy_kv(float* lk_s, float* lv_s, const float* kb,
                                              const float* vb, int kbytes, int vbytes, int wt,
                                              int lane) {
   attn_copy_lds(lk_s, kb, kbytes, wt, lane);
   attn_copy_lds(lv_s, vb, vbytes, wt, lane);
-}
-
-// A workgroup barrier that leaves this wavefront's LDS-DMA copies in flight:
-// its own LDS accesses complete (lgkmcnt), then s_barrier.  __syncthreads()
-// would wait for the copies too (its fence covers them).  The empty asm
-// statements keep the compiler from moving memory accesses across it.
-__device__ __forceinline__ void attn_barrier_in_flight() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0); vmcnt and expcnt not waited
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
 }
 
 // A wavefront's nq <= 16 query rows q0 .. of batch element b into
@@ -791,16 +774,12 @@ __global__ __launch_bounds__(512) void k_attention_pp(
     __builtin_amdgcn_s_waitcnt(0);  // this wave's copies and loads
   };
   // The first item has no compute to hide its copy behind.  Team 0 copies
-  // K_0 and its query rows and starts the scores as soon as they land; then
-  // team 1 copies V_0 and item 1, and V_0 lands during the score product.
-  // Barriers: (A) K_0 is in LDS, (B) V_0 is in LDS (team 0 takes it between
-  // its softmax and its value product), (C) item 1 is in LDS.  Team 1's
-  // barriers A and B leave its copies in flight.  A wavefront's copies land
-  // in the order it issued them, so waiting until at most kAttnLaterOps of
-  // them are outstanding covers V_0 whenever item 1 issued at least that
-  // many after it.
+  // K_0 and its query rows and starts the scores as soon as they land;
+  // meanwhile team 1 copies V_0 alone, and item 1 only after V_0 has landed
+  // (with item 1 in flight beside the scores as well, the launch took 0.9 us
+  // longer).  Barriers: (A) K_0 is in LDS, (B) V_0 is in LDS (team 0 takes it
+  // between its softmax and its value product), (C) item 1 is in LDS.
   {
-    constexpr int kAttnLaterOps = 16;
     int64_t b;
     int q0, nq;
     where(0, b, q0, nq);
@@ -817,17 +796,13 @@ __global__ __launch_bounds__(512) void k_attention_pp(
       else
         __syncthreads();  // (B)
     } else {
-      attn_barrier_in_flight();  // (A)
+      __syncthreads();  // (A)
       __builtin_amdgcn_s_setprio(2);
       attn_copy_lds(lds + lk * d, v + b * lk * static_cast<int64_t>(dv), lk * dv * 4, wt, lane);
       __builtin_amdgcn_s_setprio(0);
-      const bool more = n_items > 1;
-      if (more) stage_issue(1);
-      if (more && attn_copy_ops(lk * d * 4, wt) + attn_copy_ops(lk * dv * 4, wt) >= kAttnLaterOps)
-        __builtin_amdgcn_s_waitcnt(0x0f70 | (kAttnLaterOps & 15) | ((kAttnLaterOps >> 4) << 14));
-      else
-        __builtin_amdgcn_s_waitcnt(0);
-      attn_barrier_in_flight();  // (B)
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();  // (B)
+      if (n_items > 1) stage_issue(1);
       __builtin_amdgcn_s_waitcnt(0);
     }
     __syncthreads();  // (C)
