@@ -133,7 +133,9 @@ extern "C" {
  * Long rows are done in one pass when a row spans at most 64 workgroups
  * (chunks of 8192 columns up to cols = 65536, then chunks of 16384 up to
  * cols = 1048576 and, with 128-bit access only, chunks of 32768 up to
- * cols = 2097152): the
+ * cols = 2097152; probability rows keep 8192-column chunks up to
+ * cols = 524288 when the row count makes that take fewer launches or fill
+ * the device better): the
  * workgroups of a row exchange their pairs in the middle of the kernel and
  * wait for each other.  Workgroups are dispatched in ID order, so this always
  * progresses while a row's workgroups can be resident together.  Longer rows
@@ -334,11 +336,12 @@ typedef struct softmax_plan_t {
 
 /* The shape fields (kernel, vec_width, lanes_per_row, elems_per_lane,
  * block_threads, chunks_per_row) depend only on the arguments, except that
- * rows of at most 256 columns choose between GROUP_ROWS and PACKED by the
- * device's resident workgroups too; grid, launches and store_delay_ns are
- * those for the current device, and 0 when no device is present (then the
- * kernel is the choice made from the arguments alone).  No launch, no
- * allocation (the first call on a device queries its attributes). */
+ * rows of at most 256 columns choose between GROUP_ROWS and PACKED, and
+ * long rows their chunk size, by the device's resident workgroups too;
+ * grid, launches and store_delay_ns are those for the current device, and
+ * 0 when no device is present (then the shape is the choice made from the
+ * arguments alone).  No launch, no allocation (the first call on a device
+ * queries its attributes). */
 SOFTMAX_API int softmax_plan(const float* x, const float* y, int64_t rows, int64_t cols,
                              softmax_plan_t* plan);
 
