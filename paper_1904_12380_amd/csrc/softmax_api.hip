@@ -105,9 +105,10 @@ constexpr int64_t kGroupRowsOneStepDen = 10;
 // 256 x 8 ran 21.6-21.8 us on rows of 16384 to 65536 columns against
 // 21.8-22.7 for 512 x 8, but 22.5 against 21.7 on 131072 columns and 24.2
 // against 22.0 on 262144 (the row's wait for 16 or 32 partials costs more
-// than the smaller workgroups gain).  NLL outputs with 128-bit access take
-// 1024 x 8 (32768 columns): their workgroups never wait for each other and
-// keep no values.
+// than the smaller workgroups gain).  NLL outputs take 512 x 8 from the
+// first chunk: their workgroups never wait for each other and keep no
+// values; 1024 x 8 (32768 columns) measured 3-4% slower on 131072 to 524288
+// columns (64 x 262144: 15.9 against 15.3 us).
 constexpr int64_t kOnePassMaxChunks = 64;
 constexpr int64_t kSmallChunkMaxChunks = 8;
 // Probability rows past kSmallChunkMaxChunks 8192-column chunks take
@@ -139,7 +140,6 @@ constexpr int64_t kSplitThinMaxChunks = 32;
 constexpr int64_t kSplitThinPadDen = 32;  // extra padding of at least cols / 32
 constexpr int64_t kSplitWidePerCU = 3;
 constexpr int64_t kSplitWidePadDen = 16;  // extra padding of at least cols / 16
-constexpr int kNllThreads = 1024;
 
 // Split rows, two passes (rows too long for the one-pass shapes): 512 x 8
 // chunks, at most 64 workgroups per row (one exchange slot each, every
@@ -388,10 +388,6 @@ const void* shape_fn(const Shape& s, bool stats_pass) {
       if (s.threads == 512 && s.v == 8) return cast(&k_split_onepass<512, 8, VEC4, EM>);
       if constexpr (VEC4) {
         if (s.threads == 512 && s.v == 16) return cast(&k_split_onepass<512, 16, VEC4, EM>);
-        if constexpr (EM == kNllOut) {
-          if (s.threads == kNllThreads && s.v == 8)
-            return cast(&k_split_onepass<kNllThreads, 8, VEC4, EM>);
-        }
       }
       return nullptr;
     default:
@@ -534,10 +530,7 @@ Shape default_shape(const float* x, const float* y, int64_t cols, int em) {
     s.v = static_cast<int>(std::max<int64_t>(2, pow2_at_least(ceil_div(cols, 4096))));
   } else {
     s.kernel = SOFTMAX_KERNEL_SPLIT_ROW;
-    if (em == kNllOut && s.vec4 && ceil_div(cols, int64_t(4) * 8 * kNllThreads) <= kOnePassMaxChunks) {
-      s.threads = kNllThreads;
-      s.v = 8;
-    } else if (em != kNllOut && ceil_div(cols, int64_t(4) * 8 * 256) <= kSmallChunkMaxChunks) {
+    if (em != kNllOut && ceil_div(cols, int64_t(4) * 8 * 256) <= kSmallChunkMaxChunks) {
       s.threads = 256;
       s.v = 8;
     } else if (ceil_div(cols, int64_t(4) * 8 * 512) <= kOnePassMaxChunks) {
