@@ -22,7 +22,7 @@ Sources in the paper:
     max, subtract, exp, sum, scale by 1/sum, over a row-major
     [batch_size, num_classes] buffer indexed n*num_classes + c.
 
-Readings where the paper is silent (also listed in the design doc):
+Readings where the paper is silent:
   * The clip bound is CLIP_LO = -64 applied to the shifted logit before exp
     (the prose's 1e-60 is not an fp32 value and describes the effect, not the
     code).  Other bounds are a parameter, ``clip_lo``; ``clip_lo = -inf``
