@@ -70,7 +70,13 @@ extern "C" {
                                       strips: 128-bit access in the aligned
                                       strips around the row above 2048) */
 #define SOFTMAX_KERNEL_BLOCK_ROW 3 /* cols <= 16380 (NLL outputs: 32768):
-                                      one workgroup per row */
+                                      one workgroup per row; also
+                                      probability rows of 16385 to 24575
+                                      columns in whole strips when the
+                                      device has between 15/16 and 3 times
+                                      as many compute units as there are
+                                      rows (the split grid's third chunk
+                                      would be partly empty) */
 #define SOFTMAX_KERNEL_SPLIT_ROW 4 /* longer rows: several workgroups per row
                                       (chunks aligned to the row's phase for
                                       rows that are not whole strips) */
@@ -113,7 +119,8 @@ extern "C" {
  * Scratch: no entry point of this library allocates memory, so callers
  * that cannot allocate (code under stream capture, serving loops,
  * harnesses that forbid hipMalloc) can call any of them.  Rows longer than
- * 16380 columns (NLL outputs: 32768) are split over several workgroups,
+ * 16380 columns (NLL outputs: 32768) are split over several workgroups
+ * (except the block rows above),
  * which combine partial
  * (max, sum) pairs
  * through a table of 4096 row entries held in a static device array
@@ -336,8 +343,10 @@ typedef struct softmax_plan_t {
 
 /* The shape fields (kernel, vec_width, lanes_per_row, elems_per_lane,
  * block_threads, chunks_per_row) depend only on the arguments, except that
- * rows of at most 256 columns choose between GROUP_ROWS and PACKED, and
- * long rows their chunk size, by the device's resident workgroups too;
+ * rows of at most 256 columns choose between GROUP_ROWS and PACKED, long
+ * rows their chunk size, and rows of 16385 to 24575 columns between
+ * BLOCK_ROW and SPLIT_ROW, by the device's resident workgroups or compute
+ * units too;
  * grid, launches and store_delay_ns are those for the current device, and
  * 0 when no device is present (then the shape is the choice made from the
  * arguments alone).  No launch, no allocation (the first call on a device

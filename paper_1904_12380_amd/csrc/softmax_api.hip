@@ -140,6 +140,22 @@ constexpr int64_t kSplitThinMaxChunks = 32;
 constexpr int64_t kSplitThinPadDen = 32;  // extra padding of at least cols / 32
 constexpr int64_t kSplitWidePerCU = 3;
 constexpr int64_t kSplitWidePadDen = 16;  // extra padding of at least cols / 16
+// Probability rows of three 8192-column chunks whose last one is partly
+// empty (16384 < cols < 24576, whole strips) take one workgroup per row
+// (library_shape) when there are at least 1/3 and at most 15/16 as many rows
+// as compute units: then every row has a CU to itself and the split grid
+// would spend a third of its workgroups on the part-empty chunk.  Measured
+// at 8 and 16 MiB (85-240 rows): 17408 to 22528 columns ran 8.1-8.4 us
+// against 8.7-8.9 and 9.8-10.0 against 10.5-10.9 (5-9% faster); 24576
+// columns (no empty part) 1-9% slower in one workgroup, and 16388 columns x
+// 255 rows 1.3% slower.  At the bounds: 46-81 rows ran 3-6% faster split,
+// 89-105 rows 5-7% faster in one workgroup; 243 and 256 rows of 20480
+// columns 1.5-2.5% faster split.  With more rows than CUs the split kernel
+// was level or faster except at 17408 and 18432 columns x 455-481 rows
+// (4.5% slower).
+constexpr int64_t kBlockOverSplitMinRowsDen = 3;   // rows >= CUs / 3
+constexpr int64_t kBlockOverSplitMaxRowsNum = 15;  // rows <= CUs * 15/16
+constexpr int64_t kBlockOverSplitMaxRowsDen = 16;
 
 // Split rows, two passes (rows too long for the one-pass shapes): 512 x 8
 // chunks, at most 64 workgroups per row (one exchange slot each, every
@@ -739,6 +755,16 @@ int library_shape(const float* x, const float* y, int64_t rows, int64_t cols, in
         if (fewer_launches || sparse || thin || padded) s = small;
       }
     }
+  } else if (s.kernel == SOFTMAX_KERNEL_SPLIT_ROW && !s.two_pass && !s.ph && s.vec4 &&
+             s.threads == 256 && s.v == 8 && em != kLogOut && em != kNllOut &&
+             cols > 2 * chunk_cols(s) && cols < 3 * chunk_cols(s) &&
+             rows * kBlockOverSplitMinRowsDen >= f.cus &&
+             rows * kBlockOverSplitMaxRowsDen <= kBlockOverSplitMaxRowsNum * f.cus) {
+    // Three 8192-column chunks, the last partly empty, and a CU per row:
+    // one workgroup per row (kBlockOverSplitMinRowsDen).
+    s.kernel = SOFTMAX_KERNEL_BLOCK_ROW;
+    s.threads = kBlockThreads;
+    s.v = static_cast<int>(std::max<int64_t>(2, pow2_at_least(ceil_div(cols, 4096))));
   }
   *out = s;
   return SOFTMAX_OK;

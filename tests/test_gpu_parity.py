@@ -441,6 +441,35 @@ def test_split_rows_chunk_by_row_count(rows, cols):
     assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
 
 
+@pytest.mark.parametrize("rows_of_cus,cols,kernel", [
+    (lambda c: c * 204 // 256, 20480, "block_row"),
+    (lambda c: c // 3 + 1, 17408, "block_row"),
+    (lambda c: c * 15 // 16, 22528, "block_row"),
+    (lambda c: c // 3 - 1, 20480, "split_row"),
+    (lambda c: c * 15 // 16 + 1, 18432, "split_row"),
+    (lambda c: c * 170 // 256, 24576, "split_row"),
+])
+def test_three_chunk_rows_by_row_count(rows_of_cus, cols, kernel):
+    """Rows of 16384 to 24576 columns whose third 8192-column chunk would be
+    partly empty take one workgroup per row when there are between 1/3 and
+    15/16 as many rows as compute units; outside that band, or with whole
+    chunks, the split kernel.  The row counts follow the device's CU count.
+    The output must match the oracle and repeat bit for bit."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    rows = rows_of_cus(cus)
+    log(f"[parity] three-chunk rows by row count {rows}x{cols} ({cus} CUs)")
+    p = sm.softmax_plan(rows, cols)
+    assert p["kernel_name"] == kernel and p["vec_width"] == 4, p
+    if kernel == "block_row":
+        assert p["block_threads"] == 1024 and p["grid"] == rows
+    x = workloads.random_logits(rows, cols, seed=rows * 3 + cols, kind="offset")
+    y1 = run_gpu(x)
+    check_parity(x, y1, f"{rows}x{cols}")
+    y2 = run_gpu(x)
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
 @pytest.mark.parametrize("rows,cols", [(3, 1048580), (2, 2097152), (1, 1048576), (5, 524292)])
 def test_split_rows_large_chunks(rows, cols):
     """Rows past 64 chunks of 16384 columns use 32768-column chunks (with
