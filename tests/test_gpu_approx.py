@@ -101,3 +101,17 @@ def test_exp_probe_fast_bound():
     bound = 1.5e-7 * np.minimum(np.abs(dd), 64.0) + 1.2e-7
     assert np.all(rel <= bound), float((rel / bound).max())
     log(f"[approx] exp probe: max rel err {rel.max():.3e}, worst / bound {(rel / bound).max():.3f}")
+
+
+def test_three_chunk_block_rows():
+    """Rows of 20480 columns with about 0.8 rows per compute unit take one
+    1024-thread workgroup per row rather than the split kernel."""
+    import torch
+    rows = torch.cuda.get_device_properties(0).multi_processor_count * 204 // 256
+    cols = 20480
+    p = sm.softmax_plan(rows, cols)
+    assert p["kernel_name"] == "block_row" and p["elems_per_lane"] == 32, p
+    for kind in ("clip_heavy", "normal", "offset"):
+        x = workloads.random_logits(rows, cols, seed=rows * 31 + 5, kind=kind, scale=10.0)
+        worst = check_approx(x, run_approx(x), -64.0, f"{rows}x{cols} {kind}")
+        log(f"[approx] {rows}x{cols} {kind}: max rel err {worst:.3e}")

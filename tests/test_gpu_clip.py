@@ -200,3 +200,20 @@ def test_graph_capture_without_clip():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(yg.view(torch.int32), want.view(torch.int32)), rep
+
+
+def test_bounds_on_three_chunk_block_rows():
+    """Rows of 20480 columns with about 0.8 rows per compute unit take one
+    1024-thread workgroup per row (8 strips per lane) rather than the split
+    kernel; every bound on that instance."""
+    import torch
+    rows = torch.cuda.get_device_properties(0).multi_processor_count * 204 // 256
+    cols = 20480
+    p = sm.softmax_plan(rows, cols)
+    assert p["kernel_name"] == "block_row" and p["elems_per_lane"] == 32, p
+    log(f"[clip] bounds on block rows {rows}x{cols}")
+    for kind in ("clip_heavy", "normal"):
+        x = workloads.random_logits(rows, cols, seed=rows + 7, kind=kind, scale=30.0)
+        for lo in BOUNDS:
+            worst = check_clip(x, run_clip(x, lo), lo, f"{rows}x{cols} {kind}")
+            log(f"[clip] {rows}x{cols} {kind} lo={lo}: max rel err (normal range) {worst:.3e}")

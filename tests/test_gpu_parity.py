@@ -448,7 +448,8 @@ def test_split_rows_chunk_by_row_count(rows, cols):
     (lambda c: c // 3 - 1, 20480, "split_row"),
     (lambda c: c * 15 // 16 + 1, 18432, "split_row"),
     (lambda c: c * 170 // 256, 24576, "split_row"),
-])
+], ids=["0.8cus-20480", "cus/3+1-17408", "15/16cus-22528", "cus/3-1-20480",
+        "15/16cus+1-18432", "0.66cus-24576"])
 def test_three_chunk_rows_by_row_count(rows_of_cus, cols, kernel):
     """Rows of 16384 to 24576 columns whose third 8192-column chunk would be
     partly empty take one workgroup per row when there are between 1/3 and
